@@ -1,0 +1,287 @@
+"""Pins of the oracle's codec (CPU only).
+
+Each test fixes part of ``oracle.codec`` by something other than the code
+itself: closed forms, identities the paper states (eq. design_kfac_norm_vec /
+trace, design_sphere_proof, design_vec_whiten, design_input_side_sphere), the
+identity-transform special case (Euclidean FP8), exact arithmetic on inputs
+chosen to be representable, and the paper's own printed metrics.
+"""
+
+import os
+
+import numpy as np
+import pytest
+import scipy.linalg
+
+from oracle import codec, e4m3
+from synth import factor_inputs, gradient_set, haar
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _rng(s=0):
+    return np.random.default_rng(s)
+
+
+def _spiked(dim, lams, sigma2, seed=1):
+    """A = Q diag(lams, sigma2, ..., sigma2) Q^T built exactly from a Haar Q."""
+    q = haar(_rng(seed), dim, dim)
+    spec = np.full(dim, sigma2)
+    spec[:len(lams)] = lams
+    return (q * spec) @ q.T, q
+
+
+# ---------------------------------------------------------------- statistics
+
+def test_statistics_orthogonal_columns_give_diagonal():
+    T, n = 64, 8
+    q = haar(_rng(2), T, n)
+    norms = np.arange(1, n + 1, dtype=np.float64)
+    X = q * norms                      # orthogonal columns with known norms
+    A = codec.factor_statistics(X)
+    np.testing.assert_allclose(A, np.diag(norms ** 2 / T), atol=1e-14)
+
+
+def test_statistics_psd_and_scale():
+    X, _ = factor_inputs(5, 256, 32)
+    A = codec.factor_statistics(X)
+    assert np.allclose(A, A.T)
+    assert np.linalg.eigvalsh(A).min() > -1e-12
+    # E[x x^T] of 2x is 4 E[x x^T]
+    np.testing.assert_allclose(codec.factor_statistics(2 * X.astype(np.float64)), 4 * A, rtol=1e-13)
+
+
+# ---------------------------------------------------------------- low-rank factor
+
+def test_spiked_covariance_closed_form():
+    dim, lams, s2 = 40, np.array([9.0, 4.0, 2.5, 1.7]), 0.3
+    A, q = _spiked(dim, lams, s2)
+    f = codec.lowrank_factor(A, 4)
+    assert f.sigma2 == pytest.approx(s2, rel=1e-12)
+    expect = np.eye(dim) + (q[:, :4] * (np.sqrt(s2 / lams) - 1.0)) @ q[:, :4].T
+    np.testing.assert_allclose(f.inverse_root(), expect, atol=1e-12)
+    np.testing.assert_allclose(f.c_inv, np.sqrt(lams / s2) - 1.0, rtol=1e-12)
+
+
+def test_whitening_identity():
+    A = codec.factor_statistics(factor_inputs(9, 400, 24)[0])
+    for r in (1, 5, 12):
+        f = codec.lowrank_factor(A, r)
+        w, v = np.linalg.eigh(A)
+        w, v = w[::-1], v[:, ::-1]
+        Ar = (v[:, :r] * f.lam) @ v[:, :r].T + f.sigma2 * (np.eye(24) - v[:, :r] @ v[:, :r].T)
+        Si = f.inverse_root()
+        np.testing.assert_allclose(Si @ Ar @ Si, f.sigma2 * np.eye(24), atol=1e-12 * np.trace(A))
+        # S is the sigma-normalised symmetric root of A_r
+        S = f.root()
+        np.testing.assert_allclose(S @ S * f.sigma2, Ar, atol=1e-12 * np.trace(A))
+
+
+def test_full_rank_is_sigma_times_inverse_sqrt():
+    A = codec.factor_statistics(factor_inputs(11, 300, 16)[0])
+    f = codec.lowrank_factor(A, 16)
+    assert f.sigma2 == pytest.approx(np.trace(A) / 16, rel=1e-12)
+    ref = np.sqrt(f.sigma2) * np.linalg.inv(np.real(scipy.linalg.sqrtm(A)))
+    np.testing.assert_allclose(f.inverse_root(), ref, atol=1e-9)
+
+
+def test_factor_is_invariant_to_scaling_A():
+    A = codec.factor_statistics(factor_inputs(12, 200, 20)[0])
+    f1, f2 = codec.lowrank_factor(A, 6), codec.lowrank_factor(7.5 * A, 6)
+    np.testing.assert_allclose(f1.inverse_root(), f2.inverse_root(), atol=1e-12)
+
+
+def test_coefficients_are_mutual_inverses_and_floor():
+    A = codec.factor_statistics(factor_inputs(13, 200, 20)[0])
+    f = codec.lowrank_factor(A, 8)
+    np.testing.assert_allclose((1 + f.c_fwd) * (1 + f.c_inv), 1.0, rtol=1e-14)
+    assert np.all(f.c_fwd <= 0) and np.all(f.c_inv >= 0)
+    # rank-deficient A: the damping floor keeps sigma^2 positive
+    X = np.zeros((50, 20)); X[:, :3] = _rng(4).standard_normal((50, 3))
+    g = codec.lowrank_factor(codec.factor_statistics(X), 5, damping=1e-6)
+    assert g.sigma2 == pytest.approx(1e-6 * np.trace(codec.factor_statistics(X)) / 20, rel=1e-9)
+    assert np.all(np.isfinite(g.c_fwd))
+
+
+# ---------------------------------------------------------------- transform / inverse
+
+def test_forward_then_inverse_is_identity_float64():
+    grads = gradient_set(1000, 1100, 2, 48, 40)
+    fA = codec.lowrank_factor(codec.factor_statistics(factor_inputs(1001, 256, 40)[0]), 8)
+    fG = codec.lowrank_factor(codec.factor_statistics(factor_inputs(1002, 256, 48)[0]), 8)
+    for a, g in ((fA, None), (None, fG), (fA, fG)):
+        back = codec.inverse(codec.forward(grads, a, g), a, g)
+        rel = np.linalg.norm(back - grads) / np.linalg.norm(grads)
+        assert rel <= 1e-10
+
+
+def test_two_sided_equals_kronecker_vec():
+    # eq. design_vec_whiten with column-major vec, at 8 x 6
+    m, n = 8, 6
+    W = _rng(5).standard_normal((m, n))
+    fA = codec.lowrank_factor(codec.factor_statistics(factor_inputs(21, 64, n)[0]), 2)
+    fG = codec.lowrank_factor(codec.factor_statistics(factor_inputs(22, 64, m)[0]), 3)
+    Wt = codec.forward(W, fA, fG)
+    vec = lambda M: M.reshape(-1, order="F")
+    np.testing.assert_allclose(vec(Wt), np.kron(fA.inverse_root(), fG.inverse_root()) @ vec(W),
+                               atol=1e-12)
+
+
+def test_kfac_norm_vec_trace_and_sphere():
+    # eq. design_kfac_norm_vec == eq. design_kfac_norm_trace == ||L_G^T dW L_A||_F^2
+    m, n = 7, 5
+    rng = _rng(6)
+    dW = rng.standard_normal((m, n))
+    A = codec.factor_statistics(rng.standard_normal((40, n))) + 0.1 * np.eye(n)
+    G = codec.factor_statistics(rng.standard_normal((40, m))) + 0.1 * np.eye(m)
+    vec = dW.reshape(-1, order="F")
+    v1 = vec @ np.kron(A, G) @ vec
+    v2 = np.trace(A @ dW.T @ G @ dW)
+    LA, LG = np.linalg.cholesky(A), np.linalg.cholesky(G)
+    v3 = np.linalg.norm(LG.T @ dW @ LA) ** 2
+    assert v1 == pytest.approx(v2, rel=1e-12) and v2 == pytest.approx(v3, rel=1e-12)
+    # eq. design_input_side_sphere
+    assert np.trace(A @ dW.T @ dW) == pytest.approx(np.linalg.norm(dW @ LA) ** 2, rel=1e-12)
+
+
+def test_sigma_normalised_roots_give_the_ball():
+    # with S S = A_r / sigma^2:  ||S_G dW S_A||^2 = tr(A_r dW^T G_r dW) / (sigma_A^2 sigma_G^2)
+    m, n = 12, 10
+    rng = _rng(8)
+    A = codec.factor_statistics(rng.standard_normal((80, n)) * np.linspace(3, 0.2, n))
+    G = codec.factor_statistics(rng.standard_normal((80, m)) * np.linspace(2, 0.3, m))
+    fA, fG = codec.lowrank_factor(A, 3), codec.lowrank_factor(G, 4)
+    SA, SG = fA.root(), fG.root()
+    Ar, Gr = fA.sigma2 * SA @ SA, fG.sigma2 * SG @ SG
+    dW = rng.standard_normal((m, n))
+    lhs = np.linalg.norm(SG @ dW @ SA) ** 2
+    rhs = np.trace(Ar @ dW.T @ Gr @ dW) / (fA.sigma2 * fG.sigma2)
+    assert lhs == pytest.approx(rhs, rel=1e-10)
+
+
+# ---------------------------------------------------------------- scale and quantize
+
+def test_identity_transform_is_euclidean_fp8():
+    grads = gradient_set(2000, 2100, 3, 32, 48)
+    base_codes, base_s, wt = codec.encode(grads, None, None)
+    np.testing.assert_array_equal(wt, grads)
+    # direct Euclidean FP8: codes of fl32(x * fl32(448/amax)) per rank
+    for j in range(3):
+        a = np.float32(np.abs(grads[j]).max())
+        inv = np.float32(448.0) / a
+        np.testing.assert_array_equal(base_codes[j], e4m3.quantize((grads[j] * inv).astype(np.float32)))
+        assert base_s[j, 0, 0] == np.float32(a / np.float32(448.0))
+    # a factor whose coefficients are zero, and a rank-0 factor, are the identity
+    zero = codec.Factor(haar(_rng(3), 48, 4), np.zeros(4), np.zeros(4), 1.0)
+    for f in (zero, codec.identity_factor(48)):
+        c, s, _ = codec.encode(grads, f, None)
+        np.testing.assert_array_equal(c, base_codes)
+        np.testing.assert_array_equal(s, base_s)
+
+
+def test_amax_element_maps_to_448_and_zero_blocks():
+    grads = gradient_set(3000, 3100, 2, 40, 64)
+    grads[1, :, 32:] = 0.0
+    codes, s, _ = codec.encode(grads, block_cols=32)
+    for j in range(2):
+        for b in range(2):
+            blk = grads[j, :, 32 * b:32 * (b + 1)]
+            if not blk.any():
+                assert s[j, 0, b] == 0.0
+                assert np.all(codes[j, :, 32 * b:32 * (b + 1)] == 0)
+                continue
+            i = np.unravel_index(np.argmax(np.abs(blk)), blk.shape)
+            assert codes[j, i[0], 32 * b + i[1]] in (0x7E, 0xFE)
+
+
+def test_shared_scale_is_max_over_ranks():
+    grads = gradient_set(3500, 3600, 4, 16, 16)
+    grads[2] *= 3.0
+    _, s_loc = codec.quantize_transformed(grads)
+    _, s_sh = codec.quantize_transformed(grads, shared=True)
+    assert np.all(s_sh == s_loc.max(axis=0))
+
+
+def test_block_grid_partial_edges():
+    assert codec.block_grid(100, 300, 0, 128) == (100, 128, 1, 3)
+    assert codec.block_grid(100, 300, 30, 0) == (30, 300, 4, 1)
+    Wt = np.arange(2 * 5 * 7, dtype=np.float32).reshape(2, 5, 7)
+    am = codec.block_amax(Wt, 2, 3)
+    assert am.shape == (2, 3, 3)
+    assert am[1, 2, 2] == Wt[1, 4, 6] and am[0, 0, 0] == Wt[0, 1, 2]
+
+
+def test_scale_edge_cases():
+    s, inv = codec.scales_from_amax(np.array([0.0, 448.0, np.inf, 1e-40], dtype=np.float32))
+    assert s[0] == 0 and inv[0] == 0
+    assert s[1] == 1.0 and inv[1] == 1.0
+    assert np.isinf(s[2]) and inv[2] == 0
+    assert inv[3] == np.finfo(np.float32).max
+
+
+# ---------------------------------------------------------------- rank sum
+
+def test_reduce_exact_on_representable_inputs():
+    # values = E4M3 value * 2^-12 with the block amax at 448 * 2^-12: scale exactly 2^-12,
+    # every step exact, so the mean is the exact float64 mean of the inputs
+    rng = _rng(10)
+    table = e4m3.decode_table()
+    finite = table[np.isfinite(table)]
+    N, m, n = 4, 9, 13
+    vals = rng.choice(finite, size=(N, m, n)) * 2.0 ** -12
+    vals[:, 0, 0] = 448.0 * 2.0 ** -12
+    vals[:, 0, 1] = -448.0 * 2.0 ** -12
+    g = vals.astype(np.float32)
+    codes, s, _ = codec.encode(g)
+    assert np.all(s == np.float32(2.0 ** -12))
+    np.testing.assert_array_equal(e4m3.dequantize(codes) * 2.0 ** -12, vals)
+    M = codec.reduce_local(codes, s)
+    np.testing.assert_array_equal(M.astype(np.float64), vals.sum(axis=0) / N)
+
+
+def test_reduce_single_rank_and_identical_ranks():
+    g = gradient_set(4000, 4100, 1, 20, 30)
+    codes, s, _ = codec.encode(g)
+    M1 = codec.reduce_local(codes, s)
+    np.testing.assert_array_equal(M1, (e4m3.dequantize(codes[0]) * s[0, 0, 0]).astype(np.float32))
+    # two identical ranks: v + v is exact and /2 is exact
+    c2, s2 = np.repeat(codes, 2, axis=0), np.repeat(s, 2, axis=0)
+    np.testing.assert_array_equal(codec.reduce_local(c2, s2), M1)
+
+
+def test_round_trip_error_is_fp8_sized():
+    g = gradient_set(4500, 4600, 4, 64, 64)
+    out = codec.round_trip(g)
+    fid = codec.fidelity(out, g.astype(np.float64).mean(axis=0))
+    # E4M3 has 3 mantissa bits: per-element relative error <= 2^-4 above the subnormals
+    assert 5e-3 < fid["RelL2"] < 6.25e-2 and fid["Cos"] > 0.998
+
+
+# ---------------------------------------------------------------- metrics
+
+def test_fidelity_special_cases():
+    g = _rng(11).standard_normal((5, 6))
+    f = codec.fidelity(g, g)
+    assert f["RelL2"] == 0 and f["Cos"] == pytest.approx(1.0) and f["MSE"] == 0
+    f2 = codec.fidelity(2 * g, g)
+    assert f2["RelL2"] == pytest.approx(1.0) and f2["Cos"] == pytest.approx(1.0)
+    assert f2["MSE"] == pytest.approx(np.mean(g * g)) and f2["MaxErr"] == pytest.approx(np.abs(g).max())
+
+
+def test_paper_metric_definitions_are_consistent():
+    # Tables I-II measure one gradient g, so MSE / RelL2^2 = ||g||^2 / n on every row
+    # (eq. recon_metrics); the 67.4% reduction follows from the RelL2 column.
+    rows = {}
+    with open(os.path.join(GOLDEN, "paper_table2_relL2.txt")) as fh:
+        for ln in fh:
+            if ln.strip() and not ln.startswith("#"):
+                name, *vals = ln.split()
+                rows[name] = [float(v) for v in vals]
+    ratios = np.array([r[3] / r[0] ** 2 for r in rows.values()])
+    assert ratios.std() / ratios.mean() < 2e-4
+    red = 100 * (rows["euclidean"][0] - rows["lowrank_32"][0]) / rows["euclidean"][0]
+    assert round(red, 1) == 67.4
+    # the same relation holds for the oracle's metrics
+    g = gradient_set(5000, 5100, 1, 30, 30)[0]
+    fid = codec.fidelity(codec.round_trip(g[None]), g)
+    assert fid["MSE"] / fid["RelL2"] ** 2 == pytest.approx(np.mean(g.astype(np.float64) ** 2), rel=1e-9)
