@@ -1,0 +1,207 @@
+/*
+ * gift.h -- C ABI of the GIFT gradient codec for AMD Instinct MI355X (gfx950).
+ *
+ * GIFT ("Geometry-Informed Low-precision Gradient Communication") communicates
+ * each weight gradient W_g in R^{d_out x d_in} (Sec. IV-A, eq. design_Wg) in FP8
+ * after mapping it into near-isotropic coordinates built from K-FAC factors
+ * (Sec. II-B, eq. kfac_fisher_block; Sec. IV-A, eq. design_full_transform and
+ * design_input_side_transform), then maps the synchronized result back
+ * (eq. design_full_inverse_transform / design_input_side_inverse).  This
+ * library is the per-layer hot path of that rule (Algorithm 1) on one GPU:
+ *
+ *   gift_factor_update   factor statistics A = E[a a^T], G = E[delta delta^T]
+ *                        and their rank-r transforms (Sec. V-B, eq. impl_A_lowrank)
+ *   gift_encode          transform, amax scale, FP8 E4M3 quantize (Algorithm 1)
+ *   gift_reduce_local    dequantize and average the N data-parallel ranks held
+ *                        on this GPU (eq. dp_grad_avg; Algorithm 1 sum and /N)
+ *   gift_decode          inverse transform of the averaged gradient
+ *
+ * Notation: m = d_out (rows), n = d_in (columns), N data-parallel ranks, r the
+ * transform rank, T tokens behind the factor statistics.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Tensors are DEVICE pointers, row-major and densely packed, allocated and
+ *   owned by the caller.  The library owns only the opaque gift_ctx and
+ *   gift_factor objects and the device workspace inside them.
+ * - Every compute call validates its arguments on the host, then enqueues
+ *   kernels on the context's HIP stream and returns without synchronizing.
+ *   A non-GIFT_OK status means nothing was enqueued, except GIFT_EHIP, which
+ *   reports a HIP runtime error seen while enqueueing.
+ * - gift_last_error() returns a thread-local message describing the last
+ *   non-OK status of the calling thread.  No C++ exception crosses the ABI.
+ * - Calls on one context are not thread-safe; use one context per host thread.
+ * - Block scaling: each rank's m x n matrix is tiled into blocks of
+ *   block_rows x block_cols elements (0 = the whole dimension; partial edge
+ *   blocks allowed), nbr = ceil(m / block_rows), nbc = ceil(n / block_cols).
+ *   Scales are stored as float32 [N, nbr, nbc].
+ * - FP8 codes are OCP E4M3 (E4M3FN) bit patterns: bias 7, largest finite 448,
+ *   NaN = 0x7F/0xFF, no infinities.  Quantization is
+ *       s   = fl32(amax / 448)           (stored scale)
+ *       y   = fl32(x * fl32(448 / amax)) (amax = 0 -> multiplier 0; an
+ *                                         overflowing multiplier -> FLT_MAX)
+ *       q   = round-to-nearest-even E4M3(y), saturating at +-448, keeping the
+ *             sign of zero, NaN -> 0x7F.
+ *   amax is the exact block maximum of |x|; a NaN in a block makes its amax
+ *   (and scale) NaN.
+ */
+#ifndef GIFT_H
+#define GIFT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GIFT_ABI_VERSION 1
+
+typedef struct gift_ctx gift_ctx;
+typedef struct gift_factor gift_factor;
+
+typedef enum {
+  GIFT_OK = 0,
+  GIFT_EINVAL = -1,        /* NULL handle/pointer, bad enum, bad count        */
+  GIFT_ESHAPE = -2,        /* sizes inconsistent or out of the supported range */
+  GIFT_ENOMEM = -3,        /* device or host allocation failed                */
+  GIFT_EHIP = -4,          /* HIP runtime error while enqueueing              */
+  GIFT_EUNSUPPORTED = -5   /* valid request this build does not implement     */
+} gift_status;
+
+typedef enum { GIFT_F32 = 0, GIFT_BF16 = 1 } gift_dtype;
+
+/* Which sides of the K-FAC geometry a factor applies (Sec. IV-A, V-A). */
+enum {
+  GIFT_SIDE_INPUT = 1,   /* right factor from A (d_in x d_in): W S_A^-1      */
+  GIFT_SIDE_OUTPUT = 2,  /* left factor from G (d_out x d_out): S_G^-1 W     */
+  GIFT_SIDE_BOTH = 3     /* both: S_G^-1 W S_A^-1                             */
+};
+
+/* Scale mode (Algorithm 1): LOCAL keeps each rank's own amax (the GIFT
+ * branch's local scaling, Sec. V-E); SHARED takes the maximum over the N ranks
+ * first (the AllReduce_MAX of the Euclidean branch and of scale-sync steps). */
+typedef enum { GIFT_SCALE_LOCAL = 0, GIFT_SCALE_SHARED = 1 } gift_scale_mode;
+
+/* Kernel families, for the optional per-kernel timing below. */
+typedef enum {
+  GIFT_KERNEL_AMAX = 0,          /* Euclidean block amax                     */
+  GIFT_KERNEL_QUANT = 1,         /* Euclidean scale + FP8 pack               */
+  GIFT_KERNEL_PROJECT = 2,       /* W U_A and U_G^T W projections             */
+  GIFT_KERNEL_UPDATE_AMAX = 3,   /* rank-r update fused with block amax       */
+  GIFT_KERNEL_UPDATE_QUANT = 4,  /* rank-r update fused with scale + FP8 pack */
+  GIFT_KERNEL_UPDATE_STORE = 5,  /* rank-r update of the inverse transform    */
+  GIFT_KERNEL_REDUCE = 6,        /* dequantize-accumulate over ranks          */
+  GIFT_KERNEL_SYRK = 7,          /* factor statistics X^T X / T               */
+  GIFT_KERNEL_FACTOR = 8,        /* subspace iteration, Rayleigh-Ritz, misc   */
+  GIFT_KERNEL_SMALL = 9,         /* small helpers (zeroing, coefficient setup) */
+  GIFT_KERNEL_COUNT = 10
+} gift_kernel;
+
+/* ABI version of the loaded library (GIFT_ABI_VERSION it was built with). */
+int32_t gift_abi_version(void);
+
+/* Thread-local description of the calling thread's last non-OK status. */
+const char *gift_last_error(void);
+
+/* Create a context bound to a HIP stream (hipStream_t passed as void*; NULL is
+ * the null stream).  No HIP call is made until the first compute call, which
+ * binds the context to the then-current device.  *out receives the handle. */
+gift_status gift_ctx_create(void *hip_stream, gift_ctx **out);
+
+/* Rebind the context to another stream of the same device. */
+gift_status gift_ctx_set_stream(gift_ctx *ctx, void *hip_stream);
+
+/* Destroy a context (synchronizes its stream, frees its workspace). NULL ok. */
+void gift_ctx_destroy(gift_ctx *ctx);
+
+/* Per-kernel timing: when enabled, every launch is bracketed by HIP events on
+ * the context stream.  gift_ctx_profile_read synchronizes the stream and
+ * returns the number of launches and their summed duration (ms) for one kernel
+ * family since the last reset; gift_ctx_profile_reset clears the counters. */
+gift_status gift_ctx_profile_enable(gift_ctx *ctx, int32_t enable);
+gift_status gift_ctx_profile_read(gift_ctx *ctx, int32_t kernel, int64_t *launches,
+                                  double *total_ms);
+gift_status gift_ctx_profile_reset(gift_ctx *ctx);
+
+/* Create the transform state of one m x n weight matrix (Algorithm 1's
+ * per-layer factor).  rank: r >= 0 (r <= n for the input side, r <= m for the
+ * output side; 0 = identity).  sides: GIFT_SIDE_*.  damping: relative floor of
+ * the isotropic level sigma^2 (>= damping * tr(A)/n), the regularization of
+ * eq. design_chol.  seed: key of the Philox4x32-10 start block of the subspace
+ * iteration.  The new factor is the identity until updated or imported.
+ * Allocates device memory on the current device (synchronous). */
+gift_status gift_factor_create(gift_ctx *ctx, int64_t m, int64_t n, int32_t rank,
+                               int32_t sides, float damping, uint64_t seed,
+                               gift_factor **out);
+
+/* Destroy a factor (synchronizes the context stream first). NULL ok. */
+void gift_factor_destroy(gift_factor *f);
+
+/* Refresh the factor from one batch of statistics (Sec. V-E: refreshed every
+ * K steps; Algorithm 1's A ~ L_A L_A^T).
+ *   acts       [T, n] layer inputs a (device; float32 or bfloat16 per dtype),
+ *              required when sides include GIFT_SIDE_INPUT, else ignored;
+ *   out_grads  [T, m] gradients delta w.r.t. the layer outputs, required when
+ *              sides include GIFT_SIDE_OUTPUT, else ignored;
+ *   iters      subspace iterations (>= 0).  The first update starts from the
+ *              Philox block; later updates warm-start from the previous
+ *              subspace.
+ * Computes A = acts^T acts / T (and G likewise), its top-r eigenpairs by
+ * block subspace iteration (k = min(dim, 2r) columns, CholeskyQR2) with
+ * Rayleigh-Ritz extraction, sigma^2 = mean of the remaining eigenvalues
+ * (floored at damping * tr/dim), and the coefficients
+ *   c_i = sqrt(sigma^2/lambda_i) - 1,  c'_i = sqrt(lambda_i/sigma^2) - 1,
+ * so that S^-1 = I + U diag(c) U^T and S = I + U diag(c') U^T. */
+gift_status gift_factor_update(gift_ctx *ctx, gift_factor *f, const void *acts,
+                               const void *out_grads, int64_t T, gift_dtype dtype,
+                               int32_t iters);
+
+/* Copy one side's transform out of / into a factor (device pointers):
+ *   U [dim, r] row-major (dim = n for GIFT_SIDE_INPUT, m for GIFT_SIDE_OUTPUT),
+ *   c_fwd [r], c_inv [r], sigma2 [1].
+ * side must be GIFT_SIDE_INPUT or GIFT_SIDE_OUTPUT and present in the factor.
+ * Import replaces the side's transform (the next update warm-starts from
+ * U).  Enqueued on the context stream. */
+gift_status gift_factor_export(gift_ctx *ctx, const gift_factor *f, int32_t side,
+                               float *U, float *c_fwd, float *c_inv, float *sigma2);
+gift_status gift_factor_import(gift_ctx *ctx, gift_factor *f, int32_t side,
+                               const float *U, const float *c_fwd, const float *c_inv,
+                               const float *sigma2);
+
+/* Encode the N ranks' gradients (Algorithm 1, both branches):
+ *   f            factor of this m x n matrix, or NULL for the Euclidean branch;
+ *   grads        [N, m, n] float32 rank gradients;
+ *   mode         GIFT_SCALE_LOCAL or GIFT_SCALE_SHARED;
+ *   ef           error-feedback residual [N, m, n] float32 in transformed
+ *                coordinates (Algorithm 1: U~ = U + R; R <- U~ - Deq(Q(U~))),
+ *                or NULL for none.  Zero it before the first step;
+ *   codes        [N, m, n] uint8 out: E4M3 codes of W~_j = S_G^-1 W_j S_A^-1 (+R);
+ *   scales       [N, nbr, nbc] float32 out;
+ *   transformed  optional [N, m, n] float32 out: W~ (+R) before quantization.
+ * Output buffers must not overlap the inputs. */
+gift_status gift_encode(gift_ctx *ctx, const gift_factor *f, const float *grads,
+                        int32_t N, int64_t m, int64_t n, int32_t block_rows,
+                        int32_t block_cols, gift_scale_mode mode, float *ef,
+                        uint8_t *codes, float *scales, float *transformed);
+
+/* Average the N ranks in transformed coordinates (eq. dp_grad_avg):
+ *   mean[e] = fl32(acc / N),  acc = fl32(acc + fl32(val(codes[j][e]) * s_j)) for
+ *   j = 0..N-1 in order (no fused multiply-add), s_j the scale of e's block.
+ * Dequantizing each rank with its own scale is Algorithm 1's
+ * Dequantize(AllReduce_SUM(Q); s) / N whenever the scales are shared.
+ *   codes [N, m, n], scales [N, nbr, nbc], mean [m, n] float32 out. */
+gift_status gift_reduce_local(gift_ctx *ctx, const uint8_t *codes, const float *scales,
+                              int32_t N, int64_t m, int64_t n, int32_t block_rows,
+                              int32_t block_cols, float *mean);
+
+/* Inverse transform (eq. design_full_inverse_transform): out = S_G mean S_A
+ * (sides absent from f are the identity; f = NULL copies).  mean and out are
+ * [m, n] float32 and must not overlap. */
+gift_status gift_decode(gift_ctx *ctx, const gift_factor *f, const float *mean,
+                        int64_t m, int64_t n, float *out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GIFT_H */

@@ -1,0 +1,10 @@
+"""GIFT gradient codec for AMD Instinct MI355X (gfx950).
+
+The HIP library ``libgift.so`` (C ABI in ``include/gift.h``) holds the whole
+hot path; :mod:`paper_2607_07494_amd.gift` is its thin Python binding.
+"""
+
+from .gift import (  # noqa: F401
+    BF16, F32, KERNELS, SCALE_LOCAL, SCALE_SHARED, SIDE_BOTH, SIDE_INPUT, SIDE_OUTPUT,
+    Context, Factor, GiftError, decode, encode, reduce_local, scale_grid,
+)

@@ -1,0 +1,586 @@
+// C ABI of the GIFT codec: argument validation, object lifetime and the
+// kernel sequence of each call.
+//
+// Transform in rank-r form (Sec. IV-A, V-A, V-B; Algorithm 1).  With
+// S_A^-1 = I + U_A C_A U_A^T (n x n) and S_G^-1 = I + U_G C_G U_G^T (m x m),
+// the encode of one rank's W computes
+//
+//   INPUT   W~ = W + P (C_A U_A^T),                 P = W U_A          (m x r)
+//   OUTPUT  W~ = W + (U_G C_G) Q,                   Q = U_G^T W        (r x n)
+//   BOTH    W~ = W + (U_G C_G) Q + L2 U_A^T,        L2 = (P + U_G C_G K) C_A,
+//                                                   K = U_G^T P        (r x r)
+//
+// i.e. W~ = S_G^-1 W S_A^-1 as one rank-r (rank-2r) update of W.  Each update
+// runs twice: once fused with the block amax, once fused with the
+// quantization (the scale needs the finished amax of the whole block, so W~
+// is recomputed rather than written to memory).  The decode applies the same
+// form with the inverse coefficients C' to the rank mean.
+
+#include <math.h>
+#include <string.h>
+
+#include <new>
+#include <string>
+
+#include "gift_internal.h"
+
+namespace gift {
+
+namespace {
+thread_local std::string g_last_error;
+}
+
+gift_status set_error(gift_status st, const std::string &msg) {
+  g_last_error = msg;
+  return st;
+}
+
+gift_status hip_error(hipError_t e, const char *what) {
+  return set_error(GIFT_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+gift_status check_launch(const char *what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_error(e, what);
+  return GIFT_OK;
+}
+
+gift_status bind_device(gift_ctx *ctx) {
+  if (ctx->device >= 0) return GIFT_OK;
+  int dev = -1;
+  GIFT_HIP_TRY(hipGetDevice(&dev));
+  ctx->device = dev;
+  return GIFT_OK;
+}
+
+gift_status workspace(gift_ctx *ctx, size_t bytes, void **out) {
+  bytes = (bytes + 255) & ~(size_t)255;
+  if (bytes == 0) bytes = 256;
+  if (bytes > ctx->ws.bytes) {
+    if (ctx->ws.ptr) {
+      GIFT_HIP_TRY(hipStreamSynchronize(ctx->stream));
+      GIFT_HIP_TRY(hipFree(ctx->ws.ptr));
+      ctx->ws.ptr = nullptr;
+      ctx->ws.bytes = 0;
+    }
+    void *p = nullptr;
+    hipError_t e = hipMalloc(&p, bytes);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return set_error(GIFT_ENOMEM, "workspace: hipMalloc of " + std::to_string(bytes) + " bytes failed");
+    }
+    ctx->ws.ptr = p;
+    ctx->ws.bytes = bytes;
+  }
+  *out = ctx->ws.ptr;
+  return GIFT_OK;
+}
+
+ProfileScope::ProfileScope(gift_ctx *c, int k) : ctx(c), kernel(k) {
+  if (!ctx || !ctx->profile) return;
+  hipEvent_t start = nullptr;
+  auto grab = [&]() -> hipEvent_t {
+    if (!ctx->event_pool.empty()) {
+      hipEvent_t e = ctx->event_pool.back();
+      ctx->event_pool.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  };
+  start = grab();
+  stop = grab();
+  if (!start || !stop) {
+    stop = nullptr;
+    return;
+  }
+  (void)hipEventRecord(start, ctx->stream);
+  ctx->prof.push_back(ProfileRec{kernel, start, stop});
+}
+
+ProfileScope::~ProfileScope() {
+  if (stop) (void)hipEventRecord(stop, ctx->stream);
+}
+
+BlockGeom block_geom(int64_t m, int64_t n, int32_t block_rows, int32_t block_cols) {
+  BlockGeom g;
+  g.br = block_rows <= 0 ? m : (block_rows < m ? block_rows : m);
+  g.bc = block_cols <= 0 ? n : (block_cols < n ? block_cols : n);
+  g.nbr = (int32_t)((m + g.br - 1) / g.br);
+  g.nbc = (int32_t)((n + g.bc - 1) / g.bc);
+  return g;
+}
+
+namespace {
+
+constexpr int64_t kMaxRows = 65535LL * 16;     // grid.y limit of the 16-row tiles
+constexpr int64_t kMaxCols = (1LL << 31) - 1;
+constexpr int32_t kMaxRanks = 65535;            // grid.z limit
+constexpr int32_t kMaxRank = 512;               // subspace block k = 2r <= 1024
+
+gift_status drain_profile(gift_ctx *ctx) {
+  if (ctx->prof.empty()) return GIFT_OK;
+  GIFT_HIP_TRY(hipStreamSynchronize(ctx->stream));
+  for (const ProfileRec &r : ctx->prof) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, r.start, r.stop) == hipSuccess) {
+      ctx->prof_ms[r.kernel] += ms;
+      ctx->prof_launches[r.kernel] += 1;
+    }
+    ctx->event_pool.push_back(r.start);
+    ctx->event_pool.push_back(r.stop);
+  }
+  ctx->prof.clear();
+  return GIFT_OK;
+}
+
+bool side_in(int32_t sides, int32_t s) { return (sides & s) != 0; }
+
+size_t a256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+gift_status check_matrix_dims(int64_t m, int64_t n) {
+  if (m <= 0 || n <= 0) return set_error(GIFT_ESHAPE, "m and n must be positive");
+  if (m > kMaxRows) return set_error(GIFT_ESHAPE, "m exceeds the supported maximum (1048560)");
+  if (n > kMaxCols) return set_error(GIFT_ESHAPE, "n exceeds the supported maximum (2^31-1)");
+  return GIFT_OK;
+}
+
+// W~ = W + (low-rank part of the transform) for all N ranks.  Fills the
+// projection buffers in `ws` and returns the update as a tile job (without
+// epilogue fields); side inverse=true builds the decode's S_G M S_A update.
+struct LowRankPlan {
+  TileJob upd;
+  bool active = false;
+};
+
+gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, int32_t N,
+                          int64_t m, int64_t n, bool inverse, char *ws, size_t *used,
+                          LowRankPlan *plan) {
+  const Side &A = f->A;
+  const Side &G = f->G;
+  const bool useA = side_in(f->sides, GIFT_SIDE_INPUT) && A.r > 0;
+  const bool useG = side_in(f->sides, GIFT_SIDE_OUTPUT) && G.r > 0;
+  plan->active = useA || useG;
+  if (!plan->active) return GIFT_OK;
+  const int64_t mn = m * n;
+  size_t off = 0;
+  float *P = nullptr, *Qm = nullptr, *Km = nullptr, *L2 = nullptr;
+  if (useA) {
+    P = reinterpret_cast<float *>(ws + off);
+    off += a256(sizeof(float) * N * m * A.r);
+  }
+  if (useG) {
+    Qm = reinterpret_cast<float *>(ws + off);
+    off += a256(sizeof(float) * N * n * G.r);
+  }
+  if (useA && useG) {
+    Km = reinterpret_cast<float *>(ws + off);
+    off += a256(sizeof(float) * N * G.r * A.r);
+    L2 = reinterpret_cast<float *>(ws + off);
+    off += a256(sizeof(float) * N * m * A.r);
+  }
+  *used = off;
+  if (ws == nullptr) return GIFT_OK;  // sizing pass
+  gift_status st;
+  const float *UcG = inverse ? G.Uci : G.Uc;
+  if (useA) {  // P = W U_A
+    TileJob j;
+    j.nseg = 1;
+    j.seg[0].a = Operand{W, n, mn, true};
+    j.seg[0].b = Operand{A.Ut, n, 0, true};
+    j.seg[0].K = n;
+    j.M = m;
+    j.N = A.r;
+    j.batch = N;
+    j.C = P;
+    j.ldc = A.r;
+    j.cbs = m * A.r;
+    j.kernel_family = GIFT_KERNEL_PROJECT;
+    if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
+  }
+  if (useG) {  // Qm = W^T U_G  (Q^T, n x r)
+    TileJob j;
+    j.nseg = 1;
+    j.seg[0].a = Operand{W, n, mn, false};
+    j.seg[0].b = Operand{G.Ut, m, 0, true};
+    j.seg[0].K = m;
+    j.M = n;
+    j.N = G.r;
+    j.batch = N;
+    j.C = Qm;
+    j.ldc = G.r;
+    j.cbs = n * G.r;
+    j.kernel_family = GIFT_KERNEL_PROJECT;
+    if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
+  }
+  if (useA && useG) {
+    {  // K = U_G^T P  (r_G x r_A)
+      TileJob j;
+      j.nseg = 1;
+      j.seg[0].a = Operand{G.Ut, m, 0, true};
+      j.seg[0].b = Operand{P, A.r, m * A.r, false};
+      j.seg[0].K = m;
+      j.M = G.r;
+      j.N = A.r;
+      j.batch = N;
+      j.C = Km;
+      j.ldc = A.r;
+      j.cbs = (int64_t)G.r * A.r;
+      j.kernel_family = GIFT_KERNEL_PROJECT;
+      if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
+    }
+    {  // L2 = (P + U_G C_G K) C_A
+      TileJob j;
+      j.nseg = 1;
+      j.seg[0].a = Operand{UcG, G.r, 0, true};
+      j.seg[0].b = Operand{Km, A.r, (int64_t)G.r * A.r, false};
+      j.seg[0].K = G.r;
+      j.M = m;
+      j.N = A.r;
+      j.batch = N;
+      j.C = L2;
+      j.ldc = A.r;
+      j.cbs = m * A.r;
+      j.D = P;
+      j.ldd = A.r;
+      j.dbs = m * A.r;
+      j.beta = 1.f;
+      j.colscale = inverse ? A.c_inv : A.c_fwd;
+      j.kernel_family = GIFT_KERNEL_PROJECT;
+      if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
+    }
+  }
+  TileJob &u = plan->upd;
+  u.M = m;
+  u.N = n;
+  u.batch = N;
+  u.nseg = 0;
+  if (useG) {  // (U_G C_G) Q, with B(k, j) = Q[k][j] = Qm[j][k]
+    Segment &s = u.seg[u.nseg++];
+    s.a = Operand{UcG, G.r, 0, true};
+    s.b = Operand{Qm, G.r, n * G.r, true};
+    s.K = G.r;
+  }
+  if (useA) {
+    Segment &s = u.seg[u.nseg++];
+    if (useG) {  // L2 U_A^T
+      s.a = Operand{L2, A.r, m * A.r, true};
+      s.b = Operand{A.U, A.r, 0, true};
+    } else {  // P (C_A U_A^T)
+      s.a = Operand{P, A.r, m * A.r, true};
+      s.b = Operand{inverse ? A.Uci : A.Uc, A.r, 0, true};
+    }
+    s.K = A.r;
+  }
+  return GIFT_OK;
+}
+
+}  // namespace
+}  // namespace gift
+
+using namespace gift;
+
+extern "C" {
+
+int32_t gift_abi_version(void) { return GIFT_ABI_VERSION; }
+
+const char *gift_last_error(void) { return g_last_error.c_str(); }
+
+gift_status gift_ctx_create(void *hip_stream, gift_ctx **out) {
+  if (!out) return set_error(GIFT_EINVAL, "gift_ctx_create: out is NULL");
+  gift_ctx *c = new (std::nothrow) gift_ctx();
+  if (!c) return set_error(GIFT_ENOMEM, "gift_ctx_create: out of host memory");
+  c->stream = static_cast<hipStream_t>(hip_stream);
+  *out = c;
+  return GIFT_OK;
+}
+
+gift_status gift_ctx_set_stream(gift_ctx *ctx, void *hip_stream) {
+  if (!ctx) return set_error(GIFT_EINVAL, "gift_ctx_set_stream: ctx is NULL");
+  ctx->stream = static_cast<hipStream_t>(hip_stream);
+  return GIFT_OK;
+}
+
+void gift_ctx_destroy(gift_ctx *ctx) {
+  if (!ctx) return;
+  if (ctx->device >= 0) {
+    (void)hipStreamSynchronize(ctx->stream);
+    for (const ProfileRec &r : ctx->prof) {
+      (void)hipEventDestroy(r.start);
+      (void)hipEventDestroy(r.stop);
+    }
+    for (hipEvent_t e : ctx->event_pool) (void)hipEventDestroy(e);
+    if (ctx->ws.ptr) (void)hipFree(ctx->ws.ptr);
+  }
+  delete ctx;
+}
+
+gift_status gift_ctx_profile_enable(gift_ctx *ctx, int32_t enable) {
+  if (!ctx) return set_error(GIFT_EINVAL, "gift_ctx_profile_enable: ctx is NULL");
+  ctx->profile = enable != 0;
+  return GIFT_OK;
+}
+
+gift_status gift_ctx_profile_read(gift_ctx *ctx, int32_t kernel, int64_t *launches,
+                                  double *total_ms) {
+  if (!ctx || !launches || !total_ms)
+    return set_error(GIFT_EINVAL, "gift_ctx_profile_read: NULL argument");
+  if (kernel < 0 || kernel >= GIFT_KERNEL_COUNT)
+    return set_error(GIFT_EINVAL, "gift_ctx_profile_read: unknown kernel family");
+  gift_status st = drain_profile(ctx);
+  if (st != GIFT_OK) return st;
+  *launches = ctx->prof_launches[kernel];
+  *total_ms = ctx->prof_ms[kernel];
+  return GIFT_OK;
+}
+
+gift_status gift_ctx_profile_reset(gift_ctx *ctx) {
+  if (!ctx) return set_error(GIFT_EINVAL, "gift_ctx_profile_reset: ctx is NULL");
+  gift_status st = drain_profile(ctx);
+  if (st != GIFT_OK) return st;
+  for (int k = 0; k < GIFT_KERNEL_COUNT; ++k) {
+    ctx->prof_ms[k] = 0.0;
+    ctx->prof_launches[k] = 0;
+  }
+  return GIFT_OK;
+}
+
+gift_status gift_factor_create(gift_ctx *ctx, int64_t m, int64_t n, int32_t rank, int32_t sides,
+                               float damping, uint64_t seed, gift_factor **out) {
+  if (!ctx || !out) return set_error(GIFT_EINVAL, "gift_factor_create: NULL argument");
+  if (sides < GIFT_SIDE_INPUT || sides > GIFT_SIDE_BOTH)
+    return set_error(GIFT_EINVAL, "gift_factor_create: sides must be INPUT, OUTPUT or BOTH");
+  if (!(damping >= 0.f) || isinf(damping))
+    return set_error(GIFT_EINVAL, "gift_factor_create: damping must be finite and >= 0");
+  gift_status st = check_matrix_dims(m, n);
+  if (st != GIFT_OK) return st;
+  if (rank < 0 || rank > kMaxRank)
+    return set_error(GIFT_ESHAPE, "gift_factor_create: rank must be in [0, 512]");
+  if (side_in(sides, GIFT_SIDE_INPUT) && rank > n)
+    return set_error(GIFT_ESHAPE, "gift_factor_create: rank exceeds n (input side)");
+  if (side_in(sides, GIFT_SIDE_OUTPUT) && rank > m)
+    return set_error(GIFT_ESHAPE, "gift_factor_create: rank exceeds m (output side)");
+  if ((st = bind_device(ctx)) != GIFT_OK) return st;
+
+  gift_factor *f = new (std::nothrow) gift_factor();
+  if (!f) return set_error(GIFT_ENOMEM, "gift_factor_create: out of host memory");
+  f->ctx = ctx;
+  f->m = m;
+  f->n = n;
+  f->rank = rank;
+  f->sides = sides;
+  f->damping = damping;
+  f->seed = seed;
+  Side *list[2] = {&f->A, &f->G};
+  const bool on[2] = {side_in(sides, GIFT_SIDE_INPUT), side_in(sides, GIFT_SIDE_OUTPUT)};
+  const int64_t dims[2] = {n, m};
+  size_t total = 0;
+  for (int i = 0; i < 2; ++i) {
+    Side &s = *list[i];
+    s.dim = dims[i];
+    s.r = on[i] ? rank : 0;
+    s.k = (int32_t)(2 * (int64_t)s.r < s.dim ? 2 * s.r : s.dim);
+    if (s.r == 0) continue;
+    total += 4 * a256(sizeof(float) * s.dim * s.r) + 3 * a256(sizeof(float) * s.r) + a256(sizeof(float)) +
+             a256(sizeof(float) * (size_t)s.k * s.dim);
+  }
+  if (total > 0) {
+    hipError_t e = hipMalloc(&f->alloc, total);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      delete f;
+      return set_error(GIFT_ENOMEM, "gift_factor_create: device allocation failed");
+    }
+    char *p = static_cast<char *>(f->alloc);
+    for (int i = 0; i < 2; ++i) {
+      Side &s = *list[i];
+      if (s.r == 0) continue;
+      auto take = [&](size_t bytes) {
+        float *q = reinterpret_cast<float *>(p);
+        p += a256(bytes);
+        return q;
+      };
+      s.Ut = take(sizeof(float) * s.dim * s.r);
+      s.U = take(sizeof(float) * s.dim * s.r);
+      s.Uc = take(sizeof(float) * s.dim * s.r);
+      s.Uci = take(sizeof(float) * s.dim * s.r);
+      s.c_fwd = take(sizeof(float) * s.r);
+      s.c_inv = take(sizeof(float) * s.r);
+      s.lam = take(sizeof(float) * s.r);
+      s.sigma2 = take(sizeof(float));
+      s.Qt = take(sizeof(float) * (size_t)s.k * s.dim);
+      if ((st = side_set_identity(ctx, s)) != GIFT_OK) {
+        (void)hipFree(f->alloc);
+        delete f;
+        return st;
+      }
+    }
+  }
+  *out = f;
+  return GIFT_OK;
+}
+
+void gift_factor_destroy(gift_factor *f) {
+  if (!f) return;
+  if (f->alloc) {
+    (void)hipStreamSynchronize(f->ctx->stream);
+    (void)hipFree(f->alloc);
+  }
+  delete f;
+}
+
+gift_status gift_factor_update(gift_ctx *ctx, gift_factor *f, const void *acts,
+                               const void *out_grads, int64_t T, gift_dtype dtype, int32_t iters) {
+  if (!ctx || !f) return set_error(GIFT_EINVAL, "gift_factor_update: NULL ctx or factor");
+  if (dtype != GIFT_F32 && dtype != GIFT_BF16)
+    return set_error(GIFT_EINVAL, "gift_factor_update: dtype must be GIFT_F32 or GIFT_BF16");
+  if (iters < 0) return set_error(GIFT_EINVAL, "gift_factor_update: iters must be >= 0");
+  if (T <= 0) return set_error(GIFT_ESHAPE, "gift_factor_update: T must be positive");
+  const bool needA = f->A.r > 0, needG = f->G.r > 0;
+  if (needA && !acts) return set_error(GIFT_EINVAL, "gift_factor_update: acts is NULL");
+  if (needG && !out_grads) return set_error(GIFT_EINVAL, "gift_factor_update: out_grads is NULL");
+  gift_status st = bind_device(ctx);
+  if (st != GIFT_OK) return st;
+  if (needA && (st = factor_refresh_side(ctx, f, f->A, acts, T, dtype, iters, f->seed)) != GIFT_OK)
+    return st;
+  if (needG && (st = factor_refresh_side(ctx, f, f->G, out_grads, T, dtype, iters, f->seed + 1)) != GIFT_OK)
+    return st;
+  return GIFT_OK;
+}
+
+static gift_status pick_side(const gift_factor *f, int32_t side, const Side **s) {
+  if (side == GIFT_SIDE_INPUT) *s = &f->A;
+  else if (side == GIFT_SIDE_OUTPUT) *s = &f->G;
+  else return set_error(GIFT_EINVAL, "side must be GIFT_SIDE_INPUT or GIFT_SIDE_OUTPUT");
+  if ((*s)->r == 0 && !side_in(f->sides, side))
+    return set_error(GIFT_EINVAL, "the factor does not have this side");
+  return GIFT_OK;
+}
+
+gift_status gift_factor_export(gift_ctx *ctx, const gift_factor *f, int32_t side, float *U,
+                               float *c_fwd, float *c_inv, float *sigma2) {
+  if (!ctx || !f || !sigma2) return set_error(GIFT_EINVAL, "gift_factor_export: NULL argument");
+  const Side *s = nullptr;
+  gift_status st = pick_side(f, side, &s);
+  if (st != GIFT_OK) return st;
+  if (s->r > 0 && (!U || !c_fwd || !c_inv))
+    return set_error(GIFT_EINVAL, "gift_factor_export: NULL output");
+  if ((st = bind_device(ctx)) != GIFT_OK) return st;
+  return side_export(ctx, *s, U, c_fwd, c_inv, sigma2);
+}
+
+gift_status gift_factor_import(gift_ctx *ctx, gift_factor *f, int32_t side, const float *U,
+                               const float *c_fwd, const float *c_inv, const float *sigma2) {
+  if (!ctx || !f || !sigma2) return set_error(GIFT_EINVAL, "gift_factor_import: NULL argument");
+  const Side *cs = nullptr;
+  gift_status st = pick_side(f, side, &cs);
+  if (st != GIFT_OK) return st;
+  Side *s = const_cast<Side *>(cs);
+  if (s->r > 0 && (!U || !c_fwd || !c_inv))
+    return set_error(GIFT_EINVAL, "gift_factor_import: NULL input");
+  if ((st = bind_device(ctx)) != GIFT_OK) return st;
+  return side_import(ctx, *s, U, c_fwd, c_inv, sigma2);
+}
+
+gift_status gift_encode(gift_ctx *ctx, const gift_factor *f, const float *grads, int32_t N,
+                        int64_t m, int64_t n, int32_t block_rows, int32_t block_cols,
+                        gift_scale_mode mode, float *ef, uint8_t *codes, float *scales,
+                        float *transformed) {
+  if (!ctx) return set_error(GIFT_EINVAL, "gift_encode: ctx is NULL");
+  if (!grads || !codes || !scales) return set_error(GIFT_EINVAL, "gift_encode: NULL tensor");
+  if (mode != GIFT_SCALE_LOCAL && mode != GIFT_SCALE_SHARED)
+    return set_error(GIFT_EINVAL, "gift_encode: unknown scale mode");
+  if (N <= 0 || N > kMaxRanks) return set_error(GIFT_ESHAPE, "gift_encode: N must be in [1, 65535]");
+  gift_status st = check_matrix_dims(m, n);
+  if (st != GIFT_OK) return st;
+  if (block_rows < 0 || block_cols < 0)
+    return set_error(GIFT_ESHAPE, "gift_encode: block sizes must be >= 0");
+  if (f && (f->m != m || f->n != n))
+    return set_error(GIFT_ESHAPE, "gift_encode: factor was created for another shape");
+  if ((st = bind_device(ctx)) != GIFT_OK) return st;
+  const BlockGeom g = block_geom(m, n, block_rows, block_cols);
+  const size_t amax_bytes = a256(sizeof(uint32_t) * (size_t)N * g.nbr * g.nbc);
+  LowRankPlan plan;
+  size_t proj_bytes = 0;
+  if (f && (st = plan_low_rank(ctx, f, grads, N, m, n, false, nullptr, &proj_bytes, &plan)) != GIFT_OK)
+    return st;
+  void *ws = nullptr;
+  if ((st = workspace(ctx, amax_bytes + proj_bytes, &ws)) != GIFT_OK) return st;
+  uint32_t *amax = static_cast<uint32_t *>(ws);
+  if ((st = launch_zero_u32(ctx, amax, (int64_t)N * g.nbr * g.nbc)) != GIFT_OK) return st;
+  TileJob job;
+  if (f) {
+    if ((st = plan_low_rank(ctx, f, grads, N, m, n, false, static_cast<char *>(ws) + amax_bytes,
+                            &proj_bytes, &plan)) != GIFT_OK)
+      return st;
+    if (plan.active) job = plan.upd;
+  }
+  job.M = m;
+  job.N = n;
+  job.batch = N;
+  job.D = grads;
+  job.ldd = n;
+  job.dbs = m * n;
+  job.amax = amax;
+  job.geom = g;
+  job.shared = mode == GIFT_SCALE_SHARED;
+  job.ef = ef;
+  job.scales = scales;
+  const bool gemm = job.nseg > 0;
+  job.transformed = transformed;
+  job.kernel_family = gemm ? GIFT_KERNEL_UPDATE_AMAX : GIFT_KERNEL_AMAX;
+  if ((st = launch_tile(ctx, job)) != GIFT_OK) return st;
+  job.transformed = nullptr;
+  job.codes = codes;
+  job.kernel_family = gemm ? GIFT_KERNEL_UPDATE_QUANT : GIFT_KERNEL_QUANT;
+  return launch_tile(ctx, job);
+}
+
+gift_status gift_reduce_local(gift_ctx *ctx, const uint8_t *codes, const float *scales, int32_t N,
+                              int64_t m, int64_t n, int32_t block_rows, int32_t block_cols,
+                              float *mean) {
+  if (!ctx) return set_error(GIFT_EINVAL, "gift_reduce_local: ctx is NULL");
+  if (!codes || !scales || !mean) return set_error(GIFT_EINVAL, "gift_reduce_local: NULL tensor");
+  if (N <= 0 || N > kMaxRanks)
+    return set_error(GIFT_ESHAPE, "gift_reduce_local: N must be in [1, 65535]");
+  gift_status st = check_matrix_dims(m, n);
+  if (st != GIFT_OK) return st;
+  if (block_rows < 0 || block_cols < 0)
+    return set_error(GIFT_ESHAPE, "gift_reduce_local: block sizes must be >= 0");
+  if ((st = bind_device(ctx)) != GIFT_OK) return st;
+  return launch_reduce(ctx, codes, scales, N, m, n, block_geom(m, n, block_rows, block_cols), mean);
+}
+
+gift_status gift_decode(gift_ctx *ctx, const gift_factor *f, const float *mean, int64_t m,
+                        int64_t n, float *out) {
+  if (!ctx) return set_error(GIFT_EINVAL, "gift_decode: ctx is NULL");
+  if (!mean || !out) return set_error(GIFT_EINVAL, "gift_decode: NULL tensor");
+  if (mean == out) return set_error(GIFT_EINVAL, "gift_decode: out must not alias mean");
+  gift_status st = check_matrix_dims(m, n);
+  if (st != GIFT_OK) return st;
+  if (f && (f->m != m || f->n != n))
+    return set_error(GIFT_ESHAPE, "gift_decode: factor was created for another shape");
+  if ((st = bind_device(ctx)) != GIFT_OK) return st;
+  LowRankPlan plan;
+  size_t bytes = 0;
+  if (f && (st = plan_low_rank(ctx, f, mean, 1, m, n, true, nullptr, &bytes, &plan)) != GIFT_OK)
+    return st;
+  if (!plan.active) return launch_copy_f32(ctx, out, mean, m * n);
+  void *ws = nullptr;
+  if ((st = workspace(ctx, bytes, &ws)) != GIFT_OK) return st;
+  if ((st = plan_low_rank(ctx, f, mean, 1, m, n, true, static_cast<char *>(ws), &bytes, &plan)) != GIFT_OK)
+    return st;
+  TileJob job = plan.upd;
+  job.C = out;
+  job.ldc = n;
+  job.cbs = m * n;
+  job.D = mean;
+  job.ldd = n;
+  job.dbs = m * n;
+  job.beta = 1.f;
+  job.kernel_family = GIFT_KERNEL_UPDATE_STORE;
+  return launch_tile(ctx, job);
+}
+
+}  // extern "C"

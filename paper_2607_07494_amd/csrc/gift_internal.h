@@ -1,0 +1,175 @@
+// Internal declarations of the GIFT codec library (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "gift.h"
+
+namespace gift {
+
+// ---------------------------------------------------------------------------
+// Error reporting
+// ---------------------------------------------------------------------------
+gift_status set_error(gift_status st, const std::string &msg);
+gift_status hip_error(hipError_t e, const char *what);
+
+#define GIFT_HIP_TRY(expr)                                  \
+  do {                                                      \
+    hipError_t _e = (expr);                                 \
+    if (_e != hipSuccess) return ::gift::hip_error(_e, #expr); \
+  } while (0)
+
+// ---------------------------------------------------------------------------
+// Context and factor state
+// ---------------------------------------------------------------------------
+struct Workspace {
+  void *ptr = nullptr;
+  size_t bytes = 0;
+};
+
+struct ProfileRec {
+  int kernel;
+  hipEvent_t start, stop;
+};
+
+}  // namespace gift
+
+struct gift_ctx {
+  hipStream_t stream = nullptr;
+  int device = -1;                 // bound at the first compute call
+  gift::Workspace ws;              // grow-only device workspace
+  bool profile = false;
+  std::vector<gift::ProfileRec> prof;
+  int64_t prof_launches[GIFT_KERNEL_COUNT] = {};
+  double prof_ms[GIFT_KERNEL_COUNT] = {};
+  std::vector<hipEvent_t> event_pool;
+};
+
+namespace gift {
+
+// One side's transform S^-1 = I + U diag(c) U^T, kept in the layouts the
+// kernels read with unit stride along the contraction index.
+struct Side {
+  int64_t dim = 0;       // n for the input side, m for the output side
+  int32_t r = 0;
+  int32_t k = 0;         // subspace block width (min(dim, 2r))
+  float *Ut = nullptr;   // [r, dim]   U^T (rows = eigenvectors)
+  float *U = nullptr;    // [dim, r]   U
+  float *Uc = nullptr;   // [dim, r]   U diag(c_fwd)
+  float *Uci = nullptr;  // [dim, r]   U diag(c_inv)
+  float *c_fwd = nullptr, *c_inv = nullptr;   // [r]
+  float *sigma2 = nullptr;                    // [1]
+  float *lam = nullptr;                       // [r]
+  float *Qt = nullptr;   // [k, dim]   warm-start block (rows orthonormal)
+  bool have_basis = false;  // Qt holds a previous subspace
+  bool fill_tail = false;   // Qt rows r..k-1 still need start-block rows
+};
+
+}  // namespace gift
+
+struct gift_factor {
+  gift_ctx *ctx = nullptr;
+  int64_t m = 0, n = 0;
+  int32_t rank = 0, sides = 0;
+  float damping = 0.f;
+  uint64_t seed = 0;
+  gift::Side A;   // input side (dim n)
+  gift::Side G;   // output side (dim m)
+  void *alloc = nullptr;
+};
+
+namespace gift {
+
+// ---------------------------------------------------------------------------
+// Launch plumbing
+// ---------------------------------------------------------------------------
+gift_status bind_device(gift_ctx *ctx);
+// Device scratch of at least `bytes`, 256-byte aligned; may reallocate (and
+// synchronize the stream) when it grows.
+gift_status workspace(gift_ctx *ctx, size_t bytes, void **out);
+// Bracket launches of one kernel family with events when profiling is on.
+struct ProfileScope {
+  gift_ctx *ctx;
+  int kernel;
+  hipEvent_t stop = nullptr;
+  ProfileScope(gift_ctx *c, int k);
+  ~ProfileScope();
+};
+gift_status check_launch(const char *what);
+
+// ---------------------------------------------------------------------------
+// Block geometry of the scale grid
+// ---------------------------------------------------------------------------
+struct BlockGeom {
+  int64_t br, bc;      // block extent in rows / cols
+  int32_t nbr, nbc;    // blocks per column / row
+};
+BlockGeom block_geom(int64_t m, int64_t n, int32_t block_rows, int32_t block_cols);
+
+// ---------------------------------------------------------------------------
+// Kernel launchers (enqueue on ctx->stream; no validation beyond asserts)
+// ---------------------------------------------------------------------------
+
+// Strided fp32 operand: element (i, k) of A at ptr[b*bs + i*ld + k] when
+// kmajor, else ptr[b*bs + k*ld + i]; element (k, j) of B at
+// ptr[b*bs + j*ld + k] when kmajor, else ptr[b*bs + k*ld + j].
+struct Operand {
+  const float *ptr = nullptr;
+  int64_t ld = 0;
+  int64_t bs = 0;
+  bool kmajor = true;
+};
+
+struct Segment {
+  Operand a, b;
+  int64_t K = 0;
+};
+
+enum Epilogue { EPI_STORE = 0, EPI_AMAX = 1, EPI_QUANT = 2 };
+
+struct TileJob {
+  // C = sum_s A_s B_s over up to two segments (nseg = 0: no product)
+  Segment seg[2];
+  int nseg = 0;
+  int64_t M = 0, N = 0;     // output rows / cols
+  int32_t batch = 1;
+  int32_t ksplit = 1;         // STORE only: partial sums to C + (b*ksplit+s)*cbs
+  // STORE: C = (alpha*acc + beta*D) * colscale[j]
+  float *C = nullptr;
+  int64_t ldc = 0, cbs = 0;
+  const float *D = nullptr;  // addend (required for the codec epilogues)
+  int64_t ldd = 0, dbs = 0;
+  float alpha = 1.f, beta = 0.f;
+  const float *colscale = nullptr;
+  // codec epilogues (W~ = D + acc [+ R]); matrices are [batch, M, N] dense
+  uint32_t *amax = nullptr;     // [batch, nbr, nbc] float bits
+  uint8_t *codes = nullptr;
+  float *scales = nullptr;
+  float *transformed = nullptr;
+  float *ef = nullptr;
+  BlockGeom geom{};
+  bool shared = false;
+  int kernel_family = GIFT_KERNEL_FACTOR;
+};
+
+gift_status launch_tile(gift_ctx *ctx, const TileJob &job);
+gift_status launch_zero_u32(gift_ctx *ctx, uint32_t *p, int64_t count);
+gift_status launch_reduce(gift_ctx *ctx, const uint8_t *codes, const float *scales,
+                          int32_t N, int64_t m, int64_t n, BlockGeom g, float *mean);
+gift_status launch_copy_f32(gift_ctx *ctx, float *dst, const float *src, int64_t count);
+
+// factor pipeline (k_factor.hip)
+gift_status factor_refresh_side(gift_ctx *ctx, gift_factor *f, Side &s, const void *x,
+                                int64_t T, gift_dtype dtype, int32_t iters,
+                                uint64_t seed);
+gift_status side_import(gift_ctx *ctx, Side &s, const float *U, const float *c_fwd,
+                        const float *c_inv, const float *sigma2);
+gift_status side_export(gift_ctx *ctx, const Side &s, float *U, float *c_fwd,
+                        float *c_inv, float *sigma2);
+gift_status side_set_identity(gift_ctx *ctx, Side &s);
+
+}  // namespace gift

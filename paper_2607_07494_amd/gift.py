@@ -1,0 +1,235 @@
+"""Thin ctypes binding of ``libgift.so`` (the C ABI in ``include/gift.h``).
+
+Argument marshalling only: every computation runs in the library's HIP
+kernels.  Tensors are torch tensors on the GPU (device memory and streams are
+all torch is used for); the wrappers check dtype, device and contiguity, pass
+``data_ptr()`` and raise :class:`GiftError` with the library's message when a
+call fails.  There is no fallback: if ``libgift.so`` is missing, importing
+this module raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libgift.so")
+
+OK, EINVAL, ESHAPE, ENOMEM, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+F32, BF16 = 0, 1
+SIDE_INPUT, SIDE_OUTPUT, SIDE_BOTH = 1, 2, 3
+SCALE_LOCAL, SCALE_SHARED = 0, 1
+KERNELS = {
+    "amax": 0, "quant": 1, "project": 2, "update_amax": 3, "update_quant": 4,
+    "update_store": 5, "reduce": 6, "syrk": 7, "factor": 8, "small": 9,
+}
+
+_STATUS = {OK: "GIFT_OK", EINVAL: "GIFT_EINVAL", ESHAPE: "GIFT_ESHAPE", ENOMEM: "GIFT_ENOMEM",
+           EHIP: "GIFT_EHIP", EUNSUPPORTED: "GIFT_EUNSUPPORTED"}
+
+
+class GiftError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{_STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2607_07494_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, U64, F = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_float
+    PP = ctypes.POINTER(ctypes.c_void_p)
+    sigs = {
+        "gift_abi_version": ([], I32),
+        "gift_last_error": ([], ctypes.c_char_p),
+        "gift_ctx_create": ([P, PP], I32),
+        "gift_ctx_set_stream": ([P, P], I32),
+        "gift_ctx_destroy": ([P], None),
+        "gift_ctx_profile_enable": ([P, I32], I32),
+        "gift_ctx_profile_read": ([P, I32, ctypes.POINTER(I64), ctypes.POINTER(ctypes.c_double)], I32),
+        "gift_ctx_profile_reset": ([P], I32),
+        "gift_factor_create": ([P, I64, I64, I32, I32, F, U64, PP], I32),
+        "gift_factor_destroy": ([P], None),
+        "gift_factor_update": ([P, P, P, P, I64, I32, I32], I32),
+        "gift_factor_export": ([P, P, I32, P, P, P, P], I32),
+        "gift_factor_import": ([P, P, I32, P, P, P, P], I32),
+        "gift_encode": ([P, P, P, I32, I64, I64, I32, I32, I32, P, P, P, P], I32),
+        "gift_reduce_local": ([P, P, P, I32, I64, I64, I32, I32, P], I32),
+        "gift_decode": ([P, P, P, I64, I64, P], I32),
+    }
+    for name, (args, res) in sigs.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    return lib
+
+
+LIB = _load()
+
+
+def _check(status: int):
+    if status != OK:
+        raise GiftError(status, LIB.gift_last_error().decode(errors="replace"))
+
+
+def exported_symbols():
+    """Names declared by include/gift.h that this binding calls."""
+    return sorted(n for n in dir(LIB) if n.startswith("gift_"))
+
+
+def _ptr(t, dtype=None, name="tensor"):
+    if t is None:
+        return None
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must have dtype {dtype}, not {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def scale_grid(m: int, n: int, block_rows: int = 0, block_cols: int = 0):
+    """``(nbr, nbc)``: scale-grid shape for allocating the scales output."""
+    br = m if block_rows <= 0 else min(block_rows, m)
+    bc = n if block_cols <= 0 else min(block_cols, n)
+    return -(-m // br), -(-n // bc)
+
+
+class Context:
+    """A library context bound to one HIP stream (default: torch's current)."""
+
+    def __init__(self, stream=None):
+        if stream is None:
+            import torch
+            stream = torch.cuda.current_stream().cuda_stream if torch.cuda.is_available() else 0
+        self._h = ctypes.c_void_p()
+        _check(LIB.gift_ctx_create(ctypes.c_void_p(int(stream)), ctypes.byref(self._h)))
+
+    @property
+    def handle(self):
+        return self._h
+
+    def set_stream(self, stream):
+        _check(LIB.gift_ctx_set_stream(self._h, ctypes.c_void_p(int(stream))))
+
+    def profile(self, enable: bool = True):
+        _check(LIB.gift_ctx_profile_enable(self._h, 1 if enable else 0))
+
+    def profile_read(self, kernel):
+        k = KERNELS[kernel] if isinstance(kernel, str) else int(kernel)
+        n = ctypes.c_int64()
+        ms = ctypes.c_double()
+        _check(LIB.gift_ctx_profile_read(self._h, k, ctypes.byref(n), ctypes.byref(ms)))
+        return n.value, ms.value
+
+    def profile_reset(self):
+        _check(LIB.gift_ctx_profile_reset(self._h))
+
+    def close(self):
+        if self._h:
+            LIB.gift_ctx_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Factor:
+    """Transform state of one m x n weight matrix (``gift_factor``)."""
+
+    def __init__(self, ctx: Context, m: int, n: int, rank: int, sides: int = SIDE_INPUT,
+                 damping: float = 1e-6, seed: int = 0):
+        self.ctx, self.m, self.n, self.rank, self.sides = ctx, m, n, rank, sides
+        self._h = ctypes.c_void_p()
+        _check(LIB.gift_factor_create(ctx.handle, m, n, rank, sides, damping, seed,
+                                      ctypes.byref(self._h)))
+
+    @property
+    def handle(self):
+        return self._h
+
+    def update(self, acts=None, out_grads=None, iters: int = 4):
+        import torch
+        x = acts if acts is not None else out_grads
+        if x is None:
+            raise ValueError("update needs acts and/or out_grads")
+        if x.dtype == torch.float32:
+            dt = F32
+        elif x.dtype == torch.bfloat16:
+            dt = BF16
+        else:
+            raise TypeError("statistics inputs must be float32 or bfloat16")
+        T = x.shape[0]
+        for t, nm in ((acts, "acts"), (out_grads, "out_grads")):
+            if t is not None and (t.dim() != 2 or t.shape[0] != T or t.dtype != x.dtype):
+                raise ValueError(f"{nm} must be [T, dim] with the common T and dtype")
+        _check(LIB.gift_factor_update(self.ctx.handle, self._h, _ptr(acts, None, "acts"),
+                                      _ptr(out_grads, None, "out_grads"), T, dt, iters))
+
+    def export(self, side: int):
+        import torch
+        dim = self.n if side == SIDE_INPUT else self.m
+        dev = torch.device("cuda", torch.cuda.current_device())
+        U = torch.empty((dim, self.rank), dtype=torch.float32, device=dev)
+        cf = torch.empty(self.rank, dtype=torch.float32, device=dev)
+        ci = torch.empty(self.rank, dtype=torch.float32, device=dev)
+        s2 = torch.empty(1, dtype=torch.float32, device=dev)
+        _check(LIB.gift_factor_export(self.ctx.handle, self._h, side, _ptr(U), _ptr(cf), _ptr(ci),
+                                      _ptr(s2)))
+        return U, cf, ci, s2
+
+    def import_(self, side: int, U, c_fwd, c_inv, sigma2):
+        import torch
+        f = torch.float32
+        _check(LIB.gift_factor_import(self.ctx.handle, self._h, side, _ptr(U, f, "U"),
+                                      _ptr(c_fwd, f, "c_fwd"), _ptr(c_inv, f, "c_inv"),
+                                      _ptr(sigma2, f, "sigma2")))
+
+    def close(self):
+        if self._h:
+            LIB.gift_factor_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def encode(ctx: Context, factor, grads, codes, scales, block_rows: int = 0, block_cols: int = 0,
+           mode: int = SCALE_LOCAL, ef=None, transformed=None):
+    """``gift_encode``: grads [N, m, n] f32 -> codes [N, m, n] u8, scales [N, nbr, nbc] f32."""
+    import torch
+    N, m, n = grads.shape
+    _check(LIB.gift_encode(ctx.handle, factor.handle if factor is not None else None,
+                           _ptr(grads, torch.float32, "grads"), N, m, n, block_rows, block_cols,
+                           mode, _ptr(ef, torch.float32, "ef"), _ptr(codes, torch.uint8, "codes"),
+                           _ptr(scales, torch.float32, "scales"),
+                           _ptr(transformed, torch.float32, "transformed")))
+
+
+def reduce_local(ctx: Context, codes, scales, mean, block_rows: int = 0, block_cols: int = 0):
+    """``gift_reduce_local``: codes [N, m, n], scales -> mean [m, n] f32."""
+    import torch
+    N, m, n = codes.shape
+    _check(LIB.gift_reduce_local(ctx.handle, _ptr(codes, torch.uint8, "codes"),
+                                 _ptr(scales, torch.float32, "scales"), N, m, n, block_rows,
+                                 block_cols, _ptr(mean, torch.float32, "mean")))
+
+
+def decode(ctx: Context, factor, mean, out):
+    """``gift_decode``: inverse transform of the rank mean [m, n] f32 into out."""
+    import torch
+    m, n = mean.shape
+    _check(LIB.gift_decode(ctx.handle, factor.handle if factor is not None else None,
+                           _ptr(mean, torch.float32, "mean"), m, n, _ptr(out, torch.float32, "out")))

@@ -1,0 +1,112 @@
+"""The C ABI library loads and validates arguments on the host (no GPU needed).
+
+Every symbol declared in include/gift.h must be exported by libgift.so.  The
+error paths below return before any HIP call, so they run in a CPU-only
+container; pointers are fake non-NULL addresses that are never dereferenced.
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gift.h")
+
+gift = pytest.importorskip("paper_2607_07494_amd.gift")
+LIB = gift.LIB
+FAKE = ctypes.c_void_p(0x1000)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gift_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) >= 16
+    for name in names:
+        assert hasattr(LIB, name), name
+    assert LIB.gift_abi_version() == 1
+
+
+def _err():
+    return LIB.gift_last_error().decode()
+
+
+def test_null_handles_are_einval():
+    assert LIB.gift_encode(None, None, FAKE, 1, 4, 4, 0, 0, 0, None, FAKE, FAKE, None) == gift.EINVAL
+    assert LIB.gift_reduce_local(None, FAKE, FAKE, 1, 4, 4, 0, 0, FAKE) == gift.EINVAL
+    assert LIB.gift_decode(None, None, FAKE, 4, 4, FAKE) == gift.EINVAL
+    assert LIB.gift_factor_update(None, None, FAKE, None, 8, 0, 1) == gift.EINVAL
+    assert LIB.gift_ctx_create(None, None) == gift.EINVAL
+    LIB.gift_ctx_destroy(None)
+    LIB.gift_factor_destroy(None)
+
+
+@pytest.fixture
+def ctx():
+    c = gift.Context(stream=0)   # creating a context makes no HIP call
+    yield c
+    c.close()
+
+
+def test_encode_validation(ctx):
+    h = ctx.handle
+    enc = LIB.gift_encode
+    assert enc(h, None, None, 1, 4, 4, 0, 0, 0, None, FAKE, FAKE, None) == gift.EINVAL
+    assert enc(h, None, FAKE, 1, 4, 4, 0, 0, 0, None, None, FAKE, None) == gift.EINVAL
+    assert enc(h, None, FAKE, 0, 4, 4, 0, 0, 0, None, FAKE, FAKE, None) == gift.ESHAPE
+    assert "N must be" in _err()
+    assert enc(h, None, FAKE, -3, 4, 4, 0, 0, 0, None, FAKE, FAKE, None) == gift.ESHAPE
+    assert enc(h, None, FAKE, 1, 0, 4, 0, 0, 0, None, FAKE, FAKE, None) == gift.ESHAPE
+    assert enc(h, None, FAKE, 1, 4, -1, 0, 0, 0, None, FAKE, FAKE, None) == gift.ESHAPE
+    assert enc(h, None, FAKE, 1, 4, 4, -1, 0, 0, None, FAKE, FAKE, None) == gift.ESHAPE
+    assert enc(h, None, FAKE, 1, 4, 4, 0, 0, 7, None, FAKE, FAKE, None) == gift.EINVAL
+    assert "scale mode" in _err()
+    assert enc(h, None, FAKE, 1, 2_000_000, 4, 0, 0, 0, None, FAKE, FAKE, None) == gift.ESHAPE
+
+
+def test_reduce_and_decode_validation(ctx):
+    h = ctx.handle
+    assert LIB.gift_reduce_local(h, FAKE, FAKE, 0, 4, 4, 0, 0, FAKE) == gift.ESHAPE
+    assert LIB.gift_reduce_local(h, None, FAKE, 2, 4, 4, 0, 0, FAKE) == gift.EINVAL
+    assert LIB.gift_reduce_local(h, FAKE, FAKE, 2, 4, 4, 0, -2, FAKE) == gift.ESHAPE
+    assert LIB.gift_decode(h, None, FAKE, 4, 4, FAKE) == gift.EINVAL
+    assert "alias" in _err()
+    assert LIB.gift_decode(h, None, FAKE, 0, 4, ctypes.c_void_p(0x2000)) == gift.ESHAPE
+
+
+def test_factor_validation(ctx):
+    h = ctx.handle
+    out = ctypes.c_void_p()
+    mk = LIB.gift_factor_create
+    assert mk(h, 8, 8, 2, 0, 0.0, 0, ctypes.byref(out)) == gift.EINVAL       # sides
+    assert mk(h, 8, 8, 2, 4, 0.0, 0, ctypes.byref(out)) == gift.EINVAL
+    assert mk(h, 8, 8, 2, 1, -1.0, 0, ctypes.byref(out)) == gift.EINVAL      # damping
+    assert mk(h, 8, 8, 2, 1, float("inf"), 0, ctypes.byref(out)) == gift.EINVAL
+    assert mk(h, 8, 8, 9, 1, 0.0, 0, ctypes.byref(out)) == gift.ESHAPE       # rank > n
+    assert mk(h, 4, 8, 5, 2, 0.0, 0, ctypes.byref(out)) == gift.ESHAPE       # rank > m
+    assert mk(h, 8, 8, -1, 1, 0.0, 0, ctypes.byref(out)) == gift.ESHAPE
+    assert mk(h, 0, 8, 1, 1, 0.0, 0, ctypes.byref(out)) == gift.ESHAPE
+    assert mk(h, 8, 8, 1, 1, 0.0, 0, None) == gift.EINVAL
+
+
+def test_profile_api_host_side(ctx):
+    h = ctx.handle
+    n = ctypes.c_int64()
+    ms = ctypes.c_double()
+    assert LIB.gift_ctx_profile_read(h, 99, ctypes.byref(n), ctypes.byref(ms)) == gift.EINVAL
+    assert LIB.gift_ctx_profile_enable(h, 1) == gift.OK
+    # nothing recorded yet: reading makes no HIP call
+    assert LIB.gift_ctx_profile_read(h, 0, ctypes.byref(n), ctypes.byref(ms)) == gift.OK
+    assert n.value == 0 and ms.value == 0.0
+
+
+def test_scale_grid_shapes():
+    assert gift.scale_grid(100, 300, 0, 128) == (1, 3)
+    assert gift.scale_grid(100, 300, 30, 0) == (4, 1)
+    assert gift.scale_grid(5, 7, 100, 100) == (1, 1)

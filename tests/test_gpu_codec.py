@@ -1,0 +1,255 @@
+"""GPU parity of the codec against the CPU oracle (runs on an MI355X).
+
+Bars (BASELINE targets): FP8 codes bit-exact with the oracle's codes of the
+same transformed tensor; scales bit-exact; the rank sum bit-exact (it is a
+fixed sequence of float32 operations); decoded gradients within 2e-3 relative
+Frobenius error of the oracle's with a shared factor.  The transformed tensor
+itself is an FP32-MFMA product: it must match the float64 oracle within 1e-5
+relative Frobenius error (float32 accumulation over at most a few thousand
+terms).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import codec, e4m3
+from synth import factor_inputs, gradient_set
+
+pytestmark = pytest.mark.gpu
+
+gift = pytest.importorskip("paper_2607_07494_amd.gift")
+
+DEV = "cuda"
+TRANSFORM_RTOL = 1e-5
+DECODE_RTOL = 2e-3
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def rel(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    c = gift.Context()
+    yield c
+    torch.cuda.synchronize()
+    c.close()
+
+
+def t(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+
+
+def gpu_encode(ctx, f, grads, br=0, bc=0, shared=False, want_t=True, ef=None):
+    N, m, n = grads.shape
+    nbr, nbc = gift.scale_grid(m, n, br, bc)
+    g = t(grads)
+    codes = torch.empty((N, m, n), dtype=torch.uint8, device=DEV)
+    scales = torch.empty((N, nbr, nbc), dtype=torch.float32, device=DEV)
+    tr = torch.empty((N, m, n), dtype=torch.float32, device=DEV) if want_t else None
+    gift.encode(ctx, f, g, codes, scales, br, bc,
+                gift.SCALE_SHARED if shared else gift.SCALE_LOCAL, ef=ef, transformed=tr)
+    torch.cuda.synchronize()
+    return (codes.cpu().numpy(), scales.cpu().numpy(),
+            tr.cpu().numpy() if tr is not None else None)
+
+
+def gpu_reduce(ctx, codes, scales, br=0, bc=0):
+    N, m, n = codes.shape
+    mean = torch.empty((m, n), dtype=torch.float32, device=DEV)
+    gift.reduce_local(ctx, t(codes), t(scales), mean, br, bc)
+    torch.cuda.synchronize()
+    return mean.cpu().numpy()
+
+
+def gpu_decode(ctx, f, mean):
+    out = torch.empty_like(t(mean))
+    gift.decode(ctx, f, t(mean), out)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def make_factor(ctx, m, n, r, sides, seed=0, T=None):
+    """GPU factor with an imported oracle factor (shared-factor parity)."""
+    fA = fG = None
+    f = gift.Factor(ctx, m, n, r, sides)
+    T = T or 4 * max(m, n)
+    if sides & gift.SIDE_INPUT:
+        fA = codec.lowrank_factor(codec.factor_statistics(factor_inputs(seed + 1, T, n)[0]), r).to_f32()
+        f.import_(gift.SIDE_INPUT, t(fA.U.astype(np.float32)), t(fA.c_fwd.astype(np.float32)),
+                  t(fA.c_inv.astype(np.float32)), t(np.array([fA.sigma2], np.float32)))
+    if sides & gift.SIDE_OUTPUT:
+        fG = codec.lowrank_factor(codec.factor_statistics(factor_inputs(seed + 2, T, m)[0]), r).to_f32()
+        f.import_(gift.SIDE_OUTPUT, t(fG.U.astype(np.float32)), t(fG.c_fwd.astype(np.float32)),
+                  t(fG.c_inv.astype(np.float32)), t(np.array([fG.sigma2], np.float32)))
+    return f, fA, fG
+
+
+# ------------------------------------------------------------ Euclidean branch
+
+EUCLID_CASES = [
+    # (N, m, n, block_rows, block_cols, shared)
+    (1, 1, 1, 0, 0, False),
+    (1, 5, 3, 0, 0, False),
+    (3, 77, 131, 0, 0, False),
+    (2, 130, 200, 0, 64, False),
+    (4, 64, 96, 16, 32, True),
+    (2, 33, 300, 7, 50, False),
+    (8, 256, 256, 0, 0, True),
+    (2, 40, 20, 1, 16, False),     # 40 x 2 blocks of 1 x 16 (many blocks per tile)
+    (3, 1000, 260, 0, 128, False),
+]
+
+
+@pytest.mark.parametrize("N,m,n,br,bc,shared", EUCLID_CASES)
+def test_euclidean_encode_bit_exact(ctx, N, m, n, br, bc, shared):
+    say(f"euclidean encode N={N} m={m} n={n} block=({br},{bc}) shared={shared}")
+    grads = gradient_set(100 + m, 200 + n, N, m, n)
+    codes, scales, tr = gpu_encode(ctx, None, grads, br, bc, shared)
+    ref_codes, ref_scales = codec.quantize_transformed(grads, br, bc, shared)
+    np.testing.assert_array_equal(tr, grads)
+    np.testing.assert_array_equal(scales, ref_scales)
+    np.testing.assert_array_equal(codes, ref_codes)
+
+
+def test_special_values_and_zero_blocks(ctx):
+    say("special values")
+    N, m, n = 3, 16, 64
+    g = gradient_set(7, 8, N, m, n)
+    g[0, :, 32:] = 0.0                       # an all-zero block: scale 0, codes 0
+    g[0, 3, 5] = -0.0
+    g[1, 2, 2] = np.inf                      # inf amax: multiplier 0, inf -> NaN code
+    g[2, 4, 40] = np.nan                     # NaN amax: NaN scale, all codes NaN
+    g[2, 1, 1] = 1e-42                       # subnormal input
+    codes, scales, _ = gpu_encode(ctx, None, g, 0, 32, False)
+    ref_codes, ref_scales = codec.quantize_transformed(g, 0, 32, False)
+    np.testing.assert_array_equal(codes, ref_codes)
+    np.testing.assert_array_equal(np.isnan(scales), np.isnan(ref_scales))
+    ok = ~np.isnan(ref_scales)
+    np.testing.assert_array_equal(scales[ok], ref_scales[ok])
+    tiny = np.full((1, 4, 4), 1e-40, np.float32)   # multiplier overflows -> FLT_MAX
+    tiny[0, 0, 0] = 0.0
+    c2, s2, _ = gpu_encode(ctx, None, tiny)
+    r2, rs2 = codec.quantize_transformed(tiny)
+    np.testing.assert_array_equal(c2, r2)
+    np.testing.assert_array_equal(s2, rs2)
+
+
+def test_quantizer_sweep_bit_exact(ctx):
+    # every E4M3 value, every rounding midpoint and their float32 neighbours,
+    # pushed through the quantizer with the multiplier exactly 1 (amax = 448)
+    say("quantizer sweep")
+    table = e4m3.decode_table()
+    pos = table[:0x7F]
+    mids = 0.5 * (pos[1:] + pos[:-1])
+    base = np.concatenate([pos, mids, [447.9, 448.0, 2.0 ** -10, 1e-38]]).astype(np.float32)
+    vals = np.concatenate([base, np.nextafter(base, np.float32(np.inf)),
+                           np.nextafter(base, np.float32(0))])
+    vals = np.concatenate([vals, -vals]).astype(np.float32)
+    vals = np.clip(vals, -448, 448)
+    rng = np.random.default_rng(0)
+    extra = (rng.uniform(-448, 448, 60000)).astype(np.float32)
+    allv = np.concatenate([vals, extra])
+    pad = (-len(allv)) % 256
+    allv = np.concatenate([allv, np.zeros(pad, np.float32)])
+    allv[0] = 448.0                                   # amax 448 -> multiplier 1
+    g = allv.reshape(1, -1, 256)
+    codes, scales, _ = gpu_encode(ctx, None, g, want_t=False)
+    assert scales.ravel()[0] == 1.0
+    np.testing.assert_array_equal(codes.ravel(), e4m3.quantize(allv))
+
+
+# ------------------------------------------------------------ rank sum
+
+@pytest.mark.parametrize("N,m,n,br,bc", [(1, 9, 13, 0, 0), (4, 77, 131, 0, 0),
+                                         (8, 128, 256, 0, 128), (16, 50, 300, 10, 64),
+                                         (3, 33, 100, 1, 16)])
+def test_reduce_bit_exact(ctx, N, m, n, br, bc):
+    say(f"reduce N={N} m={m} n={n} block=({br},{bc})")
+    grads = gradient_set(300 + N, 400 + m, N, m, n)
+    codes, scales = codec.quantize_transformed(grads, br, bc, False)
+    mean = gpu_reduce(ctx, codes, scales, br, bc)
+    ref = codec.reduce_local(codes, scales, br, bc)
+    np.testing.assert_array_equal(mean.view(np.uint32), ref.view(np.uint32))
+
+
+# ------------------------------------------------------------ GIFT branch
+
+TRANSFORM_CASES = [
+    # (N, m, n, r, sides, block_rows, block_cols)
+    (3, 150, 130, 8, gift.SIDE_INPUT, 0, 0),
+    (2, 150, 130, 8, gift.SIDE_OUTPUT, 0, 0),
+    (2, 150, 130, 8, gift.SIDE_BOTH, 0, 0),
+    (4, 256, 256, 16, gift.SIDE_INPUT, 0, 0),
+    (2, 200, 384, 32, gift.SIDE_BOTH, 0, 128),
+    (2, 97, 61, 5, gift.SIDE_BOTH, 0, 0),
+    (1, 64, 64, 64, gift.SIDE_INPUT, 0, 0),      # r = n: sigma A^-1/2
+]
+
+
+@pytest.mark.parametrize("N,m,n,r,sides,br,bc", TRANSFORM_CASES)
+def test_transform_encode_decode_parity(ctx, N, m, n, r, sides, br, bc):
+    say(f"transform N={N} m={m} n={n} r={r} sides={sides} block=({br},{bc})")
+    grads = gradient_set(500 + m, 600 + n, N, m, n)
+    f, fA, fG = make_factor(ctx, m, n, r, sides, seed=m + n)
+    codes, scales, tr = gpu_encode(ctx, f, grads, br, bc, False)
+    # the transformed tensor is the oracle's S_G^-1 W S_A^-1 to float32 accuracy
+    ref_t = codec.forward(grads, fA, fG)
+    assert rel(tr, ref_t) <= TRANSFORM_RTOL
+    # codes and scales are bit-exact on the same transformed tensor
+    ref_codes, ref_scales = codec.quantize_transformed(tr, br, bc, False)
+    np.testing.assert_array_equal(scales, ref_scales)
+    np.testing.assert_array_equal(codes, ref_codes)
+    # rank sum bit-exact, decode to float32 accuracy
+    mean = gpu_reduce(ctx, codes, scales, br, bc)
+    np.testing.assert_array_equal(mean, codec.reduce_local(codes, scales, br, bc))
+    out = gpu_decode(ctx, f, mean)
+    assert rel(out, codec.decode(mean, fA, fG)) <= TRANSFORM_RTOL
+    # end to end against the oracle's own encode -> reduce -> decode
+    ref_out = codec.round_trip(grads, fA, fG, br, bc, False)
+    assert rel(out, ref_out) <= DECODE_RTOL
+    f.close()
+
+
+def test_identity_factor_is_euclidean(ctx):
+    say("identity factor")
+    grads = gradient_set(11, 12, 2, 48, 80)
+    f = gift.Factor(ctx, 48, 80, 4, gift.SIDE_BOTH)   # never updated: c = 0
+    c1, s1, _ = gpu_encode(ctx, f, grads)
+    c0, s0, _ = gpu_encode(ctx, None, grads)
+    np.testing.assert_array_equal(c1, c0)
+    np.testing.assert_array_equal(s1, s0)
+    f.close()
+
+
+def test_shared_scale_with_transform(ctx):
+    say("shared scale with transform")
+    grads = gradient_set(21, 22, 4, 96, 64)
+    grads[1] *= 4.0
+    f, fA, fG = make_factor(ctx, 96, 64, 8, gift.SIDE_INPUT, seed=5)
+    codes, scales, tr = gpu_encode(ctx, f, grads, 0, 0, True)
+    ref_codes, ref_scales = codec.quantize_transformed(tr, 0, 0, True)
+    np.testing.assert_array_equal(scales, ref_scales)
+    np.testing.assert_array_equal(codes, ref_codes)
+    assert np.all(scales == scales[0])
+    f.close()
+
+
+def test_deterministic(ctx):
+    say("determinism")
+    grads = gradient_set(31, 32, 4, 256, 192)
+    f, _, _ = make_factor(ctx, 256, 192, 16, gift.SIDE_BOTH, seed=9)
+    a = gpu_encode(ctx, f, grads, 0, 64)
+    b = gpu_encode(ctx, f, grads, 0, 64)
+    for x, y in zip(a, b):
+        np.testing.assert_array_equal(x, y)
+    f.close()
