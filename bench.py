@@ -1,0 +1,303 @@
+"""Throughput of the GIFT codec hot path on one MI355X.
+
+One step = one pass of the whole per-layer hot path over a full synthetic
+gradient set: the factor refresh of every GIFT matrix (statistics, rank-r
+transform), the encode of every matrix (transform + amax + FP8 E4M3 for the
+GIFT matrices, amax + FP8 for the Euclidean ones), the local rank sum and the
+inverse transform.  Inputs are resident in HBM before the timed region.
+
+Default workload: the Llama-300M-like gradient set (24 layers, hidden 1024,
+MLP 2816, vocab 32000; 8 simulated ranks; GIFT on gate/up/down with rank 64,
+Euclidean with a shared scale on q/k/v/o, embedding and LM head; factor
+refresh every step from 16384 bf16 tokens).
+
+Prints one JSON line (metric = BASELINE metric: gradient GB/s through
+encode+decode).  ``--gpus N`` with N > 1 is not supported: this codec runs
+its N data-parallel ranks locally on one GPU.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+FP32_MFMA_TFLOPS = 157.3
+BF16_MFMA_TFLOPS = 2500.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=4, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--sides", choices=["input", "both"], default="input")
+    ap.add_argument("--iters", type=int, default=1, help="subspace iterations per warm refresh")
+    ap.add_argument("--cold-iters", type=int, default=6, help="subspace iterations of the first refresh")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    return ap.parse_args()
+
+
+class Job:
+    """Device buffers of one gradient matrix."""
+
+    def __init__(self, layer, mat, wl, sides_flag, dev, torch, gift):
+        self.layer, self.mat = layer, mat
+        N, m, n = wl.N, mat.m, mat.n
+        self.N, self.m, self.n = N, m, n
+        self.gift_branch = mat.gift
+        self.br, self.bc = wl.block_rows, wl.block_cols
+        nbr, nbc = gift.scale_grid(m, n, self.br, self.bc)
+        self.grads = torch.empty((N, m, n), dtype=torch.float32, device=dev)
+        self.codes = torch.empty((N, m, n), dtype=torch.uint8, device=dev)
+        self.scales = torch.empty((N, nbr, nbc), dtype=torch.float32, device=dev)
+        self.mean = torch.empty((m, n), dtype=torch.float32, device=dev)
+        self.out = torch.empty((m, n), dtype=torch.float32, device=dev) if mat.gift else None
+        self.factor = None
+        self.sides = sides_flag if mat.gift else 0
+        self.acts = self.dgrads = None
+
+
+def build_workload(args, torch, gift, synth, dev):
+    from synth.configs import WORKLOADS
+    wl = WORKLOADS[args.config]
+    sides = gift.SIDE_INPUT if args.sides == "input" else gift.SIDE_BOTH
+    jobs = [Job(layer, mat, wl, sides, dev, torch, gift) for layer, mat in wl.all_matrices()]
+    # one random set per distinct shape, copied into every matrix's own buffer
+    cache = {}
+    for jb in jobs:
+        key = (jb.m, jb.n)
+        if key not in cache:
+            cache[key] = synth.gradient_set_torch(synth.seed_for(wl.cfg, 0, 0, jb.mat.kind),
+                                                  wl.N, jb.m, jb.n, dev)
+        jb.grads.copy_(cache[key])
+    del cache
+    # factor inputs: per layer, one activation stream per layer input and one
+    # output-gradient stream per GIFT matrix (copies of one draw per shape)
+    xcache = {}
+
+    def stream(dim, role):
+        key = (dim, role)
+        if key not in xcache:
+            xcache[key] = synth.factor_inputs_torch(synth.seed_for(wl.cfg, role, 0, dim % 97), wl.T,
+                                                    dim, dev, dtype=wl.act_dtype)
+        return xcache[key]
+
+    per_layer_acts = {}
+    for jb in jobs:
+        if not jb.gift_branch:
+            continue
+        akey = (jb.layer, jb.mat.act)
+        if akey not in per_layer_acts:
+            per_layer_acts[akey] = stream(jb.n, 1).clone()
+        jb.acts = per_layer_acts[akey]
+        if jb.sides & gift.SIDE_OUTPUT:
+            jb.dgrads = stream(jb.m, 2).clone()
+        jb.factor = gift.Factor(ctx_holder["ctx"], jb.m, jb.n, wl.rank, jb.sides,
+                                seed=synth.seed_for(wl.cfg, 50, jb.layer, jb.mat.kind))
+    del xcache
+    return wl, jobs
+
+
+ctx_holder = {}
+
+
+def algorithmic_work(wl, jobs, args):
+    """Algorithmic flops / bytes per step for each kernel family."""
+    r = wl.rank
+    fam = {}
+
+    def add(name, flops=0.0, bytes_=0.0):
+        f, b = fam.get(name, (0.0, 0.0))
+        fam[name] = (f + flops, b + bytes_)
+
+    refresh = 1.0 / wl.refresh
+    for jb in jobs:
+        N, m, n = jb.N, jb.m, jb.n
+        e = float(N) * m * n
+        if not jb.gift_branch:
+            add("amax", 0, 4 * e)
+            add("quant", 0, 5 * e)
+            add("reduce", 0, float(m) * n * (N + 4))
+            continue
+        ra = r if jb.sides & 1 else 0
+        rg = r if jb.sides & 2 else 0
+        # encode: projections (2r flops/elem per side), update twice (amax, quant)
+        add("project", 2 * e * (ra + rg) + (2 * N * rg * ra * m if ra and rg else 0)
+            + (2 * N * m * rg * ra if ra and rg else 0), 4 * e * ((ra > 0) + (rg > 0)))
+        add("update_amax", 2 * e * (ra + rg), 4 * e)
+        add("update_quant", 2 * e * (ra + rg), 5 * e)
+        add("reduce", 0, float(m) * n * (N + 4))
+        mn = float(m) * n
+        add("project", 2 * mn * (ra + rg), 4 * mn * ((ra > 0) + (rg > 0)))
+        add("update_store", 2 * mn * (ra + rg), 8 * mn)
+        # factor refresh (amortised by the cadence)
+        for dim, on in ((n, ra), (m, rg)):
+            if not on:
+                continue
+            T = wl.T
+            k = min(dim, 2 * r)
+            add("syrk", refresh * T * dim * (dim + 1), refresh * T * dim * 2)
+            q = args.iters
+            sub = 8 * dim * k * k + q * (2 * dim * dim * k + 8 * dim * k * k) + \
+                2 * dim * dim * k + 2 * dim * k * k + 2 * dim * k * r
+            add("factor", refresh * sub, 0)
+    return fam
+
+
+def cpu_baseline(wl, seconds):
+    """The oracle on one GIFT matrix of the workload, timed on the host cores."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+    from oracle import codec
+    from synth import factor_inputs, gradient_set, seed_for
+
+    mat = next(mt for _, mt in wl.all_matrices() if mt.gift)
+    N, m, n, r = wl.N, mat.m, mat.n, wl.rank
+    grads = gradient_set(seed_for(wl.cfg, 0), seed_for(wl.cfg, 100), N, m, n)
+    X, _ = factor_inputs(seed_for(wl.cfg, 1), wl.T, n, dtype=wl.act_dtype)
+    cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    t0 = time.perf_counter()
+    reps = 0
+    while True:
+        fA = codec.lowrank_factor(codec.factor_statistics(X), r).to_f32()
+        codec.round_trip(grads, fA, None, wl.block_rows, wl.block_cols, False)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds or reps >= 3:
+            break
+    per = el / reps
+    gbs = N * m * n * 4 / per / 1e9
+    return {"value": round(gbs, 4), "unit": "GB/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"one {mat.name} matrix ({m}x{n}, N={N}, r={r}, input side, factor from "
+                      f"{wl.T} tokens): factor + encode + reduce + decode, {reps} rep(s), "
+                      f"{per:.2f} s each"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU: the codec simulates its N data-parallel ranks locally "
+              f"and has no multi-GPU path (asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2607_07494_amd as gift
+    import synth
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    ctx = gift.Context()
+    ctx_holder["ctx"] = ctx
+    wl, jobs = build_workload(args, torch, gift, synth, dev)
+    torch.cuda.synchronize()
+    print(f"[bench] workload {wl.name}: {len(jobs)} matrices, "
+          f"{sum(j.N * j.m * j.n for j in jobs) * 4 / 1e9:.2f} GB of rank gradients", file=sys.stderr,
+          flush=True)
+
+    def step(iters):
+        for jb in jobs:
+            if jb.factor is not None:
+                jb.factor.update(acts=jb.acts, out_grads=jb.dgrads, iters=iters)
+        for jb in jobs:
+            gift.encode(ctx, jb.factor, jb.grads, jb.codes, jb.scales, jb.br, jb.bc,
+                        gift.SCALE_LOCAL if jb.gift_branch else gift.SCALE_SHARED)
+        for jb in jobs:
+            gift.reduce_local(ctx, jb.codes, jb.scales, jb.mean, jb.br, jb.bc)
+        for jb in jobs:
+            if jb.gift_branch:
+                gift.decode(ctx, jb.factor, jb.mean, jb.out)
+
+    for w in range(max(args.warmup, 1)):
+        step(args.cold_iters if w == 0 else args.iters)
+        torch.cuda.synchronize()
+        print(f"[bench] warmup step {w} done", file=sys.stderr, flush=True)
+
+    ctx.profile_reset()
+    ctx.profile(True)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record()
+    for s in range(args.steps):
+        step(args.iters)
+    stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = start.elapsed_time(stop) / args.steps
+    fam_ms = {}
+    for name in gift.KERNELS:
+        launches, ms = ctx.profile_read(name)
+        if launches:
+            fam_ms[name] = (launches / args.steps, ms / args.steps)
+    ctx.profile(False)
+    print(f"[bench] timed {args.steps} steps: {ms_step:.3f} ms/step (wall {wall:.2f} s)",
+          file=sys.stderr, flush=True)
+
+    grad_bytes = sum(j.N * j.m * j.n * 4 for j in jobs)
+    value = grad_bytes / (ms_step * 1e-3) / 1e9
+    work = algorithmic_work(wl, jobs, args)
+    kernels = {}
+    for name, (launches, ms) in fam_ms.items():
+        fl, by = work.get(name, (0.0, 0.0))
+        kernels[name] = {"ms_per_step": round(ms, 4), "launches_per_step": round(launches, 2),
+                         "tflops": round(fl / (ms * 1e-3) / 1e12, 3) if ms > 0 else None,
+                         "gbs": round(by / (ms * 1e-3) / 1e9, 2) if ms > 0 else None}
+    dom = max(fam_ms, key=lambda k: fam_ms[k][1])
+    fl, by = work.get(dom, (0.0, 0.0))
+    dom_launches, dom_ms = fam_ms[dom]
+    avg_ms = dom_ms / dom_launches
+    peak_f = BF16_MFMA_TFLOPS if dom == "syrk" and wl.act_dtype == "bf16" else FP32_MFMA_TFLOPS
+    frac_f = fl / (dom_ms * 1e-3) / 1e12 / peak_f if fl else 0.0
+    frac_b = by / (dom_ms * 1e-3) / 1e9 / HBM_PEAK_GBS if by else 0.0
+    if frac_f >= frac_b:
+        roof = {"bound": "mfma", "achieved": round(fl / dom_launches / (avg_ms * 1e-3) / 1e12, 3),
+                "peak": peak_f, "unit": "TFLOP/s", "frac": round(frac_f, 4)}
+    else:
+        roof = {"bound": "hbm", "achieved": round(by / dom_launches / (avg_ms * 1e-3) / 1e9, 2),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(frac_b, 4)}
+    roof.update({"kernel": dom, "avg_launch_ms": round(avg_ms, 5), "traffic": None})
+    tf_fams = ("project", "update_amax", "update_quant", "update_store")
+    tf_ms = sum(fam_ms[k][1] for k in tf_fams if k in fam_ms)
+    tf_flops = sum(work[k][0] for k in tf_fams if k in work)
+    line = {
+        "metric": "gradient GB/s through GIFT encode+decode",
+        "value": round(value, 3),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name} (config {wl.cfg})", "ranks": wl.N, "rank": wl.rank,
+                   "sides": args.sides, "tokens": wl.T, "matrices": len(jobs),
+                   "grad_gb": round(grad_bytes / 1e9, 3), "factor_refresh_every": wl.refresh,
+                   "subspace_iters": args.iters},
+        "transform_tflops": round(tf_flops / (tf_ms * 1e-3) / 1e12, 3) if tf_ms else None,
+        "roofline": roof,
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    for jb in jobs:
+        if jb.factor is not None:
+            jb.factor.close()
+    ctx.close()
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()
