@@ -203,10 +203,12 @@ def main():
           f"{sum(j.N * j.m * j.n for j in jobs) * 4 / 1e9:.2f} GB of rank gradients", file=sys.stderr,
           flush=True)
 
+    fjobs = [jb for jb in jobs if jb.factor is not None]
+
     def step(iters):
-        for jb in jobs:
-            if jb.factor is not None:
-                jb.factor.update(acts=jb.acts, out_grads=jb.dgrads, iters=iters)
+        if fjobs:
+            gift.factor_update_batch(ctx, [jb.factor for jb in fjobs], [jb.acts for jb in fjobs],
+                                     [jb.dgrads for jb in fjobs], iters=iters)
         for jb in jobs:
             gift.encode(ctx, jb.factor, jb.grads, jb.codes, jb.scales, jb.br, jb.bc,
                         gift.SCALE_LOCAL if jb.gift_branch else gift.SCALE_SHARED)

@@ -111,7 +111,8 @@ gift_status gift_ctx_create(void *hip_stream, gift_ctx **out);
 /* Rebind the context to another stream of the same device. */
 gift_status gift_ctx_set_stream(gift_ctx *ctx, void *hip_stream);
 
-/* Destroy a context (synchronizes its stream, frees its workspace). NULL ok. */
+/* Destroy a context (synchronizes its stream, frees its workspace). NULL ok.
+ * Destroy the factors created on it first. */
 void gift_ctx_destroy(gift_ctx *ctx);
 
 /* Per-kernel timing: when enabled, every launch is bracketed by HIP events on
@@ -128,13 +129,15 @@ gift_status gift_ctx_profile_reset(gift_ctx *ctx);
  * output side; 0 = identity).  sides: GIFT_SIDE_*.  damping: relative floor of
  * the isotropic level sigma^2 (>= damping * tr(A)/n), the regularization of
  * eq. design_chol.  seed: key of the Philox4x32-10 start block of the subspace
- * iteration.  The new factor is the identity until updated or imported.
+ * iteration (input side: seed; output side: seed + 1).  The new factor is the
+ * identity until updated or imported.
  * Allocates device memory on the current device (synchronous). */
 gift_status gift_factor_create(gift_ctx *ctx, int64_t m, int64_t n, int32_t rank,
                                int32_t sides, float damping, uint64_t seed,
                                gift_factor **out);
 
-/* Destroy a factor (synchronizes the context stream first). NULL ok. */
+/* Destroy a factor (synchronizes the context stream first). NULL ok.  A
+ * factor must be destroyed before the context it was created on. */
 void gift_factor_destroy(gift_factor *f);
 
 /* Refresh the factor from one batch of statistics (Sec. V-E: refreshed every
@@ -155,6 +158,17 @@ void gift_factor_destroy(gift_factor *f);
 gift_status gift_factor_update(gift_ctx *ctx, gift_factor *f, const void *acts,
                                const void *out_grads, int64_t T, gift_dtype dtype,
                                int32_t iters);
+
+/* Refresh many factors at once (same T and dtype): factor sides with equal
+ * (dim, rank) share one launch sequence, so the small per-factor steps run
+ * side by side on the GPU.  factors, acts and out_grads are HOST arrays of
+ * count entries; acts[i] / out_grads[i] are the device inputs of factors[i]
+ * (an entry may be NULL when that factor lacks the side; the whole array may
+ * be NULL when no factor has the side).  A factor may appear only once.
+ * Results equal count separate gift_factor_update calls. */
+gift_status gift_factor_update_batch(gift_ctx *ctx, int32_t count, gift_factor *const *factors,
+                                     const void *const *acts, const void *const *out_grads,
+                                     int64_t T, gift_dtype dtype, int32_t iters);
 
 /* Copy one side's transform out of / into a factor (device pointers):
  *   U [dim, r] row-major (dim = n for GIFT_SIDE_INPUT, m for GIFT_SIDE_OUTPUT),

@@ -430,23 +430,43 @@ void gift_factor_destroy(gift_factor *f) {
   delete f;
 }
 
-gift_status gift_factor_update(gift_ctx *ctx, gift_factor *f, const void *acts,
-                               const void *out_grads, int64_t T, gift_dtype dtype, int32_t iters) {
-  if (!ctx || !f) return set_error(GIFT_EINVAL, "gift_factor_update: NULL ctx or factor");
+gift_status gift_factor_update_batch(gift_ctx *ctx, int32_t count, gift_factor *const *factors,
+                                     const void *const *acts, const void *const *out_grads,
+                                     int64_t T, gift_dtype dtype, int32_t iters) {
+  if (!ctx) return set_error(GIFT_EINVAL, "gift_factor_update: ctx is NULL");
+  if (count < 0) return set_error(GIFT_EINVAL, "gift_factor_update: count must be >= 0");
+  if (count > 0 && !factors) return set_error(GIFT_EINVAL, "gift_factor_update: factors is NULL");
   if (dtype != GIFT_F32 && dtype != GIFT_BF16)
     return set_error(GIFT_EINVAL, "gift_factor_update: dtype must be GIFT_F32 or GIFT_BF16");
   if (iters < 0) return set_error(GIFT_EINVAL, "gift_factor_update: iters must be >= 0");
   if (T <= 0) return set_error(GIFT_ESHAPE, "gift_factor_update: T must be positive");
-  const bool needA = f->A.r > 0, needG = f->G.r > 0;
-  if (needA && !acts) return set_error(GIFT_EINVAL, "gift_factor_update: acts is NULL");
-  if (needG && !out_grads) return set_error(GIFT_EINVAL, "gift_factor_update: out_grads is NULL");
+  std::vector<SideJob> jobs;
+  for (int32_t i = 0; i < count; ++i) {
+    gift_factor *f = factors[i];
+    if (!f) return set_error(GIFT_EINVAL, "gift_factor_update: NULL factor in the batch");
+    for (int32_t j = 0; j < i; ++j)
+      if (factors[j] == f) return set_error(GIFT_EINVAL, "gift_factor_update: a factor appears twice");
+    const void *a = acts ? acts[i] : nullptr;
+    const void *d = out_grads ? out_grads[i] : nullptr;
+    if (f->A.r > 0) {
+      if (!a) return set_error(GIFT_EINVAL, "gift_factor_update: acts is NULL for an input-side factor");
+      jobs.push_back(SideJob{&f->A, a, f->seed, f->damping});
+    }
+    if (f->G.r > 0) {
+      if (!d) return set_error(GIFT_EINVAL, "gift_factor_update: out_grads is NULL for an output-side factor");
+      jobs.push_back(SideJob{&f->G, d, f->seed + 1, f->damping});
+    }
+  }
+  if (jobs.empty()) return GIFT_OK;
   gift_status st = bind_device(ctx);
   if (st != GIFT_OK) return st;
-  if (needA && (st = factor_refresh_side(ctx, f, f->A, acts, T, dtype, iters, f->seed)) != GIFT_OK)
-    return st;
-  if (needG && (st = factor_refresh_side(ctx, f, f->G, out_grads, T, dtype, iters, f->seed + 1)) != GIFT_OK)
-    return st;
-  return GIFT_OK;
+  return factor_refresh_batch(ctx, jobs, T, dtype, iters);
+}
+
+gift_status gift_factor_update(gift_ctx *ctx, gift_factor *f, const void *acts,
+                               const void *out_grads, int64_t T, gift_dtype dtype, int32_t iters) {
+  if (!ctx || !f) return set_error(GIFT_EINVAL, "gift_factor_update: NULL ctx or factor");
+  return gift_factor_update_batch(ctx, 1, &f, &acts, &out_grads, T, dtype, iters);
 }
 
 static gift_status pick_side(const gift_factor *f, int32_t side, const Side **s) {

@@ -162,10 +162,16 @@ gift_status launch_reduce(gift_ctx *ctx, const uint8_t *codes, const float *scal
                           int32_t N, int64_t m, int64_t n, BlockGeom g, float *mean);
 gift_status launch_copy_f32(gift_ctx *ctx, float *dst, const float *src, int64_t count);
 
-// factor pipeline (k_factor.hip)
-gift_status factor_refresh_side(gift_ctx *ctx, gift_factor *f, Side &s, const void *x,
-                                int64_t T, gift_dtype dtype, int32_t iters,
-                                uint64_t seed);
+// factor pipeline (k_factor.hip): sides with equal (dim, r) are refreshed
+// together in one launch sequence
+struct SideJob {
+  Side *side;
+  const void *x;      // [T, dim] statistics input (device)
+  uint64_t seed;      // Philox key of the start block
+  float damping;
+};
+gift_status factor_refresh_batch(gift_ctx *ctx, const std::vector<SideJob> &jobs, int64_t T,
+                                 gift_dtype dtype, int32_t iters);
 gift_status side_import(gift_ctx *ctx, Side &s, const float *U, const float *c_fwd,
                         const float *c_inv, const float *sigma2);
 gift_status side_export(gift_ctx *ctx, const Side &s, float *U, float *c_fwd,

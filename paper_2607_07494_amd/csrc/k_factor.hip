@@ -1,4 +1,5 @@
-// Factor refresh: K-FAC statistics and their rank-r transform.
+// Factor refresh: K-FAC statistics and their rank-r transform, batched over
+// all factor sides of one dimension.
 //
 // A = X^T X / T (eq. kfac_fisher_block, eq. impl_A_psd), then its leading r
 // eigenpairs (eq. impl_A_lowrank) by block subspace iteration with
@@ -8,13 +9,19 @@
 //   B = Q^T A Q;  B = V diag(theta) V^T (theta descending);  U = Q V[:, :r]
 //
 // (Golub & Van Loan, Matrix Computations, Sec. 8.2.4 and 8.1.6; CholeskyQR2
-// after Fukaya et al. 2014.)  The dense products run on the tile kernel's
-// FP32 MFMA path; the k x k steps (Cholesky, triangular inverse, symmetric
-// eigensolver) are small single-workgroup kernels in float64.  The
-// eigensolver is one-sided (Hestenes) Jacobi with round-robin parallel
-// ordering: rotating the columns of the symmetric positive semidefinite B
-// until they are mutually orthogonal yields B V = V diag(theta), so column
-// norms are the eigenvalues and normalised columns the eigenvectors.
+// after Fukaya et al. 2014.)  The dense products run on the tile kernel's FP32
+// MFMA path with the members of a batch as its batch dimension.  The k x k
+// steps (Cholesky with its triangular inverse, the symmetric eigensolver) are
+// single-workgroup kernels in float64, one workgroup per member, working in
+// LDS when k <= 128.  The eigensolver is one-sided (Hestenes) Jacobi with
+// round-robin parallel ordering: rotating the columns of the symmetric
+// positive semidefinite B until they are mutually orthogonal yields
+// B V = V diag(theta), so column norms are the eigenvalues and normalised
+// columns the eigenvectors.
+//
+// The next refresh warm-starts from the rotated basis Q V (all k columns,
+// descending Ritz values), which leaves B nearly diagonal after one more
+// iteration, so the eigensolver then needs few sweeps.
 //
 // The isotropic level and the coefficients follow the low-rank transform
 // S^-1 = I + U diag(c) U^T with c_i = sqrt(sigma^2/lambda_i) - 1 and
@@ -27,13 +34,29 @@
 
 #include <math.h>
 
+#include <algorithm>
+#include <map>
+#include <vector>
+
 #include "gift_internal.h"
 
 namespace gift {
 
+gift_status launch_syrk_bf16(gift_ctx *ctx, const uint16_t *const *x_table, int members,
+                             int64_t T, int64_t dim, float scale, float *A);
+
 namespace {
 
 constexpr int kSmallThreads = 1024;
+constexpr int kLdsK = 128;   // k handled in LDS by the small kernels
+
+// Per-member state pointers, read by the gather / scatter kernels.
+struct Member {
+  float *Qt, *Ut, *U, *Uc, *Uci, *c_fwd, *c_inv, *lam, *sigma2;
+  uint32_t seed_lo, seed_hi;
+  int mode;        // 0 cold start, 1 warm start, 2 imported U + start rows
+  float damping;
+};
 
 __device__ __forceinline__ uint32_t philox_word0(uint32_t c0, uint32_t c1, uint32_t c2,
                                                  uint32_t c3, uint32_t k0, uint32_t k1) {
@@ -56,16 +79,26 @@ __device__ __forceinline__ uint32_t philox_word0(uint32_t c0, uint32_t c1, uint3
   return c0;
 }
 
-// Qt[j][i] for rows j in [row0, k): the start block transposed.
-__global__ void start_block_kernel(float *Qt, int64_t dim, int k, int row0, uint32_t k0,
-                                   uint32_t k1) {
-  const int64_t total = (int64_t)(k - row0) * dim;
+// Qw[member] (k x dim, rows = basis vectors): warm rows from the member's
+// Qt, the others from the start block.
+__global__ void gather_start_kernel(const Member *mem, float *Qw, int64_t dim, int k, int r) {
+  const int g = blockIdx.y;
+  const Member M = mem[g];
+  const int64_t total = (int64_t)k * dim;
+  float *dst = Qw + (int64_t)g * total;
   for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total;
        t += (int64_t)gridDim.x * blockDim.x) {
-    const int j = row0 + (int)(t / dim);
+    const int j = (int)(t / dim);
     const int64_t i = t % dim;
-    const uint32_t w = philox_word0((uint32_t)i, (uint32_t)j, 0u, 0u, k0, k1);
-    Qt[(int64_t)j * dim + i] = (float)(((int32_t)w) >> 8) * 1.1920928955078125e-7f;
+    const bool warm = M.mode == 1 || (M.mode == 2 && j < r);
+    float v;
+    if (warm) {
+      v = M.Qt[t];
+    } else {
+      const uint32_t w = philox_word0((uint32_t)i, (uint32_t)j, 0u, 0u, M.seed_lo, M.seed_hi);
+      v = (float)(((int32_t)w) >> 8) * 1.1920928955078125e-7f;
+    }
+    dst[t] = v;
   }
 }
 
@@ -73,16 +106,6 @@ __global__ void bf16_to_f32_kernel(float *dst, const uint16_t *src, int64_t n) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x)
     dst[i] = __uint_as_float((uint32_t)src[i] << 16);
-}
-
-// Sum split-K partials [ks][k][k] (float32) into W (float64, k x k).
-__device__ void sum_partials(double *W, const float *part, int ks, int k) {
-  const int64_t kk = (int64_t)k * k;
-  for (int64_t t = threadIdx.x; t < kk; t += blockDim.x) {
-    double s = 0.0;
-    for (int z = 0; z < ks; ++z) s += (double)part[z * kk + t];
-    W[t] = s;
-  }
 }
 
 __device__ double block_sum(double v, double *red) {
@@ -98,20 +121,26 @@ __device__ double block_sum(double v, double *red) {
   return r;
 }
 
-// Gram partials -> R (upper Cholesky, pivots floored) -> Rinv (float32).
-// W and X are float64 k x k scratch.
-__global__ __launch_bounds__(kSmallThreads) void chol_inv_kernel(const float *part, int ks, int k,
-                                                                 double *W, double *X,
-                                                                 float *Rinv) {
-  __shared__ double red[kSmallThreads];
+// ---------------------------------------------------------------------------
+// Cholesky of the Gram matrix and its triangular inverse.
+// W (k x k, float64) is LDS or global scratch.  R (upper, pivots floored at
+// 1e-12 tr/k) replaces the upper triangle; X = R^-1 is kept transposed in the
+// strict lower triangle with its diagonal in xdiag.  Output Rinv (float32).
+// ---------------------------------------------------------------------------
+__device__ void chol_inv_body(const float *part, int ks, int k, double *W, double *xdiag,
+                              double *red, float *Rinv) {
   const int tid = threadIdx.x, nt = blockDim.x;
-  sum_partials(W, part, ks, k);
+  const int64_t kk = (int64_t)k * k;
+  for (int64_t t = tid; t < kk; t += nt) {
+    double s = 0.0;
+    for (int z = 0; z < ks; ++z) s += (double)part[z * kk + t];
+    W[t] = s;
+  }
   __syncthreads();
   double tr = 0.0;
   for (int i = tid; i < k; i += nt) tr += W[(int64_t)i * k + i];
   tr = block_sum(tr, red);
   const double floor = 1e-12 * (tr > 0.0 ? tr : 0.0) / (k > 0 ? k : 1) + 1e-300;
-  // right-looking Cholesky on the upper triangle: W <- R
   for (int j = 0; j < k; ++j) {
     if (tid == 0) {
       const double d = W[(int64_t)j * k + j];
@@ -128,41 +157,60 @@ __global__ __launch_bounds__(kSmallThreads) void chol_inv_kernel(const float *pa
     }
     __syncthreads();
   }
-  // X = R^-1 (upper), row by row from the bottom; columns in parallel
+  // X = R^-1, bottom row first; 8 lanes per column share each dot product
   for (int i = k - 1; i >= 0; --i) {
     const double rii = W[(int64_t)i * k + i];
-    for (int c = tid; c < k; c += nt) {
-      double v;
-      if (c < i) {
-        v = 0.0;
-      } else if (c == i) {
-        v = 1.0 / rii;
-      } else {
-        double s = 0.0;
-        for (int l = i + 1; l <= c; ++l) s += W[(int64_t)i * k + l] * X[(int64_t)l * k + c];
-        v = -s / rii;
+    for (int base = 0; base < k; base += nt / 8) {
+      const int c = i + 1 + base + tid / 8, part8 = tid & 7;
+      double s = 0.0;
+      if (c < k) {
+        for (int l = i + 1 + part8; l <= c; l += 8)
+          s += W[(int64_t)i * k + l] * (l == c ? xdiag[c] : W[(int64_t)c * k + l]);
       }
-      X[(int64_t)i * k + c] = v;
+      s += __shfl_xor(s, 1);
+      s += __shfl_xor(s, 2);
+      s += __shfl_xor(s, 4);
+      if (c < k && part8 == 0) W[(int64_t)c * k + i] = -s / rii;
     }
+    if (tid == 0) xdiag[i] = 1.0 / rii;
     __syncthreads();
   }
-  for (int64_t t = tid; t < (int64_t)k * k; t += nt) Rinv[t] = (float)X[t];
+  for (int64_t t = tid; t < kk; t += nt) {
+    const int i = (int)(t / k), c = (int)(t % k);
+    double v = 0.0;
+    if (c > i) v = W[(int64_t)c * k + i];
+    else if (c == i) v = xdiag[i];
+    Rinv[t] = (float)v;
+  }
 }
 
-// Rayleigh-Ritz: B partials -> eigenpairs by one-sided Jacobi -> top r.
-// W: float64 k x k scratch (column-major working copy: W[c*k + row]),
-// theta: float64 [k] out (sorted, top r), Vr: float32 [k][r] out.
-__global__ __launch_bounds__(kSmallThreads) void rr_eig_kernel(const float *part, int ks, int k,
-                                                               int r, double *W, double *norms,
-                                                               double *theta, float *Vr,
-                                                               int max_sweeps) {
+__global__ __launch_bounds__(kSmallThreads) void chol_inv_lds_kernel(const float *part, int ks, int k,
+                                                                     float *Rinv) {
+  __shared__ double W[kLdsK * kLdsK];
+  __shared__ double xdiag[kLdsK];
   __shared__ double red[kSmallThreads];
-  __shared__ int pair_p[512], pair_q[512];
-  __shared__ double rot_c[512], rot_s[512];
-  __shared__ int any_rot;
+  const int g = blockIdx.x;
+  chol_inv_body(part + (int64_t)g * ks * k * k, ks, k, W, xdiag, red, Rinv + (int64_t)g * k * k);
+}
+
+__global__ __launch_bounds__(kSmallThreads) void chol_inv_global_kernel(const float *part, int ks,
+                                                                        int k, double *Wg,
+                                                                        double *xdg, float *Rinv) {
+  __shared__ double red[kSmallThreads];
+  const int g = blockIdx.x;
+  chol_inv_body(part + (int64_t)g * ks * k * k, ks, k, Wg + (int64_t)g * k * k, xdg + (int64_t)g * k,
+                red, Rinv + (int64_t)g * k * k);
+}
+
+// ---------------------------------------------------------------------------
+// Rayleigh-Ritz eigensolver: B (partials, symmetrised) -> V (k x k, columns
+// sorted by descending eigenvalue) and theta (k).  One-sided Jacobi on the
+// columns of W (column-major, W[c*k + row]); 16 lanes per column pair.
+// ---------------------------------------------------------------------------
+__device__ void rr_eig_body(const float *part, int ks, int k, double *W, double *norms,
+                            int *any_rot, float *V, float *theta, int max_sweeps) {
   const int tid = threadIdx.x, nt = blockDim.x;
   const int64_t kk = (int64_t)k * k;
-  // symmetrised B, stored column-major (columns are the rotated vectors)
   for (int64_t t = tid; t < kk; t += nt) {
     const int i = (int)(t / k), j = (int)(t % k);
     double a = 0.0, b = 0.0;
@@ -173,79 +221,76 @@ __global__ __launch_bounds__(kSmallThreads) void rr_eig_kernel(const float *part
     W[(int64_t)j * k + i] = 0.5 * (a + b);
   }
   __syncthreads();
-  const int kp = (k + 1) & ~1;  // players (one dummy when k is odd)
+  const int kp = (k + 1) & ~1;
   const int npairs = kp / 2;
+  const int lanes = 16;
+  const int groups = nt / lanes;
   for (int sweep = 0; sweep < max_sweeps; ++sweep) {
-    if (tid == 0) any_rot = 0;
+    if (tid == 0) *any_rot = 0;
     __syncthreads();
     for (int round = 0; round < kp - 1; ++round) {
-      // circle method: player kp-1 fixed, the others rotate
-      for (int pi = tid; pi < npairs; pi += nt) {
-        int p, q;
-        if (pi == 0) {
-          p = round;
-          q = kp - 1;
-        } else {
-          p = (round + pi) % (kp - 1);
-          q = (round - pi + kp - 1) % (kp - 1);
+      for (int pb = 0; pb < npairs; pb += groups) {
+        const int pi = pb + tid / lanes, part16 = tid % lanes;
+        int p = 0, q = 0;
+        bool valid = pi < npairs;
+        if (valid) {
+          if (pi == 0) {
+            p = round;
+            q = kp - 1;
+          } else {
+            p = (round + pi) % (kp - 1);
+            q = (round - pi + kp - 1) % (kp - 1);
+          }
+          if (p > q) {
+            const int tt = p;
+            p = q;
+            q = tt;
+          }
+          valid = q < k;
         }
-        if (p > q) {
-          const int t = p;
-          p = q;
-          q = t;
-        }
-        pair_p[pi] = p;
-        pair_q[pi] = q;
-      }
-      __syncthreads();
-      // rotation per pair from the column dot products
-      for (int pi = tid; pi < npairs; pi += nt) {
-        const int p = pair_p[pi], q = pair_q[pi];
-        double c = 1.0, s = 0.0;
-        if (q < k) {
+        double alpha = 0.0, beta = 0.0, gamma = 0.0;
+        if (valid) {
           const double *cp = W + (int64_t)p * k, *cq = W + (int64_t)q * k;
-          double alpha = 0.0, beta = 0.0, gamma = 0.0;
-          for (int i = 0; i < k; ++i) {
-            alpha += cp[i] * cp[i];
-            beta += cq[i] * cq[i];
-            gamma += cp[i] * cq[i];
-          }
-          if (fabs(gamma) > 1e-12 * sqrt(alpha * beta) && gamma != 0.0) {
-            const double zeta = (beta - alpha) / (2.0 * gamma);
-            const double t = (zeta >= 0.0 ? 1.0 : -1.0) / (fabs(zeta) + sqrt(1.0 + zeta * zeta));
-            c = 1.0 / sqrt(1.0 + t * t);
-            s = c * t;
-            any_rot = 1;
+          for (int i = part16; i < k; i += lanes) {
+            const double a = cp[i], b = cq[i];
+            alpha += a * a;
+            beta += b * b;
+            gamma += a * b;
           }
         }
-        rot_c[pi] = c;
-        rot_s[pi] = s;
-      }
-      __syncthreads();
-      for (int64_t t = tid; t < (int64_t)npairs * k; t += nt) {
-        const int pi = (int)(t / k), i = (int)(t % k);
-        const int p = pair_p[pi], q = pair_q[pi];
-        if (q >= k) continue;
-        const double c = rot_c[pi], s = rot_s[pi];
-        if (s == 0.0) continue;
-        double *cp = W + (int64_t)p * k, *cq = W + (int64_t)q * k;
-        const double a = cp[i], b = cq[i];
-        cp[i] = c * a - s * b;
-        cq[i] = s * a + c * b;
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) {
+          alpha += __shfl_xor(alpha, o);
+          beta += __shfl_xor(beta, o);
+          gamma += __shfl_xor(gamma, o);
+        }
+        if (valid && gamma != 0.0 && fabs(gamma) > 1e-12 * sqrt(alpha * beta)) {
+          const double zeta = (beta - alpha) / (2.0 * gamma);
+          const double t = (zeta >= 0.0 ? 1.0 : -1.0) / (fabs(zeta) + sqrt(1.0 + zeta * zeta));
+          const double c = 1.0 / sqrt(1.0 + t * t);
+          const double s = c * t;
+          double *cp = W + (int64_t)p * k, *cq = W + (int64_t)q * k;
+          for (int i = part16; i < k; i += lanes) {
+            const double a = cp[i], b = cq[i];
+            cp[i] = c * a - s * b;
+            cq[i] = s * a + c * b;
+          }
+          if (part16 == 0) *any_rot = 1;
+        }
+        if (npairs > groups) __syncthreads();
       }
       __syncthreads();
     }
-    if (!any_rot) break;
+    const int rotated = *any_rot;
     __syncthreads();
+    if (!rotated) break;
   }
-  // eigenvalue = column norm, eigenvector = column / norm
   for (int j = tid; j < k; j += nt) {
     double s = 0.0;
     for (int i = 0; i < k; ++i) s += W[(int64_t)j * k + i] * W[(int64_t)j * k + i];
     norms[j] = sqrt(s);
   }
   __syncthreads();
-  // rank columns by descending eigenvalue (ties by index), keep the top r
   for (int j = tid; j < k; j += nt) {
     const double v = norms[j];
     int rank = 0;
@@ -253,30 +298,56 @@ __global__ __launch_bounds__(kSmallThreads) void rr_eig_kernel(const float *part
       const double u = norms[l];
       rank += (u > v) || (u == v && l < j);
     }
-    if (rank < r) {
-      theta[rank] = v;
-      const double inv = v > 0.0 ? 1.0 / v : 0.0;
-      for (int i = 0; i < k; ++i) Vr[(int64_t)i * r + rank] = (float)(W[(int64_t)j * k + i] * inv);
-    }
+    theta[rank] = (float)v;
+    const double inv = v > 0.0 ? 1.0 / v : 0.0;
+    for (int i = 0; i < k; ++i) V[(int64_t)i * k + rank] = (float)(W[(int64_t)j * k + i] * inv);
   }
 }
 
-// sigma^2, coefficients and the U layouts from Ut and theta.
-__global__ __launch_bounds__(kSmallThreads) void finalize_kernel(
-    const float *Amat, int64_t dim, const double *theta, int r, float damping, const float *Ut,
-    float *U, float *Uc, float *Uci, float *c_fwd, float *c_inv, float *lam_out, float *sigma2_out,
-    double *scratch) {
+__global__ __launch_bounds__(kSmallThreads) void rr_eig_lds_kernel(const float *part, int ks, int k,
+                                                                   float *V, float *theta,
+                                                                   int max_sweeps) {
+  __shared__ double W[kLdsK * kLdsK];
+  __shared__ double norms[kLdsK];
+  __shared__ int any_rot;
+  const int g = blockIdx.x;
+  rr_eig_body(part + (int64_t)g * ks * k * k, ks, k, W, norms, &any_rot, V + (int64_t)g * k * k,
+              theta + (int64_t)g * k, max_sweeps);
+}
+
+__global__ __launch_bounds__(kSmallThreads) void rr_eig_global_kernel(const float *part, int ks,
+                                                                      int k, double *Wg,
+                                                                      double *ng, float *V,
+                                                                      float *theta,
+                                                                      int max_sweeps) {
+  __shared__ int any_rot;
+  const int g = blockIdx.x;
+  rr_eig_body(part + (int64_t)g * ks * k * k, ks, k, Wg + (int64_t)g * k * k, ng + (int64_t)g * k,
+              &any_rot, V + (int64_t)g * k * k, theta + (int64_t)g * k, max_sweeps);
+}
+
+// sigma^2, coefficients, U layouts and the warm-start block of each member.
+__global__ __launch_bounds__(kSmallThreads) void finalize_kernel(const Member *mem,
+                                                                 const float *Amat, int64_t dim,
+                                                                 const float *theta, int k, int r,
+                                                                 const float *Qrot) {
   __shared__ double red[kSmallThreads];
+  __shared__ double coef[2 * 512];
+  const int g = blockIdx.x;
+  const Member M = mem[g];
+  const float *A = Amat + (int64_t)g * dim * dim;
+  const float *th = theta + (int64_t)g * k;
+  const float *Q = Qrot + (int64_t)g * k * dim;
   const int tid = threadIdx.x, nt = blockDim.x;
   double tr = 0.0;
-  for (int64_t i = tid; i < dim; i += nt) tr += (double)Amat[i * dim + i];
+  for (int64_t i = tid; i < dim; i += nt) tr += (double)A[i * dim + i];
   tr = block_sum(tr, red);
   double top = 0.0;
-  for (int i = tid; i < r; i += nt) top += theta[i] > 0.0 ? theta[i] : 0.0;
+  for (int i = tid; i < r; i += nt) top += th[i] > 0.f ? (double)th[i] : 0.0;
   top = block_sum(top, red);
-  double sigma2 = 0.0;
   const bool identity = !(tr > 0.0) || r == 0;
-  const double floor = (double)damping * tr / (double)dim;
+  const double floor = (double)M.damping * tr / (double)dim;
+  double sigma2 = 0.0;
   if (!identity) {
     if (r >= dim) {
       sigma2 = tr / (double)dim;
@@ -286,7 +357,7 @@ __global__ __launch_bounds__(kSmallThreads) void finalize_kernel(
     }
   }
   for (int i = tid; i < r; i += nt) {
-    double l = theta[i] > 0.0 ? theta[i] : 0.0;
+    double l = th[i] > 0.f ? (double)th[i] : 0.0;
     double cf = 0.0, ci = 0.0;
     if (!identity) {
       const double fl = r >= dim ? floor : sigma2;
@@ -294,21 +365,23 @@ __global__ __launch_bounds__(kSmallThreads) void finalize_kernel(
       cf = sqrt(sigma2 / l) - 1.0;
       ci = sqrt(l / sigma2) - 1.0;
     }
-    scratch[2 * i] = cf;
-    scratch[2 * i + 1] = ci;
-    c_fwd[i] = (float)cf;
-    c_inv[i] = (float)ci;
-    lam_out[i] = (float)l;
+    coef[2 * i] = cf;
+    coef[2 * i + 1] = ci;
+    M.c_fwd[i] = (float)cf;
+    M.c_inv[i] = (float)ci;
+    M.lam[i] = (float)l;
   }
-  if (tid == 0) sigma2_out[0] = (float)sigma2;
+  if (tid == 0) M.sigma2[0] = (float)sigma2;
   __syncthreads();
+  for (int64_t t = tid; t < (int64_t)k * dim; t += nt) M.Qt[t] = Q[t];
+  for (int64_t t = tid; t < (int64_t)r * dim; t += nt) M.Ut[t] = Q[t];
   for (int64_t t = tid; t < dim * r; t += nt) {
     const int64_t i = t / r;
     const int a = (int)(t % r);
-    const float u = Ut[(int64_t)a * dim + i];
-    U[t] = u;
-    Uc[t] = (float)((double)u * scratch[2 * a]);
-    Uci[t] = (float)((double)u * scratch[2 * a + 1]);
+    const float u = Q[(int64_t)a * dim + i];
+    M.U[t] = u;
+    M.Uc[t] = (float)((double)u * coef[2 * a]);
+    M.Uci[t] = (float)((double)u * coef[2 * a + 1]);
   }
 }
 
@@ -346,15 +419,15 @@ size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 gift_status side_set_identity(gift_ctx *ctx, Side &s) {
   const int64_t nr = s.dim * s.r;
-  hipLaunchKernelGGL(fill_f32_kernel, dim3(grid_for(nr)), dim3(256), 0, ctx->stream, s.U, nr, 0.f);
-  hipLaunchKernelGGL(fill_f32_kernel, dim3(grid_for(nr)), dim3(256), 0, ctx->stream, s.Ut, nr, 0.f);
-  hipLaunchKernelGGL(fill_f32_kernel, dim3(grid_for(nr)), dim3(256), 0, ctx->stream, s.Uc, nr, 0.f);
-  hipLaunchKernelGGL(fill_f32_kernel, dim3(grid_for(nr)), dim3(256), 0, ctx->stream, s.Uci, nr, 0.f);
-  hipLaunchKernelGGL(fill_f32_kernel, dim3(1), dim3(256), 0, ctx->stream, s.c_fwd, (int64_t)s.r, 0.f);
-  hipLaunchKernelGGL(fill_f32_kernel, dim3(1), dim3(256), 0, ctx->stream, s.c_inv, (int64_t)s.r, 0.f);
-  hipLaunchKernelGGL(fill_f32_kernel, dim3(1), dim3(256), 0, ctx->stream, s.lam, (int64_t)s.r, 0.f);
+  float *bufs[4] = {s.U, s.Ut, s.Uc, s.Uci};
+  for (float *b : bufs)
+    hipLaunchKernelGGL(fill_f32_kernel, dim3(grid_for(nr)), dim3(256), 0, ctx->stream, b, nr, 0.f);
+  float *small[3] = {s.c_fwd, s.c_inv, s.lam};
+  for (float *b : small)
+    hipLaunchKernelGGL(fill_f32_kernel, dim3(1), dim3(256), 0, ctx->stream, b, (int64_t)s.r, 0.f);
   hipLaunchKernelGGL(fill_f32_kernel, dim3(1), dim3(64), 0, ctx->stream, s.sigma2, (int64_t)1, 0.f);
   s.have_basis = false;
+  s.fill_tail = false;
   return check_launch("side_set_identity");
 }
 
@@ -366,7 +439,7 @@ gift_status side_import(gift_ctx *ctx, Side &s, const float *U, const float *c_f
   GIFT_HIP_TRY(hipMemcpyAsync(s.sigma2, sigma2, sizeof(float), hipMemcpyDeviceToDevice, ctx->stream));
   hipLaunchKernelGGL(import_layouts_kernel, dim3(grid_for(s.dim * s.r)), dim3(256), 0, ctx->stream,
                      U, c_fwd, c_inv, s.dim, s.r, s.Ut, s.U, s.Uc, s.Uci);
-  // warm start of the next refresh: U's rows, then fresh start-block rows
+  // warm start of the next refresh: U's rows, then start-block rows
   GIFT_HIP_TRY(hipMemcpyAsync(s.Qt, s.Ut, sizeof(float) * s.dim * s.r, hipMemcpyDeviceToDevice,
                               ctx->stream));
   s.have_basis = true;
@@ -385,14 +458,16 @@ gift_status side_export(gift_ctx *ctx, const Side &s, float *U, float *c_fwd, fl
   return GIFT_OK;
 }
 
-// One side's refresh.  x: [T, dim] activations (input side) or output
-// gradients (output side).
-gift_status factor_refresh_side(gift_ctx *ctx, gift_factor *f, Side &s, const void *x,
-                                int64_t T, gift_dtype dtype, int32_t iters, uint64_t seed) {
-  if (s.r == 0) return GIFT_OK;
-  const int64_t dim = s.dim;
-  const int k = s.k, r = s.r;
-  const int ks = (int)((dim + 255) / 256);  // split-K factor of the k x k products
+// Refresh a group of sides with equal (dim, r): one launch sequence for all.
+static gift_status refresh_group(gift_ctx *ctx, const std::vector<SideJob> &jobs, int64_t T,
+                                 gift_dtype dtype, int32_t iters) {
+  const int G = (int)jobs.size();
+  const Side &s0 = *jobs[0].side;
+  const int64_t dim = s0.dim;
+  const int k = s0.k, r = s0.r;
+  const int ks = (int)((dim + 255) / 256);   // split-K factor of the k x k products
+  const bool lds = k <= kLdsK;
+  const bool bf16_direct = dtype == GIFT_BF16 && dim % 8 == 0;
   // workspace carve-up
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -400,171 +475,233 @@ gift_status factor_refresh_side(gift_ctx *ctx, gift_factor *f, Side &s, const vo
     off += align256(bytes);
     return o;
   };
-  const size_t o_A = take(sizeof(float) * dim * dim);
-  const size_t o_X = dtype == GIFT_BF16 ? take(sizeof(float) * T * dim) : 0;
-  const size_t o_Y = take(sizeof(float) * (size_t)k * dim);
-  const size_t o_P = take(sizeof(float) * (size_t)ks * k * k);
-  const size_t o_R = take(sizeof(float) * (size_t)k * k);
-  const size_t o_W = take(sizeof(double) * (size_t)k * k);
-  const size_t o_X2 = take(sizeof(double) * (size_t)k * k);
-  const size_t o_th = take(sizeof(double) * (size_t)k);
-  const size_t o_nm = take(sizeof(double) * (size_t)k);
-  const size_t o_V = take(sizeof(float) * (size_t)k * r);
-  const size_t o_sc = take(sizeof(double) * 2 * (size_t)r);
+  const size_t o_tab = take(sizeof(Member) * G);
+  const size_t o_xt = take(sizeof(void *) * G);
+  const size_t o_A = take(sizeof(float) * G * dim * dim);
+  const size_t o_X = (dtype == GIFT_BF16 && !bf16_direct) ? take(sizeof(float) * T * dim) : 0;
+  const size_t o_Q = take(sizeof(float) * G * (size_t)k * dim);
+  const size_t o_Y = take(sizeof(float) * G * (size_t)k * dim);
+  const size_t o_P = take(sizeof(float) * G * (size_t)ks * k * k);
+  const size_t o_R = take(sizeof(float) * G * (size_t)k * k);
+  const size_t o_V = take(sizeof(float) * G * (size_t)k * k);
+  const size_t o_th = take(sizeof(float) * G * (size_t)k);
+  const size_t o_W = lds ? 0 : take(sizeof(double) * G * (size_t)k * k);
+  const size_t o_x2 = lds ? 0 : take(sizeof(double) * G * (size_t)k);
   void *base = nullptr;
   gift_status st = workspace(ctx, off, &base);
   if (st != GIFT_OK) return st;
   char *b = static_cast<char *>(base);
+  Member *tab = reinterpret_cast<Member *>(b + o_tab);
+  const void **xtab = reinterpret_cast<const void **>(b + o_xt);
   float *Amat = reinterpret_cast<float *>(b + o_A);
+  float *Qw = reinterpret_cast<float *>(b + o_Q);
   float *Y = reinterpret_cast<float *>(b + o_Y);
   float *part = reinterpret_cast<float *>(b + o_P);
   float *Rinv = reinterpret_cast<float *>(b + o_R);
-  double *W = reinterpret_cast<double *>(b + o_W);
-  double *X2 = reinterpret_cast<double *>(b + o_X2);
-  double *theta = reinterpret_cast<double *>(b + o_th);
-  double *norms = reinterpret_cast<double *>(b + o_nm);
-  float *Vr = reinterpret_cast<float *>(b + o_V);
-  double *sc = reinterpret_cast<double *>(b + o_sc);
+  float *V = reinterpret_cast<float *>(b + o_V);
+  float *theta = reinterpret_cast<float *>(b + o_th);
+  double *Wg = lds ? nullptr : reinterpret_cast<double *>(b + o_W);
+  double *x2 = lds ? nullptr : reinterpret_cast<double *>(b + o_x2);
   hipStream_t stream = ctx->stream;
 
-  // 1. statistics A = X^T X / T
-  const float *X32 = static_cast<const float *>(x);
-  if (dtype == GIFT_BF16) {
-    float *Xc = reinterpret_cast<float *>(b + o_X);
-    {
-      ProfileScope prof(ctx, GIFT_KERNEL_SYRK);
-      hipLaunchKernelGGL(bf16_to_f32_kernel, dim3(grid_for(T * dim)), dim3(256), 0, stream, Xc,
-                         static_cast<const uint16_t *>(x), T * dim);
-    }
-    if ((st = check_launch("bf16_to_f32_kernel")) != GIFT_OK) return st;
-    X32 = Xc;
+  // member table (copied from pageable host memory: staged before returning)
+  std::vector<Member> host(G);
+  std::vector<const void *> xs(G);
+  bool any_cold = false;
+  for (int g = 0; g < G; ++g) {
+    const Side &s = *jobs[g].side;
+    Member &M = host[g];
+    M.Qt = s.Qt;
+    M.Ut = s.Ut;
+    M.U = s.U;
+    M.Uc = s.Uc;
+    M.Uci = s.Uci;
+    M.c_fwd = s.c_fwd;
+    M.c_inv = s.c_inv;
+    M.lam = s.lam;
+    M.sigma2 = s.sigma2;
+    M.seed_lo = (uint32_t)(jobs[g].seed & 0xffffffffu);
+    M.seed_hi = (uint32_t)(jobs[g].seed >> 32);
+    M.mode = !s.have_basis ? 0 : (s.fill_tail ? 2 : 1);
+    M.damping = jobs[g].damping;
+    any_cold = any_cold || M.mode != 1;
+    xs[g] = jobs[g].x;
   }
+  GIFT_HIP_TRY(hipMemcpyAsync(tab, host.data(), sizeof(Member) * G, hipMemcpyHostToDevice, stream));
+  GIFT_HIP_TRY(hipMemcpyAsync(xtab, xs.data(), sizeof(void *) * G, hipMemcpyHostToDevice, stream));
+
+  // 1. statistics A_g = X_g^T X_g / T
+  const float inv_T = (float)(1.0 / (double)T);
+  if (bf16_direct) {
+    if ((st = launch_syrk_bf16(ctx, reinterpret_cast<const uint16_t *const *>(xtab), G, T, dim,
+                               inv_T, Amat)) != GIFT_OK)
+      return st;
+  } else {
+    for (int g = 0; g < G; ++g) {
+      const float *X32 = static_cast<const float *>(jobs[g].x);
+      if (dtype == GIFT_BF16) {
+        float *Xc = reinterpret_cast<float *>(b + o_X);
+        {
+          ProfileScope prof(ctx, GIFT_KERNEL_SYRK);
+          hipLaunchKernelGGL(bf16_to_f32_kernel, dim3(grid_for(T * dim)), dim3(256), 0, stream, Xc,
+                             static_cast<const uint16_t *>(jobs[g].x), T * dim);
+        }
+        if ((st = check_launch("bf16_to_f32_kernel")) != GIFT_OK) return st;
+        X32 = Xc;
+      }
+      TileJob j;
+      j.nseg = 1;
+      j.seg[0].a = Operand{X32, dim, 0, false};   // (i, t) = X[t][i]
+      j.seg[0].b = Operand{X32, dim, 0, false};   // (t, j) = X[t][j]
+      j.seg[0].K = T;
+      j.M = dim;
+      j.N = dim;
+      j.C = Amat + (int64_t)g * dim * dim;
+      j.ldc = dim;
+      j.alpha = inv_T;
+      j.kernel_family = GIFT_KERNEL_SYRK;
+      if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
+    }
+  }
+
+  // 2. start blocks
   {
-    TileJob j;
-    j.nseg = 1;
-    j.seg[0].a = Operand{X32, dim, 0, false};   // (i, t) = X[t][i]
-    j.seg[0].b = Operand{X32, dim, 0, false};   // (t, j) = X[t][j]
-    j.seg[0].K = T;
-    j.M = dim;
-    j.N = dim;
-    j.C = Amat;
-    j.ldc = dim;
-    j.alpha = (float)(1.0 / (double)T);
-    j.kernel_family = GIFT_KERNEL_SYRK;
-    if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
+    ProfileScope prof(ctx, GIFT_KERNEL_FACTOR);
+    hipLaunchKernelGGL(gather_start_kernel, dim3(grid_for((int64_t)k * dim, 256, 2048), G), dim3(256),
+                       0, stream, tab, Qw, dim, k, r);
   }
+  if ((st = check_launch("gather_start_kernel")) != GIFT_OK) return st;
 
-  // 2. start block (cold), or the imported basis completed with start rows
-  if (!s.have_basis || s.fill_tail) {
-    const int row0 = s.have_basis ? r : 0;
-    if (row0 < k) {
-      ProfileScope prof(ctx, GIFT_KERNEL_FACTOR);
-      hipLaunchKernelGGL(start_block_kernel, dim3(grid_for((int64_t)(k - row0) * dim)), dim3(256),
-                         0, stream, s.Qt, dim, k, row0, (uint32_t)(seed & 0xffffffffu),
-                         (uint32_t)(seed >> 32));
-    }
-    if ((st = check_launch("start_block_kernel")) != GIFT_OK) return st;
-    s.fill_tail = false;
-  }
-
-  // Gram / projected-matrix partials: part[z] = Lt_z Rt_z^T over K slice z
+  const int64_t kd = (int64_t)k * dim, k2 = (int64_t)k * k;
+  // part[g][z] = Lt_g Rt_g^T over K slice z
   auto kk_product = [&](const float *Lt, const float *Rt) -> gift_status {
     TileJob j;
     j.nseg = 1;
-    j.seg[0].a = Operand{Lt, dim, 0, true};
-    j.seg[0].b = Operand{Rt, dim, 0, true};
+    j.seg[0].a = Operand{Lt, dim, kd, true};
+    j.seg[0].b = Operand{Rt, dim, kd, true};
     j.seg[0].K = dim;
     j.M = k;
     j.N = k;
+    j.batch = G;
     j.ksplit = ks;
     j.C = part;
     j.ldc = k;
-    j.cbs = (int64_t)k * k;
+    j.cbs = k2;
     j.kernel_family = GIFT_KERNEL_FACTOR;
     return launch_tile(ctx, j);
   };
-  // Qt <- Rinv^T Src  (Q = Y R^-1)
-  auto apply_rinv = [&](const float *Src) -> gift_status {
+  // Qw <- Rinv^T Y  (Q = Y R^-1)
+  auto apply_rinv = [&]() -> gift_status {
     TileJob j;
     j.nseg = 1;
-    j.seg[0].a = Operand{Rinv, k, 0, false};   // (a, c) = Rinv[c][a]
-    j.seg[0].b = Operand{Src, dim, 0, false};  // (c, i) = Src[c][i]
+    j.seg[0].a = Operand{Rinv, k, k2, false};   // (a, c) = Rinv[c][a]
+    j.seg[0].b = Operand{Y, dim, kd, false};    // (c, i) = Y[c][i]
     j.seg[0].K = k;
     j.M = k;
     j.N = dim;
-    j.C = s.Qt;
+    j.batch = G;
+    j.C = Qw;
     j.ldc = dim;
+    j.cbs = kd;
     j.kernel_family = GIFT_KERNEL_FACTOR;
     return launch_tile(ctx, j);
   };
-  auto cholqr_pass = [&](const float *Src) -> gift_status {
-    gift_status e = kk_product(Src, Src);
+  auto cholqr_pass = [&]() -> gift_status {
+    gift_status e = kk_product(Y, Y);
     if (e != GIFT_OK) return e;
     {
       ProfileScope prof(ctx, GIFT_KERNEL_FACTOR);
-      hipLaunchKernelGGL(chol_inv_kernel, dim3(1), dim3(kSmallThreads), 0, stream, part, ks, k, W,
-                         X2, Rinv);
+      if (lds)
+        hipLaunchKernelGGL(chol_inv_lds_kernel, dim3(G), dim3(kSmallThreads), 0, stream, part, ks, k, Rinv);
+      else
+        hipLaunchKernelGGL(chol_inv_global_kernel, dim3(G), dim3(kSmallThreads), 0, stream, part, ks, k,
+                           Wg, x2, Rinv);
     }
     if ((e = check_launch("chol_inv_kernel")) != GIFT_OK) return e;
-    return apply_rinv(Src);
+    return apply_rinv();
   };
-  // Yt = Qt A (A symmetric, so (c, i) = A[i][c] reads K-major)
+  // CholQR2 of Y into Qw
+  auto cholqr2 = [&]() -> gift_status {
+    gift_status e = cholqr_pass();
+    if (e != GIFT_OK) return e;
+    GIFT_HIP_TRY(hipMemcpyAsync(Y, Qw, sizeof(float) * G * kd, hipMemcpyDeviceToDevice, stream));
+    return cholqr_pass();
+  };
+  // Y_g = Qw_g A_g  (A symmetric, so (c, i) = A[i][c] reads K-major)
   auto times_A = [&]() -> gift_status {
     TileJob j;
     j.nseg = 1;
-    j.seg[0].a = Operand{s.Qt, dim, 0, true};
-    j.seg[0].b = Operand{Amat, dim, 0, true};
+    j.seg[0].a = Operand{Qw, dim, kd, true};
+    j.seg[0].b = Operand{Amat, dim, dim * dim, true};
     j.seg[0].K = dim;
     j.M = k;
     j.N = dim;
+    j.batch = G;
     j.C = Y;
     j.ldc = dim;
+    j.cbs = kd;
     j.kernel_family = GIFT_KERNEL_FACTOR;
     return launch_tile(ctx, j);
   };
 
-  // CholQR2 of Y into Qt: two passes, each reading Y and writing Qt
-  auto cholqr2 = [&]() -> gift_status {
-    gift_status e = cholqr_pass(Y);
-    if (e != GIFT_OK) return e;
-    GIFT_HIP_TRY(hipMemcpyAsync(Y, s.Qt, sizeof(float) * k * dim, hipMemcpyDeviceToDevice, stream));
-    return cholqr_pass(Y);
-  };
-  GIFT_HIP_TRY(hipMemcpyAsync(Y, s.Qt, sizeof(float) * k * dim, hipMemcpyDeviceToDevice, stream));
-  if ((st = cholqr2()) != GIFT_OK) return st;
+  if (any_cold) {
+    GIFT_HIP_TRY(hipMemcpyAsync(Y, Qw, sizeof(float) * G * kd, hipMemcpyDeviceToDevice, stream));
+    if ((st = cholqr2()) != GIFT_OK) return st;
+  }
   for (int it = 0; it < iters; ++it) {
     if ((st = times_A()) != GIFT_OK) return st;
     if ((st = cholqr2()) != GIFT_OK) return st;
   }
-  // Rayleigh-Ritz
+  // Rayleigh-Ritz: B = Qw A Qw^T, eigenpairs, rotated basis V^T Qw -> Y
   if ((st = times_A()) != GIFT_OK) return st;
-  if ((st = kk_product(s.Qt, Y)) != GIFT_OK) return st;
+  if ((st = kk_product(Qw, Y)) != GIFT_OK) return st;
   {
     ProfileScope prof(ctx, GIFT_KERNEL_FACTOR);
-    hipLaunchKernelGGL(rr_eig_kernel, dim3(1), dim3(kSmallThreads), 0, stream, part, ks, k, r, W,
-                       norms, theta, Vr, 30);
+    if (lds)
+      hipLaunchKernelGGL(rr_eig_lds_kernel, dim3(G), dim3(kSmallThreads), 0, stream, part, ks, k, V,
+                         theta, 40);
+    else
+      hipLaunchKernelGGL(rr_eig_global_kernel, dim3(G), dim3(kSmallThreads), 0, stream, part, ks, k,
+                         Wg, x2, V, theta, 40);
   }
   if ((st = check_launch("rr_eig_kernel")) != GIFT_OK) return st;
   {
-    TileJob j;  // Ut = Vr^T Qt
+    TileJob j;  // Y = V^T Qw
     j.nseg = 1;
-    j.seg[0].a = Operand{Vr, r, 0, false};     // (a, c) = Vr[c][a]
-    j.seg[0].b = Operand{s.Qt, dim, 0, false}; // (c, i) = Qt[c][i]
+    j.seg[0].a = Operand{V, k, k2, false};     // (a, c) = V[c][a]
+    j.seg[0].b = Operand{Qw, dim, kd, false};  // (c, i) = Qw[c][i]
     j.seg[0].K = k;
-    j.M = r;
+    j.M = k;
     j.N = dim;
-    j.C = s.Ut;
+    j.batch = G;
+    j.C = Y;
     j.ldc = dim;
+    j.cbs = kd;
     j.kernel_family = GIFT_KERNEL_FACTOR;
     if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
   }
   {
     ProfileScope prof(ctx, GIFT_KERNEL_FACTOR);
-    hipLaunchKernelGGL(finalize_kernel, dim3(1), dim3(kSmallThreads), 0, stream, Amat, dim, theta, r,
-                       f->damping, s.Ut, s.U, s.Uc, s.Uci, s.c_fwd, s.c_inv, s.lam, s.sigma2, sc);
+    hipLaunchKernelGGL(finalize_kernel, dim3(G), dim3(kSmallThreads), 0, stream, tab, Amat, dim, theta,
+                       k, r, Y);
   }
   if ((st = check_launch("finalize_kernel")) != GIFT_OK) return st;
-  s.have_basis = true;
+  for (const SideJob &jb : jobs) {
+    jb.side->have_basis = true;
+    jb.side->fill_tail = false;
+  }
+  return GIFT_OK;
+}
+
+gift_status factor_refresh_batch(gift_ctx *ctx, const std::vector<SideJob> &jobs, int64_t T,
+                                 gift_dtype dtype, int32_t iters) {
+  std::map<std::pair<int64_t, int>, std::vector<SideJob>> groups;
+  for (const SideJob &j : jobs)
+    if (j.side->r > 0) groups[{j.side->dim, j.side->r}].push_back(j);
+  for (auto &kv : groups) {
+    gift_status st = refresh_group(ctx, kv.second, T, dtype, iters);
+    if (st != GIFT_OK) return st;
+  }
   return GIFT_OK;
 }
 

@@ -12,6 +12,7 @@ from __future__ import annotations
 
 import ctypes
 import os
+import weakref
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libgift.so")
@@ -53,6 +54,7 @@ def _load():
         "gift_factor_create": ([P, I64, I64, I32, I32, F, U64, PP], I32),
         "gift_factor_destroy": ([P], None),
         "gift_factor_update": ([P, P, P, P, I64, I32, I32], I32),
+        "gift_factor_update_batch": ([P, I32, P, P, P, I64, I32, I32], I32),
         "gift_factor_export": ([P, P, I32, P, P, P, P], I32),
         "gift_factor_import": ([P, P, I32, P, P, P, P], I32),
         "gift_encode": ([P, P, P, I32, I64, I64, I32, I32, I32, P, P, P, P], I32),
@@ -109,6 +111,7 @@ class Context:
             import torch
             stream = torch.cuda.current_stream().cuda_stream if torch.cuda.is_available() else 0
         self._h = ctypes.c_void_p()
+        self._factors = weakref.WeakSet()
         _check(LIB.gift_ctx_create(ctypes.c_void_p(int(stream)), ctypes.byref(self._h)))
 
     @property
@@ -132,7 +135,10 @@ class Context:
         _check(LIB.gift_ctx_profile_reset(self._h))
 
     def close(self):
+        """Destroy the context; factors created on it are destroyed first."""
         if self._h:
+            for f in list(self._factors):
+                f.close()
             LIB.gift_ctx_destroy(self._h)
             self._h = ctypes.c_void_p()
 
@@ -150,8 +156,11 @@ class Factor:
                  damping: float = 1e-6, seed: int = 0):
         self.ctx, self.m, self.n, self.rank, self.sides = ctx, m, n, rank, sides
         self._h = ctypes.c_void_p()
+        if not ctx.handle:
+            raise GiftError(EINVAL, "the context is closed")
         _check(LIB.gift_factor_create(ctx.handle, m, n, rank, sides, damping, seed,
                                       ctypes.byref(self._h)))
+        ctx._factors.add(self)
 
     @property
     def handle(self):
@@ -204,6 +213,42 @@ class Factor:
             self.close()
         except Exception:
             pass
+
+
+def _stats_dtype(x):
+    import torch
+    if x.dtype == torch.float32:
+        return F32
+    if x.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError("statistics inputs must be float32 or bfloat16")
+
+
+def factor_update_batch(ctx: Context, factors, acts=None, out_grads=None, iters: int = 4):
+    """``gift_factor_update_batch``: refresh many factors in one launch sequence.
+
+    ``acts`` / ``out_grads`` are lists (one entry per factor, ``None`` where a
+    factor lacks that side) of [T, dim] tensors with a common T and dtype.
+    """
+    count = len(factors)
+    if count == 0:
+        return
+    acts = list(acts) if acts is not None else [None] * count
+    out_grads = list(out_grads) if out_grads is not None else [None] * count
+    if len(acts) != count or len(out_grads) != count:
+        raise ValueError("acts / out_grads must have one entry per factor")
+    tensors = [x for x in acts + out_grads if x is not None]
+    if not tensors:
+        raise ValueError("factor_update_batch needs statistics inputs")
+    T, dt = tensors[0].shape[0], _stats_dtype(tensors[0])
+    for x in tensors:
+        if x.dim() != 2 or x.shape[0] != T or _stats_dtype(x) != dt:
+            raise ValueError("statistics inputs must be [T, dim] with a common T and dtype")
+    arr = ctypes.c_void_p * count
+    fa = arr(*[f.handle.value for f in factors])
+    aa = arr(*[(_ptr(x).value if x is not None else None) for x in acts])
+    ga = arr(*[(_ptr(x).value if x is not None else None) for x in out_grads])
+    _check(LIB.gift_factor_update_batch(ctx.handle, count, fa, aa, ga, T, dt, iters))
 
 
 def encode(ctx: Context, factor, grads, codes, scales, block_rows: int = 0, block_cols: int = 0,

@@ -131,3 +131,30 @@ def test_export_import_round_trip_and_errors(ctx):
         f.export(gift.SIDE_OUTPUT)
     f.close()
     g.close()
+
+
+def test_batch_equals_single_updates(ctx):
+    say("batch refresh == single refreshes")
+    T = 1024
+    shapes = [(64, 96, 8, gift.SIDE_INPUT), (96, 64, 8, gift.SIDE_BOTH), (48, 96, 8, gift.SIDE_OUTPUT),
+              (96, 96, 4, gift.SIDE_INPUT)]
+    xs = {d: t(bf16_round(factor_inputs(300 + d, T, d)[0])).to(torch.bfloat16) for d in (48, 64, 96)}
+    batch, single = [], []
+    for i, (m, n, r, sides) in enumerate(shapes):
+        batch.append(gift.Factor(ctx, m, n, r, sides, seed=10 + i))
+        single.append(gift.Factor(ctx, m, n, r, sides, seed=10 + i))
+    acts = [xs[n] if s & gift.SIDE_INPUT else None for (m, n, r, s) in shapes]
+    dgr = [xs[m] if s & gift.SIDE_OUTPUT else None for (m, n, r, s) in shapes]
+    for rep in range(2):   # cold, then warm
+        gift.factor_update_batch(ctx, batch, acts, dgr, iters=3)
+        for f, a, d in zip(single, acts, dgr):
+            f.update(acts=a, out_grads=d, iters=3)
+        torch.cuda.synchronize()
+        for (m, n, r, s), fb, fs in zip(shapes, batch, single):
+            for side in (gift.SIDE_INPUT, gift.SIDE_OUTPUT):
+                if s & side:
+                    a, b = exported(fb, side), exported(fs, side)
+                    np.testing.assert_array_equal(a.U, b.U)
+                    np.testing.assert_array_equal(a.c_fwd, b.c_fwd)
+    for f in batch + single:
+        f.close()
