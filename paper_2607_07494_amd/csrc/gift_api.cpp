@@ -520,19 +520,22 @@ gift_status gift_encode(gift_ctx *ctx, const gift_factor *f, const float *grads,
     return set_error(GIFT_ESHAPE, "gift_encode: factor was created for another shape");
   if ((st = bind_device(ctx)) != GIFT_OK) return st;
   const BlockGeom g = block_geom(m, n, block_rows, block_cols);
-  const size_t amax_bytes = a256(sizeof(uint32_t) * (size_t)N * g.nbr * g.nbc);
+  const int64_t nblk = (int64_t)g.nbr * g.nbc;
+  const size_t raw_bytes = a256(sizeof(uint32_t) * (size_t)N * nblk * kAmaxSlots);
+  const size_t fin_bytes = a256(sizeof(uint32_t) * (size_t)N * nblk);
   LowRankPlan plan;
   size_t proj_bytes = 0;
   if (f && (st = plan_low_rank(ctx, f, grads, N, m, n, false, nullptr, &proj_bytes, &plan)) != GIFT_OK)
     return st;
   void *ws = nullptr;
-  if ((st = workspace(ctx, amax_bytes + proj_bytes, &ws)) != GIFT_OK) return st;
-  uint32_t *amax = static_cast<uint32_t *>(ws);
-  if ((st = launch_zero_u32(ctx, amax, (int64_t)N * g.nbr * g.nbc)) != GIFT_OK) return st;
+  if ((st = workspace(ctx, raw_bytes + fin_bytes + proj_bytes, &ws)) != GIFT_OK) return st;
+  uint32_t *amax_raw = static_cast<uint32_t *>(ws);
+  uint32_t *amax_fin = reinterpret_cast<uint32_t *>(static_cast<char *>(ws) + raw_bytes);
+  if ((st = launch_zero_u32(ctx, amax_raw, (int64_t)N * nblk * kAmaxSlots)) != GIFT_OK) return st;
   TileJob job;
   if (f) {
-    if ((st = plan_low_rank(ctx, f, grads, N, m, n, false, static_cast<char *>(ws) + amax_bytes,
-                            &proj_bytes, &plan)) != GIFT_OK)
+    if ((st = plan_low_rank(ctx, f, grads, N, m, n, false,
+                            static_cast<char *>(ws) + raw_bytes + fin_bytes, &proj_bytes, &plan)) != GIFT_OK)
       return st;
     if (plan.active) job = plan.upd;
   }
@@ -542,7 +545,7 @@ gift_status gift_encode(gift_ctx *ctx, const gift_factor *f, const float *grads,
   job.D = grads;
   job.ldd = n;
   job.dbs = m * n;
-  job.amax = amax;
+  job.amax = amax_raw;
   job.geom = g;
   job.shared = mode == GIFT_SCALE_SHARED;
   job.ef = ef;
@@ -551,6 +554,10 @@ gift_status gift_encode(gift_ctx *ctx, const gift_factor *f, const float *grads,
   job.transformed = transformed;
   job.kernel_family = gemm ? GIFT_KERNEL_UPDATE_AMAX : GIFT_KERNEL_AMAX;
   if ((st = launch_tile(ctx, job)) != GIFT_OK) return st;
+  // max over the sub-slots (and the ranks for a shared scale) and the scales
+  if ((st = launch_finalize_amax(ctx, amax_raw, N, nblk, job.shared, amax_fin, scales)) != GIFT_OK)
+    return st;
+  job.amax = amax_fin;
   job.transformed = nullptr;
   job.codes = codes;
   job.kernel_family = gemm ? GIFT_KERNEL_UPDATE_QUANT : GIFT_KERNEL_QUANT;

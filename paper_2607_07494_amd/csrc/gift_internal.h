@@ -131,6 +131,12 @@ struct Segment {
 
 enum Epilogue { EPI_STORE = 0, EPI_AMAX = 1, EPI_QUANT = 2 };
 
+// Block maxima are accumulated with atomicMax into kAmaxSlots sub-slots per
+// (rank, block) -- producers pick a slot from their wave id, so no single
+// address sees more than a few atomics -- and finalize_amax reduces the slots
+// (and the ranks, for a shared scale) into one value per (rank, block).
+constexpr int kAmaxSlots = 64;
+
 struct TileJob {
   // C = sum_s A_s B_s over up to two segments (nseg = 0: no product)
   Segment seg[2];
@@ -146,7 +152,9 @@ struct TileJob {
   float alpha = 1.f, beta = 0.f;
   const float *colscale = nullptr;
   // codec epilogues (W~ = D + acc [+ R]); matrices are [batch, M, N] dense
-  uint32_t *amax = nullptr;     // [batch, nbr, nbc] float bits
+  // amax: AMAX pass -> raw slots [batch, nbr, nbc, kAmaxSlots] (atomicMax of
+  //       float bits); QUANT pass -> finished values [batch, nbr, nbc]
+  uint32_t *amax = nullptr;
   uint8_t *codes = nullptr;
   float *scales = nullptr;
   float *transformed = nullptr;
@@ -157,7 +165,23 @@ struct TileJob {
 };
 
 gift_status launch_tile(gift_ctx *ctx, const TileJob &job);
+// k_update.hip: register-direct rank-r update / projection (used by
+// launch_tile when the job's shapes allow)
+bool update_kernel_eligible(const TileJob &job);
+gift_status launch_update(gift_ctx *ctx, const TileJob &job);
+bool proj_kernel_eligible(const TileJob &job);
+// k_stream.hip: streaming Euclidean amax / quantize and rank sum
+bool stream_eligible(int64_t m, int64_t n, const BlockGeom &g, const void *x, const void *codes,
+                     const void *a, const void *b);
+gift_status launch_stream_codec(gift_ctx *ctx, const TileJob &job);
+gift_status launch_stream_reduce(gift_ctx *ctx, const uint8_t *codes, const float *scales, int32_t N,
+                                 int64_t m, int64_t n, BlockGeom g, float *mean);
+gift_status launch_proj(gift_ctx *ctx, const TileJob &job);
 gift_status launch_zero_u32(gift_ctx *ctx, uint32_t *p, int64_t count);
+// raw [N, nblk, kAmaxSlots] -> final [N, nblk] (max over slots, and over ranks
+// when shared) and scales s = amax / 448
+gift_status launch_finalize_amax(gift_ctx *ctx, const uint32_t *raw, int32_t N, int64_t nblk,
+                                 bool shared, uint32_t *final_amax, float *scales);
 gift_status launch_reduce(gift_ctx *ctx, const uint8_t *codes, const float *scales,
                           int32_t N, int64_t m, int64_t n, BlockGeom g, float *mean);
 gift_status launch_copy_f32(gift_ctx *ctx, float *dst, const float *src, int64_t count);

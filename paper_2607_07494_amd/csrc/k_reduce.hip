@@ -106,6 +106,8 @@ __global__ __launch_bounds__(kThreads) void reduce_kernel(const RArgs p) {
 gift_status launch_reduce(gift_ctx *ctx, const uint8_t *codes, const float *scales, int32_t N,
                           int64_t m, int64_t n, BlockGeom g, float *mean) {
   if (m <= 0 || n <= 0) return GIFT_OK;
+  if (stream_eligible(m, n, g, mean, codes, nullptr, nullptr))
+    return launch_stream_reduce(ctx, codes, scales, N, m, n, g, mean);
   RArgs a;
   a.codes = codes;
   a.scales = scales;

@@ -29,7 +29,6 @@ namespace {
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
-constexpr int kBK = 32;        // K slice staged per LDS round
 constexpr int kKPad = 4;       // LDS row padding (floats)
 constexpr int kMaxLocalBlocks = 256;
 
@@ -66,7 +65,7 @@ struct KArgs {
   int vec_out;  // 16-byte epilogue access allowed
 };
 
-template <int ROWS, bool KMAJOR>
+template <int ROWS, bool KMAJOR, int kBK>
 struct TileLoader {
   // float4 slots of one ROWS x kBK slice
   static constexpr int kSlots = ROWS * kBK / 4;
@@ -137,7 +136,7 @@ struct TileLoader {
   }
 };
 
-template <int BM, int BN>
+template <int BM, int BN, int kBK>
 struct Smem {
   static constexpr int kAB = (BM + BN) * (kBK + kKPad);
   static constexpr int kC = BM * (BN + 4);
@@ -160,13 +159,13 @@ struct LocalBlocks {
   }
 };
 
-template <int BM, int BN, int WM, int WN, bool AK, bool BKM, bool GEMM, int EPI>
+template <int BM, int BN, int WM, int WN, bool AK, bool BKM, bool GEMM, int EPI, int kBK>
 __global__ __launch_bounds__(kThreads) void tile_kernel(const KArgs p) {
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int TI = WTM / 16, TJ = WTN / 16;
   static_assert(WM * WN == 4, "four waves per workgroup");
   static_assert(TI >= 1 && TJ >= 1, "wave tile must hold whole 16x16 MFMA tiles");
-  constexpr int kSmemFloats = GEMM ? Smem<BM, BN>::kFloats : 4;
+  constexpr int kSmemFloats = GEMM ? Smem<BM, BN, kBK>::kFloats : 4;
   __shared__ __attribute__((aligned(16))) float smem[kSmemFloats];
   __shared__ uint32_t lds_amax[kMaxLocalBlocks];
   __shared__ float lds_inv[kMaxLocalBlocks];
@@ -180,6 +179,7 @@ __global__ __launch_bounds__(kThreads) void tile_kernel(const KArgs p) {
   const int64_t j0 = (int64_t)blockIdx.x * BN;
   const int64_t i1 = i0 + BM < p.M ? i0 + BM : p.M;
   const int64_t j1 = j0 + BN < p.N ? j0 + BN : p.N;
+  const int slot = (int)((blockIdx.y * gridDim.x + blockIdx.x) % kAmaxSlots);
 
   LocalBlocks lb;
   if (EPI != EPI_STORE) {
@@ -190,25 +190,52 @@ __global__ __launch_bounds__(kThreads) void tile_kernel(const KArgs p) {
       if (EPI == EPI_AMAX) {
         if (l < kMaxLocalBlocks) lds_amax[l] = 0u;
       } else {
-        float a;
-        if (p.shared) {
-          uint32_t m = 0u;
-          for (int r = 0; r < p.batch; ++r) {
-            const uint32_t v = p.amax[r * nblk + bi * p.nbc + bj];
-            m = v > m ? v : m;
-          }
-          a = __uint_as_float(m);
-        } else {
-          a = __uint_as_float(p.amax[b * nblk + bi * p.nbc + bj]);
-        }
-        const float s = e4m3_scale(a);
+        const float a = __uint_as_float(p.amax[b * nblk + bi * p.nbc + bj]);
         if (l < kMaxLocalBlocks) {
           lds_inv[l] = e4m3_multiplier(a);
-          lds_scale[l] = s;
+          lds_scale[l] = e4m3_scale(a);
         }
-        // the tile holding the block's first element writes its scale
-        const int64_t oi = bi * p.br, oj = bj * p.bc;
-        if (oi >= i0 && oi < i1 && oj >= j0 && oj < j1) p.scales[b * nblk + bi * p.nbc + bj] = s;
+      }
+    }
+  }
+
+  // Codec epilogue operands (W, residual) are fetched before the product so
+  // their memory latency overlaps it.  Lane mapping: row tid / TPR of each
+  // pass, four 4-wide column chunks interleaved across the lanes of a row.
+  constexpr int TPR = BN / 16;                   // lanes per tile row
+  constexpr int RPP = kThreads / TPR;            // rows per pass
+  constexpr int NPASS = (BM + RPP - 1) / RPP;
+  const int64_t MN = p.M * p.N;
+  float4 dpre[NPASS][4], rpre[NPASS][4];
+  if (EPI != EPI_STORE) {
+#pragma unroll
+    for (int ps = 0; ps < NPASS; ++ps) {
+      const int row_l = ps * RPP + tid / TPR;
+      const int64_t gi = i0 + row_l;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int64_t gj = j0 + 4 * (tid % TPR) + (BN / 4) * v;
+        float4 d = make_float4(0.f, 0.f, 0.f, 0.f), rr = d;
+        if (row_l < BM && gi < p.M && gj < p.N) {
+          const int64_t off = (int64_t)b * MN + gi * p.N + gj;
+          if (p.vec_out && gj + 3 < p.N) {
+            d = *reinterpret_cast<const float4 *>(p.D + off);
+            if (p.ef) rr = *reinterpret_cast<const float4 *>(p.ef + off);
+          } else {
+            d.x = p.D[off];
+            d.y = gj + 1 < p.N ? p.D[off + 1] : 0.f;
+            d.z = gj + 2 < p.N ? p.D[off + 2] : 0.f;
+            d.w = gj + 3 < p.N ? p.D[off + 3] : 0.f;
+            if (p.ef) {
+              rr.x = p.ef[off];
+              rr.y = gj + 1 < p.N ? p.ef[off + 1] : 0.f;
+              rr.z = gj + 2 < p.N ? p.ef[off + 2] : 0.f;
+              rr.w = gj + 3 < p.N ? p.ef[off + 3] : 0.f;
+            }
+          }
+        }
+        dpre[ps][v] = d;
+        rpre[ps][v] = rr;
       }
     }
   }
@@ -236,8 +263,8 @@ __global__ __launch_bounds__(kThreads) void tile_kernel(const KArgs p) {
         kend = kbeg + chunk < sg.K ? kbeg + chunk : sg.K;
       }
       if (kbeg >= kend) continue;
-      TileLoader<BM, AK> la;
-      TileLoader<BN, BKM> lbd;
+      TileLoader<BM, AK, kBK> la;
+      TileLoader<BN, BKM, kBK> lbd;
       la.load(sg.a, b, i0, p.M, kbeg, kend, tid);
       lbd.load(sg.b, b, j0, p.N, kbeg, kend, tid);
       for (int64_t k0 = kbeg; k0 < kend; k0 += kBK) {
@@ -260,15 +287,27 @@ __global__ __launch_bounds__(kThreads) void tile_kernel(const KArgs p) {
           for (int tj = 0; tj < TJ; ++tj)
             b4[tj] = *reinterpret_cast<const float4 *>(
                 Bs + (wn * WTN + tj * 16 + fr) * (kBK + kKPad) + kg * 16 + 4 * fg);
+          // independent accumulators back to back, so the matrix pipe overlaps them
 #pragma unroll
           for (int ti = 0; ti < TI; ++ti)
 #pragma unroll
-            for (int tj = 0; tj < TJ; ++tj) {
+            for (int tj = 0; tj < TJ; ++tj)
               acc[ti][tj] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[ti].x, b4[tj].x, acc[ti][tj], 0, 0, 0);
+#pragma unroll
+          for (int ti = 0; ti < TI; ++ti)
+#pragma unroll
+            for (int tj = 0; tj < TJ; ++tj)
               acc[ti][tj] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[ti].y, b4[tj].y, acc[ti][tj], 0, 0, 0);
+#pragma unroll
+          for (int ti = 0; ti < TI; ++ti)
+#pragma unroll
+            for (int tj = 0; tj < TJ; ++tj)
               acc[ti][tj] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[ti].z, b4[tj].z, acc[ti][tj], 0, 0, 0);
+#pragma unroll
+          for (int ti = 0; ti < TI; ++ti)
+#pragma unroll
+            for (int tj = 0; tj < TJ; ++tj)
               acc[ti][tj] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[ti].w, b4[tj].w, acc[ti][tj], 0, 0, 0);
-            }
         }
       }
     }
@@ -288,17 +327,16 @@ __global__ __launch_bounds__(kThreads) void tile_kernel(const KArgs p) {
   // ---------------------------------------------------------------- epilogue
   // Each lane takes four 4-wide column chunks of one row; the chunks of the
   // lanes of one row are interleaved so that a wave's access is contiguous.
-  constexpr int TPR = BN / 16;                   // lanes per tile row
-  constexpr int RPP = kThreads / TPR;            // rows per pass
   const float *Cs = smem;
-  const int64_t MN = p.M * p.N;
   uint32_t run_max = 0u;
   int run_lb = -1;
   int64_t run_gb = -1;
 
-  for (int row_l = tid / TPR; row_l < BM; row_l += RPP) {
+#pragma unroll
+  for (int ps = 0; ps < NPASS; ++ps) {
+    const int row_l = ps * RPP + tid / TPR;
     const int64_t gi = i0 + row_l;
-    if (gi >= p.M) break;
+    if (row_l >= BM || gi >= p.M) break;
     const int q = tid % TPR;
     const int64_t lbi = (EPI != EPI_STORE) ? (gi / p.br - lb.bi0) : 0;
 #pragma unroll
@@ -338,25 +376,16 @@ __global__ __launch_bounds__(kThreads) void tile_kernel(const KArgs p) {
       const int64_t off = (int64_t)b * MN + gi * p.N + gj;
       float w[4];
       // (without a product W~ = W exactly: adding a zero would turn -0 into +0)
-      if (full) {
-        const float4 d = *reinterpret_cast<const float4 *>(p.D + off);
+      {
+        const float4 d = dpre[ps][v];
         if (GEMM) {
           w[0] = d.x + acc4[0]; w[1] = d.y + acc4[1]; w[2] = d.z + acc4[2]; w[3] = d.w + acc4[3];
         } else {
           w[0] = d.x; w[1] = d.y; w[2] = d.z; w[3] = d.w;
         }
         if (p.ef) {
-          const float4 rr = *reinterpret_cast<const float4 *>(p.ef + off);
+          const float4 rr = rpre[ps][v];
           w[0] += rr.x; w[1] += rr.y; w[2] += rr.z; w[3] += rr.w;
-        }
-      } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          w[e] = 0.f;
-          if (gj + e < p.N) {
-            w[e] = GEMM ? p.D[off + e] + acc4[e] : p.D[off + e];
-            if (p.ef) w[e] += p.ef[off + e];
-          }
         }
       }
       if (EPI == EPI_AMAX) {
@@ -378,7 +407,7 @@ __global__ __launch_bounds__(kThreads) void tile_kernel(const KArgs p) {
           if (l != run_lb) {
             if (run_lb >= 0) {
               if (lb.nlb <= kMaxLocalBlocks) atomicMax(&lds_amax[run_lb], run_max);
-              else atomicMax(&p.amax[run_gb], run_max);
+              else atomicMax(&p.amax[run_gb * kAmaxSlots + slot], run_max);
             }
             run_lb = l;
             run_max = 0u;
@@ -399,19 +428,8 @@ __global__ __launch_bounds__(kThreads) void tile_kernel(const KArgs p) {
             inv = lds_inv[l];
             sc = lds_scale[l];
           } else {
-            const int64_t nblk = (int64_t)p.nbr * p.nbc;
             const int64_t gb = (gi / p.br) * p.nbc + (gj + e) / p.bc;
-            float a;
-            if (p.shared) {
-              uint32_t m = 0u;
-              for (int r = 0; r < p.batch; ++r) {
-                const uint32_t t = p.amax[r * nblk + gb];
-                m = t > m ? t : m;
-              }
-              a = __uint_as_float(m);
-            } else {
-              a = __uint_as_float(p.amax[b * nblk + gb]);
-            }
+            const float a = __uint_as_float(p.amax[b * (int64_t)p.nbr * p.nbc + gb]);
             inv = e4m3_multiplier(a);
             sc = e4m3_scale(a);
           }
@@ -444,7 +462,7 @@ __global__ __launch_bounds__(kThreads) void tile_kernel(const KArgs p) {
   if (EPI == EPI_AMAX) {
     if (run_lb >= 0) {
       if (lb.nlb <= kMaxLocalBlocks) atomicMax(&lds_amax[run_lb], run_max);
-      else atomicMax(&p.amax[run_gb], run_max);
+      else atomicMax(&p.amax[run_gb * kAmaxSlots + slot], run_max);
     }
     __syncthreads();
     if (lb.nlb <= kMaxLocalBlocks) {
@@ -452,11 +470,28 @@ __global__ __launch_bounds__(kThreads) void tile_kernel(const KArgs p) {
         const uint32_t v = lds_amax[l];
         if (v != 0u) {
           const int64_t bi = lb.bi0 + l / lb.nlbj, bj = lb.bj0 + l % lb.nlbj;
-          atomicMax(&p.amax[(int64_t)b * p.nbr * p.nbc + bi * p.nbc + bj], v);
+          atomicMax(&p.amax[((int64_t)b * p.nbr * p.nbc + bi * p.nbc + bj) * kAmaxSlots + slot], v);
         }
       }
     }
   }
+}
+
+// One thread per (rank, block): max over the sub-slots (and over the ranks
+// for a shared scale), then the stored scale s = fl32(amax / 448).
+__global__ void finalize_amax_kernel(const uint32_t *raw, int N, int64_t nblk, int shared,
+                                     uint32_t *fin, float *scales) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)N * nblk) return;
+  const int b = (int)(t / nblk);
+  const int64_t blk = t % nblk;
+  uint32_t m = 0u;
+  for (int r = shared ? 0 : b; r < (shared ? N : b + 1); ++r) {
+    const uint32_t *q = raw + ((int64_t)r * nblk + blk) * kAmaxSlots;
+    for (int s = 0; s < kAmaxSlots; ++s) m = q[s] > m ? q[s] : m;
+  }
+  fin[t] = m;
+  scales[t] = e4m3_scale(__uint_as_float(m));
 }
 
 __global__ void zero_u32_kernel(uint32_t *p, int64_t n) {
@@ -521,10 +556,10 @@ KArgs make_args(const TileJob &j) {
   return a;
 }
 
-template <int BM, int BN, int WM, int WN, bool AK, bool BKM, bool GEMM, int EPI>
+template <int BM, int BN, int WM, int WN, bool AK, bool BKM, bool GEMM, int EPI, int BK = 32>
 void launch(const KArgs &a, int zdim, hipStream_t st) {
   dim3 grid((unsigned)((a.N + BN - 1) / BN), (unsigned)((a.M + BM - 1) / BM), (unsigned)zdim);
-  hipLaunchKernelGGL((tile_kernel<BM, BN, WM, WN, AK, BKM, GEMM, EPI>), grid, dim3(kThreads), 0,
+  hipLaunchKernelGGL((tile_kernel<BM, BN, WM, WN, AK, BKM, GEMM, EPI, BK>), grid, dim3(kThreads), 0,
                      st, a);
 }
 
@@ -540,10 +575,17 @@ void launch_layouts(const KArgs &a, bool ak, bool bk, int zdim, hipStream_t st) 
 
 gift_status launch_tile(gift_ctx *ctx, const TileJob &job) {
   if (job.M <= 0 || job.N <= 0 || job.batch <= 0) return GIFT_OK;
+  // register-direct kernels for the rank-r update and the projections
+  if (job.nseg > 0 && (job.amax != nullptr || job.D != nullptr) && update_kernel_eligible(job))
+    return launch_update(ctx, job);
+  if (job.amax == nullptr && job.nseg > 0 && proj_kernel_eligible(job)) return launch_proj(ctx, job);
+  const bool gemm = job.nseg > 0;
+  if (job.amax != nullptr && !gemm &&
+      stream_eligible(job.M, job.N, job.geom, job.D, job.codes, job.ef, job.transformed))
+    return launch_stream_codec(ctx, job);
   KArgs a = make_args(job);
   hipStream_t st = ctx->stream;
   ProfileScope prof(ctx, job.kernel_family);
-  const bool gemm = job.nseg > 0;
   if (job.amax == nullptr) {  // EPI_STORE; split K writes partials [batch][ksplit][M][N]
     if (!gemm) return set_error(GIFT_EINVAL, "internal: store tile without a product");
     const bool ak = job.seg[0].a.kmajor, bk = job.seg[0].b.kmajor;
@@ -575,6 +617,16 @@ gift_status launch_zero_u32(gift_ctx *ctx, uint32_t *ptr, int64_t count) {
   if (blocks > 4096) blocks = 4096;
   hipLaunchKernelGGL(zero_u32_kernel, dim3((unsigned)blocks), dim3(256), 0, ctx->stream, ptr, count);
   return check_launch("zero_u32_kernel");
+}
+
+gift_status launch_finalize_amax(gift_ctx *ctx, const uint32_t *raw, int32_t N, int64_t nblk,
+                                 bool shared, uint32_t *fin, float *scales) {
+  const int64_t total = (int64_t)N * nblk;
+  if (total <= 0) return GIFT_OK;
+  ProfileScope prof(ctx, GIFT_KERNEL_SMALL);
+  hipLaunchKernelGGL(finalize_amax_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, ctx->stream,
+                     raw, N, nblk, shared ? 1 : 0, fin, scales);
+  return check_launch("finalize_amax_kernel");
 }
 
 gift_status launch_copy_f32(gift_ctx *ctx, float *dst, const float *src, int64_t count) {

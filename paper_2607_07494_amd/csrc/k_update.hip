@@ -1,0 +1,533 @@
+// Register-direct FP32 MFMA kernels for the codec's rank-r transform.
+//
+// Both kernels keep every operand in registers: no LDS staging, no barriers
+// in the main loop.  A wave owns a strip of 16 rows of one rank's matrix and
+// computes its block of the product transposed, so that the
+// v_mfma_f32_16x16x4_f32 result puts four consecutive columns of one row in
+// each lane (lane (fr, fg) holds row fr, columns 4fg..4fg+3 of each 16-column
+// group).  Each lane also supplies its MFMA operands as 16-byte vectors: the
+// four k values a lane feeds into four consecutive MFMA steps are four
+// consecutive elements along the contraction index (any assignment of k to
+// (lane group, step) gives the same sum as long as both operands use it).
+//
+// update_kernel: W~ = D + sum_s Row_s Col_s^T over up to two segments with
+//   K_s <= 128 (the rank-r update of the forward and inverse transforms,
+//   Sec. IV-A eq. design_full_transform / design_full_inverse_transform in
+//   low-rank form), fused with
+//     EPI_AMAX   block max |W~| (Algorithm 1's Scale): wave-reduced, one atomic
+//                per wave and block into one of the block's sub-slots;
+//                optional store of W~
+//     EPI_QUANT  E4M3 codes with the finished block scale and the
+//                error-feedback residual R <- W~ - Deq(Q(W~))
+//     EPI_STORE  the inverse transform's output
+// proj_kernel: out[b][i][c] = sum_k X[b][i][k] Y[c][k] (P = W U from U^T),
+//   split over the contraction index across the waves of a workgroup and
+//   reduced through LDS in a fixed order.
+
+#include <type_traits>
+
+#include "fp8_e4m3.h"
+#include "gift_internal.h"
+
+namespace gift {
+namespace {
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+constexpr int kMaxK16 = 8;      // K <= 128 per segment
+constexpr int kColsPerUnit = 256;
+
+struct USeg {
+  const float *row;   // [batch][M][K] (row_bs = 0: shared)
+  int64_t row_ld, row_bs;
+  const float *col;   // [batch][N][K]
+  int64_t col_ld, col_bs;
+  int K;
+};
+
+struct UArgs {
+  USeg seg[2];
+  int nseg;
+  int64_t M, N;
+  int batch;
+  const float *D;       // [batch][M][N]
+  float *C;             // STORE output [batch][M][N]
+  uint32_t *amax;       // [batch][nbr][nbc]
+  uint8_t *codes;
+  float *scales;
+  float *transformed;
+  float *ef;
+  int64_t br, bc;
+  int nbr, nbc;
+  int shared;
+};
+
+__device__ __forceinline__ float4 ld4(const float *p) { return *reinterpret_cast<const float4 *>(p); }
+
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint32_t u = (uint32_t)__shfl_xor((int)v, o);
+    v = u > v ? u : v;
+  }
+  return v;
+}
+
+// finished block amax (sub-slots and ranks already reduced)
+__device__ __forceinline__ float block_amax_value(const UArgs &p, int b, int64_t gb) {
+  return __uint_as_float(p.amax[(int64_t)b * p.nbr * p.nbc + gb]);
+}
+
+// One workgroup = 4 waves = 64 rows (a 16-row strip per wave) x a chunk of
+// kColsPerUnit columns, walked in 64-column tiles.  The column-side operand
+// of a tile (64 columns x K, shared by the 4 waves) is staged in LDS, double
+// buffered: while the waves run the MFMAs of tile c, they hold the global
+// loads of tile c+1's operand and of its W / residual values in registers.
+template <int EPI, bool EF, int NSEG, int K16>
+__global__ __launch_bounds__(kThreads) void update_kernel(const UArgs p) {
+  constexpr int KT = 16 * K16 * NSEG;          // total contraction length
+  constexpr int ROW = KT + 4;                  // LDS row stride (floats)
+  constexpr int SLOTS = 64 * KT / 4;           // float4 slots of one tile
+  constexpr int PER = SLOTS / kThreads;        // per thread (K16*NSEG)
+  __shared__ __attribute__((aligned(16))) float lds[2][64 * ROW];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int fr = lane & 15, fg = lane >> 4;
+  const int b = blockIdx.z;
+  const int64_t i0 = (int64_t)blockIdx.y * 64 + wave * 16;
+  const int64_t ri = i0 + fr;
+  const bool rv = ri < p.M;
+  const bool wave_live = i0 < p.M;
+  const int64_t MN = p.M * p.N;
+  const int64_t c_begin = (int64_t)blockIdx.x * kColsPerUnit;
+  const int slot = (int)((((int64_t)blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x) * 4 + wave) %
+                   kAmaxSlots;
+  const int ntiles = (int)((p.N - c_begin + 63) / 64 < kColsPerUnit / 64 ? (p.N - c_begin + 63) / 64
+                                                                          : kColsPerUnit / 64);
+
+  // row-side operand fragments of the strip, kept for all column tiles
+  float4 bfr[NSEG][K16];
+#pragma unroll
+  for (int s = 0; s < NSEG; ++s)
+#pragma unroll
+    for (int q = 0; q < K16; ++q)
+      bfr[s][q] = rv ? ld4(p.seg[s].row + (int64_t)b * p.seg[s].row_bs + ri * p.seg[s].row_ld + 16 * q + 4 * fg)
+                     : make_float4(0.f, 0.f, 0.f, 0.f);
+
+  // cooperative load of a column tile's operand: slot -> (column, k quad)
+  float4 creg[PER];
+  auto load_cols = [&](int64_t j0) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int slot = tid + u * kThreads;
+      const int col = slot / (KT / 4), kq = slot % (KT / 4);
+      const int s = (4 * kq) / (16 * K16), kk = 4 * kq - s * 16 * K16;
+      const int64_t cj = j0 + col;
+      creg[u] = cj < p.N ? ld4(p.seg[s].col + (int64_t)b * p.seg[s].col_bs + cj * p.seg[s].col_ld + kk)
+                         : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  auto store_cols = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int slot = tid + u * kThreads;
+      const int col = slot / (KT / 4), kq = slot % (KT / 4);
+      *reinterpret_cast<float4 *>(&lds[buf][col * ROW + 4 * kq]) = creg[u];
+    }
+  };
+  float4 d[4], rr[4];
+  auto load_w = [&](int64_t j0) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int64_t cj = j0 + 16 * t + 4 * fg;
+      const bool ok = rv && cj < p.N;
+      const int64_t off = (int64_t)b * MN + ri * p.N + cj;
+      d[t] = ok ? ld4(p.D + off) : make_float4(0.f, 0.f, 0.f, 0.f);
+      if (EF) rr[t] = ok ? ld4(p.ef + off) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+
+  uint32_t run_max = 0u;
+  int64_t run_blk = -1;
+  load_cols(c_begin);
+  load_w(c_begin);
+  store_cols(0);
+  __syncthreads();
+  for (int ct = 0; ct < ntiles; ++ct) {
+    const int buf = ct & 1;
+    const int64_t j0 = c_begin + 64 * ct;
+    const bool more = ct + 1 < ntiles;
+    float4 dcur[4], rcur[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      dcur[t] = d[t];
+      if (EF) rcur[t] = rr[t];
+    }
+    if (more) {
+      load_cols(j0 + 64);
+      load_w(j0 + 64);
+    }
+    floatx4 acc[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < NSEG; ++s)
+#pragma unroll
+      for (int q = 0; q < K16; ++q) {
+        const float4 bb = bfr[s][q];
+        float4 a[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          a[t] = *reinterpret_cast<const float4 *>(
+              &lds[buf][(16 * t + fr) * ROW + s * 16 * K16 + 16 * q + 4 * fg]);
+        // independent accumulators back to back, so the matrix pipe overlaps them
+#pragma unroll
+        for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[t].x, bb.x, acc[t], 0, 0, 0);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[t].y, bb.y, acc[t], 0, 0, 0);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[t].z, bb.z, acc[t], 0, 0, 0);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[t].w, bb.w, acc[t], 0, 0, 0);
+      }
+    if (more) store_cols(buf ^ 1);
+
+    if (wave_live) {
+      // lane holds W~[ri][j0 + 16t + 4fg + v] = d + acc[t][v] (+ residual)
+      float w[4][4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        w[t][0] = dcur[t].x + acc[t][0];
+        w[t][1] = dcur[t].y + acc[t][1];
+        w[t][2] = dcur[t].z + acc[t][2];
+        w[t][3] = dcur[t].w + acc[t][3];
+        if (EF) {
+          w[t][0] += rcur[t].x;
+          w[t][1] += rcur[t].y;
+          w[t][2] += rcur[t].z;
+          w[t][3] += rcur[t].w;
+        }
+      }
+      if (EPI == EPI_STORE) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int64_t cj = j0 + 16 * t + 4 * fg;
+          if (rv && cj < p.N)
+            *reinterpret_cast<float4 *>(p.C + (int64_t)b * MN + ri * p.N + cj) =
+                make_float4(w[t][0], w[t][1], w[t][2], w[t][3]);
+        }
+      } else {
+        // scale-block geometry of this wave tile (wave-uniform, two divisions)
+        const int64_t rlast = (i0 + 15 < p.M ? i0 + 15 : p.M - 1);
+        const int64_t clast = (j0 + 63 < p.N ? j0 + 63 : p.N - 1);
+        const int bi_lo = __builtin_amdgcn_readfirstlane((int)(i0 / p.br));
+        const int bj_lo = __builtin_amdgcn_readfirstlane((int)(j0 / p.bc));
+        const bool uniform = (int64_t)(bi_lo + 1) * p.br > rlast && (int64_t)(bj_lo + 1) * p.bc > clast;
+        const int64_t u_gb = (int64_t)bi_lo * p.nbc + bj_lo;
+        if (EPI == EPI_AMAX) {
+          if (p.transformed) {
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              const int64_t cj = j0 + 16 * t + 4 * fg;
+              if (rv && cj < p.N)
+                *reinterpret_cast<float4 *>(p.transformed + (int64_t)b * MN + ri * p.N + cj) =
+                    make_float4(w[t][0], w[t][1], w[t][2], w[t][3]);
+            }
+          }
+          if (uniform) {
+            uint32_t m = 0u;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              const int64_t cj = j0 + 16 * t + 4 * fg;
+              if (rv && cj < p.N) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  const uint32_t a = __float_as_uint(w[t][e]) & 0x7fffffffu;
+                  m = a > m ? a : m;
+                }
+              }
+            }
+            m = wave_max_u32(m);
+            const int64_t blk = u_gb;
+            if (blk != run_blk) {
+              if (run_blk >= 0 && lane == 0 && run_max)
+                atomicMax(&p.amax[((int64_t)b * p.nbr * p.nbc + run_blk) * kAmaxSlots + slot], run_max);
+              run_blk = blk;
+              run_max = 0u;
+            }
+            run_max = m > run_max ? m : run_max;
+          } else {
+            // a block edge cuts the tile: per element
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              const int64_t cj = j0 + 16 * t + 4 * fg;
+              if (!(rv && cj < p.N)) continue;
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const uint32_t a = __float_as_uint(w[t][e]) & 0x7fffffffu;
+                const int64_t gb = (ri / p.br) * p.nbc + (cj + e) / p.bc;
+                if (a) atomicMax(&p.amax[((int64_t)b * p.nbr * p.nbc + gb) * kAmaxSlots + slot], a);
+              }
+            }
+          }
+        } else {  // EPI_QUANT
+          float u_inv = 0.f, u_s = 0.f;
+          if (uniform) {
+            const float a = block_amax_value(p, b, u_gb);
+            u_inv = e4m3_multiplier(a);
+            u_s = e4m3_scale(a);
+          }
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const int64_t cj = j0 + 16 * t + 4 * fg;
+            if (!(rv && cj < p.N)) continue;
+            uint32_t packed = 0u;
+            float res[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              float inv = u_inv, sc = u_s;
+              if (!uniform) {
+                const float a = block_amax_value(p, b, (ri / p.br) * p.nbc + (cj + e) / p.bc);
+                inv = e4m3_multiplier(a);
+                sc = e4m3_scale(a);
+              }
+              const uint32_t code = e4m3_encode(w[t][e] * inv);
+              packed |= code << (8 * e);
+              if (EF) res[e] = w[t][e] - e4m3_decode(code) * sc;
+            }
+            const int64_t off = (int64_t)b * MN + ri * p.N + cj;
+            *reinterpret_cast<uint32_t *>(p.codes + off) = packed;
+            if (EF) *reinterpret_cast<float4 *>(p.ef + off) = make_float4(res[0], res[1], res[2], res[3]);
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+  if (EPI == EPI_AMAX && wave_live && run_blk >= 0 && lane == 0 && run_max)
+    atomicMax(&p.amax[((int64_t)b * p.nbr * p.nbc + run_blk) * kAmaxSlots + slot], run_max);
+}
+
+struct PArgs {
+  const float *X;     // [batch][M][K]
+  int64_t x_ld, x_bs;
+  const float *Y;     // [C][K]
+  int64_t y_ld;
+  int64_t M, K;
+  int C;
+  float *out;         // [batch][M][C]
+  int64_t out_ld, out_bs;
+};
+
+// KS waves of a workgroup share one 16-row strip and split K; 4 / KS strips
+// per workgroup.  NT = 16-column tiles of the output per wave (C <= 16 NT).
+template <int KS, int NT>
+__global__ __launch_bounds__(kThreads) void proj_kernel(const PArgs p) {
+  __shared__ float red[kThreads / 64][NT][64][4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int fr = lane & 15, fg = lane >> 4;
+  const int b = blockIdx.z;
+  const int strip = wave / KS, part = wave % KS;
+  const int64_t i0 = ((int64_t)blockIdx.y * (4 / KS) + strip) * 16;
+  const int c0 = blockIdx.x * 16 * NT;
+  const int64_t ri = i0 + fr;
+  const bool rv = ri < p.M;
+  const float *xrow = p.X + (int64_t)b * p.x_bs + ri * p.x_ld;
+  const int64_t nk16 = (p.K + 15) / 16;
+  const int64_t per = (nk16 + KS - 1) / KS;
+  const int64_t qb = part * per, qe = qb + per < nk16 ? qb + per : nk16;
+  floatx4 acc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  auto fetch = [&](int64_t q, float4 &xb, float4 (&ya)[NT]) {
+    const int64_t k = 16 * q + 4 * fg;
+    const bool kv = k < p.K;
+    xb = (rv && kv) ? ld4(xrow + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const int c = c0 + 16 * t + fr;
+      ya[t] = (kv && c < p.C) ? ld4(p.Y + (int64_t)c * p.y_ld + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  float4 xb0, ya0[NT], xb1, ya1[NT];
+  if (qb < qe) fetch(qb, xb0, ya0);
+  for (int64_t q = qb; q < qe; q += 2) {
+    if (q + 1 < qe) fetch(q + 1, xb1, ya1);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(ya0[t].x, xb0.x, acc[t], 0, 0, 0);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(ya0[t].y, xb0.y, acc[t], 0, 0, 0);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(ya0[t].z, xb0.z, acc[t], 0, 0, 0);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(ya0[t].w, xb0.w, acc[t], 0, 0, 0);
+    if (q + 1 >= qe) break;
+    if (q + 2 < qe) fetch(q + 2, xb0, ya0);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(ya1[t].x, xb1.x, acc[t], 0, 0, 0);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(ya1[t].y, xb1.y, acc[t], 0, 0, 0);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(ya1[t].z, xb1.z, acc[t], 0, 0, 0);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(ya1[t].w, xb1.w, acc[t], 0, 0, 0);
+  }
+  if (KS > 1) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) red[wave][t][lane][v] = acc[t][v];
+    __syncthreads();
+    if (part != 0) return;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        float sum = acc[t][v];
+#pragma unroll
+        for (int o = 1; o < KS; ++o) sum += red[wave + o][t][lane][v];
+        acc[t][v] = sum;
+      }
+  }
+  if (!rv) return;
+  // lane holds out[ri][c0 + 16t + 4fg + v]
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const int c = c0 + 16 * t + 4 * fg;
+    if (c < p.C)
+      *reinterpret_cast<float4 *>(p.out + (int64_t)b * p.out_bs + ri * p.out_ld + c) =
+          make_float4(acc[t][0], acc[t][1], acc[t][2], acc[t][3]);
+  }
+}
+
+bool al16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+}  // namespace
+
+bool update_kernel_eligible(const TileJob &j) {
+  if (j.N % 4 != 0 || j.nseg < 1 || j.nseg > 2) return false;
+  const int64_t K = j.seg[0].K;
+  if (K != 16 && K != 32 && K != 64 && K != 128) return false;
+  for (int s = 0; s < j.nseg; ++s) {
+    const Segment &g = j.seg[s];
+    if (!g.a.kmajor || !g.b.kmajor || g.K != K) return false;
+    if (g.a.ld % 4 || g.b.ld % 4 || g.a.bs % 4 || g.b.bs % 4) return false;
+    if (!al16(g.a.ptr) || !al16(g.b.ptr)) return false;
+  }
+  if (!al16(j.D) || (j.C && !al16(j.C)) || (j.transformed && !al16(j.transformed)) ||
+      (j.ef && !al16(j.ef)) || (j.codes && (reinterpret_cast<uintptr_t>(j.codes) & 3)))
+    return false;
+  if (j.amax == nullptr) {  // decode store: dense output, D dense
+    if (j.ldc != j.N || j.cbs != j.M * j.N || j.ldd != j.N || j.dbs != j.M * j.N || j.beta != 1.f ||
+        j.alpha != 1.f || j.colscale || j.ksplit > 1)
+      return false;
+  }
+  return true;
+}
+
+gift_status launch_update(gift_ctx *ctx, const TileJob &j) {
+  UArgs a{};
+  for (int s = 0; s < j.nseg; ++s) {
+    a.seg[s].row = j.seg[s].a.ptr;
+    a.seg[s].row_ld = j.seg[s].a.ld;
+    a.seg[s].row_bs = j.seg[s].a.bs;
+    a.seg[s].col = j.seg[s].b.ptr;
+    a.seg[s].col_ld = j.seg[s].b.ld;
+    a.seg[s].col_bs = j.seg[s].b.bs;
+    a.seg[s].K = (int)j.seg[s].K;
+  }
+  a.nseg = j.nseg;
+  a.M = j.M;
+  a.N = j.N;
+  a.batch = j.batch;
+  a.D = j.D;
+  a.C = j.C;
+  a.amax = j.amax;
+  a.codes = j.codes;
+  a.scales = j.scales;
+  a.transformed = j.transformed;
+  a.ef = j.ef;
+  a.br = j.geom.br > 0 ? j.geom.br : j.M;
+  a.bc = j.geom.bc > 0 ? j.geom.bc : j.N;
+  a.nbr = j.geom.nbr;
+  a.nbc = j.geom.nbc;
+  a.shared = j.shared ? 1 : 0;
+  ProfileScope prof(ctx, j.kernel_family);
+  dim3 grid((unsigned)((j.N + kColsPerUnit - 1) / kColsPerUnit), (unsigned)((j.M + 63) / 64),
+            (unsigned)j.batch);
+  const int epi = j.amax == nullptr ? EPI_STORE : (j.codes == nullptr ? EPI_AMAX : EPI_QUANT);
+  const bool ef = j.ef != nullptr && epi != EPI_STORE;
+  const int k16 = (int)(j.seg[0].K / 16);
+  auto go = [&](auto epi_c, auto ef_c, auto nseg_c, auto k16_c) {
+    hipLaunchKernelGGL((update_kernel<decltype(epi_c)::value, decltype(ef_c)::value,
+                                      decltype(nseg_c)::value, decltype(k16_c)::value>),
+                       grid, dim3(kThreads), 0, ctx->stream, a);
+  };
+  auto by_k = [&](auto epi_c, auto ef_c, auto nseg_c) {
+    switch (k16) {
+      case 1: go(epi_c, ef_c, nseg_c, std::integral_constant<int, 1>{}); break;
+      case 2: go(epi_c, ef_c, nseg_c, std::integral_constant<int, 2>{}); break;
+      case 4: go(epi_c, ef_c, nseg_c, std::integral_constant<int, 4>{}); break;
+      default: go(epi_c, ef_c, nseg_c, std::integral_constant<int, 8>{}); break;
+    }
+  };
+  auto by_seg = [&](auto epi_c, auto ef_c) {
+    if (j.nseg == 1) by_k(epi_c, ef_c, std::integral_constant<int, 1>{});
+    else by_k(epi_c, ef_c, std::integral_constant<int, 2>{});
+  };
+  using T_ = std::true_type;
+  using F_ = std::false_type;
+  if (epi == EPI_STORE) by_seg(std::integral_constant<int, EPI_STORE>{}, F_{});
+  else if (epi == EPI_AMAX) {
+    if (ef) by_seg(std::integral_constant<int, EPI_AMAX>{}, T_{});
+    else by_seg(std::integral_constant<int, EPI_AMAX>{}, F_{});
+  } else {
+    if (ef) by_seg(std::integral_constant<int, EPI_QUANT>{}, T_{});
+    else by_seg(std::integral_constant<int, EPI_QUANT>{}, F_{});
+  }
+  return check_launch("update_kernel");
+}
+
+bool proj_kernel_eligible(const TileJob &j) {
+  const Segment &g = j.seg[0];
+  return j.nseg == 1 && j.amax == nullptr && g.a.kmajor && g.b.kmajor && g.b.bs == 0 &&
+         g.K % 4 == 0 && g.a.ld % 4 == 0 && g.a.bs % 4 == 0 && g.b.ld % 4 == 0 && j.N % 4 == 0 &&
+         j.ldc % 4 == 0 && j.cbs % 4 == 0 && al16(g.a.ptr) && al16(g.b.ptr) && al16(j.C) &&
+         j.D == nullptr && j.colscale == nullptr && j.alpha == 1.f && j.ksplit <= 1;
+}
+
+gift_status launch_proj(gift_ctx *ctx, const TileJob &j) {
+  PArgs a;
+  a.X = j.seg[0].a.ptr;
+  a.x_ld = j.seg[0].a.ld;
+  a.x_bs = j.seg[0].a.bs;
+  a.Y = j.seg[0].b.ptr;
+  a.y_ld = j.seg[0].b.ld;
+  a.M = j.M;
+  a.K = j.seg[0].K;
+  a.C = (int)j.N;
+  a.out = j.C;
+  a.out_ld = j.ldc;
+  a.out_bs = j.cbs;
+  ProfileScope prof(ctx, j.kernel_family);
+  // split K over the waves of a workgroup when strips alone would not fill the GPU
+  const int64_t strips = (j.M + 15) / 16 * j.batch;
+  const int ks = strips >= 4096 ? 1 : (strips >= 2048 ? 2 : 4);
+  const int nt = j.N <= 16 ? 1 : (j.N <= 32 ? 2 : 4);
+  const int rows_per_wg = 16 * (4 / ks);
+  dim3 grid((unsigned)((j.N + 16 * nt - 1) / (16 * nt)), (unsigned)((j.M + rows_per_wg - 1) / rows_per_wg),
+            (unsigned)j.batch);
+#define GIFT_PROJ(KS, NT) hipLaunchKernelGGL((proj_kernel<KS, NT>), grid, dim3(kThreads), 0, ctx->stream, a)
+  if (ks == 1) {
+    if (nt == 1) GIFT_PROJ(1, 1); else if (nt == 2) GIFT_PROJ(1, 2); else GIFT_PROJ(1, 4);
+  } else if (ks == 2) {
+    if (nt == 1) GIFT_PROJ(2, 1); else if (nt == 2) GIFT_PROJ(2, 2); else GIFT_PROJ(2, 4);
+  } else {
+    if (nt == 1) GIFT_PROJ(4, 1); else if (nt == 2) GIFT_PROJ(4, 2); else GIFT_PROJ(4, 4);
+  }
+#undef GIFT_PROJ
+  return check_launch("proj_kernel");
+}
+
+}  // namespace gift
