@@ -108,7 +108,9 @@ const char *gift_last_error(void);
  * binds the context to the then-current device.  *out receives the handle. */
 gift_status gift_ctx_create(void *hip_stream, gift_ctx **out);
 
-/* Rebind the context to another stream of the same device. */
+/* Rebind the context to another stream of the same device.  Work already
+ * queued on the old stream is waited for first: the context's scratch memory
+ * is ordered by the stream it was used on. */
 gift_status gift_ctx_set_stream(gift_ctx *ctx, void *hip_stream);
 
 /* Destroy a context (synchronizes its stream, frees its workspace). NULL ok.

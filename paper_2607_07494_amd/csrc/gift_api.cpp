@@ -76,6 +76,29 @@ gift_status workspace(gift_ctx *ctx, size_t bytes, void **out) {
   return GIFT_OK;
 }
 
+gift_status amax_slots(gift_ctx *ctx, size_t words, uint32_t **out) {
+  const size_t bytes = ((words * sizeof(uint32_t)) + 255) & ~(size_t)255;
+  if (bytes > ctx->slots.bytes) {
+    if (ctx->slots.ptr) {
+      GIFT_HIP_TRY(hipStreamSynchronize(ctx->stream));
+      GIFT_HIP_TRY(hipFree(ctx->slots.ptr));
+      ctx->slots.ptr = nullptr;
+      ctx->slots.bytes = 0;
+    }
+    void *p = nullptr;
+    if (hipMalloc(&p, bytes) != hipSuccess) {
+      (void)hipGetLastError();
+      return set_error(GIFT_ENOMEM, "amax slots: hipMalloc failed");
+    }
+    ctx->slots.ptr = p;
+    ctx->slots.bytes = bytes;
+    gift_status st = launch_zero_u32(ctx, static_cast<uint32_t *>(p), (int64_t)(bytes / 4));
+    if (st != GIFT_OK) return st;
+  }
+  *out = static_cast<uint32_t *>(ctx->slots.ptr);
+  return GIFT_OK;
+}
+
 ProfileScope::ProfileScope(gift_ctx *c, int k) : ctx(c), kernel(k) {
   if (!ctx || !ctx->profile) return;
   hipEvent_t start = nullptr;
@@ -298,6 +321,9 @@ gift_status gift_ctx_create(void *hip_stream, gift_ctx **out) {
 
 gift_status gift_ctx_set_stream(gift_ctx *ctx, void *hip_stream) {
   if (!ctx) return set_error(GIFT_EINVAL, "gift_ctx_set_stream: ctx is NULL");
+  // the workspace and the amax sub-slots are ordered by the old stream
+  if (ctx->device >= 0 && ctx->stream != static_cast<hipStream_t>(hip_stream))
+    GIFT_HIP_TRY(hipStreamSynchronize(ctx->stream));
   ctx->stream = static_cast<hipStream_t>(hip_stream);
   return GIFT_OK;
 }
@@ -312,6 +338,7 @@ void gift_ctx_destroy(gift_ctx *ctx) {
     }
     for (hipEvent_t e : ctx->event_pool) (void)hipEventDestroy(e);
     if (ctx->ws.ptr) (void)hipFree(ctx->ws.ptr);
+    if (ctx->slots.ptr) (void)hipFree(ctx->slots.ptr);
   }
   delete ctx;
 }
@@ -521,21 +548,20 @@ gift_status gift_encode(gift_ctx *ctx, const gift_factor *f, const float *grads,
   if ((st = bind_device(ctx)) != GIFT_OK) return st;
   const BlockGeom g = block_geom(m, n, block_rows, block_cols);
   const int64_t nblk = (int64_t)g.nbr * g.nbc;
-  const size_t raw_bytes = a256(sizeof(uint32_t) * (size_t)N * nblk * kAmaxSlots);
   const size_t fin_bytes = a256(sizeof(uint32_t) * (size_t)N * nblk);
   LowRankPlan plan;
   size_t proj_bytes = 0;
   if (f && (st = plan_low_rank(ctx, f, grads, N, m, n, false, nullptr, &proj_bytes, &plan)) != GIFT_OK)
     return st;
+  uint32_t *amax_raw = nullptr;
+  if ((st = amax_slots(ctx, (size_t)N * nblk * kAmaxSlots, &amax_raw)) != GIFT_OK) return st;
   void *ws = nullptr;
-  if ((st = workspace(ctx, raw_bytes + fin_bytes + proj_bytes, &ws)) != GIFT_OK) return st;
-  uint32_t *amax_raw = static_cast<uint32_t *>(ws);
-  uint32_t *amax_fin = reinterpret_cast<uint32_t *>(static_cast<char *>(ws) + raw_bytes);
-  if ((st = launch_zero_u32(ctx, amax_raw, (int64_t)N * nblk * kAmaxSlots)) != GIFT_OK) return st;
+  if ((st = workspace(ctx, fin_bytes + proj_bytes, &ws)) != GIFT_OK) return st;
+  uint32_t *amax_fin = static_cast<uint32_t *>(ws);
   TileJob job;
   if (f) {
-    if ((st = plan_low_rank(ctx, f, grads, N, m, n, false,
-                            static_cast<char *>(ws) + raw_bytes + fin_bytes, &proj_bytes, &plan)) != GIFT_OK)
+    if ((st = plan_low_rank(ctx, f, grads, N, m, n, false, static_cast<char *>(ws) + fin_bytes,
+                            &proj_bytes, &plan)) != GIFT_OK)
       return st;
     if (plan.active) job = plan.upd;
   }

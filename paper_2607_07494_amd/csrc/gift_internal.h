@@ -42,6 +42,7 @@ struct gift_ctx {
   hipStream_t stream = nullptr;
   int device = -1;                 // bound at the first compute call
   gift::Workspace ws;              // grow-only device workspace
+  gift::Workspace slots;           // block-amax sub-slots, zero between encodes
   bool profile = false;
   std::vector<gift::ProfileRec> prof;
   int64_t prof_launches[GIFT_KERNEL_COUNT] = {};
@@ -179,9 +180,11 @@ gift_status launch_stream_reduce(gift_ctx *ctx, const uint8_t *codes, const floa
 gift_status launch_proj(gift_ctx *ctx, const TileJob &job);
 gift_status launch_zero_u32(gift_ctx *ctx, uint32_t *p, int64_t count);
 // raw [N, nblk, kAmaxSlots] -> final [N, nblk] (max over slots, and over ranks
-// when shared) and scales s = amax / 448
-gift_status launch_finalize_amax(gift_ctx *ctx, const uint32_t *raw, int32_t N, int64_t nblk,
+// when shared) and scales s = amax / 448; clears the raw slots it read
+gift_status launch_finalize_amax(gift_ctx *ctx, uint32_t *raw, int32_t N, int64_t nblk,
                                  bool shared, uint32_t *final_amax, float *scales);
+// context-owned amax sub-slots, all zero between encodes (grown on demand)
+gift_status amax_slots(gift_ctx *ctx, size_t words, uint32_t **out);
 gift_status launch_reduce(gift_ctx *ctx, const uint8_t *codes, const float *scales,
                           int32_t N, int64_t m, int64_t n, BlockGeom g, float *mean);
 gift_status launch_copy_f32(gift_ctx *ctx, float *dst, const float *src, int64_t count);

@@ -3,11 +3,12 @@
 //
 // X is [T, dim] row-major bfloat16 (one token per row).  The contraction runs
 // over tokens, which are strided in memory, while the MFMA operands need
-// consecutive contraction indices per lane.  Each K step of 32 tokens is
-// therefore loaded as 16-byte rows of 8 features for two adjacent tokens and
+// consecutive contraction indices per lane.  Each K step of 64 tokens is
+// therefore loaded as 16-byte rows of 8 features for four adjacent tokens and
 // re-packed in registers into 32-bit (token, token+1) pairs per feature
-// before it goes to LDS as [feature][token] with tokens contiguous; a lane's
-// MFMA fragment (8 tokens of one feature) is then one 16-byte LDS read.
+// before it goes to LDS as [feature][token] with tokens contiguous (8-byte
+// stores of two pairs); a lane's MFMA fragment (8 tokens of one feature) is
+// then one 16-byte LDS read.
 //
 // Only tiles on or below the diagonal are computed (A is symmetric); each
 // tile is written to both of its mirror positions through an LDS transpose.
@@ -24,9 +25,17 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kTile = 128;       // output tile (features x features)
-constexpr int kKStep = 32;       // tokens per LDS round
-constexpr int kRowWords = 16 + 4;  // 16 token pairs per feature row + pad
+constexpr int kKStep = 64;       // tokens per LDS round
+constexpr int kRowWords = 32;    // 64 tokens = 32 token-pair words per feature row
 constexpr int kThreads = 256;
+
+// LDS layout of one operand: [feature row][32 words], word w of row R holds
+// tokens (2w, 2w+1) of that feature.  Words are grouped in 2-word slots
+// (4 tokens); slot s of row R is stored at slot s ^ swz(R).  swz(R) is even,
+// so the two slots of an aligned 16-byte fragment stay adjacent and in order,
+// while the 16 rows written by one store instruction (rows 8 apart) and the 8
+// rows read by one 128-byte phase of a fragment load land in different banks.
+__device__ __forceinline__ int swz(int row) { return 2 * ((row & 7) ^ ((row >> 3) & 7)); }
 
 __device__ __forceinline__ void pack_pairs(const uint4 &lo, const uint4 &hi, uint32_t w[8]) {
   // lo: features f..f+7 of token t; hi: the same features of token t+1.
@@ -48,9 +57,10 @@ struct SyrkArgs {
 };
 
 __global__ __launch_bounds__(kThreads) void syrk_bf16_kernel(const SyrkArgs p) {
-  __shared__ __attribute__((aligned(16))) uint32_t smem[(kTile * (kTile + 4) > 2 * 2 * kTile * kRowWords)
-                                                            ? kTile * (kTile + 4)
-                                                            : 2 * 2 * kTile * kRowWords];
+  constexpr int kOperand = kTile * kRowWords;             // words per operand buffer
+  constexpr int kStage = 2 * 2 * kOperand;                // double-buffered A and B
+  constexpr int kEpi = kTile * (kTile + 4);
+  __shared__ __attribute__((aligned(16))) uint32_t smem[kStage > kEpi ? kStage : kEpi];
   const int tid = threadIdx.x;
   const int member = blockIdx.z;
   // lower-triangle tile (ti >= tj) from the linear block index
@@ -63,32 +73,39 @@ __global__ __launch_bounds__(kThreads) void syrk_bf16_kernel(const SyrkArgs p) {
   const uint16_t *X = p.X[member];
   const int64_t T = p.T, dim = p.dim;
 
-  // load mapping: thread -> token pair tp (0..15) x feature group fgp (0..15):
-  // 16 pairs = 32 tokens, 16 groups of 8 = 128 features of each operand
-  const int tp = tid >> 4, fgp = tid & 15;
-  uint4 ra[2], rb[2];  // [token t / t+1]
+  // load mapping: lane -> feature group fgp (8 features, 16 bytes per token
+  // row; consecutive lanes read consecutive 16 bytes of a token row) and
+  // token quad tq (4 tokens = 2 pair words = one slot).
+  const int fgp = tid & 15, tq = tid >> 4;
+  uint4 ra[4], rb[4];
   auto load = [&](int64_t t0) {
-    const int64_t t = t0 + 2 * tp;
     const int64_t fi = i0 + 8 * fgp, fj = j0 + 8 * fgp;
 #pragma unroll
-    for (int d = 0; d < 2; ++d) {
-      const bool tok = t + d < T;
-      ra[d] = (tok && fi < dim) ? *reinterpret_cast<const uint4 *>(X + (t + d) * dim + fi)
-                                : make_uint4(0, 0, 0, 0);
-      rb[d] = (tok && fj < dim) ? *reinterpret_cast<const uint4 *>(X + (t + d) * dim + fj)
-                                : make_uint4(0, 0, 0, 0);
+    for (int d = 0; d < 4; ++d) {
+      const int64_t t = t0 + 4 * tq + d;
+      const bool tok = t < T;
+      ra[d] = (tok && fi < dim) ? *reinterpret_cast<const uint4 *>(X + t * dim + fi) : make_uint4(0, 0, 0, 0);
+      rb[d] = (tok && fj < dim) ? *reinterpret_cast<const uint4 *>(X + t * dim + fj) : make_uint4(0, 0, 0, 0);
     }
   };
   auto store = [&](int buf) {
-    uint32_t *As = smem + buf * 2 * kTile * kRowWords;
-    uint32_t *Bs = As + kTile * kRowWords;
-    uint32_t w[8];
-    pack_pairs(ra[0], ra[1], w);
+    uint32_t *As = smem + buf * 2 * kOperand;
+    uint32_t *Bs = As + kOperand;
+    uint32_t w01[8], w23[8];
+    pack_pairs(ra[0], ra[1], w01);
+    pack_pairs(ra[2], ra[3], w23);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) As[(8 * fgp + e) * kRowWords + tp] = w[e];
-    pack_pairs(rb[0], rb[1], w);
+    for (int e = 0; e < 8; ++e) {
+      const int row = 8 * fgp + e;
+      *reinterpret_cast<uint2 *>(As + row * kRowWords + 2 * (tq ^ swz(row))) = make_uint2(w01[e], w23[e]);
+    }
+    pack_pairs(rb[0], rb[1], w01);
+    pack_pairs(rb[2], rb[3], w23);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) Bs[(8 * fgp + e) * kRowWords + tp] = w[e];
+    for (int e = 0; e < 8; ++e) {
+      const int row = 8 * fgp + e;
+      *reinterpret_cast<uint2 *>(Bs + row * kRowWords + 2 * (tq ^ swz(row))) = make_uint2(w01[e], w23[e]);
+    }
   };
 
   const int lane = tid & 63, wave = tid >> 6;
@@ -107,24 +124,31 @@ __global__ __launch_bounds__(kThreads) void syrk_bf16_kernel(const SyrkArgs p) {
   for (int64_t s = 0; s < nsteps; ++s) {
     const int buf = (int)(s & 1);
     if (s + 1 < nsteps) load((s + 1) * kKStep);
-    const uint32_t *As = smem + buf * 2 * kTile * kRowWords;
-    const uint32_t *Bs = As + kTile * kRowWords;
-    bf16x8 af[4], bfr[4];
+    const uint32_t *As = smem + buf * 2 * kOperand;
+    const uint32_t *Bs = As + kOperand;
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {
-      const uint4 v = *reinterpret_cast<const uint4 *>(As + (wm * 64 + a * 16 + fr) * kRowWords + 4 * fg);
-      af[a] = __builtin_bit_cast(bf16x8, v);
+    for (int kk = 0; kk < 2; ++kk) {
+      // tokens 32 kk + 8 fg .. +7 = slots 8 kk + 2 fg and the next one
+      const int slot = 8 * kk + 2 * fg;
+      bf16x8 af[4], bfr[4];
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        const int row = wm * 64 + a * 16 + fr;
+        const uint4 v = *reinterpret_cast<const uint4 *>(As + row * kRowWords + 2 * (slot ^ swz(row)));
+        af[a] = __builtin_bit_cast(bf16x8, v);
+      }
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int row = wn * 64 + b * 16 + fr;
+        const uint4 v = *reinterpret_cast<const uint4 *>(Bs + row * kRowWords + 2 * (slot ^ swz(row)));
+        bfr[b] = __builtin_bit_cast(bf16x8, v);
+      }
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], bfr[b], acc[a][b], 0, 0, 0);
     }
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const uint4 v = *reinterpret_cast<const uint4 *>(Bs + (wn * 64 + b * 16 + fr) * kRowWords + 4 * fg);
-      bfr[b] = __builtin_bit_cast(bf16x8, v);
-    }
-#pragma unroll
-    for (int a = 0; a < 4; ++a)
-#pragma unroll
-      for (int b = 0; b < 4; ++b)
-        acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], bfr[b], acc[a][b], 0, 0, 0);
     if (s + 1 < nsteps) store(buf ^ 1);
     __syncthreads();
   }

@@ -477,21 +477,29 @@ __global__ __launch_bounds__(kThreads) void tile_kernel(const KArgs p) {
   }
 }
 
-// One thread per (rank, block): max over the sub-slots (and over the ranks
-// for a shared scale), then the stored scale s = fl32(amax / 448).
-__global__ void finalize_amax_kernel(const uint32_t *raw, int N, int64_t nblk, int shared,
+// One thread per (rank, block), or per block for a shared scale: max over the
+// sub-slots (and the ranks), the finished amax and scale s = fl32(amax / 448)
+// of every rank, and the sub-slots cleared for the next encode (each slot is
+// read by exactly one thread).
+__global__ void finalize_amax_kernel(uint32_t *raw, int N, int64_t nblk, int shared,
                                      uint32_t *fin, float *scales) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= (int64_t)N * nblk) return;
-  const int b = (int)(t / nblk);
-  const int64_t blk = t % nblk;
+  if (t >= (shared ? nblk : (int64_t)N * nblk)) return;
+  const int b = shared ? 0 : (int)(t / nblk);
+  const int64_t blk = shared ? t : t % nblk;
   uint32_t m = 0u;
-  for (int r = shared ? 0 : b; r < (shared ? N : b + 1); ++r) {
-    const uint32_t *q = raw + ((int64_t)r * nblk + blk) * kAmaxSlots;
-    for (int s = 0; s < kAmaxSlots; ++s) m = q[s] > m ? q[s] : m;
+  for (int r = b; r < (shared ? N : b + 1); ++r) {
+    uint32_t *q = raw + ((int64_t)r * nblk + blk) * kAmaxSlots;
+    for (int s = 0; s < kAmaxSlots; ++s) {
+      m = q[s] > m ? q[s] : m;
+      q[s] = 0u;
+    }
   }
-  fin[t] = m;
-  scales[t] = e4m3_scale(__uint_as_float(m));
+  const float sc = e4m3_scale(__uint_as_float(m));
+  for (int r = b; r < (shared ? N : b + 1); ++r) {
+    fin[(int64_t)r * nblk + blk] = m;
+    scales[(int64_t)r * nblk + blk] = sc;
+  }
 }
 
 __global__ void zero_u32_kernel(uint32_t *p, int64_t n) {
@@ -619,9 +627,9 @@ gift_status launch_zero_u32(gift_ctx *ctx, uint32_t *ptr, int64_t count) {
   return check_launch("zero_u32_kernel");
 }
 
-gift_status launch_finalize_amax(gift_ctx *ctx, const uint32_t *raw, int32_t N, int64_t nblk,
+gift_status launch_finalize_amax(gift_ctx *ctx, uint32_t *raw, int32_t N, int64_t nblk,
                                  bool shared, uint32_t *fin, float *scales) {
-  const int64_t total = (int64_t)N * nblk;
+  const int64_t total = shared ? nblk : (int64_t)N * nblk;
   if (total <= 0) return GIFT_OK;
   ProfileScope prof(ctx, GIFT_KERNEL_SMALL);
   hipLaunchKernelGGL(finalize_amax_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, ctx->stream,

@@ -312,12 +312,13 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const UArgs p) {
 struct PArgs {
   const float *X;     // [batch][M][K]
   int64_t x_ld, x_bs;
-  const float *Y;     // [C][K]
-  int64_t y_ld;
+  const float *Y;     // [batch][C][K] (y_bs = 0: shared)
+  int64_t y_ld, y_bs;
   int64_t M, K;
   int C;
-  float *out;         // [batch][M][C]
+  float *out;         // [batch][M][C], or [batch][C][M] when out_t
   int64_t out_ld, out_bs;
+  int out_t;
 };
 
 // KS waves of a workgroup share one 16-row strip and split K; 4 / KS strips
@@ -334,6 +335,7 @@ __global__ __launch_bounds__(kThreads) void proj_kernel(const PArgs p) {
   const int64_t ri = i0 + fr;
   const bool rv = ri < p.M;
   const float *xrow = p.X + (int64_t)b * p.x_bs + ri * p.x_ld;
+  const float *yb = p.Y + (int64_t)b * p.y_bs;
   const int64_t nk16 = (p.K + 15) / 16;
   const int64_t per = (nk16 + KS - 1) / KS;
   const int64_t qb = part * per, qe = qb + per < nk16 ? qb + per : nk16;
@@ -347,7 +349,7 @@ __global__ __launch_bounds__(kThreads) void proj_kernel(const PArgs p) {
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
       const int c = c0 + 16 * t + fr;
-      ya[t] = (kv && c < p.C) ? ld4(p.Y + (int64_t)c * p.y_ld + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+      ya[t] = (kv && c < p.C) ? ld4(yb + (int64_t)c * p.y_ld + k) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   };
   float4 xb0, ya0[NT], xb1, ya1[NT];
@@ -392,6 +394,17 @@ __global__ __launch_bounds__(kThreads) void proj_kernel(const PArgs p) {
   }
   if (!rv) return;
   // lane holds out[ri][c0 + 16t + 4fg + v]
+  if (p.out_t) {
+    // transposed: 16 lanes of equal fg write 16 consecutive rows ri of column c
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int c = c0 + 16 * t + 4 * fg + v;
+        if (c < p.C) p.out[(int64_t)b * p.out_bs + (int64_t)c * p.out_ld + ri] = acc[t][v];
+      }
+    return;
+  }
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
     const int c = c0 + 16 * t + 4 * fg;
@@ -489,34 +502,47 @@ gift_status launch_update(gift_ctx *ctx, const TileJob &j) {
   return check_launch("update_kernel");
 }
 
+// The projection kernel takes its 16-row strips from the larger output
+// dimension: rows of A (out[i][c] = C[i][c]) or, for a short-and-wide output,
+// rows of B (out[j][i] stored transposed into C[i][j]).
+static bool proj_strip_is_b(const TileJob &j) { return j.M <= 256 && j.N > j.M; }
+
 bool proj_kernel_eligible(const TileJob &j) {
   const Segment &g = j.seg[0];
-  return j.nseg == 1 && j.amax == nullptr && g.a.kmajor && g.b.kmajor && g.b.bs == 0 &&
-         g.K % 4 == 0 && g.a.ld % 4 == 0 && g.a.bs % 4 == 0 && g.b.ld % 4 == 0 && j.N % 4 == 0 &&
-         j.ldc % 4 == 0 && j.cbs % 4 == 0 && al16(g.a.ptr) && al16(g.b.ptr) && al16(j.C) &&
-         j.D == nullptr && j.colscale == nullptr && j.alpha == 1.f && j.ksplit <= 1;
+  const bool base = j.nseg == 1 && j.amax == nullptr && g.a.kmajor && g.b.kmajor && g.K % 4 == 0 &&
+                    g.a.ld % 4 == 0 && g.a.bs % 4 == 0 && g.b.ld % 4 == 0 && g.b.bs % 4 == 0 &&
+                    al16(g.a.ptr) && al16(g.b.ptr) && j.D == nullptr && j.colscale == nullptr &&
+                    j.alpha == 1.f && j.ksplit <= 1;
+  if (!base) return false;
+  if (proj_strip_is_b(j)) return true;              // transposed, scalar stores
+  return j.N % 4 == 0 && j.ldc % 4 == 0 && j.cbs % 4 == 0 && al16(j.C);
 }
 
 gift_status launch_proj(gift_ctx *ctx, const TileJob &j) {
   PArgs a;
-  a.X = j.seg[0].a.ptr;
-  a.x_ld = j.seg[0].a.ld;
-  a.x_bs = j.seg[0].a.bs;
-  a.Y = j.seg[0].b.ptr;
-  a.y_ld = j.seg[0].b.ld;
-  a.M = j.M;
+  const bool tr = proj_strip_is_b(j);
+  const Operand &xs = tr ? j.seg[0].b : j.seg[0].a;   // strip side
+  const Operand &ys = tr ? j.seg[0].a : j.seg[0].b;
+  a.X = xs.ptr;
+  a.x_ld = xs.ld;
+  a.x_bs = xs.bs;
+  a.Y = ys.ptr;
+  a.y_ld = ys.ld;
+  a.y_bs = ys.bs;
+  a.M = tr ? j.N : j.M;
   a.K = j.seg[0].K;
-  a.C = (int)j.N;
+  a.C = (int)(tr ? j.M : j.N);
   a.out = j.C;
   a.out_ld = j.ldc;
   a.out_bs = j.cbs;
+  a.out_t = tr ? 1 : 0;
   ProfileScope prof(ctx, j.kernel_family);
   // split K over the waves of a workgroup when strips alone would not fill the GPU
-  const int64_t strips = (j.M + 15) / 16 * j.batch;
+  const int64_t strips = (a.M + 15) / 16 * j.batch;
   const int ks = strips >= 4096 ? 1 : (strips >= 2048 ? 2 : 4);
-  const int nt = j.N <= 16 ? 1 : (j.N <= 32 ? 2 : 4);
+  const int nt = a.C <= 16 ? 1 : (a.C <= 32 ? 2 : 4);
   const int rows_per_wg = 16 * (4 / ks);
-  dim3 grid((unsigned)((j.N + 16 * nt - 1) / (16 * nt)), (unsigned)((j.M + rows_per_wg - 1) / rows_per_wg),
+  dim3 grid((unsigned)((a.C + 16 * nt - 1) / (16 * nt)), (unsigned)((a.M + rows_per_wg - 1) / rows_per_wg),
             (unsigned)j.batch);
 #define GIFT_PROJ(KS, NT) hipLaunchKernelGGL((proj_kernel<KS, NT>), grid, dim3(kThreads), 0, ctx->stream, a)
   if (ks == 1) {
