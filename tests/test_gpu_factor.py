@@ -75,7 +75,9 @@ def test_spiked_statistics_recover_exact_factor(ctx):
 
 @pytest.mark.parametrize("T,n,r,iters,dtype", [(1024, 256, 16, 6, "f32"),
                                                 (4096, 512, 32, 4, "bf16"),
-                                                (2048, 200, 20, 3, "f32")])
+                                                (2048, 200, 20, 3, "f32"),
+                                                # k = 2r = 160 > 128: the global-memory k x k kernels
+                                                (2048, 320, 80, 6, "f32")])
 def test_matches_float64_mirror(ctx, T, n, r, iters, dtype):
     say(f"factor mirror T={T} n={n} r={r} iters={iters} {dtype}")
     X, bits = factor_inputs(40 + n, T, n, dtype=dtype)
