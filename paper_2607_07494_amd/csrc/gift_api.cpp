@@ -76,27 +76,48 @@ gift_status workspace(gift_ctx *ctx, size_t bytes, void **out) {
   return GIFT_OK;
 }
 
-gift_status amax_slots(gift_ctx *ctx, size_t words, uint32_t **out) {
-  const size_t bytes = ((words * sizeof(uint32_t)) + 255) & ~(size_t)255;
-  if (bytes > ctx->slots.bytes) {
-    if (ctx->slots.ptr) {
-      GIFT_HIP_TRY(hipStreamSynchronize(ctx->stream));
-      GIFT_HIP_TRY(hipFree(ctx->slots.ptr));
-      ctx->slots.ptr = nullptr;
-      ctx->slots.bytes = 0;
+gift_status amax_slots(gift_ctx *ctx, size_t words, uint32_t **cur, uint32_t **other,
+                       size_t *other_dirty) {
+  if (words > ctx->slot_words || ctx->slots_unknown) {
+    if (words > ctx->slot_words) {
+      size_t cap = ctx->slot_words ? ctx->slot_words : 4096;
+      while (cap < words) cap *= 2;
+      if (ctx->slots.ptr) {
+        GIFT_HIP_TRY(hipStreamSynchronize(ctx->stream));
+        GIFT_HIP_TRY(hipFree(ctx->slots.ptr));
+        ctx->slots.ptr = nullptr;
+        ctx->slots.bytes = 0;
+        ctx->slot_words = 0;
+      }
+      void *p = nullptr;
+      if (hipMalloc(&p, 2 * cap * sizeof(uint32_t)) != hipSuccess) {
+        (void)hipGetLastError();
+        return set_error(GIFT_ENOMEM, "amax slots: hipMalloc failed");
+      }
+      ctx->slots.ptr = p;
+      ctx->slots.bytes = 2 * cap * sizeof(uint32_t);
+      ctx->slot_words = cap;
     }
-    void *p = nullptr;
-    if (hipMalloc(&p, bytes) != hipSuccess) {
-      (void)hipGetLastError();
-      return set_error(GIFT_ENOMEM, "amax slots: hipMalloc failed");
-    }
-    ctx->slots.ptr = p;
-    ctx->slots.bytes = bytes;
-    gift_status st = launch_zero_u32(ctx, static_cast<uint32_t *>(p), (int64_t)(bytes / 4));
+    gift_status st = launch_zero_u32(ctx, static_cast<uint32_t *>(ctx->slots.ptr), (int64_t)(2 * ctx->slot_words));
     if (st != GIFT_OK) return st;
+    ctx->slot_dirty[0] = ctx->slot_dirty[1] = 0;
+    ctx->slots_unknown = false;
   }
-  *out = static_cast<uint32_t *>(ctx->slots.ptr);
+  uint32_t *base = static_cast<uint32_t *>(ctx->slots.ptr);
+  const int s = ctx->slot_set;
+  *cur = base + (size_t)s * ctx->slot_words;
+  *other = base + (size_t)(1 - s) * ctx->slot_words;
+  *other_dirty = ctx->slot_dirty[1 - s];
+  ctx->slots_unknown = true;   // until amax_slots_done
   return GIFT_OK;
+}
+
+void amax_slots_done(gift_ctx *ctx, size_t left) {
+  const int s = ctx->slot_set;
+  ctx->slot_dirty[s] = left;
+  ctx->slot_dirty[1 - s] = 0;
+  ctx->slot_set = 1 - s;
+  ctx->slots_unknown = false;
 }
 
 ProfileScope::ProfileScope(gift_ctx *c, int k) : ctx(c), kernel(k) {
@@ -553,17 +574,27 @@ gift_status gift_encode(gift_ctx *ctx, const gift_factor *f, const float *grads,
   size_t proj_bytes = 0;
   if (f && (st = plan_low_rank(ctx, f, grads, N, m, n, false, nullptr, &proj_bytes, &plan)) != GIFT_OK)
     return st;
-  uint32_t *amax_raw = nullptr;
-  if ((st = amax_slots(ctx, (size_t)N * nblk * kAmaxSlots, &amax_raw)) != GIFT_OK) return st;
+  // With a transform, the AMAX pass stores W~ (+ R) and the QUANT pass streams
+  // it instead of recomputing the rank-r update: scratch unless the caller
+  // asked for W~ itself.
+  const bool gemm = f && plan.active;
+  const bool store_wt = gemm && n % 4 == 0 && g.bc % 4 == 0;
+  const size_t wt_bytes = store_wt && !transformed ? a256(sizeof(float) * (size_t)N * m * n) : 0;
+  const size_t raw_words = (size_t)N * nblk * kAmaxSlots;
+  uint32_t *amax_raw = nullptr, *prev_set = nullptr;
+  size_t prev_dirty = 0;
+  if ((st = amax_slots(ctx, raw_words, &amax_raw, &prev_set, &prev_dirty)) != GIFT_OK) return st;
   void *ws = nullptr;
-  if ((st = workspace(ctx, fin_bytes + proj_bytes, &ws)) != GIFT_OK) return st;
+  if ((st = workspace(ctx, fin_bytes + proj_bytes + wt_bytes, &ws)) != GIFT_OK) return st;
   uint32_t *amax_fin = static_cast<uint32_t *>(ws);
+  float *wt = transformed;
+  if (wt_bytes) wt = reinterpret_cast<float *>(static_cast<char *>(ws) + fin_bytes + proj_bytes);
   TileJob job;
-  if (f) {
-    if ((st = plan_low_rank(ctx, f, grads, N, m, n, false, static_cast<char *>(ws) + fin_bytes,
-                            &proj_bytes, &plan)) != GIFT_OK)
+  if (gemm) {
+    if ((st = plan_low_rank(ctx, f, grads, N, m, n, false, static_cast<char *>(ws) + fin_bytes, &proj_bytes,
+                            &plan)) != GIFT_OK)
       return st;
-    if (plan.active) job = plan.upd;
+    job = plan.upd;
   }
   job.M = m;
   job.N = n;
@@ -576,18 +607,36 @@ gift_status gift_encode(gift_ctx *ctx, const gift_factor *f, const float *grads,
   job.shared = mode == GIFT_SCALE_SHARED;
   job.ef = ef;
   job.scales = scales;
-  const bool gemm = job.nseg > 0;
-  job.transformed = transformed;
+  job.transformed = gemm ? wt : transformed;
   job.kernel_family = gemm ? GIFT_KERNEL_UPDATE_AMAX : GIFT_KERNEL_AMAX;
   if ((st = launch_tile(ctx, job)) != GIFT_OK) return st;
-  // max over the sub-slots (and the ranks for a shared scale) and the scales
-  if ((st = launch_finalize_amax(ctx, amax_raw, N, nblk, job.shared, amax_fin, scales)) != GIFT_OK)
-    return st;
-  job.amax = amax_fin;
   job.transformed = nullptr;
   job.codes = codes;
+  // QUANT pass: the streaming kernel reads the raw sub-slots itself (on the
+  // stored W~ + R with a transform, on W without); otherwise a finalize
+  // launch reduces them first
+  const float *qsrc = gemm ? wt : grads;
+  if (qsrc && stream_eligible(m, n, g, qsrc, codes, ef, nullptr)) {
+    TileJob q = job;
+    q.nseg = 0;
+    q.D = qsrc;
+    q.ef_added = gemm;
+    q.from_raw = true;
+    q.clear = prev_set;
+    q.clear_words = (int64_t)prev_dirty;
+    q.kernel_family = gemm ? GIFT_KERNEL_UPDATE_QUANT : GIFT_KERNEL_QUANT;
+    if ((st = launch_stream_codec(ctx, q)) != GIFT_OK) return st;
+    amax_slots_done(ctx, raw_words);
+    return GIFT_OK;
+  }
+  if ((st = launch_finalize_amax(ctx, amax_raw, N, nblk, job.shared, amax_fin, scales, prev_set,
+                                 (int64_t)prev_dirty)) != GIFT_OK)
+    return st;
+  job.amax = amax_fin;
   job.kernel_family = gemm ? GIFT_KERNEL_UPDATE_QUANT : GIFT_KERNEL_QUANT;
-  return launch_tile(ctx, job);
+  if ((st = launch_tile(ctx, job)) != GIFT_OK) return st;
+  amax_slots_done(ctx, 0);
+  return GIFT_OK;
 }
 
 gift_status gift_reduce_local(gift_ctx *ctx, const uint8_t *codes, const float *scales, int32_t N,

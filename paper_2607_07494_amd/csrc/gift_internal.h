@@ -42,7 +42,14 @@ struct gift_ctx {
   hipStream_t stream = nullptr;
   int device = -1;                 // bound at the first compute call
   gift::Workspace ws;              // grow-only device workspace
-  gift::Workspace slots;           // block-amax sub-slots, zero between encodes
+  // Block-amax sub-slots: two sets used by alternate encodes.  The set an
+  // encode starts with is all zero; the kernel that consumes a set's maxima
+  // also clears what the previous encode left in the other set.
+  gift::Workspace slots;
+  size_t slot_words = 0;           // capacity of one set
+  int slot_set = 0;                // set of the next encode
+  size_t slot_dirty[2] = {0, 0};   // words of each set still to clear
+  bool slots_unknown = false;      // an encode stopped between its passes
   bool profile = false;
   std::vector<gift::ProfileRec> prof;
   int64_t prof_launches[GIFT_KERNEL_COUNT] = {};
@@ -160,6 +167,13 @@ struct TileJob {
   float *scales = nullptr;
   float *transformed = nullptr;
   float *ef = nullptr;
+  bool ef_added = false;     // D already holds W~ + R (quantize a stored W~)
+  // QUANT pass of the streaming kernel straight from the AMAX pass's raw
+  // sub-slots (amax = raw): block maxima and scales in the kernel, and
+  // clear_words words at clear zeroed
+  bool from_raw = false;
+  uint32_t *clear = nullptr;
+  int64_t clear_words = 0;
   BlockGeom geom{};
   bool shared = false;
   int kernel_family = GIFT_KERNEL_FACTOR;
@@ -180,11 +194,19 @@ gift_status launch_stream_reduce(gift_ctx *ctx, const uint8_t *codes, const floa
 gift_status launch_proj(gift_ctx *ctx, const TileJob &job);
 gift_status launch_zero_u32(gift_ctx *ctx, uint32_t *p, int64_t count);
 // raw [N, nblk, kAmaxSlots] -> final [N, nblk] (max over slots, and over ranks
-// when shared) and scales s = amax / 448; clears the raw slots it read
+// when shared) and scales s = amax / 448; clears the raw slots it read and
+// `clear_words` words at `clear`
 gift_status launch_finalize_amax(gift_ctx *ctx, uint32_t *raw, int32_t N, int64_t nblk,
-                                 bool shared, uint32_t *final_amax, float *scales);
-// context-owned amax sub-slots, all zero between encodes (grown on demand)
-gift_status amax_slots(gift_ctx *ctx, size_t words, uint32_t **out);
+                                 bool shared, uint32_t *final_amax, float *scales, uint32_t *clear,
+                                 int64_t clear_words);
+// Sub-slot set for an encode that needs `words` words: *cur (all zero) and the
+// other set with the words it still holds from the previous encode (to be
+// cleared by this encode's last kernel).  Grows both sets on demand.
+gift_status amax_slots(gift_ctx *ctx, size_t words, uint32_t **cur, uint32_t **other,
+                       size_t *other_dirty);
+// Book-keeping after this encode's last kernel: the current set holds
+// `left` words (0 if its consumer cleared it), the other set is clean.
+void amax_slots_done(gift_ctx *ctx, size_t left);
 gift_status launch_reduce(gift_ctx *ctx, const uint8_t *codes, const float *scales,
                           int32_t N, int64_t m, int64_t n, BlockGeom g, float *mean);
 gift_status launch_copy_f32(gift_ctx *ctx, float *dst, const float *src, int64_t count);

@@ -35,6 +35,9 @@ struct SArgs {
   float *scales;       // [N][nbr][nbc]
   uint32_t *amax;      // [N][nbr][nbc]
   float *transformed;  // optional W~ out (amax pass)
+  const uint32_t *raw; // quantize from raw sub-slots [N][nbr][nbc][kAmaxSlots]
+  uint32_t *clear;     // words to zero (the previous encode's slot set)
+  int64_t clear_words;
   float *mean;         // [m][n] (reduce)
   int m, n, N;
   int br, bc, nbr, nbc;
@@ -142,18 +145,49 @@ __global__ __launch_bounds__(kThreads) void stream_amax_kernel(const SArgs p) {
   flush(bi);  // the block row still open (a no-op when it was just flushed)
 }
 
-template <bool EF>
+// EF: write the residual R <- x - Deq(Q(x)); ADD: x = input + R first (the
+// input is W itself), otherwise the input already is W~ + R.
+// RAW: the block maxima come straight from the AMAX pass's sub-slots: the G
+// lanes that share a block column reduce its kAmaxSlots slots (of every rank
+// for a shared scale), the wave that holds the block's first row writes its
+// scale, and the grid zeroes clear_words words at clear on the way.
+template <bool EF, bool ADD, bool RAW>
 __global__ __launch_bounds__(kThreads) void stream_quant_kernel(const SArgs p) {
+  if (RAW) {
+    const int64_t nthreads = (int64_t)gridDim.x * gridDim.y * gridDim.z * kThreads;
+    const int64_t gt = (((int64_t)blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x) * kThreads +
+                       threadIdx.x;
+    for (int64_t i = gt; i < p.clear_words; i += nthreads) p.clear[i] = 0u;
+  }
   const Run w = wave_run(p, true);
-  if (w.r0 >= p.m || !w.cv) return;
+  if (w.r0 >= p.m) return;
+  const int lane = threadIdx.x & 63;
   const int64_t mn = (int64_t)p.m * p.n;
   const int64_t nblk = (int64_t)p.nbr * p.nbc;
-  const int bj = w.cj / p.bc;
+  // lanes past column n keep to the last block column (their group's)
+  const int bj = w.cv ? w.cj / p.bc : p.nbc - 1;
   int bi = w.r0 / p.br;
   int next = (bi + 1) * p.br;
   float inv = 0.f, sc = 0.f;
+  // block bi's amax; with RAW every lane of the wave takes part (group sums)
+  // and the lane at the block's first column writes the scale when the block
+  // starts inside this wave's rows
   auto load_scale = [&]() {
-    const float a = __uint_as_float(p.amax[(int64_t)w.b * nblk + (int64_t)bi * p.nbc + bj]);
+    const int64_t blk = (int64_t)bi * p.nbc + bj;
+    float a;
+    if (RAW) {
+      const int rb = p.shared ? 0 : w.b, re = p.shared ? p.N : w.b + 1;
+      uint32_t m = 0u;
+      for (int r = rb; r < re; ++r) {
+        const uint32_t *q = p.raw + ((int64_t)r * nblk + blk) * kAmaxSlots;
+        for (int s = lane & (p.group - 1); s < kAmaxSlots; s += p.group) m = q[s] > m ? q[s] : m;
+      }
+      m = group_max(m, p.group);
+      a = __uint_as_float(m);
+      if (w.cv && (int64_t)bi * p.br >= w.r0 && w.cj % p.bc == 0) p.scales[(int64_t)w.b * nblk + blk] = e4m3_scale(a);
+    } else {
+      a = __uint_as_float(p.amax[(int64_t)w.b * nblk + blk]);
+    }
     inv = e4m3_multiplier(a);
     sc = e4m3_scale(a);
   };
@@ -165,9 +199,10 @@ __global__ __launch_bounds__(kThreads) void stream_quant_kernel(const SArgs p) {
       next += p.br;
       load_scale();
     }
+    if (!w.cv) continue;
     const int64_t off = (int64_t)r * p.n + w.cj;
     float4 v = ld4(xb + off);
-    if (EF) {
+    if (EF && ADD) {
       const float4 e = ld4(p.ef_in + (int64_t)w.b * mn + off);
       v.x += e.x; v.y += e.y; v.z += e.z; v.w += e.w;
     }
@@ -279,12 +314,20 @@ gift_status launch_stream_codec(gift_ctx *ctx, const TileJob &j) {
   shape_grid(a, j.batch, grid);
   ProfileScope prof(ctx, j.kernel_family);
   const bool ef = j.ef != nullptr;
+  a.raw = j.from_raw ? j.amax : nullptr;
+  a.clear = j.clear;
+  a.clear_words = j.from_raw ? j.clear_words : 0;
   if (j.codes == nullptr) {
     if (ef) hipLaunchKernelGGL(stream_amax_kernel<true>, grid, dim3(kThreads), 0, ctx->stream, a);
     else hipLaunchKernelGGL(stream_amax_kernel<false>, grid, dim3(kThreads), 0, ctx->stream, a);
+  } else if (j.from_raw) {
+    if (ef && j.ef_added) hipLaunchKernelGGL((stream_quant_kernel<true, false, true>), grid, dim3(kThreads), 0, ctx->stream, a);
+    else if (ef) hipLaunchKernelGGL((stream_quant_kernel<true, true, true>), grid, dim3(kThreads), 0, ctx->stream, a);
+    else hipLaunchKernelGGL((stream_quant_kernel<false, false, true>), grid, dim3(kThreads), 0, ctx->stream, a);
   } else {
-    if (ef) hipLaunchKernelGGL(stream_quant_kernel<true>, grid, dim3(kThreads), 0, ctx->stream, a);
-    else hipLaunchKernelGGL(stream_quant_kernel<false>, grid, dim3(kThreads), 0, ctx->stream, a);
+    if (ef && j.ef_added) hipLaunchKernelGGL((stream_quant_kernel<true, false, false>), grid, dim3(kThreads), 0, ctx->stream, a);
+    else if (ef) hipLaunchKernelGGL((stream_quant_kernel<true, true, false>), grid, dim3(kThreads), 0, ctx->stream, a);
+    else hipLaunchKernelGGL((stream_quant_kernel<false, false, false>), grid, dim3(kThreads), 0, ctx->stream, a);
   }
   return check_launch("stream codec kernel");
 }

@@ -480,25 +480,29 @@ __global__ __launch_bounds__(kThreads) void tile_kernel(const KArgs p) {
 // One thread per (rank, block), or per block for a shared scale: max over the
 // sub-slots (and the ranks), the finished amax and scale s = fl32(amax / 448)
 // of every rank, and the sub-slots cleared for the next encode (each slot is
-// read by exactly one thread).
+// read by exactly one thread), and the previous encode's slot set cleared.
 __global__ void finalize_amax_kernel(uint32_t *raw, int N, int64_t nblk, int shared,
-                                     uint32_t *fin, float *scales) {
+                                     uint32_t *fin, float *scales, uint32_t *clear,
+                                     int64_t clear_words) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= (shared ? nblk : (int64_t)N * nblk)) return;
-  const int b = shared ? 0 : (int)(t / nblk);
-  const int64_t blk = shared ? t : t % nblk;
-  uint32_t m = 0u;
-  for (int r = b; r < (shared ? N : b + 1); ++r) {
-    uint32_t *q = raw + ((int64_t)r * nblk + blk) * kAmaxSlots;
-    for (int s = 0; s < kAmaxSlots; ++s) {
-      m = q[s] > m ? q[s] : m;
-      q[s] = 0u;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = t; i < clear_words; i += stride) clear[i] = 0u;
+  for (int64_t u = t; u < (shared ? nblk : (int64_t)N * nblk); u += stride) {
+    const int b = shared ? 0 : (int)(u / nblk);
+    const int64_t blk = shared ? u : u % nblk;
+    uint32_t m = 0u;
+    for (int r = b; r < (shared ? N : b + 1); ++r) {
+      uint32_t *q = raw + ((int64_t)r * nblk + blk) * kAmaxSlots;
+      for (int s = 0; s < kAmaxSlots; ++s) {
+        m = q[s] > m ? q[s] : m;
+        q[s] = 0u;
+      }
     }
-  }
-  const float sc = e4m3_scale(__uint_as_float(m));
-  for (int r = b; r < (shared ? N : b + 1); ++r) {
-    fin[(int64_t)r * nblk + blk] = m;
-    scales[(int64_t)r * nblk + blk] = sc;
+    const float sc = e4m3_scale(__uint_as_float(m));
+    for (int r = b; r < (shared ? N : b + 1); ++r) {
+      fin[(int64_t)r * nblk + blk] = m;
+      scales[(int64_t)r * nblk + blk] = sc;
+    }
   }
 }
 
@@ -628,12 +632,16 @@ gift_status launch_zero_u32(gift_ctx *ctx, uint32_t *ptr, int64_t count) {
 }
 
 gift_status launch_finalize_amax(gift_ctx *ctx, uint32_t *raw, int32_t N, int64_t nblk,
-                                 bool shared, uint32_t *fin, float *scales) {
+                                 bool shared, uint32_t *fin, float *scales, uint32_t *clear,
+                                 int64_t clear_words) {
   const int64_t total = shared ? nblk : (int64_t)N * nblk;
-  if (total <= 0) return GIFT_OK;
+  const int64_t work = total > clear_words ? total : clear_words;
+  if (work <= 0) return GIFT_OK;
+  int64_t blocks = (work + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
   ProfileScope prof(ctx, GIFT_KERNEL_SMALL);
-  hipLaunchKernelGGL(finalize_amax_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, ctx->stream,
-                     raw, N, nblk, shared ? 1 : 0, fin, scales);
+  hipLaunchKernelGGL(finalize_amax_kernel, dim3((unsigned)blocks), dim3(256), 0, ctx->stream,
+                     raw, N, nblk, shared ? 1 : 0, fin, scales, clear, clear_words);
   return check_launch("finalize_amax_kernel");
 }
 
