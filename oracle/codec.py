@@ -255,6 +255,42 @@ def quantize_transformed(Wt: np.ndarray, block_rows: int = 0, block_cols: int = 
     return codes, s.astype(np.float32)
 
 
+def dequantize_blocks(codes: np.ndarray, scales: np.ndarray, block_rows: int = 0,
+                      block_cols: int = 0) -> np.ndarray:
+    """Per-rank ``fl32(val(q) * s_block)`` of ``[N, m, n]`` codes."""
+    codes = np.asarray(codes, dtype=np.uint8)
+    N, m, n = codes.shape
+    sc = expand_blocks(np.asarray(scales, dtype=np.float32), m, n, block_rows, block_cols)
+    with np.errstate(over="ignore", invalid="ignore"):
+        return (e4m3.dequantize(codes).astype(np.float32) * sc).astype(np.float32)
+
+
+def encode_ef(grads: np.ndarray, residual: np.ndarray, fA: Factor | None = None,
+              fG: Factor | None = None, block_rows: int = 0, block_cols: int = 0,
+              shared: bool = False):
+    """Encode with error feedback in the transformed coordinates.
+
+    The GIFT branch of the selective-communication algorithm (Sec. V-E):
+    ``U = W S^-1``, ``U~ = U + R``, scale and quantize ``U~``, and the new
+    residual ``R <- U~ - Dequantize(Q(U~))``, all float32 values
+    (``U~ = fl32(U + R)``, ``R = fl32(U~ - fl32(val * s))``).  Returns
+    ``(codes, scales, U~, R_new)``.
+    """
+    grads = np.asarray(grads, dtype=np.float32)
+    U = forward(grads, fA, fG).astype(np.float32)
+    Ut = (U + np.asarray(residual, dtype=np.float32)).astype(np.float32)
+    codes, s = quantize_transformed(Ut, block_rows, block_cols, shared)
+    return codes, s, Ut, residual_after(Ut, codes, s, block_rows, block_cols)
+
+
+def residual_after(Ut: np.ndarray, codes: np.ndarray, scales: np.ndarray, block_rows: int = 0,
+                   block_cols: int = 0) -> np.ndarray:
+    """Error-feedback residual ``fl32(U~ - fl32(val(q) * s))``."""
+    deq = dequantize_blocks(codes, scales, block_rows, block_cols)
+    with np.errstate(over="ignore", invalid="ignore"):
+        return (np.asarray(Ut, dtype=np.float32) - deq).astype(np.float32)
+
+
 # --------------------------------------------------------------------------
 # Rank sum (eq. dp_grad_avg; Algorithm 1 AllReduce_SUM + Dequantize / N)
 # --------------------------------------------------------------------------

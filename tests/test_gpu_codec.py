@@ -253,3 +253,38 @@ def test_deterministic(ctx):
     for x, y in zip(a, b):
         np.testing.assert_array_equal(x, y)
     f.close()
+
+
+# ------------------------------------------------ error feedback (Sec. V-E)
+
+EF_CASES = [
+    # (N, m, n, r, sides, block_rows, block_cols); r = 0: no transform
+    (3, 96, 128, 8, gift.SIDE_INPUT, 0, 0),      # streaming quantize of the stored W~ + R
+    (2, 64, 96, 0, 0, 0, 32),                    # Euclidean streaming path
+    (2, 33, 50, 4, gift.SIDE_INPUT, 0, 0),       # n % 4 != 0: recomputing quantize pass
+    (2, 40, 30, 0, 0, 8, 6),                     # Euclidean tile-kernel path
+]
+
+
+@pytest.mark.parametrize("N,m,n,r,sides,br,bc", EF_CASES)
+def test_error_feedback_two_steps(ctx, N, m, n, r, sides, br, bc):
+    say(f"error feedback N={N} m={m} n={n} r={r} block=({br},{bc})")
+    f, fA, fG = make_factor(ctx, m, n, r, sides, seed=m) if r else (None, None, None)
+    R = torch.zeros((N, m, n), dtype=torch.float32, device=DEV)
+    R_prev = np.zeros((N, m, n), np.float32)
+    for step in range(2):
+        grads = gradient_set(700 + step, 800 + m, N, m, n)
+        codes, scales, tr = gpu_encode(ctx, f, grads, br, bc, False, ef=R)
+        R_new = R.cpu().numpy()
+        ref_Ut = (codec.forward(grads, fA, fG).astype(np.float32) + R_prev).astype(np.float32)
+        if f is None:
+            np.testing.assert_array_equal(tr, ref_Ut)
+        else:
+            assert rel(tr, ref_Ut) <= TRANSFORM_RTOL
+        ref_codes, ref_scales = codec.quantize_transformed(tr, br, bc, False)
+        np.testing.assert_array_equal(scales, ref_scales)
+        np.testing.assert_array_equal(codes, ref_codes)
+        np.testing.assert_array_equal(R_new, codec.residual_after(tr, codes, scales, br, bc))
+        R_prev = R_new
+    if f is not None:
+        f.close()

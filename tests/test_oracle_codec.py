@@ -285,3 +285,46 @@ def test_paper_metric_definitions_are_consistent():
     g = gradient_set(5000, 5100, 1, 30, 30)[0]
     fid = codec.fidelity(codec.round_trip(g[None]), g)
     assert fid["MSE"] / fid["RelL2"] ** 2 == pytest.approx(np.mean(g.astype(np.float64) ** 2), rel=1e-9)
+
+
+# ---------------------------------------------- error feedback (Sec. V-E)
+
+def test_error_feedback_zero_residual_is_plain_encode():
+    grads = gradient_set(41, 42, 3, 24, 40)
+    fA = codec.lowrank_factor(codec.factor_statistics(factor_inputs(43, 400, 40)[0]), 6).to_f32()
+    codes, s, Ut, R = codec.encode_ef(grads, np.zeros_like(grads), fA, None, 0, 8)
+    c0, s0, t0 = codec.encode(grads, fA, None, 0, 8)
+    np.testing.assert_array_equal(codes, c0)
+    np.testing.assert_array_equal(s, s0)
+    np.testing.assert_array_equal(Ut, t0)
+    # the residual is what the dequantized codes miss
+    np.testing.assert_array_equal(R, (t0 - codec.dequantize_blocks(codes, s, 0, 8)).astype(np.float32))
+
+
+def test_error_feedback_residual_is_exact_and_bounded():
+    # Sterbenz: a value and its E4M3 round-off (relative error <= 2^-4 on
+    # normals) are within a factor 2, so U~ - deq is exact and deq + R == U~
+    rng = np.random.default_rng(7)
+    U = (rng.standard_normal((2, 30, 50)) * 1e-3).astype(np.float32)
+    R0 = (rng.standard_normal(U.shape) * 1e-5).astype(np.float32)
+    codes, s, Ut, R = codec.encode_ef(U, R0)
+    np.testing.assert_array_equal(Ut, (U + R0).astype(np.float32))
+    deq = codec.dequantize_blocks(codes, s).astype(np.float64)
+    np.testing.assert_array_equal(deq + R.astype(np.float64), Ut.astype(np.float64))
+    # half an E4M3 spacing: 2^-4 relative on normals, 2^-10 s on subnormals
+    bound = np.abs(Ut.astype(np.float64)) * 2.0 ** -4 + s.reshape(-1, 1, 1) * 2.0 ** -9
+    assert np.all(np.abs(R) <= bound)
+
+
+def test_error_feedback_telescopes():
+    # sum of what was sent + the final residual == sum of the inputs
+    rng = np.random.default_rng(8)
+    R = np.zeros((1, 16, 24), np.float32)
+    sent = np.zeros((1, 16, 24), np.float64)
+    total = np.zeros((1, 16, 24), np.float64)
+    for step in range(6):
+        U = (rng.standard_normal(R.shape) * 10.0 ** -(step % 3)).astype(np.float32)
+        codes, s, Ut, R = codec.encode_ef(U, R)
+        sent += codec.dequantize_blocks(codes, s)
+        total += U
+    np.testing.assert_allclose(sent + R, total, rtol=0, atol=1e-6 * np.abs(total).max())
