@@ -208,11 +208,18 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
   plan->active = useA || useG;
   if (!plan->active) return GIFT_OK;
   const int64_t mn = m * n;
+  // input side alone: the projection may split its contraction into partials
+  // that the update kernel sums (same conditions as that kernel's)
+  const bool aligned = (reinterpret_cast<uintptr_t>(W) & 15) == 0;
+  const int pparts = useA && !useG && aligned && n % 4 == 0 &&
+                             (A.r == 16 || A.r == 32 || A.r == 64 || A.r == 128)
+                         ? proj_parts(m, n, A.r, N)
+                         : 1;
   size_t off = 0;
   float *P = nullptr, *Qm = nullptr, *Km = nullptr, *L2 = nullptr;
   if (useA) {
     P = reinterpret_cast<float *>(ws + off);
-    off += a256(sizeof(float) * N * m * A.r);
+    off += a256(sizeof(float) * N * pparts * m * A.r);
   }
   if (useG) {
     Qm = reinterpret_cast<float *>(ws + off);
@@ -240,6 +247,7 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
     j.C = P;
     j.ldc = A.r;
     j.cbs = m * A.r;
+    j.ksplit = pparts;
     j.kernel_family = GIFT_KERNEL_PROJECT;
     if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
   }
@@ -311,8 +319,8 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
     if (useG) {  // L2 U_A^T
       s.a = Operand{L2, A.r, m * A.r, true};
       s.b = Operand{A.U, A.r, 0, true};
-    } else {  // P (C_A U_A^T)
-      s.a = Operand{P, A.r, m * A.r, true};
+    } else {  // P (C_A U_A^T), P summed from its partials
+      s.a = Operand{P, A.r, m * A.r, true, pparts};
       s.b = Operand{inverse ? A.Uci : A.Uc, A.r, 0, true};
     }
     s.K = A.r;

@@ -130,6 +130,9 @@ struct Operand {
   int64_t ld = 0;
   int64_t bs = 0;
   bool kmajor = true;
+  // the operand is the sum of `parts` split-K partials, partial z of batch b
+  // at ptr + (b * parts + z) * bs (register-direct update kernel only)
+  int parts = 1;
 };
 
 struct Segment {
@@ -192,6 +195,9 @@ gift_status launch_stream_codec(gift_ctx *ctx, const TileJob &job);
 gift_status launch_stream_reduce(gift_ctx *ctx, const uint8_t *codes, const float *scales, int32_t N,
                                  int64_t m, int64_t n, BlockGeom g, float *mean);
 gift_status launch_proj(gift_ctx *ctx, const TileJob &job);
+// split-K factor the projection kernel uses for an [batch, M, K] x [C, K]^T
+// product whose consumer can sum partials (1 = a single result)
+int proj_parts(int64_t M, int64_t K, int C, int32_t batch);
 gift_status launch_zero_u32(gift_ctx *ctx, uint32_t *p, int64_t count);
 // raw [N, nblk, kAmaxSlots] -> final [N, nblk] (max over slots, and over ranks
 // when shared) and scales s = amax / 448; clears the raw slots it read and

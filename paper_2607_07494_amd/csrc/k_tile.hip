@@ -590,6 +590,9 @@ gift_status launch_tile(gift_ctx *ctx, const TileJob &job) {
   // register-direct kernels for the rank-r update and the projections
   if (job.nseg > 0 && (job.amax != nullptr || job.D != nullptr) && update_kernel_eligible(job))
     return launch_update(ctx, job);
+  for (int s = 0; s < job.nseg; ++s)
+    if (job.seg[s].a.parts != 1 || job.seg[s].b.parts != 1)
+      return set_error(GIFT_EUNSUPPORTED, "split-K partial operand outside the update kernel");
   if (job.amax == nullptr && job.nseg > 0 && proj_kernel_eligible(job)) return launch_proj(ctx, job);
   const bool gemm = job.nseg > 0;
   if (job.amax != nullptr && !gemm &&

@@ -30,6 +30,9 @@
 #include "gift_internal.h"
 
 namespace gift {
+
+static bool proj_strip_is_b(const TileJob &j);
+
 namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
@@ -39,8 +42,9 @@ constexpr int kMaxK16 = 8;      // K <= 128 per segment
 constexpr int kColsPerUnit = 256;
 
 struct USeg {
-  const float *row;   // [batch][M][K] (row_bs = 0: shared)
+  const float *row;   // [batch][parts][M][K] (row_bs = 0: shared)
   int64_t row_ld, row_bs;
+  int row_parts;      // split-K partials summed on load (in order)
   const float *col;   // [batch][N][K]
   int64_t col_ld, col_bs;
   int K;
@@ -111,9 +115,22 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const UArgs p) {
 #pragma unroll
   for (int s = 0; s < NSEG; ++s)
 #pragma unroll
-    for (int q = 0; q < K16; ++q)
-      bfr[s][q] = rv ? ld4(p.seg[s].row + (int64_t)b * p.seg[s].row_bs + ri * p.seg[s].row_ld + 16 * q + 4 * fg)
-                     : make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int q = 0; q < K16; ++q) {
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (rv) {
+        const int np = p.seg[s].row_parts;
+        const float *base = p.seg[s].row + (int64_t)b * np * p.seg[s].row_bs + ri * p.seg[s].row_ld + 16 * q + 4 * fg;
+        v = ld4(base);
+        for (int z = 1; z < np; ++z) {
+          const float4 u = ld4(base + (int64_t)z * p.seg[s].row_bs);
+          v.x += u.x;
+          v.y += u.y;
+          v.z += u.z;
+          v.w += u.w;
+        }
+      }
+      bfr[s][q] = v;
+    }
 
   // cooperative load of a column tile's operand: slot -> (column, k quad)
   float4 creg[PER];
@@ -414,9 +431,121 @@ __global__ __launch_bounds__(kThreads) void proj_kernel(const PArgs p) {
   }
 }
 
+// Projection with the short operand staged in LDS: out[z][b][i][c] =
+// sum_{k in part z} X[b][i][k] Y[c][k] for C = 16 NT columns.  A workgroup
+// is four 16-row strips (one per wave) of one rank and one contraction part
+// (blockIdx.y); the 16 NT x 64 chunk of Y for the next 64 contraction steps
+// is loaded by the whole workgroup while the waves run the current one, and
+// each wave holds the next chunk's X values in registers.  Sharing Y through
+// LDS cuts the L2 requests for it by the four strips, which otherwise bound
+// this skinny product.
+template <int NT>
+__global__ __launch_bounds__(kThreads) void proj_staged_kernel(const PArgs p, int parts) {
+  constexpr int C = 16 * NT;
+  constexpr int KC = 64;                // contraction steps per chunk
+  constexpr int LD = KC + 4;            // padded LDS row (floats)
+  constexpr int PER = C * KC / 4 / kThreads;   // float4 per thread per chunk (NT)
+  __shared__ __attribute__((aligned(16))) float ys[2][C * LD];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int fr = lane & 15, fg = lane >> 4;
+  const int b = blockIdx.z, z = blockIdx.y;
+  const int64_t ri = ((int64_t)blockIdx.x * 4 + wave) * 16 + fr;
+  const bool rv = ri < p.M;
+  const int64_t kper = ((p.K + parts - 1) / parts + KC - 1) / KC * KC;
+  const int64_t k0 = z * kper, k1 = k0 + kper < p.K ? k0 + kper : p.K;
+  const int nchunks = k1 > k0 ? (int)((k1 - k0 + KC - 1) / KC) : 0;
+  const float *xrow = p.X + (int64_t)b * p.x_bs + ri * p.x_ld;
+  const float *yb = p.Y + (int64_t)b * p.y_bs;
+  float4 yreg[PER], xn[4];
+  auto load_y = [&](int64_t kc) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int slot = tid + u * kThreads;
+      const int c = slot / (KC / 4), k4 = slot % (KC / 4);
+      const int64_t k = kc + 4 * k4;
+      yreg[u] = (c < p.C && k < k1) ? ld4(yb + (int64_t)c * p.y_ld + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  auto store_y = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int slot = tid + u * kThreads;
+      const int c = slot / (KC / 4), k4 = slot % (KC / 4);
+      *reinterpret_cast<float4 *>(&ys[buf][c * LD + 4 * k4]) = yreg[u];
+    }
+  };
+  auto load_x = [&](int64_t kc) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int64_t k = kc + 16 * q + 4 * fg;
+      xn[q] = (rv && k < k1) ? ld4(xrow + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  floatx4 acc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  if (nchunks > 0) {
+    load_y(k0);
+    load_x(k0);
+    store_y(0);
+  }
+  __syncthreads();
+  for (int ch = 0; ch < nchunks; ++ch) {
+    const int buf = ch & 1;
+    float4 xc[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) xc[q] = xn[q];
+    const bool more = ch + 1 < nchunks;
+    if (more) {
+      load_y(k0 + (int64_t)(ch + 1) * KC);
+      load_x(k0 + (int64_t)(ch + 1) * KC);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      float4 ya[NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+        ya[t] = *reinterpret_cast<const float4 *>(&ys[buf][(16 * t + fr) * LD + 16 * q + 4 * fg]);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(ya[t].x, xc[q].x, acc[t], 0, 0, 0);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(ya[t].y, xc[q].y, acc[t], 0, 0, 0);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(ya[t].z, xc[q].z, acc[t], 0, 0, 0);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(ya[t].w, xc[q].w, acc[t], 0, 0, 0);
+    }
+    if (more) store_y(buf ^ 1);
+    __syncthreads();
+  }
+  if (!rv) return;
+  // lane holds part z of out[ri][16t + 4fg + v]
+  float *ob = p.out + ((int64_t)b * parts + z) * p.out_bs + ri * p.out_ld;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const int c = 16 * t + 4 * fg;
+    if (c < p.C) *reinterpret_cast<float4 *>(ob + c) = make_float4(acc[t][0], acc[t][1], acc[t][2], acc[t][3]);
+  }
+}
+
 bool al16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
+bool staged_eligible(const TileJob &j) {
+  const Segment &g = j.seg[0];
+  return !proj_strip_is_b(j) && g.b.bs == 0 && j.N % 16 == 0 && j.N <= 128 && g.K % 4 == 0 && j.ldc % 4 == 0 &&
+         j.cbs % 4 == 0 && al16(j.C);
+}
+
 }  // namespace
+
+int proj_parts(int64_t M, int64_t K, int C, int32_t batch) {
+  if (C % 16 != 0 || C > 128) return 1;
+  // enough waves to cover the chip about twice, each part at least 256 deep
+  const int64_t waves = (M + 15) / 16 * batch;
+  int parts = 1;
+  while (parts < 8 && waves * parts < 2048 && K / (2 * parts) >= 256) parts *= 2;
+  return parts;
+}
 
 bool update_kernel_eligible(const TileJob &j) {
   if (j.N % 4 != 0 || j.nseg < 1 || j.nseg > 2) return false;
@@ -445,6 +574,7 @@ gift_status launch_update(gift_ctx *ctx, const TileJob &j) {
     a.seg[s].row = j.seg[s].a.ptr;
     a.seg[s].row_ld = j.seg[s].a.ld;
     a.seg[s].row_bs = j.seg[s].a.bs;
+    a.seg[s].row_parts = j.seg[s].a.parts;
     a.seg[s].col = j.seg[s].b.ptr;
     a.seg[s].col_ld = j.seg[s].b.ld;
     a.seg[s].col_bs = j.seg[s].b.bs;
@@ -512,8 +642,9 @@ bool proj_kernel_eligible(const TileJob &j) {
   const bool base = j.nseg == 1 && j.amax == nullptr && g.a.kmajor && g.b.kmajor && g.K % 4 == 0 &&
                     g.a.ld % 4 == 0 && g.a.bs % 4 == 0 && g.b.ld % 4 == 0 && g.b.bs % 4 == 0 &&
                     al16(g.a.ptr) && al16(g.b.ptr) && j.D == nullptr && j.colscale == nullptr &&
-                    j.alpha == 1.f && j.ksplit <= 1;
+                    j.alpha == 1.f;
   if (!base) return false;
+  if (j.ksplit > 1) return staged_eligible(j);       // partials: staged kernel only
   if (proj_strip_is_b(j)) return true;              // transposed, scalar stores
   return j.N % 4 == 0 && j.ldc % 4 == 0 && j.cbs % 4 == 0 && al16(j.C);
 }
@@ -537,6 +668,24 @@ gift_status launch_proj(gift_ctx *ctx, const TileJob &j) {
   a.out_bs = j.cbs;
   a.out_t = tr ? 1 : 0;
   ProfileScope prof(ctx, j.kernel_family);
+  if (staged_eligible(j)) {
+    const int parts = j.ksplit > 1 ? j.ksplit : 1;
+    const int nt = (int)(j.N / 16);
+    const dim3 sgrid((unsigned)((a.M + 63) / 64), (unsigned)parts, (unsigned)j.batch);
+#define GIFT_PROJS(NT) hipLaunchKernelGGL((proj_staged_kernel<NT>), sgrid, dim3(kThreads), 0, ctx->stream, a, parts)
+    switch (nt) {
+      case 1: GIFT_PROJS(1); break;
+      case 2: GIFT_PROJS(2); break;
+      case 3: GIFT_PROJS(3); break;
+      case 4: GIFT_PROJS(4); break;
+      case 5: GIFT_PROJS(5); break;
+      case 6: GIFT_PROJS(6); break;
+      case 7: GIFT_PROJS(7); break;
+      default: GIFT_PROJS(8); break;
+    }
+#undef GIFT_PROJS
+    return check_launch("proj_staged_kernel");
+  }
   // split K over the waves of a workgroup when strips alone would not fill the GPU
   const int64_t strips = (a.M + 15) / 16 * j.batch;
   const int ks = strips >= 4096 ? 1 : (strips >= 2048 ? 2 : 4);

@@ -193,6 +193,8 @@ TRANSFORM_CASES = [
     (2, 200, 384, 32, gift.SIDE_BOTH, 0, 128),
     (2, 97, 61, 5, gift.SIDE_BOTH, 0, 0),
     (1, 64, 64, 64, gift.SIDE_INPUT, 0, 0),      # r = n: sigma A^-1/2
+    (2, 200, 1024, 32, gift.SIDE_INPUT, 0, 0),   # projection split into 4 partials
+    (1, 70, 2048, 64, gift.SIDE_INPUT, 0, 256),  # 8 partials, ragged strips
 ]
 
 
