@@ -37,6 +37,11 @@ class GiftError(RuntimeError):
 
 
 def _load():
+    # torch first: its bundled HIP runtime then satisfies libgift.so's
+    # libamdhip64 dependency by soname.  Loaded the other way round, the
+    # process holds two HIP runtimes and the second one sees no device.
+    import torch  # noqa: F401
+
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2607_07494_amd.build`")
     lib = ctypes.CDLL(LIB_PATH)

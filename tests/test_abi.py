@@ -110,3 +110,11 @@ def test_scale_grid_shapes():
     assert gift.scale_grid(100, 300, 0, 128) == (1, 3)
     assert gift.scale_grid(100, 300, 30, 0) == (4, 1)
     assert gift.scale_grid(5, 7, 100, 100) == (1, 1)
+
+
+def test_one_hip_runtime_in_the_process():
+    """The library must share torch's HIP runtime: with two copies loaded,
+    the second one reports no device on a GPU machine."""
+    maps = open("/proc/self/maps").read().split("\n")
+    hip = {line.split()[-1] for line in maps if "libamdhip64" in line}
+    assert len(hip) == 1, hip
