@@ -117,11 +117,15 @@ gift_status gift_ctx_set_stream(gift_ctx *ctx, void *hip_stream);
  * Destroy the factors created on it first. */
 void gift_ctx_destroy(gift_ctx *ctx);
 
-/* Per-kernel timing: when enabled, every launch is bracketed by HIP events on
- * the context stream.  gift_ctx_profile_read synchronizes the stream and
- * returns the number of launches and their summed duration (ms) for one kernel
- * family since the last reset; gift_ctx_profile_reset clears the counters. */
+/* Per-kernel timing: when enabled, every launch of a selected kernel family
+ * is bracketed by HIP events on the context stream (all families are selected
+ * until gift_ctx_profile_select is called).  gift_ctx_profile_read
+ * synchronizes the stream and returns the number of launches and their summed
+ * duration (ms) for one kernel family since the last reset;
+ * gift_ctx_profile_reset clears the counters.  family_mask: bit k selects
+ * kernel family k (gift_kernel). */
 gift_status gift_ctx_profile_enable(gift_ctx *ctx, int32_t enable);
+gift_status gift_ctx_profile_select(gift_ctx *ctx, uint32_t family_mask);
 gift_status gift_ctx_profile_read(gift_ctx *ctx, int32_t kernel, int64_t *launches,
                                   double *total_ms);
 gift_status gift_ctx_profile_reset(gift_ctx *ctx);
@@ -160,6 +164,16 @@ void gift_factor_destroy(gift_factor *f);
 gift_status gift_factor_update(gift_ctx *ctx, gift_factor *f, const void *acts,
                                const void *out_grads, int64_t T, gift_dtype dtype,
                                int32_t iters);
+
+/* Factor statistics alone (eq. kfac_fisher_block, eq. impl_A_psd): the
+ * uncentred second moment A = X^T X / T of one statistics input, the first
+ * step of gift_factor_update.
+ *   x  [T, dim] row-major, float32 or bfloat16 per dtype (device);
+ *   A  [dim, dim] float32 out (device), full symmetric matrix.
+ * bfloat16 products are exact in float32 and every sum is accumulated in
+ * float32.  Uses the context workspace. */
+gift_status gift_statistics(gift_ctx *ctx, const void *x, int64_t T, int64_t dim, gift_dtype dtype,
+                            float *A);
 
 /* Refresh many factors at once (same T and dtype): factor sides with equal
  * (dim, rank) share one launch sequence, so the small per-factor steps run

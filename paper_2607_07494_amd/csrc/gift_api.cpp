@@ -121,7 +121,7 @@ void amax_slots_done(gift_ctx *ctx, size_t left) {
 }
 
 ProfileScope::ProfileScope(gift_ctx *c, int k) : ctx(c), kernel(k) {
-  if (!ctx || !ctx->profile) return;
+  if (!ctx || !ctx->profile || !((ctx->profile_mask >> kernel) & 1u)) return;
   hipEvent_t start = nullptr;
   auto grab = [&]() -> hipEvent_t {
     if (!ctx->event_pool.empty()) {
@@ -378,6 +378,12 @@ gift_status gift_ctx_profile_enable(gift_ctx *ctx, int32_t enable) {
   return GIFT_OK;
 }
 
+gift_status gift_ctx_profile_select(gift_ctx *ctx, uint32_t family_mask) {
+  if (!ctx) return set_error(GIFT_EINVAL, "gift_ctx_profile_select: ctx is NULL");
+  ctx->profile_mask = family_mask;
+  return GIFT_OK;
+}
+
 gift_status gift_ctx_profile_read(gift_ctx *ctx, int32_t kernel, int64_t *launches,
                                   double *total_ms) {
   if (!ctx || !launches || !total_ms)
@@ -484,6 +490,24 @@ void gift_factor_destroy(gift_factor *f) {
     (void)hipFree(f->alloc);
   }
   delete f;
+}
+
+gift_status gift_statistics(gift_ctx *ctx, const void *x, int64_t T, int64_t dim, gift_dtype dtype,
+                            float *A) {
+  if (!ctx || !x || !A) return set_error(GIFT_EINVAL, "gift_statistics: NULL argument");
+  if (dtype != GIFT_F32 && dtype != GIFT_BF16)
+    return set_error(GIFT_EINVAL, "gift_statistics: dtype must be GIFT_F32 or GIFT_BF16");
+  if (T <= 0 || dim <= 0) return set_error(GIFT_ESHAPE, "gift_statistics: T and dim must be positive");
+  if (dim > kMaxRows) return set_error(GIFT_ESHAPE, "gift_statistics: dim exceeds the supported maximum (1048560)");
+  gift_status st = bind_device(ctx);
+  if (st != GIFT_OK) return st;
+  const bool widen = dtype == GIFT_BF16 && !statistics_direct(dtype, dim);
+  void *ws = nullptr;
+  if ((st = workspace(ctx, 256 + (widen ? sizeof(float) * (size_t)T * dim : 0), &ws)) != GIFT_OK) return st;
+  const void **d_tab = static_cast<const void **>(ws);
+  float *Xc = widen ? reinterpret_cast<float *>(static_cast<char *>(ws) + 256) : nullptr;
+  GIFT_HIP_TRY(hipMemcpyAsync(d_tab, &x, sizeof(void *), hipMemcpyHostToDevice, ctx->stream));
+  return launch_statistics(ctx, d_tab, &x, 1, T, dim, dtype, A, Xc);
 }
 
 gift_status gift_factor_update_batch(gift_ctx *ctx, int32_t count, gift_factor *const *factors,

@@ -51,6 +51,7 @@ struct gift_ctx {
   size_t slot_dirty[2] = {0, 0};   // words of each set still to clear
   bool slots_unknown = false;      // an encode stopped between its passes
   bool profile = false;
+  uint32_t profile_mask = ~0u;     // kernel families timed when profiling
   std::vector<gift::ProfileRec> prof;
   int64_t prof_launches[GIFT_KERNEL_COUNT] = {};
   double prof_ms[GIFT_KERNEL_COUNT] = {};
@@ -225,6 +226,13 @@ struct SideJob {
   uint64_t seed;      // Philox key of the start block
   float damping;
 };
+// A_m = X_m^T X_m / T for G inputs of one dimension into A [G, dim, dim]:
+// bf16 inputs with dim % 8 == 0 on the bf16 SYRK kernel (device pointer table
+// d_xtab), otherwise the float32 tile kernel (host pointers h_x; bf16 inputs
+// are widened into Xc [T, dim] first).
+bool statistics_direct(gift_dtype dtype, int64_t dim);
+gift_status launch_statistics(gift_ctx *ctx, const void *const *d_xtab, const void *const *h_x, int G,
+                              int64_t T, int64_t dim, gift_dtype dtype, float *A, float *Xc);
 gift_status factor_refresh_batch(gift_ctx *ctx, const std::vector<SideJob> &jobs, int64_t T,
                                  gift_dtype dtype, int32_t iters);
 gift_status side_import(gift_ctx *ctx, Side &s, const float *U, const float *c_fwd,

@@ -718,6 +718,41 @@ struct Group {
 
 }  // namespace
 
+bool statistics_direct(gift_dtype dtype, int64_t dim) { return dtype == GIFT_BF16 && dim % 8 == 0; }
+
+gift_status launch_statistics(gift_ctx *ctx, const void *const *d_xtab, const void *const *h_x, int G,
+                              int64_t T, int64_t dim, gift_dtype dtype, float *A, float *Xc) {
+  const float inv_T = (float)(1.0 / (double)T);
+  gift_status st;
+  if (statistics_direct(dtype, dim))
+    return launch_syrk_bf16(ctx, reinterpret_cast<const uint16_t *const *>(d_xtab), G, T, dim, inv_T, A);
+  for (int m = 0; m < G; ++m) {
+    const float *X32 = static_cast<const float *>(h_x[m]);
+    if (dtype == GIFT_BF16) {
+      {
+        ProfileScope prof(ctx, GIFT_KERNEL_SYRK);
+        hipLaunchKernelGGL(bf16_to_f32_kernel, dim3(grid_for(T * dim)), dim3(256), 0, ctx->stream, Xc,
+                           static_cast<const uint16_t *>(h_x[m]), T * dim);
+      }
+      if ((st = check_launch("bf16_to_f32_kernel")) != GIFT_OK) return st;
+      X32 = Xc;
+    }
+    TileJob j;
+    j.nseg = 1;
+    j.seg[0].a = Operand{X32, dim, 0, false};   // (i, t) = X[t][i]
+    j.seg[0].b = Operand{X32, dim, 0, false};   // (t, j) = X[t][j]
+    j.seg[0].K = T;
+    j.M = dim;
+    j.N = dim;
+    j.C = A + (int64_t)m * dim * dim;
+    j.ldc = dim;
+    j.alpha = inv_T;
+    j.kernel_family = GIFT_KERNEL_SYRK;
+    if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
+  }
+  return GIFT_OK;
+}
+
 gift_status factor_refresh_batch(gift_ctx *ctx, const std::vector<SideJob> &jobs, int64_t T,
                                  gift_dtype dtype, int32_t iters) {
   // groups in launch order: LDS-sized k first, so the small-kernel tables
@@ -742,7 +777,7 @@ gift_status factor_refresh_batch(gift_ctx *ctx, const std::vector<SideJob> &jobs
     g.ks = (int)((g.dim + 255) / 256);   // split-K factor of the k x k products
     g.G = (int)g.jobs.size();
     g.first = total;
-    g.bf16_direct = dtype == GIFT_BF16 && g.dim % 8 == 0;
+    g.bf16_direct = statistics_direct(dtype, g.dim);
     total += g.G;
     if (g.k <= kLdsK) n_lds += g.G;
     for (const SideJob &j : g.jobs) any_cold = any_cold || !j.side->have_basis || j.side->fill_tail;
@@ -855,38 +890,11 @@ gift_status factor_refresh_batch(gift_ctx *ctx, const std::vector<SideJob> &jobs
   GIFT_HIP_TRY(hipMemcpyAsync(b, host.data(), tables_bytes, hipMemcpyHostToDevice, stream));
 
   // 1. statistics A_g = X_g^T X_g / T
-  const float inv_T = (float)(1.0 / (double)T);
   for (Group &g : groups) {
-    if (g.bf16_direct) {
-      if ((st = launch_syrk_bf16(ctx, reinterpret_cast<const uint16_t *const *>(g.xtab), g.G, T, g.dim,
-                                 inv_T, g.Amat)) != GIFT_OK)
-        return st;
-      continue;
-    }
-    for (int m = 0; m < g.G; ++m) {
-      const float *X32 = static_cast<const float *>(g.jobs[m].x);
-      if (dtype == GIFT_BF16) {
-        {
-          ProfileScope prof(ctx, GIFT_KERNEL_SYRK);
-          hipLaunchKernelGGL(bf16_to_f32_kernel, dim3(grid_for(T * g.dim)), dim3(256), 0, stream, g.Xc,
-                             static_cast<const uint16_t *>(g.jobs[m].x), T * g.dim);
-        }
-        if ((st = check_launch("bf16_to_f32_kernel")) != GIFT_OK) return st;
-        X32 = g.Xc;
-      }
-      TileJob j;
-      j.nseg = 1;
-      j.seg[0].a = Operand{X32, g.dim, 0, false};   // (i, t) = X[t][i]
-      j.seg[0].b = Operand{X32, g.dim, 0, false};   // (t, j) = X[t][j]
-      j.seg[0].K = T;
-      j.M = g.dim;
-      j.N = g.dim;
-      j.C = g.Amat + (int64_t)m * g.dim * g.dim;
-      j.ldc = g.dim;
-      j.alpha = inv_T;
-      j.kernel_family = GIFT_KERNEL_SYRK;
-      if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
-    }
+    std::vector<const void *> xs;
+    for (const SideJob &j : g.jobs) xs.push_back(j.x);
+    if ((st = launch_statistics(ctx, g.xtab, xs.data(), g.G, T, g.dim, dtype, g.Amat, g.Xc)) != GIFT_OK)
+      return st;
   }
 
   // 2. start blocks of every member

@@ -10,8 +10,20 @@
 // stores of two pairs); a lane's MFMA fragment (8 tokens of one feature) is
 // then one 16-byte LDS read.
 //
-// Only tiles on or below the diagonal are computed (A is symmetric); each
-// tile is written to both of its mirror positions through an LDS transpose.
+// A workgroup computes one 256 x 256 output tile with eight waves of 128 x 64
+// each (128 accumulator registers per lane, two waves per SIMD): per 16-byte
+// fragment read a wave issues 2.7 MFMAs on average, and the 256-wide strips
+// are re-read from L2 half as often as with 128-wide tiles.
+// Only tiles on or below the diagonal are computed (A is symmetric); each is
+// written to both mirror positions straight from the accumulators.
+//
+// Scheduling: workgroups are handed to the 8 XCDs round-robin by linear id,
+// so the launch renumbers them so that each XCD walks a contiguous run of
+// (member, tile) pairs, a member's tiles in row-major triangle order.  The
+// ~32 tiles resident on one XCD then share a handful of feature strips that
+// advance through the tokens together, and the strips are fetched into that
+// XCD's L2 once instead of once per tile.
+//
 // Products of two bfloat16 values are exact in float32 and the sums are
 // accumulated in float32 by v_mfma_f32_16x16x32_bf16.  Members of a batch
 // (one per factor side with the same dimension) run in one launch.
@@ -24,17 +36,18 @@ namespace {
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-constexpr int kTile = 128;       // output tile (features x features)
-constexpr int kKStep = 64;       // tokens per LDS round
+constexpr int kTile = 256;       // output tile (features x features)
+constexpr int kKStep = 64;       // tokens per LDS stage
 constexpr int kRowWords = 32;    // 64 tokens = 32 token-pair words per feature row
-constexpr int kThreads = 256;
+constexpr int kThreads = 512;
+constexpr int kXcds = 8;         // MI355X: 8 XCDs of 32 CUs, each with its own L2
 
 // LDS layout of one operand: [feature row][32 words], word w of row R holds
 // tokens (2w, 2w+1) of that feature.  Words are grouped in 2-word slots
 // (4 tokens); slot s of row R is stored at slot s ^ swz(R).  swz(R) is even,
 // so the two slots of an aligned 16-byte fragment stay adjacent and in order,
-// while the 16 rows written by one store instruction (rows 8 apart) and the 8
-// rows read by one 128-byte phase of a fragment load land in different banks.
+// while the rows written by one store instruction and the rows read by one
+// 128-byte phase of a fragment load land in different banks.
 __device__ __forceinline__ int swz(int row) { return 2 * ((row & 7) ^ ((row >> 3) & 7)); }
 
 __device__ __forceinline__ void pack_pairs(const uint4 &lo, const uint4 &hi, uint32_t w[8]) {
@@ -54,17 +67,23 @@ struct SyrkArgs {
   float *A;                  // [members, dim, dim]
   int64_t T, dim;
   float scale;               // 1 / T
+  int tiles;                 // lower-triangle tiles per member
+  int total;                 // members * tiles
+  int per_xcd;               // ceil(total / kXcds)
 };
 
-__global__ __launch_bounds__(kThreads) void syrk_bf16_kernel(const SyrkArgs p) {
-  constexpr int kOperand = kTile * kRowWords;             // words per operand buffer
-  constexpr int kStage = 2 * 2 * kOperand;                // double-buffered A and B
-  constexpr int kEpi = kTile * (kTile + 4);
-  __shared__ __attribute__((aligned(16))) uint32_t smem[kStage > kEpi ? kStage : kEpi];
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void syrk_bf16_kernel(const SyrkArgs p) {
+  constexpr int kOperand = kTile * kRowWords;   // words per operand and stage (32 KiB)
+  constexpr int kStage = 2 * kOperand;          // A and B strips of one stage
+  __shared__ __attribute__((aligned(16))) uint32_t smem[2 * kStage];
   const int tid = threadIdx.x;
-  const int member = blockIdx.z;
-  // lower-triangle tile (ti >= tj) from the linear block index
-  const int x = blockIdx.x;
+  // XCD-contiguous renumbering of the linear workgroup id
+  const int lin = (int)(blockIdx.x % kXcds) * p.per_xcd + (int)(blockIdx.x / kXcds);
+  if (lin >= p.total) return;
+  const int member = lin / p.tiles;
+  const int x = lin - member * p.tiles;
+  // lower-triangle tile (ti >= tj) from the index inside the member
   int ti = (int)((sqrtf(8.0f * x + 1.0f) - 1.0f) * 0.5f);
   while ((ti + 1) * (ti + 2) / 2 <= x) ++ti;
   while (ti * (ti + 1) / 2 > x) --ti;
@@ -73,24 +92,35 @@ __global__ __launch_bounds__(kThreads) void syrk_bf16_kernel(const SyrkArgs p) {
   const uint16_t *X = p.X[member];
   const int64_t T = p.T, dim = p.dim;
 
-  // load mapping: lane -> feature group fgp (8 features, 16 bytes per token
-  // row; consecutive lanes read consecutive 16 bytes of a token row) and
-  // token quad tq (4 tokens = 2 pair words = one slot).
-  const int fgp = tid & 15, tq = tid >> 4;
+  // load mapping: lane -> feature group fgp (8 features = 16 bytes of a token
+  // row; 32 consecutive lanes read 512 contiguous bytes) and token quad tqb
+  // (4 tokens = 2 pair words = one slot)
+  const int fgp = tid & 31, tqb = tid >> 5;
+  const int64_t fi = i0 + 8 * fgp, fj = j0 + 8 * fgp;
+  // Buffer loads: the resource of a stage starts at token t0 and covers only
+  // the tokens that exist, so reads past T come back as zero from the range
+  // check; a lane whose features lie past dim gets an offset beyond any
+  // stage's range and reads zeros too.
+  constexpr uint32_t kOutside = 0x40000000u;   // > 64 * dim * 2 for dim < 2^23
+  const uint32_t row_bytes = (uint32_t)dim * 2u;
+  const uint32_t offi = fi < dim ? (uint32_t)(4 * tqb) * row_bytes + (uint32_t)fi * 2u : kOutside;
+  const uint32_t offj = fj < dim ? (uint32_t)(4 * tqb) * row_bytes + (uint32_t)fj * 2u : kOutside;
   uint4 ra[4], rb[4];
   auto load = [&](int64_t t0) {
-    const int64_t fi = i0 + 8 * fgp, fj = j0 + 8 * fgp;
+    const int64_t left = T - t0 < kKStep ? T - t0 : kKStep;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(X + t0 * dim), (short)0, (int)(left * dim * 2), 0x00020000);
 #pragma unroll
     for (int d = 0; d < 4; ++d) {
-      const int64_t t = t0 + 4 * tq + d;
-      const bool tok = t < T;
-      ra[d] = (tok && fi < dim) ? *reinterpret_cast<const uint4 *>(X + t * dim + fi) : make_uint4(0, 0, 0, 0);
-      rb[d] = (tok && fj < dim) ? *reinterpret_cast<const uint4 *>(X + t * dim + fj) : make_uint4(0, 0, 0, 0);
+      const uint32_t tok = (uint32_t)d * row_bytes;
+      ra[d] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)(offi + tok), 0, 0));
+      rb[d] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)(offj + tok), 0, 0));
     }
   };
   auto store = [&](int buf) {
-    uint32_t *As = smem + buf * 2 * kOperand;
+    uint32_t *As = smem + buf * kStage;
     uint32_t *Bs = As + kOperand;
+    const int tq = tqb;
     uint32_t w01[8], w23[8];
     pack_pairs(ra[0], ra[1], w01);
     pack_pairs(ra[2], ra[3], w23);
@@ -109,11 +139,11 @@ __global__ __launch_bounds__(kThreads) void syrk_bf16_kernel(const SyrkArgs p) {
   };
 
   const int lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave >> 2, wn = wave & 3;
   const int fr = lane & 15, fg = lane >> 4;
-  floatx4 acc[4][4];
+  floatx4 acc[8][4];
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int a = 0; a < 8; ++a)
 #pragma unroll
     for (int b = 0; b < 4; ++b) acc[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
 
@@ -124,16 +154,16 @@ __global__ __launch_bounds__(kThreads) void syrk_bf16_kernel(const SyrkArgs p) {
   for (int64_t s = 0; s < nsteps; ++s) {
     const int buf = (int)(s & 1);
     if (s + 1 < nsteps) load((s + 1) * kKStep);
-    const uint32_t *As = smem + buf * 2 * kOperand;
+    const uint32_t *As = smem + buf * kStage;
     const uint32_t *Bs = As + kOperand;
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
       // tokens 32 kk + 8 fg .. +7 = slots 8 kk + 2 fg and the next one
       const int slot = 8 * kk + 2 * fg;
-      bf16x8 af[4], bfr[4];
+      bf16x8 af[8], bfr[4];
 #pragma unroll
-      for (int a = 0; a < 4; ++a) {
-        const int row = wm * 64 + a * 16 + fr;
+      for (int a = 0; a < 8; ++a) {
+        const int row = wm * 128 + a * 16 + fr;
         const uint4 v = *reinterpret_cast<const uint4 *>(As + row * kRowWords + 2 * (slot ^ swz(row)));
         af[a] = __builtin_bit_cast(bf16x8, v);
       }
@@ -144,7 +174,7 @@ __global__ __launch_bounds__(kThreads) void syrk_bf16_kernel(const SyrkArgs p) {
         bfr[b] = __builtin_bit_cast(bf16x8, v);
       }
 #pragma unroll
-      for (int a = 0; a < 4; ++a)
+      for (int a = 0; a < 8; ++a)
 #pragma unroll
         for (int b = 0; b < 4; ++b)
           acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], bfr[b], acc[a][b], 0, 0, 0);
@@ -153,29 +183,25 @@ __global__ __launch_bounds__(kThreads) void syrk_bf16_kernel(const SyrkArgs p) {
     __syncthreads();
   }
 
-  // epilogue: tile -> LDS [128][132] -> both mirror positions, coalesced
-  float *Cs = reinterpret_cast<float *>(smem);
-#pragma unroll
-  for (int a = 0; a < 4; ++a)
-#pragma unroll
-    for (int b = 0; b < 4; ++b)
-#pragma unroll
-      for (int v = 0; v < 4; ++v)
-        Cs[(wm * 64 + a * 16 + 4 * fg + v) * (kTile + 4) + wn * 64 + b * 16 + fr] = acc[a][b][v] * p.scale;
-  __syncthreads();
+  // epilogue straight from the accumulators: lane (fr, fg) of block (a, b)
+  // holds rows 4 fg + v, column fr of that 16 x 16 block
   float *A = p.A + (int64_t)member * dim * dim;
-  for (int q = tid; q < kTile * kTile; q += kThreads) {
-    const int r = q / kTile, c = q % kTile;
-    const int64_t gi = i0 + r, gj = j0 + c;
-    if (gi < dim && gj < dim) A[gi * dim + gj] = Cs[r * (kTile + 4) + c];
-  }
-  if (ti != tj) {
-    for (int q = tid; q < kTile * kTile; q += kThreads) {
-      const int r = q / kTile, c = q % kTile;  // output (j0 + r, i0 + c) = tile (c, r)
-      const int64_t gi = j0 + r, gj = i0 + c;
-      if (gi < dim && gj < dim) A[gi * dim + gj] = Cs[c * (kTile + 4) + r];
+  const float sc = p.scale;
+#pragma unroll
+  for (int a = 0; a < 8; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int64_t gi = i0 + wm * 128 + a * 16 + 4 * fg;
+      const int64_t gj = j0 + wn * 64 + b * 16 + fr;
+      if (gi < dim && gj < dim) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) A[(gi + v) * dim + gj] = acc[a][b][v] * sc;
+        // mirror: (gj, gi..gi+3) is 16 contiguous bytes (dim % 8 == 0)
+        if (ti != tj)
+          *reinterpret_cast<float4 *>(A + gj * dim + gi) =
+              make_float4(acc[a][b][0] * sc, acc[a][b][1] * sc, acc[a][b][2] * sc, acc[a][b][3] * sc);
+      }
     }
-  }
 }
 
 }  // namespace
@@ -193,9 +219,13 @@ gift_status launch_syrk_bf16(gift_ctx *ctx, const uint16_t *const *x_table, int 
   a.dim = dim;
   a.scale = scale;
   const int64_t nt = (dim + kTile - 1) / kTile;
+  const int64_t total = (int64_t)members * (nt * (nt + 1) / 2);
+  if (total > (1LL << 30)) return set_error(GIFT_ESHAPE, "internal: too many statistics tiles");
+  a.tiles = (int)(nt * (nt + 1) / 2);
+  a.total = (int)total;
+  a.per_xcd = (int)((total + kXcds - 1) / kXcds);
   ProfileScope prof(ctx, GIFT_KERNEL_SYRK);
-  hipLaunchKernelGGL(syrk_bf16_kernel, dim3((unsigned)(nt * (nt + 1) / 2), 1, (unsigned)members),
-                     dim3(kThreads), 0, ctx->stream, a);
+  hipLaunchKernelGGL(syrk_bf16_kernel, dim3((unsigned)(a.per_xcd * kXcds)), dim3(kThreads), 0, ctx->stream, a);
   return check_launch("syrk_bf16_kernel");
 }
 

@@ -54,11 +54,13 @@ def _load():
         "gift_ctx_set_stream": ([P, P], I32),
         "gift_ctx_destroy": ([P], None),
         "gift_ctx_profile_enable": ([P, I32], I32),
+        "gift_ctx_profile_select": ([P, ctypes.c_uint32], I32),
         "gift_ctx_profile_read": ([P, I32, ctypes.POINTER(I64), ctypes.POINTER(ctypes.c_double)], I32),
         "gift_ctx_profile_reset": ([P], I32),
         "gift_factor_create": ([P, I64, I64, I32, I32, F, U64, PP], I32),
         "gift_factor_destroy": ([P], None),
         "gift_factor_update": ([P, P, P, P, I64, I32, I32], I32),
+        "gift_statistics": ([P, P, I64, I64, I32, P], I32),
         "gift_factor_update_batch": ([P, I32, P, P, P, I64, I32, I32], I32),
         "gift_factor_export": ([P, P, I32, P, P, P, P], I32),
         "gift_factor_import": ([P, P, I32, P, P, P, P], I32),
@@ -128,6 +130,16 @@ class Context:
 
     def profile(self, enable: bool = True):
         _check(LIB.gift_ctx_profile_enable(self._h, 1 if enable else 0))
+
+    def profile_select(self, families=None):
+        """Time only these kernel families (names or ids; None = all)."""
+        if families is None:
+            mask = 0xFFFFFFFF
+        else:
+            mask = 0
+            for k in families:
+                mask |= 1 << (KERNELS[k] if isinstance(k, str) else int(k))
+        _check(LIB.gift_ctx_profile_select(self._h, mask))
 
     def profile_read(self, kernel):
         k = KERNELS[kernel] if isinstance(kernel, str) else int(kernel)
@@ -254,6 +266,18 @@ def factor_update_batch(ctx: Context, factors, acts=None, out_grads=None, iters:
     aa = arr(*[(_ptr(x).value if x is not None else None) for x in acts])
     ga = arr(*[(_ptr(x).value if x is not None else None) for x in out_grads])
     _check(LIB.gift_factor_update_batch(ctx.handle, count, fa, aa, ga, T, dt, iters))
+
+
+def statistics(ctx: Context, x, A):
+    """``gift_statistics``: x [T, dim] (float32 or bfloat16) -> A [dim, dim] = x^T x / T."""
+    import torch
+    if x.dim() != 2:
+        raise ValueError("x must be [T, dim]")
+    T, dim = x.shape
+    if tuple(A.shape) != (dim, dim):
+        raise ValueError("A must be [dim, dim]")
+    _check(LIB.gift_statistics(ctx.handle, _ptr(x, None, "x"), T, dim, _stats_dtype(x),
+                               _ptr(A, torch.float32, "A")))
 
 
 def encode(ctx: Context, factor, grads, codes, scales, block_rows: int = 0, block_cols: int = 0,

@@ -128,11 +128,13 @@ def factor_inputs(seed: int, T: int, dim: int, decay: float = 1.2,
 
 
 def _torch_haar(torch, gen, rows, cols, device):
+    # The Gaussian block is drawn on the device; its QR runs on the host in
+    # float64 (numpy), which keeps the GPU solver library out of the process.
     z = torch.randn(rows, cols, generator=gen, device=device, dtype=torch.float32)
-    q, r = torch.linalg.qr(z)
-    d = torch.sign(torch.diagonal(r))
+    q, r = np.linalg.qr(z.cpu().numpy().astype(np.float64))
+    d = np.sign(np.diagonal(r))
     d[d == 0] = 1.0
-    return q * d
+    return torch.from_numpy((q * d).astype(np.float32)).to(device)
 
 
 def gradient_set_torch(seed: int, N: int, m: int, n: int, device,

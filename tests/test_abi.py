@@ -95,11 +95,25 @@ def test_factor_validation(ctx):
     assert mk(h, 8, 8, 1, 1, 0.0, 0, None) == gift.EINVAL
 
 
+def test_statistics_validation(ctx):
+    h = ctx.handle
+    st = LIB.gift_statistics
+    assert st(None, FAKE, 8, 8, 1, FAKE) == gift.EINVAL
+    assert st(h, None, 8, 8, 1, FAKE) == gift.EINVAL
+    assert st(h, FAKE, 8, 8, 1, None) == gift.EINVAL
+    assert st(h, FAKE, 8, 8, 5, FAKE) == gift.EINVAL        # dtype
+    assert st(h, FAKE, 0, 8, 1, FAKE) == gift.ESHAPE
+    assert st(h, FAKE, 8, -4, 1, FAKE) == gift.ESHAPE
+    assert st(h, FAKE, 8, 2_000_000, 1, FAKE) == gift.ESHAPE
+
+
 def test_profile_api_host_side(ctx):
     h = ctx.handle
     n = ctypes.c_int64()
     ms = ctypes.c_double()
     assert LIB.gift_ctx_profile_read(h, 99, ctypes.byref(n), ctypes.byref(ms)) == gift.EINVAL
+    assert LIB.gift_ctx_profile_select(None, 1) == gift.EINVAL
+    assert LIB.gift_ctx_profile_select(h, 1 << 7) == gift.OK
     assert LIB.gift_ctx_profile_enable(h, 1) == gift.OK
     # nothing recorded yet: reading makes no HIP call
     assert LIB.gift_ctx_profile_read(h, 0, ctypes.byref(n), ctypes.byref(ms)) == gift.OK
