@@ -44,11 +44,16 @@ constexpr int kXcds = 8;         // MI355X: 8 XCDs of 32 CUs, each with its own 
 
 // LDS layout of one operand: [feature row][32 words], word w of row R holds
 // tokens (2w, 2w+1) of that feature.  Words are grouped in 2-word slots
-// (4 tokens); slot s of row R is stored at slot s ^ swz(R).  swz(R) is even,
-// so the two slots of an aligned 16-byte fragment stay adjacent and in order,
-// while the rows written by one store instruction and the rows read by one
-// 128-byte phase of a fragment load land in different banks.
+// (4 tokens); slot s of row R is stored at slot s ^ swz(R) of physical row
+// prow(R).  swz(R) is even, so the two slots of an aligned 16-byte fragment
+// stay adjacent and in order.  Bank spread: a fragment read covers 16
+// consecutive rows, whose (row parity, swz) pairs are all distinct; a store
+// instruction writes rows 8 apart (one feature of each lane's 8), for which
+// swz varies with bits 0-2 of the lane's feature group, the 128-byte half of
+// the bank window with bit 3 (prow swaps adjacent rows when row bit 6 is
+// set), and slot bit 0 with the lane's token quad.
 __device__ __forceinline__ int swz(int row) { return 2 * ((row & 7) ^ ((row >> 3) & 7)); }
+__device__ __forceinline__ int prow(int row) { return row ^ ((row >> 6) & 1); }
 
 __device__ __forceinline__ void pack_pairs(const uint4 &lo, const uint4 &hi, uint32_t w[8]) {
   // lo: features f..f+7 of token t; hi: the same features of token t+1.
@@ -92,10 +97,12 @@ void syrk_bf16_kernel(const SyrkArgs p) {
   const uint16_t *X = p.X[member];
   const int64_t T = p.T, dim = p.dim;
 
-  // load mapping: lane -> feature group fgp (8 features = 16 bytes of a token
-  // row; 32 consecutive lanes read 512 contiguous bytes) and token quad tqb
-  // (4 tokens = 2 pair words = one slot)
-  const int fgp = tid & 31, tqb = tid >> 5;
+  // load mapping: thread -> feature group fgp (8 features = 16 bytes of a
+  // token row) and token quad tqb (4 tokens = 2 pair words = one slot):
+  // tid bits 0-2, 4, 6 -> fgp bits 0-4; tid bits 3, 5, 7, 8 -> tqb bits 0-3.
+  // Eight consecutive lanes read 128 contiguous bytes of one token row.
+  const int fgp = (tid & 7) | (((tid >> 4) & 1) << 3) | (((tid >> 6) & 1) << 4);
+  const int tqb = ((tid >> 3) & 1) | (((tid >> 5) & 1) << 1) | ((tid >> 7) << 2);
   const int64_t fi = i0 + 8 * fgp, fj = j0 + 8 * fgp;
   // Buffer loads: the resource of a stage starts at token t0 and covers only
   // the tokens that exist, so reads past T come back as zero from the range
@@ -127,14 +134,14 @@ void syrk_bf16_kernel(const SyrkArgs p) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int row = 8 * fgp + e;
-      *reinterpret_cast<uint2 *>(As + row * kRowWords + 2 * (tq ^ swz(row))) = make_uint2(w01[e], w23[e]);
+      *reinterpret_cast<uint2 *>(As + prow(row) * kRowWords + 2 * (tq ^ swz(row))) = make_uint2(w01[e], w23[e]);
     }
     pack_pairs(rb[0], rb[1], w01);
     pack_pairs(rb[2], rb[3], w23);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int row = 8 * fgp + e;
-      *reinterpret_cast<uint2 *>(Bs + row * kRowWords + 2 * (tq ^ swz(row))) = make_uint2(w01[e], w23[e]);
+      *reinterpret_cast<uint2 *>(Bs + prow(row) * kRowWords + 2 * (tq ^ swz(row))) = make_uint2(w01[e], w23[e]);
     }
   };
 
@@ -164,13 +171,13 @@ void syrk_bf16_kernel(const SyrkArgs p) {
 #pragma unroll
       for (int a = 0; a < 8; ++a) {
         const int row = wm * 128 + a * 16 + fr;
-        const uint4 v = *reinterpret_cast<const uint4 *>(As + row * kRowWords + 2 * (slot ^ swz(row)));
+        const uint4 v = *reinterpret_cast<const uint4 *>(As + prow(row) * kRowWords + 2 * (slot ^ swz(row)));
         af[a] = __builtin_bit_cast(bf16x8, v);
       }
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
         const int row = wn * 64 + b * 16 + fr;
-        const uint4 v = *reinterpret_cast<const uint4 *>(Bs + row * kRowWords + 2 * (slot ^ swz(row)));
+        const uint4 v = *reinterpret_cast<const uint4 *>(Bs + prow(row) * kRowWords + 2 * (slot ^ swz(row)));
         bfr[b] = __builtin_bit_cast(bf16x8, v);
       }
 #pragma unroll
