@@ -22,7 +22,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libgift.so")
 ARCH = "gfx950"
 
-SOURCES = ["gift_api.cpp", "k_tile.hip", "k_reduce.hip", "k_factor.hip", "k_syrk.hip", "k_update.hip", "k_stream.hip"]
+SOURCES = ["gift_api.cpp", "k_tile.hip", "k_reduce.hip", "k_factor.hip", "k_syrk.hip", "k_update.hip", "k_stream.hip", "k_lowrank.hip"]
 
 
 def hipcc() -> str:

@@ -1,7 +1,14 @@
-// OCP FP8 E4M3 (E4M3FN) conversion on the GPU, written from the format
-// definition: 1 sign bit, 4 exponent bits (bias 7), 3 mantissa bits,
-// subnormals at exponent field 0, largest finite 448 = S.1111.110,
-// NaN = S.1111.111, no infinities.
+// OCP FP8 E4M3 (E4M3FN) conversion on the GPU: 1 sign bit, 4 exponent bits
+// (bias 7), 3 mantissa bits, subnormals at exponent field 0, largest finite
+// 448 = S.1111.110, NaN = S.1111.111, no infinities.
+//
+// gfx950's conversions between float32 and FP8 use the OCP E4M3 format:
+// v_cvt_pk_fp8_f32 rounds to nearest even and v_cvt_pk_f32_fp8 is exact.
+// The codec's quantizer is "round to nearest even, saturating at +-448,
+// keeping the sign of zero, NaN -> 0x7F": the hardware conversion of the value
+// clamped to [-448, 448] (clamping keeps -0.0 and maps +-inf to +-448), with
+// NaN inputs set to 0x7F afterwards (the clamp would have turned them into
+// -448).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -11,39 +18,40 @@ namespace gift {
 
 constexpr float kE4M3Max = 448.0f;
 
-// Round-to-nearest-even E4M3 code of a float, saturating at +-448, keeping
-// the sign of zero; NaN -> 0x7F.
-__device__ __forceinline__ uint32_t e4m3_encode(float y) {
-  const uint32_t u = __float_as_uint(y);
-  const uint32_t sign = (u >> 24) & 0x80u;
-  const uint32_t a = u & 0x7fffffffu;
-  if (a > 0x7f800000u) return 0x7fu;                 // NaN
-  if (a >= 0x43e00000u) return sign | 0x7eu;         // |y| >= 448 (and inf)
-  if (a < 0x3c800000u) {                             // |y| < 2^-6: spacing 2^-9
-    // |y| * 2^9 is exact; rint rounds half to even -> 0..8 (8 = min normal)
-    const float t = __uint_as_float(a) * 512.0f;
-    return sign | (uint32_t)__builtin_rintf(t);
-  }
-  // normal binade: drop 20 of the 23 mantissa bits with round-half-even on
-  // the exponent|mantissa field (a carry moves into the exponent), then
-  // rebias the exponent from 127 to 7.  |y| < 448 keeps the result <= 0x7e.
-  const uint32_t rounded = (a + 0x7ffffu + ((a >> 20) & 1u)) >> 20;
-  return sign | (rounded - (120u << 3));
+__device__ __forceinline__ float e4m3_clamp(float y) { return fminf(fmaxf(y, -kE4M3Max), kE4M3Max); }
+
+// Codes of four floats packed little-endian (value e in byte e).
+__device__ __forceinline__ uint32_t e4m3_encode4(float y0, float y1, float y2, float y3) {
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(e4m3_clamp(y0), e4m3_clamp(y1), 0, false);
+  w = __builtin_amdgcn_cvt_pk_fp8_f32(e4m3_clamp(y2), e4m3_clamp(y3), w, true);
+  uint32_t u = (uint32_t)w;
+  if (y0 != y0) u = (u & 0xffffff00u) | 0x0000007fu;
+  if (y1 != y1) u = (u & 0xffff00ffu) | 0x00007f00u;
+  if (y2 != y2) u = (u & 0xff00ffffu) | 0x007f0000u;
+  if (y3 != y3) u = (u & 0x00ffffffu) | 0x7f000000u;
+  return u;
 }
 
-// Exact float value of an E4M3 code (NaN for 0x7F / 0xFF).
+// Round-to-nearest-even E4M3 code of one float (saturating, sign of zero
+// kept, NaN -> 0x7F).
+__device__ __forceinline__ uint32_t e4m3_encode(float y) {
+  const uint32_t u = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(e4m3_clamp(y), 0.0f, 0, false) & 0xffu;
+  return y != y ? 0x7fu : u;
+}
+
+// Exact float values of the four codes packed in a word (NaN for 0x7F / 0xFF).
+__device__ __forceinline__ void e4m3_decode4(uint32_t w, float v[4]) {
+  const auto lo = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, false);
+  const auto hi = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, true);
+  v[0] = lo[0];
+  v[1] = lo[1];
+  v[2] = hi[0];
+  v[3] = hi[1];
+}
+
+// Exact float value of one E4M3 code.
 __device__ __forceinline__ float e4m3_decode(uint32_t c) {
-  const uint32_t sign = (c & 0x80u) << 24;
-  const uint32_t e = (c >> 3) & 0xfu;
-  const uint32_t mant = c & 0x7u;
-  float v;
-  if (e == 0) {
-    v = (float)mant * 0.001953125f;                  // mant * 2^-9, exact
-  } else {
-    v = __uint_as_float(((e + 120u) << 23) | (mant << 20));
-  }
-  v = __uint_as_float(__float_as_uint(v) | sign);
-  return (e == 0xfu && mant == 0x7u) ? __uint_as_float(0x7fc00000u) : v;
+  return __builtin_amdgcn_cvt_pk_f32_fp8((int)(c & 0xffu), false)[0];
 }
 
 // Stored (dequantization) scale s = fl32(a / 448).

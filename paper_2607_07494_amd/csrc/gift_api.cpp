@@ -190,6 +190,24 @@ gift_status check_matrix_dims(int64_t m, int64_t n) {
   return GIFT_OK;
 }
 
+bool al16p(const void *q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; }
+
+// The encode recomputes W~ in its quantize pass, instead of storing it and
+// reading it back, when the split-bf16 update kernel takes the job: with
+// cheap products, reading W again (4 B per element) costs less than writing
+// and reading W~ (8 B).  Conditions mirror lr_update_eligible.
+bool encode_recomputes(const gift_factor *f, int64_t n, const float *grads, const float *ef,
+                       const uint8_t *codes, const float *transformed) {
+  const bool useA = side_in(f->sides, GIFT_SIDE_INPUT) && f->A.r > 0;
+  const bool useG = side_in(f->sides, GIFT_SIDE_OUTPUT) && f->G.r > 0;
+  if (!useA && !useG) return false;
+  if (useA && useG && f->A.r != f->G.r) return false;
+  const int K = useA ? f->A.r : f->G.r;
+  if (K > 128 || K % 4 != 0 || n % 4 != 0) return false;
+  return al16p(grads) && (!ef || al16p(ef)) && (!transformed || al16p(transformed)) &&
+         (reinterpret_cast<uintptr_t>(codes) & 3) == 0;
+}
+
 // W~ = W + (low-rank part of the transform) for all N ranks.  Fills the
 // projection buffers in `ws` and returns the update as a tile job (without
 // epilogue fields); side inverse=true builds the decode's S_G M S_A update.
@@ -210,11 +228,10 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
   const int64_t mn = m * n;
   // input side alone: the projection may split its contraction into partials
   // that the update kernel sums (same conditions as that kernel's)
+  // (the encode's split-bf16 projection has its own partial count)
   const bool aligned = (reinterpret_cast<uintptr_t>(W) & 15) == 0;
-  const int pparts = useA && !useG && aligned && n % 4 == 0 &&
-                             (A.r == 16 || A.r == 32 || A.r == 64 || A.r == 128)
-                         ? proj_parts(m, n, A.r, N)
-                         : 1;
+  const bool pp_ok = useA && !useG && aligned && n % 4 == 0 && (A.r == 16 || A.r == 32 || A.r == 64 || A.r == 128);
+  const int pparts = !pp_ok ? 1 : (inverse ? proj_parts(m, n, A.r, N) : lr_proj_parts(m, n, N));
   size_t off = 0;
   float *P = nullptr, *Qm = nullptr, *Km = nullptr, *L2 = nullptr;
   if (useA) {
@@ -248,6 +265,7 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
     j.ldc = A.r;
     j.cbs = m * A.r;
     j.ksplit = pparts;
+    j.split3 = !inverse;
     j.kernel_family = GIFT_KERNEL_PROJECT;
     if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
   }
@@ -308,6 +326,7 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
   u.N = n;
   u.batch = N;
   u.nseg = 0;
+  u.split3 = !inverse;
   if (useG) {  // (U_G C_G) Q, with B(k, j) = Q[k][j] = Qm[j][k]
     Segment &s = u.seg[u.nseg++];
     s.a = Operand{UcG, G.r, 0, true};
@@ -606,11 +625,14 @@ gift_status gift_encode(gift_ctx *ctx, const gift_factor *f, const float *grads,
   size_t proj_bytes = 0;
   if (f && (st = plan_low_rank(ctx, f, grads, N, m, n, false, nullptr, &proj_bytes, &plan)) != GIFT_OK)
     return st;
-  // With a transform, the AMAX pass stores W~ (+ R) and the QUANT pass streams
-  // it instead of recomputing the rank-r update: scratch unless the caller
-  // asked for W~ itself.
+  // With a transform, the AMAX pass computes W~ (+ R) for the block maxima and
+  // the QUANT pass computes it again (same kernel arithmetic, so the same
+  // values) when the split-bf16 kernels take the job; otherwise the AMAX pass
+  // stores W~ (scratch unless the caller asked for it) and the QUANT pass
+  // streams it.
   const bool gemm = f && plan.active;
-  const bool store_wt = gemm && n % 4 == 0 && g.bc % 4 == 0;
+  const bool recompute = gemm && encode_recomputes(f, n, grads, ef, codes, transformed);
+  const bool store_wt = gemm && !recompute && n % 4 == 0 && g.bc % 4 == 0;
   const size_t wt_bytes = store_wt && !transformed ? a256(sizeof(float) * (size_t)N * m * n) : 0;
   const size_t raw_words = (size_t)N * nblk * kAmaxSlots;
   uint32_t *amax_raw = nullptr, *prev_set = nullptr;
@@ -641,6 +663,9 @@ gift_status gift_encode(gift_ctx *ctx, const gift_factor *f, const float *grads,
   job.scales = scales;
   job.transformed = gemm ? wt : transformed;
   job.kernel_family = gemm ? GIFT_KERNEL_UPDATE_AMAX : GIFT_KERNEL_AMAX;
+  // both passes must take the same kernel, or their W~ would differ
+  if (recompute && !lr_update_eligible(job))
+    return set_error(GIFT_EUNSUPPORTED, "gift_encode: internal: split-bf16 update not applicable");
   if ((st = launch_tile(ctx, job)) != GIFT_OK) return st;
   job.transformed = nullptr;
   job.codes = codes;
@@ -648,7 +673,7 @@ gift_status gift_encode(gift_ctx *ctx, const gift_factor *f, const float *grads,
   // stored W~ + R with a transform, on W without); otherwise a finalize
   // launch reduces them first
   const float *qsrc = gemm ? wt : grads;
-  if (qsrc && stream_eligible(m, n, g, qsrc, codes, ef, nullptr)) {
+  if (!recompute && qsrc && stream_eligible(m, n, g, qsrc, codes, ef, nullptr)) {
     TileJob q = job;
     q.nseg = 0;
     q.D = qsrc;

@@ -180,10 +180,20 @@ struct TileJob {
   int64_t clear_words = 0;
   BlockGeom geom{};
   bool shared = false;
+  // form the products from bf16 hi/lo splits of both operands on the bf16
+  // matrix cores (k_lowrank.hip) where the shapes allow; float32 otherwise
+  bool split3 = false;
   int kernel_family = GIFT_KERNEL_FACTOR;
 };
 
 gift_status launch_tile(gift_ctx *ctx, const TileJob &job);
+// k_lowrank.hip: the encode's projection and rank-r update with split bf16
+// operands; lr_proj_parts = split-K partials of the projection
+bool lr_update_eligible(const TileJob &job);
+gift_status launch_lr_update(gift_ctx *ctx, const TileJob &job);
+bool lr_proj_eligible(const TileJob &job);
+gift_status launch_lr_proj(gift_ctx *ctx, const TileJob &job);
+int lr_proj_parts(int64_t M, int64_t K, int32_t batch);
 // k_update.hip: register-direct rank-r update / projection (used by
 // launch_tile when the job's shapes allow)
 bool update_kernel_eligible(const TileJob &job);

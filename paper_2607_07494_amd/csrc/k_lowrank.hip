@@ -1,0 +1,594 @@
+// Rank-r transform of the encode on the bf16 matrix cores.
+//
+// The forward transform W~ = W + (W U) diag(c) U^T (Sec. IV-A, eq.
+// design_input_side_transform in low-rank form; Algorithm 1's L_A step) is
+// two skinny products per rank: the projection P = W U (contraction over the
+// n columns of W) and the rank-r update W + P (U diag(c))^T (contraction over
+// r).  Both are memory-bound once their products are cheap, so they run on
+// v_mfma_f32_16x16x32_bf16 with every float32 operand x split as
+//     x = hi + lo + e,  hi = bf16(x),  lo = bf16(x - hi),  |e| <= 2^-18 |x|
+// (x - hi is exact in float32) and each product formed as
+//     a b ~ hi_a hi_b + hi_a lo_b + lo_a hi_b
+// (the omitted lo_a lo_b is below 2^-16 |a b|).  Every partial product of two
+// bf16 values is exact in float32 and the MFMA sums in float32, so W~ is
+// within a few 1e-6 (relative Frobenius) of the float64 transform, where a
+// float32 product chain on the FP32 matrix cores would run at 1/5 of this
+// rate.  The inverse transform keeps float32 products: its coefficients
+// sqrt(lambda / sigma^2) - 1 amplify the operand error.
+//
+// MFMA layout: lane (fr, fg) = (lane % 16, lane / 16) supplies row fr and
+// eight contraction steps of each operand fragment and receives rows
+// 4 fg .. 4 fg + 3, column fr of the 16 x 16 result.  The products are set up
+// transposed (A operand = the column side, B operand = the row side) so that a
+// lane ends up with four consecutive columns of one output row.  Within a
+// 32-step chunk, lane group fg feeds contraction indices 4 fg .. 4 fg + 3 and
+// 16 + 4 fg .. 16 + 4 fg + 3: two 16-byte float32 loads per row, 64 contiguous
+// bytes per four lanes.  Both operands use this assignment, so the sum is the
+// plain dot product.
+//
+// Column-side operands are staged through LDS as split [chunk][column][fg]
+// 16-byte entries; entry fg of column c sits at fg ^ ((c >> 2) & 3), which
+// puts the 16 rows read by one 16-lane phase in distinct banks.
+
+#include <type_traits>
+
+#include "fp8_e4m3.h"
+#include "gift_internal.h"
+
+namespace gift {
+namespace {
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ float4 ld4(const float *p) { return *reinterpret_cast<const float4 *>(p); }
+__device__ __forceinline__ float4 zero4() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+// 16 bytes at p when ok, else zeros (a branch around the load, never a
+// select between addresses)
+__device__ __forceinline__ float4 ld4_if(bool ok, const float *p) {
+  float4 v = zero4();
+  if (ok) v = ld4(p);
+  return v;
+}
+
+// hi / lo bf16 pairs of two float32 values (round to nearest even)
+__device__ __forceinline__ void split2(float x, float y, uint32_t &hi, uint32_t &lo) {
+  const bf16x2 h = __builtin_convertvector((floatx2){x, y}, bf16x2);
+  hi = __builtin_bit_cast(uint32_t, h);
+  const float hx = __uint_as_float(hi << 16), hy = __uint_as_float(hi & 0xffff0000u);
+  const bf16x2 l = __builtin_convertvector((floatx2){x - hx, y - hy}, bf16x2);
+  lo = __builtin_bit_cast(uint32_t, l);
+}
+
+// eight float32 values (a: steps 0-3, b: steps 4-7) -> hi and lo fragments
+__device__ __forceinline__ void split8(const float4 &a, const float4 &b, uint4 &hi, uint4 &lo) {
+  split2(a.x, a.y, hi.x, lo.x);
+  split2(a.z, a.w, hi.y, lo.y);
+  split2(b.x, b.y, hi.z, lo.z);
+  split2(b.z, b.w, hi.w, lo.w);
+}
+
+__device__ __forceinline__ bf16x8 frag(const uint4 &v) { return __builtin_bit_cast(bf16x8, v); }
+
+__device__ __forceinline__ floatx4 mfma3(const uint4 &ahi, const uint4 &alo, const uint4 &bhi,
+                                         const uint4 &blo, floatx4 acc) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag(ahi), frag(bhi), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag(ahi), frag(blo), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag(alo), frag(bhi), acc, 0, 0, 0);
+  return acc;
+}
+
+__device__ __forceinline__ int lds_slot(int c, int g) { return 4 * c + (g ^ ((c >> 2) & 3)); }
+
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint32_t u = (uint32_t)__shfl_xor((int)v, o);
+    v = u > v ? u : v;
+  }
+  return v;
+}
+
+// ---------------------------------------------------------------------------
+// Projection: out[b][z][i][c] = sum_{k in part z} X[b][i][k] Y[c][k], c < 16 NT
+// ---------------------------------------------------------------------------
+
+constexpr int kProjThreads = 512;   // 8 waves x 16 rows
+constexpr int kProjRows = 128;
+constexpr int kProjStage = 64;      // contraction steps per LDS stage (two chunks)
+
+struct LPArgs {
+  const float *X;    // [batch][M][K], row stride K
+  int64_t x_bs;
+  const float *Y;    // [C][K] shared by the batch
+  int64_t M, K;
+  float *out;        // [batch][parts][M][C]
+  int parts;
+  int64_t kper;      // contraction steps per part (multiple of kProjStage)
+};
+
+template <int NT>
+__global__ __launch_bounds__(kProjThreads) void lr_proj_kernel(const LPArgs p) {
+  constexpr int C = 16 * NT;
+  constexpr int SLOTS = 2 * C * 4;                 // (chunk, column, fg) entries per stage
+  constexpr int PER = (SLOTS + kProjThreads - 1) / kProjThreads;
+  __shared__ uint4 yhi[2][SLOTS], ylo[2][SLOTS];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int fr = lane & 15, fg = lane >> 4;
+  const int b = blockIdx.z, z = blockIdx.y;
+  const int64_t ri = (int64_t)blockIdx.x * kProjRows + wave * 16 + fr;
+  const bool rv = ri < p.M;
+  const int64_t k0 = (int64_t)z * p.kper;
+  const int64_t k1 = k0 + p.kper < p.K ? k0 + p.kper : p.K;
+  const int nst = k1 > k0 ? (int)((k1 - k0 + kProjStage - 1) / kProjStage) : 0;
+  const float *xrow = p.X + (int64_t)b * p.x_bs + (rv ? ri : 0) * p.K;
+
+  float4 yr[PER][2], xr[2][2];
+  auto load = [&](int64_t ks) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int s = tid + u * kProjThreads;
+      const int ch = s / (4 * C), c = (s >> 2) % C, g = s & 3;
+      const int64_t k = ks + 32 * ch + 4 * g;
+      const bool ok = s < SLOTS;
+      yr[u][0] = ld4_if(ok && k < k1, p.Y + (int64_t)c * p.K + k);
+      yr[u][1] = ld4_if(ok && k + 16 < k1, p.Y + (int64_t)c * p.K + k + 16);
+    }
+#pragma unroll
+    for (int ch = 0; ch < 2; ++ch) {
+      const int64_t k = ks + 32 * ch + 4 * fg;
+      xr[ch][0] = ld4_if(rv && k < k1, xrow + k);
+      xr[ch][1] = ld4_if(rv && k + 16 < k1, xrow + k + 16);
+    }
+  };
+  auto stage_y = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int s = tid + u * kProjThreads;
+      if (s >= SLOTS) continue;
+      const int ch = s / (4 * C), c = (s >> 2) % C, g = s & 3;
+      uint4 h, l;
+      split8(yr[u][0], yr[u][1], h, l);
+      yhi[buf][ch * 4 * C + lds_slot(c, g)] = h;
+      ylo[buf][ch * 4 * C + lds_slot(c, g)] = l;
+    }
+  };
+
+  floatx4 acc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  if (nst > 0) {
+    load(k0);
+    stage_y(0);
+  }
+  __syncthreads();
+  for (int st = 0; st < nst; ++st) {
+    const int buf = st & 1;
+    uint4 xh[2], xl[2];
+#pragma unroll
+    for (int ch = 0; ch < 2; ++ch) split8(xr[ch][0], xr[ch][1], xh[ch], xl[ch]);
+    const bool more = st + 1 < nst;
+    if (more) load(k0 + (int64_t)(st + 1) * kProjStage);
+#pragma unroll
+    for (int ch = 0; ch < 2; ++ch)
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const int e = ch * 4 * C + lds_slot(16 * t + fr, fg);
+        acc[t] = mfma3(yhi[buf][e], ylo[buf][e], xh[ch], xl[ch], acc[t]);
+      }
+    if (more) stage_y(buf ^ 1);
+    __syncthreads();
+  }
+  if (!rv) return;
+  // lane holds part z of out[ri][16 t + 4 fg + v]
+  float *ob = p.out + (((int64_t)b * p.parts + z) * p.M + ri) * C;
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+    *reinterpret_cast<float4 *>(ob + 16 * t + 4 * fg) = make_float4(acc[t][0], acc[t][1], acc[t][2], acc[t][3]);
+}
+
+// ---------------------------------------------------------------------------
+// Update: W~[b][i][j] = D[b][i][j] + sum_s sum_k Row_s[b][i][k] Col_s[b][j][k]
+//         (+ R[b][i][j]), fused with the block maxima (EPI_AMAX) or with the
+//         scale, E4M3 pack and residual update (EPI_QUANT)
+// ---------------------------------------------------------------------------
+
+constexpr int kUpdThreads = 256;    // 4 waves x 32 rows
+constexpr int kUpdRows = 128;
+constexpr int kUpdCols = 256;       // columns per workgroup, walked in 64-column tiles
+
+struct LUSeg {
+  const float *row;   // [batch][parts][M][K] (row_bs = 0: shared by the batch)
+  int64_t row_ld, row_bs;
+  int row_parts;      // split-K partials summed in order on load
+  const float *col;   // [batch][N][K] (col_bs = 0: shared)
+  int64_t col_ld, col_bs;
+  int K;
+};
+
+struct LUArgs {
+  LUSeg seg[2];
+  int64_t M, N;
+  const float *D;       // [batch][M][N]
+  uint32_t *amax;       // AMAX: raw sub-slots; QUANT: finished maxima [batch][nbr][nbc]
+  uint8_t *codes;
+  float *transformed;   // AMAX: optional W~ (+ R) out
+  float *ef;            // residual (read; QUANT also writes it)
+  int64_t br, bc;
+  int nbr, nbc;
+};
+
+template <int EPI, bool EF, int NSEG, int KC>
+__global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) {
+  constexpr int NCH = NSEG * KC;          // 32-step chunks over all segments
+  constexpr int SLOTS = NCH * 64 * 4;     // (chunk, column, fg) entries of a 64-column tile
+  constexpr int PER = SLOTS / kUpdThreads;  // = NCH
+  __shared__ uint4 chi[2][SLOTS], clo[2][SLOTS];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int fr = lane & 15, fg = lane >> 4;
+  const int b = blockIdx.z;
+  const int64_t i0 = (int64_t)blockIdx.y * kUpdRows + wave * 32;
+  const int64_t MN = p.M * p.N;
+  const int64_t c_begin = (int64_t)blockIdx.x * kUpdCols;
+  const int64_t c_end = c_begin + kUpdCols < p.N ? c_begin + kUpdCols : p.N;
+  const int ntiles = (int)((c_end - c_begin + 63) / 64);
+  const bool wave_live = i0 < p.M;
+  const int slot = (int)((((int64_t)blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x) * 4 + wave) %
+                   kAmaxSlots;
+  int64_t ri[2];
+  bool rv[2];
+#pragma unroll
+  for (int g = 0; g < 2; ++g) {
+    ri[g] = i0 + 16 * g + fr;
+    rv[g] = ri[g] < p.M;
+  }
+
+  // row-side fragments of the wave's 32 rows, split once for all tiles
+  uint4 rh[2][NCH], rl[2][NCH];
+#pragma unroll
+  for (int g = 0; g < 2; ++g)
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch) {
+      const LUSeg &sg = p.seg[ch / KC];
+      const int64_t k = 32 * (ch % KC) + 4 * fg;
+      float4 v0 = zero4(), v1 = zero4();
+      if (rv[g]) {
+        const float *base = sg.row + (int64_t)b * sg.row_parts * sg.row_bs + ri[g] * sg.row_ld;
+        for (int zp = 0; zp < sg.row_parts; ++zp) {
+          const float *q = base + (int64_t)zp * sg.row_bs;
+          const float4 a = ld4_if(k < sg.K, q + k);
+          const float4 c = ld4_if(k + 16 < sg.K, q + k + 16);
+          if (zp == 0) {
+            v0 = a;
+            v1 = c;
+          } else {
+            v0.x += a.x; v0.y += a.y; v0.z += a.z; v0.w += a.w;
+            v1.x += c.x; v1.y += c.y; v1.z += c.z; v1.w += c.w;
+          }
+        }
+      }
+      split8(v0, v1, rh[g][ch], rl[g][ch]);
+    }
+
+  // column-side tile: entry s -> (chunk, column, fg); two float4 per entry
+  float4 cr[PER][2];
+  auto load_cols = [&](int64_t j0) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int s = tid + u * kUpdThreads;
+      const int ch = s / 256, c = (s >> 2) & 63, g = s & 3;
+      const LUSeg &sg = p.seg[ch / KC];
+      const int64_t k = 32 * (ch % KC) + 4 * g;
+      const int64_t j = j0 + c;
+      const float *q = sg.col + (int64_t)b * sg.col_bs + (j < p.N ? j : 0) * sg.col_ld;
+      cr[u][0] = ld4_if(j < p.N && k < sg.K, q + k);
+      cr[u][1] = ld4_if(j < p.N && k + 16 < sg.K, q + k + 16);
+    }
+  };
+  auto stage_cols = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int s = tid + u * kUpdThreads;
+      const int ch = s / 256, c = (s >> 2) & 63, g = s & 3;
+      uint4 h, l;
+      split8(cr[u][0], cr[u][1], h, l);
+      chi[buf][ch * 256 + lds_slot(c, g)] = h;
+      clo[buf][ch * 256 + lds_slot(c, g)] = l;
+    }
+  };
+  // W (and residual) values of the wave's 32 x 64 tile: lane holds row
+  // ri[g], columns j0 + 16 t + 4 fg .. + 3
+  float4 d[2][4], rr[2][4];
+  auto load_w = [&](int64_t j0) {
+#pragma unroll
+    for (int g = 0; g < 2; ++g)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int64_t cj = j0 + 16 * t + 4 * fg;
+        const bool ok = rv[g] && cj < p.N;
+        const int64_t off = (int64_t)b * MN + ri[g] * p.N + cj;
+        d[g][t] = ld4_if(ok, p.D + off);
+        if (EF) rr[g][t] = ld4_if(ok, p.ef + off);
+      }
+  };
+
+  uint32_t run_max = 0u;
+  int64_t run_blk = -1;
+  load_cols(c_begin);
+  load_w(c_begin);
+  stage_cols(0);
+  __syncthreads();
+  for (int ct = 0; ct < ntiles; ++ct) {
+    const int buf = ct & 1;
+    const int64_t j0 = c_begin + 64 * ct;
+    const bool more = ct + 1 < ntiles;
+    float4 dc[2][4], rc[2][4];
+#pragma unroll
+    for (int g = 0; g < 2; ++g)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        dc[g][t] = d[g][t];
+        if (EF) rc[g][t] = rr[g][t];
+      }
+    if (more) {
+      load_cols(j0 + 64);
+      load_w(j0 + 64);
+    }
+    floatx4 acc[2][4];
+#pragma unroll
+    for (int g = 0; g < 2; ++g)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) acc[g][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int e = ch * 256 + lds_slot(16 * t + fr, fg);
+        const uint4 ah = chi[buf][e], al = clo[buf][e];
+#pragma unroll
+        for (int g = 0; g < 2; ++g) acc[g][t] = mfma3(ah, al, rh[g][ch], rl[g][ch], acc[g][t]);
+      }
+    if (more) stage_cols(buf ^ 1);
+
+    if (wave_live) {
+      float w[2][4][4];
+#pragma unroll
+      for (int g = 0; g < 2; ++g)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          w[g][t][0] = dc[g][t].x + acc[g][t][0];
+          w[g][t][1] = dc[g][t].y + acc[g][t][1];
+          w[g][t][2] = dc[g][t].z + acc[g][t][2];
+          w[g][t][3] = dc[g][t].w + acc[g][t][3];
+          if (EF) {
+            w[g][t][0] += rc[g][t].x;
+            w[g][t][1] += rc[g][t].y;
+            w[g][t][2] += rc[g][t].z;
+            w[g][t][3] += rc[g][t].w;
+          }
+        }
+      // scale-block geometry of the wave tile (wave-uniform, two divisions)
+      const int64_t rlast = i0 + 31 < p.M ? i0 + 31 : p.M - 1;
+      const int64_t clast = j0 + 63 < p.N ? j0 + 63 : p.N - 1;
+      const int bi_lo = __builtin_amdgcn_readfirstlane((int)(i0 / p.br));
+      const int bj_lo = __builtin_amdgcn_readfirstlane((int)(j0 / p.bc));
+      const bool uniform = (int64_t)(bi_lo + 1) * p.br > rlast && (int64_t)(bj_lo + 1) * p.bc > clast;
+      const int64_t u_gb = (int64_t)bi_lo * p.nbc + bj_lo;
+      const int64_t nblk = (int64_t)p.nbr * p.nbc;
+      if (EPI == EPI_AMAX) {
+        if (p.transformed) {
+#pragma unroll
+          for (int g = 0; g < 2; ++g)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              const int64_t cj = j0 + 16 * t + 4 * fg;
+              if (rv[g] && cj < p.N)
+                *reinterpret_cast<float4 *>(p.transformed + (int64_t)b * MN + ri[g] * p.N + cj) =
+                    make_float4(w[g][t][0], w[g][t][1], w[g][t][2], w[g][t][3]);
+            }
+        }
+        if (uniform) {
+          uint32_t m = 0u;
+#pragma unroll
+          for (int g = 0; g < 2; ++g)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              const int64_t cj = j0 + 16 * t + 4 * fg;
+              if (rv[g] && cj < p.N) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  const uint32_t a = __float_as_uint(w[g][t][e]) & 0x7fffffffu;
+                  m = a > m ? a : m;
+                }
+              }
+            }
+          m = wave_max_u32(m);
+          if (u_gb != run_blk) {
+            if (run_blk >= 0 && lane == 0 && run_max)
+              atomicMax(&p.amax[((int64_t)b * nblk + run_blk) * kAmaxSlots + slot], run_max);
+            run_blk = u_gb;
+            run_max = 0u;
+          }
+          run_max = m > run_max ? m : run_max;
+        } else {
+          // a block edge cuts the tile: per element
+#pragma unroll
+          for (int g = 0; g < 2; ++g)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              const int64_t cj = j0 + 16 * t + 4 * fg;
+              if (!(rv[g] && cj < p.N)) continue;
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const uint32_t a = __float_as_uint(w[g][t][e]) & 0x7fffffffu;
+                const int64_t gb = (ri[g] / p.br) * p.nbc + (cj + e) / p.bc;
+                if (a) atomicMax(&p.amax[((int64_t)b * nblk + gb) * kAmaxSlots + slot], a);
+              }
+            }
+        }
+      } else {  // EPI_QUANT with finished block maxima
+        float u_inv = 0.f, u_s = 0.f;
+        if (uniform) {
+          const float a = __uint_as_float(p.amax[(int64_t)b * nblk + u_gb]);
+          u_inv = e4m3_multiplier(a);
+          u_s = e4m3_scale(a);
+        }
+#pragma unroll
+        for (int g = 0; g < 2; ++g)
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const int64_t cj = j0 + 16 * t + 4 * fg;
+            if (!(rv[g] && cj < p.N)) continue;
+            float inv[4] = {u_inv, u_inv, u_inv, u_inv}, sc[4] = {u_s, u_s, u_s, u_s};
+            if (!uniform) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const float a = __uint_as_float(p.amax[(int64_t)b * nblk + (ri[g] / p.br) * p.nbc + (cj + e) / p.bc]);
+                inv[e] = e4m3_multiplier(a);
+                sc[e] = e4m3_scale(a);
+              }
+            }
+            const uint32_t packed = e4m3_encode4(w[g][t][0] * inv[0], w[g][t][1] * inv[1], w[g][t][2] * inv[2],
+                                                 w[g][t][3] * inv[3]);
+            float res[4];
+            if (EF) {
+              float q[4];
+              e4m3_decode4(packed, q);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) res[e] = w[g][t][e] - q[e] * sc[e];
+            }
+            const int64_t off = (int64_t)b * MN + ri[g] * p.N + cj;
+            *reinterpret_cast<uint32_t *>(p.codes + off) = packed;
+            if (EF) *reinterpret_cast<float4 *>(p.ef + off) = make_float4(res[0], res[1], res[2], res[3]);
+          }
+      }
+    }
+    __syncthreads();
+  }
+  if (EPI == EPI_AMAX && wave_live && run_blk >= 0 && lane == 0 && run_max)
+    atomicMax(&p.amax[((int64_t)b * p.nbr * p.nbc + run_blk) * kAmaxSlots + slot], run_max);
+}
+
+bool al16(const void *q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; }
+
+}  // namespace
+
+int lr_proj_parts(int64_t M, int64_t K, int32_t batch) {
+  // about four workgroups per CU, each part at least two stages deep, and at
+  // most four partials (the update reads every partial back)
+  const int64_t tiles = (M + kProjRows - 1) / kProjRows * batch;
+  int parts = 1;
+  while (parts < 4 && tiles * parts < 1024 && K / (2 * parts) >= 2 * kProjStage) parts *= 2;
+  return parts;
+}
+
+bool lr_proj_eligible(const TileJob &j) {
+  const Segment &g = j.seg[0];
+  const int64_t C = j.N;
+  return j.split3 && j.nseg == 1 && j.amax == nullptr && j.D == nullptr && j.colscale == nullptr &&
+         j.alpha == 1.f && (C == 16 || C == 32 || C == 64 || C == 128) && g.a.kmajor && g.b.kmajor &&
+         g.K % 4 == 0 && g.a.ld == g.K && g.b.ld == g.K && g.b.bs == 0 && g.a.bs % 4 == 0 && al16(g.a.ptr) &&
+         al16(g.b.ptr) && al16(j.C) && j.ldc == C && j.cbs == j.M * C;
+}
+
+gift_status launch_lr_proj(gift_ctx *ctx, const TileJob &j) {
+  LPArgs a;
+  a.X = j.seg[0].a.ptr;
+  a.x_bs = j.seg[0].a.bs;
+  a.Y = j.seg[0].b.ptr;
+  a.M = j.M;
+  a.K = j.seg[0].K;
+  a.out = j.C;
+  a.parts = j.ksplit > 1 ? j.ksplit : 1;
+  a.kper = ((a.K + a.parts - 1) / a.parts + kProjStage - 1) / kProjStage * kProjStage;
+  ProfileScope prof(ctx, j.kernel_family);
+  const dim3 grid((unsigned)((a.M + kProjRows - 1) / kProjRows), (unsigned)a.parts, (unsigned)j.batch);
+  switch (j.N) {
+    case 16: hipLaunchKernelGGL(lr_proj_kernel<1>, grid, dim3(kProjThreads), 0, ctx->stream, a); break;
+    case 32: hipLaunchKernelGGL(lr_proj_kernel<2>, grid, dim3(kProjThreads), 0, ctx->stream, a); break;
+    case 64: hipLaunchKernelGGL(lr_proj_kernel<4>, grid, dim3(kProjThreads), 0, ctx->stream, a); break;
+    default: hipLaunchKernelGGL(lr_proj_kernel<8>, grid, dim3(kProjThreads), 0, ctx->stream, a); break;
+  }
+  return check_launch("lr_proj_kernel");
+}
+
+bool lr_update_eligible(const TileJob &j) {
+  if (!j.split3 || j.amax == nullptr || j.nseg < 1 || j.nseg > 2 || j.N % 4 != 0) return false;
+  const int64_t K = j.seg[0].K;
+  if (K <= 0 || K > 128 || K % 4 != 0) return false;
+  for (int s = 0; s < j.nseg; ++s) {
+    const Segment &g = j.seg[s];
+    if (!g.a.kmajor || !g.b.kmajor || g.K != K) return false;
+    if (g.a.ld % 4 || g.b.ld % 4 || g.a.bs % 4 || g.b.bs % 4) return false;
+    if (!al16(g.a.ptr) || !al16(g.b.ptr)) return false;
+  }
+  if (!al16(j.D) || j.ldd != j.N || j.dbs != j.M * j.N) return false;
+  if ((j.transformed && !al16(j.transformed)) || (j.ef && !al16(j.ef)) ||
+      (j.codes && (reinterpret_cast<uintptr_t>(j.codes) & 3)))
+    return false;
+  return true;
+}
+
+gift_status launch_lr_update(gift_ctx *ctx, const TileJob &j) {
+  LUArgs a{};
+  for (int s = 0; s < j.nseg; ++s) {
+    a.seg[s].row = j.seg[s].a.ptr;
+    a.seg[s].row_ld = j.seg[s].a.ld;
+    a.seg[s].row_bs = j.seg[s].a.bs;
+    a.seg[s].row_parts = j.seg[s].a.parts;
+    a.seg[s].col = j.seg[s].b.ptr;
+    a.seg[s].col_ld = j.seg[s].b.ld;
+    a.seg[s].col_bs = j.seg[s].b.bs;
+    a.seg[s].K = (int)j.seg[s].K;
+  }
+  a.M = j.M;
+  a.N = j.N;
+  a.D = j.D;
+  a.amax = j.amax;
+  a.codes = j.codes;
+  a.transformed = j.transformed;
+  a.ef = j.ef;
+  a.br = j.geom.br > 0 ? j.geom.br : j.M;
+  a.bc = j.geom.bc > 0 ? j.geom.bc : j.N;
+  a.nbr = j.geom.nbr;
+  a.nbc = j.geom.nbc;
+  ProfileScope prof(ctx, j.kernel_family);
+  const dim3 grid((unsigned)((j.N + kUpdCols - 1) / kUpdCols), (unsigned)((j.M + kUpdRows - 1) / kUpdRows),
+                  (unsigned)j.batch);
+  const bool quant = j.codes != nullptr;
+  const bool ef = j.ef != nullptr;
+  const int kc = (int)((j.seg[0].K + 31) / 32);
+  auto go = [&](auto epi_c, auto ef_c, auto nseg_c, auto kc_c) {
+    hipLaunchKernelGGL((lr_update_kernel<decltype(epi_c)::value, decltype(ef_c)::value, decltype(nseg_c)::value,
+                                         decltype(kc_c)::value>),
+                       grid, dim3(kUpdThreads), 0, ctx->stream, a);
+  };
+  auto by_k = [&](auto epi_c, auto ef_c, auto nseg_c) {
+    switch (kc) {
+      case 1: go(epi_c, ef_c, nseg_c, std::integral_constant<int, 1>{}); break;
+      case 2: go(epi_c, ef_c, nseg_c, std::integral_constant<int, 2>{}); break;
+      case 3: go(epi_c, ef_c, nseg_c, std::integral_constant<int, 3>{}); break;
+      default: go(epi_c, ef_c, nseg_c, std::integral_constant<int, 4>{}); break;
+    }
+  };
+  auto by_seg = [&](auto epi_c, auto ef_c) {
+    if (j.nseg == 1) by_k(epi_c, ef_c, std::integral_constant<int, 1>{});
+    else by_k(epi_c, ef_c, std::integral_constant<int, 2>{});
+  };
+  using T_ = std::true_type;
+  using F_ = std::false_type;
+  using AMAX_ = std::integral_constant<int, EPI_AMAX>;
+  using QUANT_ = std::integral_constant<int, EPI_QUANT>;
+  if (!quant) {
+    if (ef) by_seg(AMAX_{}, T_{});
+    else by_seg(AMAX_{}, F_{});
+  } else {
+    if (ef) by_seg(QUANT_{}, T_{});
+    else by_seg(QUANT_{}, F_{});
+  }
+  return check_launch("lr_update_kernel");
+}
+
+}  // namespace gift

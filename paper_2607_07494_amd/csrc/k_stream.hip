@@ -206,13 +206,13 @@ __global__ __launch_bounds__(kThreads) void stream_quant_kernel(const SArgs p) {
       const float4 e = ld4(p.ef_in + (int64_t)w.b * mn + off);
       v.x += e.x; v.y += e.y; v.z += e.z; v.w += e.w;
     }
-    const uint32_t c0 = e4m3_encode(v.x * inv), c1 = e4m3_encode(v.y * inv);
-    const uint32_t c2 = e4m3_encode(v.z * inv), c3 = e4m3_encode(v.w * inv);
-    *reinterpret_cast<uint32_t *>(p.codes + (int64_t)w.b * mn + off) = c0 | (c1 << 8) | (c2 << 16) | (c3 << 24);
+    const uint32_t packed = e4m3_encode4(v.x * inv, v.y * inv, v.z * inv, v.w * inv);
+    *reinterpret_cast<uint32_t *>(p.codes + (int64_t)w.b * mn + off) = packed;
     if (EF) {
+      float q[4];
+      e4m3_decode4(packed, q);
       *reinterpret_cast<float4 *>(p.ef + (int64_t)w.b * mn + off) =
-          make_float4(v.x - e4m3_decode(c0) * sc, v.y - e4m3_decode(c1) * sc,
-                      v.z - e4m3_decode(c2) * sc, v.w - e4m3_decode(c3) * sc);
+          make_float4(v.x - q[0] * sc, v.y - q[1] * sc, v.z - q[2] * sc, v.w - q[3] * sc);
     }
   }
 }
@@ -249,15 +249,20 @@ __global__ __launch_bounds__(kThreads) void stream_reduce_kernel(const SArgs p) 
 #pragma unroll
       for (int j = 0; j < kCache; ++j) word[j] = *reinterpret_cast<const uint32_t *>(p.codes + j * mn + off);
 #pragma unroll
-      for (int j = 0; j < kCache; ++j)
+      for (int j = 0; j < kCache; ++j) {
+        float q[4];
+        e4m3_decode4(word[j], q);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) acc[e] = acc[e] + e4m3_decode((word[j] >> (8 * e)) & 0xffu) * s[j];
+        for (int e = 0; e < 4; ++e) acc[e] = acc[e] + q[e] * s[j];
+      }
     } else {
       for (int j = 0; j < N; ++j) {
         const uint32_t word = *reinterpret_cast<const uint32_t *>(p.codes + j * mn + off);
         const float sj = j < kCache ? s[j] : p.scales[j * nblk + (int64_t)bi * p.nbc + bj];
+        float q[4];
+        e4m3_decode4(word, q);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) acc[e] = acc[e] + e4m3_decode((word >> (8 * e)) & 0xffu) * sj;
+        for (int e = 0; e < 4; ++e) acc[e] = acc[e] + q[e] * sj;
       }
     }
     *reinterpret_cast<float4 *>(p.mean + off) = make_float4(acc[0] / fN, acc[1] / fN, acc[2] / fN, acc[3] / fN);

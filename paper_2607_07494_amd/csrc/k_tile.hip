@@ -587,6 +587,11 @@ void launch_layouts(const KArgs &a, bool ak, bool bk, int zdim, hipStream_t st) 
 
 gift_status launch_tile(gift_ctx *ctx, const TileJob &job) {
   if (job.M <= 0 || job.N <= 0 || job.batch <= 0) return GIFT_OK;
+  // the encode's products on the bf16 matrix cores (split operands)
+  if (job.split3 && job.nseg > 0 && job.amax != nullptr && lr_update_eligible(job))
+    return launch_lr_update(ctx, job);
+  if (job.split3 && job.nseg > 0 && job.amax == nullptr && lr_proj_eligible(job))
+    return launch_lr_proj(ctx, job);
   // register-direct kernels for the rank-r update and the projections
   if (job.nseg > 0 && (job.amax != nullptr || job.D != nullptr) && update_kernel_eligible(job))
     return launch_update(ctx, job);

@@ -193,8 +193,15 @@ TRANSFORM_CASES = [
     (2, 200, 384, 32, gift.SIDE_BOTH, 0, 128),
     (2, 97, 61, 5, gift.SIDE_BOTH, 0, 0),
     (1, 64, 64, 64, gift.SIDE_INPUT, 0, 0),      # r = n: sigma A^-1/2
-    (2, 200, 1024, 32, gift.SIDE_INPUT, 0, 0),   # projection split into 4 partials
-    (1, 70, 2048, 64, gift.SIDE_INPUT, 0, 256),  # 8 partials, ragged strips
+    (2, 200, 1024, 32, gift.SIDE_INPUT, 0, 0),   # projection split into partials
+    (1, 70, 2048, 64, gift.SIDE_INPUT, 0, 256),  # partials, ragged strips
+    # split-bf16 encode kernels: ragged 128-row tiles, several 256-column
+    # units, per-128-column blocks, r = 128 (four 32-step chunks), both sides
+    # through the two-segment update, scale blocks cutting the wave tiles
+    (8, 320, 384, 64, gift.SIDE_INPUT, 0, 128),
+    (2, 136, 256, 128, gift.SIDE_INPUT, 0, 0),
+    (3, 260, 520, 32, gift.SIDE_BOTH, 0, 0),
+    (2, 100, 200, 16, gift.SIDE_INPUT, 7, 12),
 ]
 
 
@@ -219,6 +226,31 @@ def test_transform_encode_decode_parity(ctx, N, m, n, r, sides, br, bc):
     # end to end against the oracle's own encode -> reduce -> decode
     ref_out = codec.round_trip(grads, fA, fG, br, bc, False)
     assert rel(out, ref_out) <= DECODE_RTOL
+    f.close()
+
+
+@pytest.mark.parametrize("N,m,n,r,sides,br,bc,use_ef", [
+    (8, 320, 384, 64, gift.SIDE_INPUT, 0, 128, False),
+    (2, 136, 256, 128, gift.SIDE_INPUT, 0, 0, True),
+    (3, 260, 520, 32, gift.SIDE_BOTH, 0, 0, False),
+    (2, 100, 200, 16, gift.SIDE_INPUT, 7, 12, True),
+])
+def test_recomputed_transform_matches_stored(ctx, N, m, n, r, sides, br, bc, use_ef):
+    """Without a `transformed` buffer the quantize pass computes W~ again
+    instead of reading it back: codes, scales and residuals must equal those
+    of an encode that stores W~."""
+    say(f"recompute N={N} m={m} n={n} r={r} sides={sides} block=({br},{bc}) ef={use_ef}")
+    grads = gradient_set(900 + m, 901 + n, N, m, n)
+    f, _, _ = make_factor(ctx, m, n, r, sides, seed=3 * m + n)
+    R0 = gradient_set(902, 903, N, m, n) * np.float32(0.01) if use_ef else None
+    Ra = torch.from_numpy(R0).to(DEV) if use_ef else None
+    Rb = torch.from_numpy(R0).to(DEV) if use_ef else None
+    ca, sa, _ = gpu_encode(ctx, f, grads, br, bc, False, want_t=True, ef=Ra)
+    cb, sb, _ = gpu_encode(ctx, f, grads, br, bc, False, want_t=False, ef=Rb)
+    np.testing.assert_array_equal(sa, sb)
+    np.testing.assert_array_equal(ca, cb)
+    if use_ef:
+        assert torch.equal(Ra, Rb)
     f.close()
 
 
@@ -261,9 +293,10 @@ def test_deterministic(ctx):
 
 EF_CASES = [
     # (N, m, n, r, sides, block_rows, block_cols); r = 0: no transform
-    (3, 96, 128, 8, gift.SIDE_INPUT, 0, 0),      # streaming quantize of the stored W~ + R
+    (3, 96, 128, 8, gift.SIDE_INPUT, 0, 0),      # split-bf16 kernels, W~ + R computed twice
+    (2, 64, 128, 6, gift.SIDE_INPUT, 0, 0),      # r % 4 != 0: streaming quantize of the stored W~ + R
     (2, 64, 96, 0, 0, 0, 32),                    # Euclidean streaming path
-    (2, 33, 50, 4, gift.SIDE_INPUT, 0, 0),       # n % 4 != 0: recomputing quantize pass
+    (2, 33, 50, 4, gift.SIDE_INPUT, 0, 0),       # n % 4 != 0: float32 tile kernels, recomputed
     (2, 40, 30, 0, 0, 8, 6),                     # Euclidean tile-kernel path
 ]
 
