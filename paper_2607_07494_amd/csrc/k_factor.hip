@@ -940,7 +940,9 @@ gift_status factor_refresh_batch(gift_ctx *ctx, const std::vector<SideJob> &jobs
     j.kernel_family = GIFT_KERNEL_FACTOR;
     return launch_tile(ctx, j);
   };
-  // Y_g = Qw_g A_g  (A symmetric, so (c, i) = A[i][c] reads K-major)
+  // Y_g = Qw_g A_g  (A symmetric, so (c, i) = A[i][c] reads K-major); the
+  // product runs on the bf16 matrix cores with split operands (relative error
+  // ~1e-6, well inside what the iteration and Rayleigh-Ritz resolve)
   auto times_A = [&](const Group &g) -> gift_status {
     const int64_t kd = (int64_t)g.k * g.dim;
     TileJob j;
@@ -954,6 +956,7 @@ gift_status factor_refresh_batch(gift_ctx *ctx, const std::vector<SideJob> &jobs
     j.C = g.Y;
     j.ldc = g.dim;
     j.cbs = kd;
+    j.split3 = true;
     j.kernel_family = GIFT_KERNEL_FACTOR;
     return launch_tile(ctx, j);
   };

@@ -92,7 +92,8 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
 }
 
 // ---------------------------------------------------------------------------
-// Projection: out[b][z][i][c] = sum_{k in part z} X[b][i][k] Y[c][k], c < 16 NT
+// Projection: out[b][z][i][c] = sum_{k in part z} X[b][i][k] Y[b][c][k], c < 16 NT
+// (also the subspace iteration's Q A, as (A Q^T)^T with A symmetric)
 // ---------------------------------------------------------------------------
 
 constexpr int kProjThreads = 512;   // 8 waves x 16 rows
@@ -102,11 +103,14 @@ constexpr int kProjStage = 64;      // contraction steps per LDS stage (two chun
 struct LPArgs {
   const float *X;    // [batch][M][K], row stride K
   int64_t x_bs;
-  const float *Y;    // [C][K] shared by the batch
+  const float *Y;    // [batch][C][K] (y_bs = 0: shared by the batch)
+  int64_t y_bs;
   int64_t M, K;
-  float *out;        // [batch][parts][M][C]
+  float *out;        // [batch][parts][M][C], or out_t: [batch] x [C][out_ld]
   int parts;
   int64_t kper;      // contraction steps per part (multiple of kProjStage)
+  int out_t;         // store transposed (parts = 1)
+  int64_t out_ld, out_bs;
 };
 
 template <int NT>
@@ -124,6 +128,7 @@ __global__ __launch_bounds__(kProjThreads) void lr_proj_kernel(const LPArgs p) {
   const int64_t k1 = k0 + p.kper < p.K ? k0 + p.kper : p.K;
   const int nst = k1 > k0 ? (int)((k1 - k0 + kProjStage - 1) / kProjStage) : 0;
   const float *xrow = p.X + (int64_t)b * p.x_bs + (rv ? ri : 0) * p.K;
+  const float *yb = p.Y + (int64_t)b * p.y_bs;
 
   float4 yr[PER][2], xr[2][2];
   auto load = [&](int64_t ks) {
@@ -133,8 +138,8 @@ __global__ __launch_bounds__(kProjThreads) void lr_proj_kernel(const LPArgs p) {
       const int ch = s / (4 * C), c = (s >> 2) % C, g = s & 3;
       const int64_t k = ks + 32 * ch + 4 * g;
       const bool ok = s < SLOTS;
-      yr[u][0] = ld4_if(ok && k < k1, p.Y + (int64_t)c * p.K + k);
-      yr[u][1] = ld4_if(ok && k + 16 < k1, p.Y + (int64_t)c * p.K + k + 16);
+      yr[u][0] = ld4_if(ok && k < k1, yb + (int64_t)c * p.K + k);
+      yr[u][1] = ld4_if(ok && k + 16 < k1, yb + (int64_t)c * p.K + k + 16);
     }
 #pragma unroll
     for (int ch = 0; ch < 2; ++ch) {
@@ -183,6 +188,15 @@ __global__ __launch_bounds__(kProjThreads) void lr_proj_kernel(const LPArgs p) {
   }
   if (!rv) return;
   // lane holds part z of out[ri][16 t + 4 fg + v]
+  if (p.out_t) {
+    // transposed: the 16 lanes of equal fg write 16 consecutive rows ri
+    float *ob = p.out + (int64_t)b * p.out_bs + ri;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) ob[(int64_t)(16 * t + 4 * fg + v) * p.out_ld] = acc[t][v];
+    return;
+  }
   float *ob = p.out + (((int64_t)b * p.parts + z) * p.M + ri) * C;
 #pragma unroll
   for (int t = 0; t < NT; ++t)
@@ -484,28 +498,46 @@ int lr_proj_parts(int64_t M, int64_t K, int32_t batch) {
   return parts;
 }
 
+// The projection kernel takes its 16-row strips from the operand with the
+// long side: rows of A (out[i][c] = C[i][c], split-K partials allowed) or,
+// for a short output (M <= 128 rows), rows of B with the result stored
+// transposed into C[c][j].
+static bool lr_strip_is_b(const TileJob &j) { return j.M <= 128 && j.N > j.M; }
+
 bool lr_proj_eligible(const TileJob &j) {
   const Segment &g = j.seg[0];
-  const int64_t C = j.N;
-  return j.split3 && j.nseg == 1 && j.amax == nullptr && j.D == nullptr && j.colscale == nullptr &&
-         j.alpha == 1.f && (C == 16 || C == 32 || C == 64 || C == 128) && g.a.kmajor && g.b.kmajor &&
-         g.K % 4 == 0 && g.a.ld == g.K && g.b.ld == g.K && g.b.bs == 0 && g.a.bs % 4 == 0 && al16(g.a.ptr) &&
-         al16(g.b.ptr) && al16(j.C) && j.ldc == C && j.cbs == j.M * C;
+  const bool tr = lr_strip_is_b(j);
+  const int64_t C = tr ? j.M : j.N;
+  const Operand &xs = tr ? g.b : g.a, &ys = tr ? g.a : g.b;
+  if (!(j.split3 && j.nseg == 1 && j.amax == nullptr && j.D == nullptr && j.colscale == nullptr &&
+        j.alpha == 1.f && (C == 16 || C == 32 || C == 64 || C == 128) && g.a.kmajor && g.b.kmajor &&
+        g.K % 4 == 0 && xs.ld == g.K && ys.ld == g.K && xs.bs % 4 == 0 && ys.bs % 4 == 0 && al16(xs.ptr) &&
+        al16(ys.ptr)))
+    return false;
+  if (tr) return j.ksplit <= 1;
+  return al16(j.C) && j.ldc == C && j.cbs == j.M * C && (j.ksplit <= 1 || ys.bs == 0);
 }
 
 gift_status launch_lr_proj(gift_ctx *ctx, const TileJob &j) {
+  const bool tr = lr_strip_is_b(j);
+  const Operand &xs = tr ? j.seg[0].b : j.seg[0].a, &ys = tr ? j.seg[0].a : j.seg[0].b;
+  const int64_t C = tr ? j.M : j.N;
   LPArgs a;
-  a.X = j.seg[0].a.ptr;
-  a.x_bs = j.seg[0].a.bs;
-  a.Y = j.seg[0].b.ptr;
-  a.M = j.M;
+  a.X = xs.ptr;
+  a.x_bs = xs.bs;
+  a.Y = ys.ptr;
+  a.y_bs = ys.bs;
+  a.M = tr ? j.N : j.M;
   a.K = j.seg[0].K;
   a.out = j.C;
   a.parts = j.ksplit > 1 ? j.ksplit : 1;
   a.kper = ((a.K + a.parts - 1) / a.parts + kProjStage - 1) / kProjStage * kProjStage;
+  a.out_t = tr ? 1 : 0;
+  a.out_ld = j.ldc;
+  a.out_bs = j.cbs;
   ProfileScope prof(ctx, j.kernel_family);
   const dim3 grid((unsigned)((a.M + kProjRows - 1) / kProjRows), (unsigned)a.parts, (unsigned)j.batch);
-  switch (j.N) {
+  switch (C) {
     case 16: hipLaunchKernelGGL(lr_proj_kernel<1>, grid, dim3(kProjThreads), 0, ctx->stream, a); break;
     case 32: hipLaunchKernelGGL(lr_proj_kernel<2>, grid, dim3(kProjThreads), 0, ctx->stream, a); break;
     case 64: hipLaunchKernelGGL(lr_proj_kernel<4>, grid, dim3(kProjThreads), 0, ctx->stream, a); break;

@@ -26,6 +26,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kColsPerWave = 256;
+constexpr int kGroup = 8;         // rows per load group (amax, quantize)
 
 struct SArgs {
   const float *x;      // [N][m][n]
@@ -74,6 +75,41 @@ __device__ __forceinline__ Run wave_run(const SArgs &p, bool per_rank) {
   return w;
 }
 
+__device__ __forceinline__ float4 ld4_if(bool ok, const float *q) {
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (ok) v = ld4(q);
+  return v;
+}
+
+__device__ __forceinline__ float4 add4(float4 a, const float4 &b) {
+  a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w;
+  return a;
+}
+
+__device__ __forceinline__ uint32_t absmax4(const float4 &v) {
+  const uint32_t a0 = __float_as_uint(v.x) & 0x7fffffffu, a1 = __float_as_uint(v.y) & 0x7fffffffu;
+  const uint32_t a2 = __float_as_uint(v.z) & 0x7fffffffu, a3 = __float_as_uint(v.w) & 0x7fffffffu;
+  uint32_t m = a0 > a1 ? a0 : a1;
+  m = m > a2 ? m : a2;
+  return m > a3 ? m : a3;
+}
+
+// A wave's rows [r0, r1) go through in groups of G rows with two register
+// sets: the loads of group g + 1 are issued before group g is processed, so a
+// wave always has a group in flight (no single-row tail: rows past r1 are
+// not loaded and not processed).
+template <int G, class Set, class Load, class Proc>
+__device__ __forceinline__ void row_pipeline(int r0, int r1, Set &a, Set &b, Load load, Proc proc) {
+  load(r0, a);
+  for (int r = r0; r < r1; r += 2 * G) {
+    if (r + G < r1) load(r + G, b);
+    proc(r, a);
+    if (r + G >= r1) break;
+    if (r + 2 * G < r1) load(r + 2 * G, a);
+    proc(r + G, b);
+  }
+}
+
 template <bool EF>
 __global__ __launch_bounds__(kThreads) void stream_amax_kernel(const SArgs p) {
   const Run w = wave_run(p, true);
@@ -93,56 +129,40 @@ __global__ __launch_bounds__(kThreads) void stream_amax_kernel(const SArgs p) {
     run = 0u;
   };
   const float *xb = p.x + (int64_t)w.b * mn;
-  int r = w.r0;
-  for (; r + 3 < w.r1 && next >= r + 4; r += 4) {   // four rows in flight
-    float4 v[4];
+  const float *eb = EF ? p.ef_in + (int64_t)w.b * mn : nullptr;
+  float *tb = p.transformed ? p.transformed + (int64_t)w.b * mn : nullptr;
+  struct Set {
+    float4 v[kGroup], e[EF ? kGroup : 1];
+  };
+  auto load = [&](int r, Set &s) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < kGroup; ++u) {
+      const bool ok = w.cv && r + u < w.r1;
       const int64_t off = (int64_t)(r + u) * p.n + w.cj;
-      v[u] = w.cv ? ld4(xb + off) : make_float4(0.f, 0.f, 0.f, 0.f);
-      if (EF && w.cv) {
-        const float4 e = ld4(p.ef_in + (int64_t)w.b * mn + off);
-        v[u].x += e.x; v[u].y += e.y; v[u].z += e.z; v[u].w += e.w;
-      }
-      if (p.transformed && w.cv)
-        *reinterpret_cast<float4 *>(p.transformed + (int64_t)w.b * mn + off) = v[u];
+      s.v[u] = ld4_if(ok, xb + off);
+      if (EF) s.e[u] = ld4_if(ok, eb + off);
     }
+  };
+  auto proc = [&](int r, Set &s) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const uint32_t a0 = __float_as_uint(v[u].x) & 0x7fffffffu, a1 = __float_as_uint(v[u].y) & 0x7fffffffu;
-      const uint32_t a2 = __float_as_uint(v[u].z) & 0x7fffffffu, a3 = __float_as_uint(v[u].w) & 0x7fffffffu;
-      uint32_t m = a0 > a1 ? a0 : a1;
-      m = m > a2 ? m : a2;
-      m = m > a3 ? m : a3;
+    for (int u = 0; u < kGroup; ++u) {
+      const int row = r + u;
+      if (row >= w.r1) break;
+      float4 x = s.v[u];
+      if (EF) x = add4(x, s.e[u]);
+      if (tb && w.cv) *reinterpret_cast<float4 *>(tb + (int64_t)row * p.n + w.cj) = x;
+      if (row == next) {
+        flush(bi);
+        ++bi;
+        next += p.br;
+      }
+      const uint32_t m = absmax4(x);
       run = m > run ? m : run;
     }
-    if (r + 4 == next) {
-      flush(bi);
-      ++bi;
-      next += p.br;
-    }
-  }
-  for (; r < w.r1; ++r) {
-    const int64_t off = (int64_t)r * p.n + w.cj;
-    float4 v = w.cv ? ld4(xb + off) : make_float4(0.f, 0.f, 0.f, 0.f);
-    if (EF && w.cv) {
-      const float4 e = ld4(p.ef_in + (int64_t)w.b * mn + off);
-      v.x += e.x; v.y += e.y; v.z += e.z; v.w += e.w;
-    }
-    if (p.transformed && w.cv) *reinterpret_cast<float4 *>(p.transformed + (int64_t)w.b * mn + off) = v;
-    const uint32_t a0 = __float_as_uint(v.x) & 0x7fffffffu, a1 = __float_as_uint(v.y) & 0x7fffffffu;
-    const uint32_t a2 = __float_as_uint(v.z) & 0x7fffffffu, a3 = __float_as_uint(v.w) & 0x7fffffffu;
-    uint32_t m = a0 > a1 ? a0 : a1;
-    m = m > a2 ? m : a2;
-    m = m > a3 ? m : a3;
-    run = m > run ? m : run;
-    if (r + 1 == next) {
-      flush(bi);
-      ++bi;
-      next += p.br;
-    }
-  }
-  flush(bi);  // the block row still open (a no-op when it was just flushed)
+  };
+  Set sa, sb;
+  row_pipeline<kGroup>(w.r0, w.r1, sa, sb, load, proc);
+  flush(bi);  // the block row still open
 }
 
 // EF: write the residual R <- x - Deq(Q(x)); ADD: x = input + R first (the
@@ -193,77 +213,151 @@ __global__ __launch_bounds__(kThreads) void stream_quant_kernel(const SArgs p) {
   };
   load_scale();
   const float *xb = p.x + (int64_t)w.b * mn;
-  for (int r = w.r0; r < w.r1; ++r) {
-    if (r == next) {
-      ++bi;
-      next += p.br;
-      load_scale();
+  const float *eb = (EF && ADD) ? p.ef_in + (int64_t)w.b * mn : nullptr;
+  uint8_t *cb = p.codes + (int64_t)w.b * mn;
+  float *rb = EF ? p.ef + (int64_t)w.b * mn : nullptr;
+  struct Set {
+    float4 v[kGroup], e[(EF && ADD) ? kGroup : 1];
+  };
+  auto load = [&](int r, Set &s) {
+#pragma unroll
+    for (int u = 0; u < kGroup; ++u) {
+      const bool ok = w.cv && r + u < w.r1;
+      const int64_t off = (int64_t)(r + u) * p.n + w.cj;
+      s.v[u] = ld4_if(ok, xb + off);
+      if (EF && ADD) s.e[u] = ld4_if(ok, eb + off);
     }
-    if (!w.cv) continue;
-    const int64_t off = (int64_t)r * p.n + w.cj;
-    float4 v = ld4(xb + off);
-    if (EF && ADD) {
-      const float4 e = ld4(p.ef_in + (int64_t)w.b * mn + off);
-      v.x += e.x; v.y += e.y; v.z += e.z; v.w += e.w;
+  };
+  auto proc = [&](int r, Set &s) {
+#pragma unroll
+    for (int u = 0; u < kGroup; ++u) {
+      const int row = r + u;
+      if (row >= w.r1) break;
+      if (row == next) {
+        ++bi;
+        next += p.br;
+        load_scale();
+      }
+      if (!w.cv) continue;
+      float4 x = s.v[u];
+      if (EF && ADD) x = add4(x, s.e[u]);
+      const int64_t off = (int64_t)row * p.n + w.cj;
+      const uint32_t packed = e4m3_encode4(x.x * inv, x.y * inv, x.z * inv, x.w * inv);
+      *reinterpret_cast<uint32_t *>(cb + off) = packed;
+      if (EF) {
+        float q[4];
+        e4m3_decode4(packed, q);
+        *reinterpret_cast<float4 *>(rb + off) =
+            make_float4(x.x - q[0] * sc, x.y - q[1] * sc, x.z - q[2] * sc, x.w - q[3] * sc);
+      }
     }
-    const uint32_t packed = e4m3_encode4(v.x * inv, v.y * inv, v.z * inv, v.w * inv);
-    *reinterpret_cast<uint32_t *>(p.codes + (int64_t)w.b * mn + off) = packed;
-    if (EF) {
-      float q[4];
-      e4m3_decode4(packed, q);
-      *reinterpret_cast<float4 *>(p.ef + (int64_t)w.b * mn + off) =
-          make_float4(v.x - q[0] * sc, v.y - q[1] * sc, v.z - q[2] * sc, v.w - q[3] * sc);
-    }
-  }
+  };
+  Set sa, sb;
+  row_pipeline<kGroup>(w.r0, w.r1, sa, sb, load, proc);
 }
 
-template <int NR>
+// Rank sum with CPL columns per lane (4: one 32-bit code word per rank and
+// row; 16: one 16-byte word), rows in groups of G pipelined as above.
+template <int NR, int CPL, int G>
 __global__ __launch_bounds__(kThreads) void stream_reduce_kernel(const SArgs p) {
+  constexpr int W = CPL / 4;                 // 32-bit code words per rank and row
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wid = blockIdx.y * (kThreads / 64) + wave;
+  const int r0 = wid * p.rows_per_wave;
+  const int r1 = r0 + p.rows_per_wave < p.m ? r0 + p.rows_per_wave : p.m;
+  const int cj = blockIdx.x * 64 * CPL + CPL * lane;
+  if (r0 >= p.m || cj >= p.n) return;
+  const int64_t mn = (int64_t)p.m * p.n;
+  const int64_t nblk = (int64_t)p.nbr * p.nbc;
+  const int bj = cj / p.bc;
+  int bi = r0 / p.br;
+  int next = (bi + 1) * p.br;
+  float s[NR];
+  auto load_scales = [&]() {
+#pragma unroll
+    for (int j = 0; j < NR; ++j) s[j] = p.scales[j * nblk + (int64_t)bi * p.nbc + bj];
+  };
+  load_scales();
+  const float fN = (float)NR;
+  struct Set {
+    uint32_t c[G][NR][W];
+  };
+  auto load = [&](int r, Set &st) {
+#pragma unroll
+    for (int u = 0; u < G; ++u) {
+      const bool ok = r + u < r1;
+      const int64_t off = (int64_t)(r + u) * p.n + cj;
+#pragma unroll
+      for (int j = 0; j < NR; ++j) {
+        if constexpr (W == 4) {
+          uint4 v = make_uint4(0u, 0u, 0u, 0u);
+          if (ok) v = *reinterpret_cast<const uint4 *>(p.codes + j * mn + off);
+          st.c[u][j][0] = v.x;
+          st.c[u][j][1] = v.y;
+          st.c[u][j][2] = v.z;
+          st.c[u][j][3] = v.w;
+        } else {
+          uint32_t v = 0u;
+          if (ok) v = *reinterpret_cast<const uint32_t *>(p.codes + j * mn + off);
+          st.c[u][j][0] = v;
+        }
+      }
+    }
+  };
+  auto proc = [&](int r, Set &st) {
+#pragma unroll
+    for (int u = 0; u < G; ++u) {
+      const int row = r + u;
+      if (row >= r1) break;
+      if (row == next) {
+        ++bi;
+        next += p.br;
+        load_scales();
+      }
+      const int64_t off = (int64_t)row * p.n + cj;
+#pragma unroll
+      for (int q = 0; q < W; ++q) {
+        float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int j = 0; j < NR; ++j) {
+          float d[4];
+          e4m3_decode4(st.c[u][j][q], d);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[e] = acc[e] + d[e] * s[j];
+        }
+        *reinterpret_cast<float4 *>(p.mean + off + 4 * q) =
+            make_float4(acc[0] / fN, acc[1] / fN, acc[2] / fN, acc[3] / fN);
+      }
+    }
+  };
+  Set sa, sb;
+  row_pipeline<G>(r0, r1, sa, sb, load, proc);
+}
+
+// any N: one row at a time, 4 columns per lane
+__global__ __launch_bounds__(kThreads) void stream_reduce_any_kernel(const SArgs p) {
   const Run w = wave_run(p, false);
   if (w.r0 >= p.m || !w.cv) return;
   const int64_t mn = (int64_t)p.m * p.n;
   const int64_t nblk = (int64_t)p.nbr * p.nbc;
-  const int N = NR > 0 ? NR : p.N;
   const int bj = w.cj / p.bc;
   int bi = w.r0 / p.br;
   int next = (bi + 1) * p.br;
-  constexpr int kCache = NR > 0 ? NR : 16;
-  float s[kCache];
-  auto load_scales = [&]() {
-#pragma unroll
-    for (int j = 0; j < kCache; ++j)
-      s[j] = j < N ? p.scales[j * nblk + (int64_t)bi * p.nbc + bj] : 0.f;
-  };
-  load_scales();
-  const float fN = (float)N;
+  const float fN = (float)p.N;
   for (int r = w.r0; r < w.r1; ++r) {
     if (r == next) {
       ++bi;
       next += p.br;
-      load_scales();
     }
     const int64_t off = (int64_t)r * p.n + w.cj;
     float acc[4] = {0.f, 0.f, 0.f, 0.f};
-    if (NR > 0) {
-      uint32_t word[kCache];
+    for (int j = 0; j < p.N; ++j) {
+      const uint32_t word = *reinterpret_cast<const uint32_t *>(p.codes + j * mn + off);
+      const float sj = p.scales[j * nblk + (int64_t)bi * p.nbc + bj];
+      float q[4];
+      e4m3_decode4(word, q);
 #pragma unroll
-      for (int j = 0; j < kCache; ++j) word[j] = *reinterpret_cast<const uint32_t *>(p.codes + j * mn + off);
-#pragma unroll
-      for (int j = 0; j < kCache; ++j) {
-        float q[4];
-        e4m3_decode4(word[j], q);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) acc[e] = acc[e] + q[e] * s[j];
-      }
-    } else {
-      for (int j = 0; j < N; ++j) {
-        const uint32_t word = *reinterpret_cast<const uint32_t *>(p.codes + j * mn + off);
-        const float sj = j < kCache ? s[j] : p.scales[j * nblk + (int64_t)bi * p.nbc + bj];
-        float q[4];
-        e4m3_decode4(word, q);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) acc[e] = acc[e] + q[e] * sj;
-      }
+      for (int e = 0; e < 4; ++e) acc[e] = acc[e] + q[e] * sj;
     }
     *reinterpret_cast<float4 *>(p.mean + off) = make_float4(acc[0] / fN, acc[1] / fN, acc[2] / fN, acc[3] / fN);
   }
@@ -277,12 +371,14 @@ int lane_group(int bc) {
   return g;
 }
 
-void shape_grid(SArgs &a, int batch, dim3 &grid) {
-  const int64_t colw = (a.n + kColsPerWave - 1) / kColsPerWave;
-  // about eight waves per SIMD over the whole launch
+// rows per wave: about eight waves per SIMD over the launch, rounded up to a
+// multiple of the row group `g`
+void shape_grid(SArgs &a, int batch, dim3 &grid, int cols_per_wave = kColsPerWave, int g = kGroup) {
+  const int64_t colw = (a.n + cols_per_wave - 1) / cols_per_wave;
   const int64_t target = 8192;
   int64_t rpw = (int64_t)a.m * colw * batch / target;
-  if (rpw < 4) rpw = 4;
+  rpw = (rpw + g - 1) / g * g;
+  if (rpw < g) rpw = g;
   if (rpw > a.m) rpw = a.m;
   a.rows_per_wave = (int)rpw;
   const int64_t waves = (a.m + rpw - 1) / rpw;
@@ -350,15 +446,24 @@ gift_status launch_stream_reduce(gift_ctx *ctx, const uint8_t *codes, const floa
   a.bc = (int)g.bc;
   a.nbr = g.nbr;
   a.nbc = g.nbc;
-  dim3 grid;
-  shape_grid(a, 1, grid);
   ProfileScope prof(ctx, GIFT_KERNEL_REDUCE);
+  dim3 grid;
+  const bool wide = n % 16 == 0 && g.bc % 16 == 0 && al16(codes) && al16(mean);
+#define GIFT_RED(NR, CPL, G)                                                                   \
+  do {                                                                                         \
+    shape_grid(a, 1, grid, 64 * (CPL), (G));                                                   \
+    hipLaunchKernelGGL((stream_reduce_kernel<NR, CPL, G>), grid, dim3(kThreads), 0, ctx->stream, a); \
+  } while (0)
   switch (N) {
-    case 4: hipLaunchKernelGGL(stream_reduce_kernel<4>, grid, dim3(kThreads), 0, ctx->stream, a); break;
-    case 8: hipLaunchKernelGGL(stream_reduce_kernel<8>, grid, dim3(kThreads), 0, ctx->stream, a); break;
-    case 16: hipLaunchKernelGGL(stream_reduce_kernel<16>, grid, dim3(kThreads), 0, ctx->stream, a); break;
-    default: hipLaunchKernelGGL(stream_reduce_kernel<0>, grid, dim3(kThreads), 0, ctx->stream, a); break;
+    case 4: if (wide) GIFT_RED(4, 16, 2); else GIFT_RED(4, 4, 4); break;
+    case 8: if (wide) GIFT_RED(8, 16, 2); else GIFT_RED(8, 4, 4); break;
+    case 16: if (wide) GIFT_RED(16, 16, 1); else GIFT_RED(16, 4, 2); break;
+    default:
+      shape_grid(a, 1, grid, kColsPerWave, 1);
+      hipLaunchKernelGGL(stream_reduce_any_kernel, grid, dim3(kThreads), 0, ctx->stream, a);
+      break;
   }
+#undef GIFT_RED
   return check_launch("stream_reduce_kernel");
 }
 
