@@ -233,10 +233,17 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
   const bool pp_ok = useA && !useG && aligned && n % 4 == 0 && (A.r == 16 || A.r == 32 || A.r == 64 || A.r == 128);
   const int pparts = !pp_ok ? 1 : (inverse ? proj_parts(m, n, A.r, N) : lr_proj_parts(m, n, N));
   size_t off = 0;
-  float *P = nullptr, *Qm = nullptr, *Km = nullptr, *L2 = nullptr;
+  float *P = nullptr, *Qm = nullptr, *Km = nullptr, *L2 = nullptr, *Psum = nullptr;
   if (useA) {
     P = reinterpret_cast<float *>(ws + off);
     off += a256(sizeof(float) * N * pparts * m * A.r);
+  }
+  // the encode sums the projection's partials once (the update then reads
+  // one P per column range instead of all partials)
+  const bool presum = !inverse && pparts > 1;
+  if (presum) {
+    Psum = reinterpret_cast<float *>(ws + off);
+    off += a256(sizeof(float) * N * m * A.r);
   }
   if (useG) {
     Qm = reinterpret_cast<float *>(ws + off);
@@ -268,6 +275,9 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
     j.split3 = !inverse;
     j.kernel_family = GIFT_KERNEL_PROJECT;
     if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
+    if (presum &&
+        (st = launch_lr_psum(ctx, P, Psum, pparts, m * A.r, N, GIFT_KERNEL_PROJECT)) != GIFT_OK)
+      return st;
   }
   if (useG) {  // Qm = W^T U_G  (Q^T, n x r)
     TileJob j;
@@ -338,6 +348,9 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
     if (useG) {  // L2 U_A^T
       s.a = Operand{L2, A.r, m * A.r, true};
       s.b = Operand{A.U, A.r, 0, true};
+    } else if (presum) {  // P (C_A U_A^T), P already summed
+      s.a = Operand{Psum, A.r, m * A.r, true, 1};
+      s.b = Operand{A.Uc, A.r, 0, true};
     } else {  // P (C_A U_A^T), P summed from its partials
       s.a = Operand{P, A.r, m * A.r, true, pparts};
       s.b = Operand{inverse ? A.Uci : A.Uc, A.r, 0, true};

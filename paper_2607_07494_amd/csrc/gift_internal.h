@@ -194,6 +194,10 @@ gift_status launch_lr_update(gift_ctx *ctx, const TileJob &job);
 bool lr_proj_eligible(const TileJob &job);
 gift_status launch_lr_proj(gift_ctx *ctx, const TileJob &job);
 int lr_proj_parts(int64_t M, int64_t K, int32_t batch);
+// out[b] = sum_z partials[b][z] (in order) for [batch][parts][per_rank] floats
+// (per_rank a multiple of 4, 16-byte aligned buffers)
+gift_status launch_lr_psum(gift_ctx *ctx, const float *partials, float *out, int parts, int64_t per_rank,
+                           int32_t batch, int kernel_family);
 // k_update.hip: register-direct rank-r update / projection (used by
 // launch_tile when the job's shapes allow)
 bool update_kernel_eligible(const TileJob &job);

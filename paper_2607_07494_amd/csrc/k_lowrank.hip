@@ -30,6 +30,7 @@
 // 16-byte entries; entry fg of column c sits at fg ^ ((c >> 2) & 3), which
 // puts the 16 rows read by one 16-lane phase in distinct banks.
 
+#include <algorithm>
 #include <type_traits>
 
 #include "fp8_e4m3.h"
@@ -203,6 +204,24 @@ __global__ __launch_bounds__(kProjThreads) void lr_proj_kernel(const LPArgs p) {
     *reinterpret_cast<float4 *>(ob + 16 * t + 4 * fg) = make_float4(acc[t][0], acc[t][1], acc[t][2], acc[t][3]);
 }
 
+// P[b][i][c] = sum_z partial[b][z][i][c], z in order (float32), so that the
+// update reads one P instead of every partial once per column range
+__global__ __launch_bounds__(256) void lr_psum_kernel(const float *part, float *out, int parts,
+                                                      int64_t per_rank, int64_t total) {
+  // per_rank = M * C floats of one rank's P, total = batch * per_rank (multiples of 4)
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x * 4;
+  for (int64_t e = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4; e < total; e += stride) {
+    const int64_t b = e / per_rank, i = e - b * per_rank;
+    const float *q = part + b * parts * per_rank + i;
+    float4 acc = ld4(q);
+    for (int z = 1; z < parts; ++z) {
+      const float4 v = ld4(q + (int64_t)z * per_rank);
+      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+    }
+    *reinterpret_cast<float4 *>(out + e) = acc;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Update: W~[b][i][j] = D[b][i][j] + sum_s sum_k Row_s[b][i][k] Col_s[b][j][k]
 //         (+ R[b][i][j]), fused with the block maxima (EPI_AMAX) or with the
@@ -211,7 +230,9 @@ __global__ __launch_bounds__(kProjThreads) void lr_proj_kernel(const LPArgs p) {
 
 constexpr int kUpdThreads = 256;    // 4 waves x 32 rows
 constexpr int kUpdRows = 128;
-constexpr int kUpdCols = 256;       // columns per workgroup, walked in 64-column tiles
+// 64-column tiles per workgroup: the column operand of all of them sits in
+// LDS (8 KiB per tile and 32-step chunk), at most 64 KiB
+constexpr int upd_tiles(int nch) { return nch <= 2 ? 4 : (nch <= 4 ? 2 : 1); }
 
 struct LUSeg {
   const float *row;   // [batch][parts][M][K] (row_bs = 0: shared by the batch)
@@ -236,17 +257,20 @@ struct LUArgs {
 
 template <int EPI, bool EF, int NSEG, int KC>
 __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) {
-  constexpr int NCH = NSEG * KC;          // 32-step chunks over all segments
-  constexpr int SLOTS = NCH * 64 * 4;     // (chunk, column, fg) entries of a 64-column tile
-  constexpr int PER = SLOTS / kUpdThreads;  // = NCH
-  __shared__ uint4 chi[2][SLOTS], clo[2][SLOTS];
+  constexpr int NCH = NSEG * KC;                // 32-step chunks over all segments
+  constexpr int TSLOTS = NCH * 64 * 4;          // (chunk, column, fg) entries of a 64-column tile
+  constexpr int TILES = upd_tiles(NCH);
+  constexpr int COLS = 64 * TILES;
+  constexpr int SLOTS = TILES * TSLOTS;         // the workgroup's whole column range
+  constexpr int PER = SLOTS / kUpdThreads;      // = TILES * NCH
+  __shared__ uint4 chi[SLOTS], clo[SLOTS];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int fr = lane & 15, fg = lane >> 4;
   const int b = blockIdx.z;
   const int64_t i0 = (int64_t)blockIdx.y * kUpdRows + wave * 32;
   const int64_t MN = p.M * p.N;
-  const int64_t c_begin = (int64_t)blockIdx.x * kUpdCols;
-  const int64_t c_end = c_begin + kUpdCols < p.N ? c_begin + kUpdCols : p.N;
+  const int64_t c_begin = (int64_t)blockIdx.x * COLS;
+  const int64_t c_end = c_begin + COLS < p.N ? c_begin + COLS : p.N;
   const int ntiles = (int)((c_end - c_begin + 63) / 64);
   const bool wave_live = i0 < p.M;
   const int slot = (int)((((int64_t)blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x) * 4 + wave) %
@@ -257,6 +281,44 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
   for (int g = 0; g < 2; ++g) {
     ri[g] = i0 + 16 * g + fr;
     rv[g] = ri[g] < p.M;
+  }
+
+  // W (and residual) values of the wave's 32 x 64 tile: lane holds row
+  // ri[g], columns j0 + 16 t + 4 fg .. + 3; two register sets alternate
+  typedef float4 WTile[2][4];
+  auto load_w = [&](int64_t j0, WTile &dd, WTile &re) {
+#pragma unroll
+    for (int g = 0; g < 2; ++g)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int64_t cj = j0 + 16 * t + 4 * fg;
+        const bool ok = rv[g] && cj < p.N;
+        const int64_t off = (int64_t)b * MN + ri[g] * p.N + cj;
+        dd[g][t] = ld4_if(ok, p.D + off);
+        if (EF) re[g][t] = ld4_if(ok, p.ef + off);
+      }
+  };
+  WTile dA, dB, rA, rB;
+  load_w(c_begin, dA, rA);
+  if (ntiles > 1) load_w(c_begin + 64, dB, rB);
+
+  // the column operand of the workgroup's whole column range, split into
+  // LDS once: entry s -> (tile, chunk, column, fg), two float4 each
+#pragma unroll 4
+  for (int u = 0; u < PER; ++u) {
+    const int s = tid + u * kUpdThreads;
+    const int ct = s / TSLOTS, rem = s % TSLOTS;
+    const int ch = rem / 256, c = (rem >> 2) & 63, g = rem & 3;
+    const LUSeg &sg = p.seg[ch / KC];
+    const int64_t k = 32 * (ch % KC) + 4 * g;
+    const int64_t j = c_begin + 64 * ct + c;
+    const float *q = sg.col + (int64_t)b * sg.col_bs + (j < p.N ? j : 0) * sg.col_ld;
+    const float4 v0 = ld4_if(j < p.N && k < sg.K, q + k);
+    const float4 v1 = ld4_if(j < p.N && k + 16 < sg.K, q + k + 16);
+    uint4 h, l;
+    split8(v0, v1, h, l);
+    chi[ct * TSLOTS + ch * 256 + lds_slot(c, g)] = h;
+    clo[ct * TSLOTS + ch * 256 + lds_slot(c, g)] = l;
   }
 
   // row-side fragments of the wave's 32 rows, split once for all tiles
@@ -286,70 +348,14 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
       split8(v0, v1, rh[g][ch], rl[g][ch]);
     }
 
-  // column-side tile: entry s -> (chunk, column, fg); two float4 per entry
-  float4 cr[PER][2];
-  auto load_cols = [&](int64_t j0) {
-#pragma unroll
-    for (int u = 0; u < PER; ++u) {
-      const int s = tid + u * kUpdThreads;
-      const int ch = s / 256, c = (s >> 2) & 63, g = s & 3;
-      const LUSeg &sg = p.seg[ch / KC];
-      const int64_t k = 32 * (ch % KC) + 4 * g;
-      const int64_t j = j0 + c;
-      const float *q = sg.col + (int64_t)b * sg.col_bs + (j < p.N ? j : 0) * sg.col_ld;
-      cr[u][0] = ld4_if(j < p.N && k < sg.K, q + k);
-      cr[u][1] = ld4_if(j < p.N && k + 16 < sg.K, q + k + 16);
-    }
-  };
-  auto stage_cols = [&](int buf) {
-#pragma unroll
-    for (int u = 0; u < PER; ++u) {
-      const int s = tid + u * kUpdThreads;
-      const int ch = s / 256, c = (s >> 2) & 63, g = s & 3;
-      uint4 h, l;
-      split8(cr[u][0], cr[u][1], h, l);
-      chi[buf][ch * 256 + lds_slot(c, g)] = h;
-      clo[buf][ch * 256 + lds_slot(c, g)] = l;
-    }
-  };
-  // W (and residual) values of the wave's 32 x 64 tile: lane holds row
-  // ri[g], columns j0 + 16 t + 4 fg .. + 3
-  float4 d[2][4], rr[2][4];
-  auto load_w = [&](int64_t j0) {
-#pragma unroll
-    for (int g = 0; g < 2; ++g)
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int64_t cj = j0 + 16 * t + 4 * fg;
-        const bool ok = rv[g] && cj < p.N;
-        const int64_t off = (int64_t)b * MN + ri[g] * p.N + cj;
-        d[g][t] = ld4_if(ok, p.D + off);
-        if (EF) rr[g][t] = ld4_if(ok, p.ef + off);
-      }
-  };
+  __syncthreads();
 
   uint32_t run_max = 0u;
   int64_t run_blk = -1;
-  load_cols(c_begin);
-  load_w(c_begin);
-  stage_cols(0);
-  __syncthreads();
-  for (int ct = 0; ct < ntiles; ++ct) {
-    const int buf = ct & 1;
+  // one 64-column tile, no barrier: products from LDS, epilogue on `cur`,
+  // then the loads of tile ct + 2 into the same register set
+  auto tile = [&](int ct, WTile &cur, WTile &curR) {
     const int64_t j0 = c_begin + 64 * ct;
-    const bool more = ct + 1 < ntiles;
-    float4 dc[2][4], rc[2][4];
-#pragma unroll
-    for (int g = 0; g < 2; ++g)
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        dc[g][t] = d[g][t];
-        if (EF) rc[g][t] = rr[g][t];
-      }
-    if (more) {
-      load_cols(j0 + 64);
-      load_w(j0 + 64);
-    }
     floatx4 acc[2][4];
 #pragma unroll
     for (int g = 0; g < 2; ++g)
@@ -359,127 +365,129 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
     for (int ch = 0; ch < NCH; ++ch)
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        const int e = ch * 256 + lds_slot(16 * t + fr, fg);
-        const uint4 ah = chi[buf][e], al = clo[buf][e];
+        const int e = ct * TSLOTS + ch * 256 + lds_slot(16 * t + fr, fg);
+        const uint4 ah = chi[e], al = clo[e];
 #pragma unroll
         for (int g = 0; g < 2; ++g) acc[g][t] = mfma3(ah, al, rh[g][ch], rl[g][ch], acc[g][t]);
       }
-    if (more) stage_cols(buf ^ 1);
-
-    if (wave_live) {
-      float w[2][4][4];
-#pragma unroll
-      for (int g = 0; g < 2; ++g)
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          w[g][t][0] = dc[g][t].x + acc[g][t][0];
-          w[g][t][1] = dc[g][t].y + acc[g][t][1];
-          w[g][t][2] = dc[g][t].z + acc[g][t][2];
-          w[g][t][3] = dc[g][t].w + acc[g][t][3];
-          if (EF) {
-            w[g][t][0] += rc[g][t].x;
-            w[g][t][1] += rc[g][t].y;
-            w[g][t][2] += rc[g][t].z;
-            w[g][t][3] += rc[g][t].w;
-          }
-        }
-      // scale-block geometry of the wave tile (wave-uniform, two divisions)
-      const int64_t rlast = i0 + 31 < p.M ? i0 + 31 : p.M - 1;
-      const int64_t clast = j0 + 63 < p.N ? j0 + 63 : p.N - 1;
-      const int bi_lo = __builtin_amdgcn_readfirstlane((int)(i0 / p.br));
-      const int bj_lo = __builtin_amdgcn_readfirstlane((int)(j0 / p.bc));
-      const bool uniform = (int64_t)(bi_lo + 1) * p.br > rlast && (int64_t)(bj_lo + 1) * p.bc > clast;
-      const int64_t u_gb = (int64_t)bi_lo * p.nbc + bj_lo;
-      const int64_t nblk = (int64_t)p.nbr * p.nbc;
-      if (EPI == EPI_AMAX) {
-        if (p.transformed) {
-#pragma unroll
-          for (int g = 0; g < 2; ++g)
-#pragma unroll
-            for (int t = 0; t < 4; ++t) {
-              const int64_t cj = j0 + 16 * t + 4 * fg;
-              if (rv[g] && cj < p.N)
-                *reinterpret_cast<float4 *>(p.transformed + (int64_t)b * MN + ri[g] * p.N + cj) =
-                    make_float4(w[g][t][0], w[g][t][1], w[g][t][2], w[g][t][3]);
+      if (wave_live) {
+        float w[2][4][4];
+  #pragma unroll
+        for (int g = 0; g < 2; ++g)
+  #pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            w[g][t][0] = cur[g][t].x + acc[g][t][0];
+            w[g][t][1] = cur[g][t].y + acc[g][t][1];
+            w[g][t][2] = cur[g][t].z + acc[g][t][2];
+            w[g][t][3] = cur[g][t].w + acc[g][t][3];
+            if (EF) {
+              w[g][t][0] += curR[g][t].x;
+              w[g][t][1] += curR[g][t].y;
+              w[g][t][2] += curR[g][t].z;
+              w[g][t][3] += curR[g][t].w;
             }
-        }
-        if (uniform) {
-          uint32_t m = 0u;
-#pragma unroll
-          for (int g = 0; g < 2; ++g)
-#pragma unroll
-            for (int t = 0; t < 4; ++t) {
-              const int64_t cj = j0 + 16 * t + 4 * fg;
-              if (rv[g] && cj < p.N) {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                  const uint32_t a = __float_as_uint(w[g][t][e]) & 0x7fffffffu;
-                  m = a > m ? a : m;
+          }
+        // scale-block geometry of the wave tile (wave-uniform, two divisions)
+        const int64_t rlast = i0 + 31 < p.M ? i0 + 31 : p.M - 1;
+        const int64_t clast = j0 + 63 < p.N ? j0 + 63 : p.N - 1;
+        const int bi_lo = __builtin_amdgcn_readfirstlane((int)(i0 / p.br));
+        const int bj_lo = __builtin_amdgcn_readfirstlane((int)(j0 / p.bc));
+        const bool uniform = (int64_t)(bi_lo + 1) * p.br > rlast && (int64_t)(bj_lo + 1) * p.bc > clast;
+        const int64_t u_gb = (int64_t)bi_lo * p.nbc + bj_lo;
+        const int64_t nblk = (int64_t)p.nbr * p.nbc;
+        if (EPI == EPI_AMAX) {
+          if (p.transformed) {
+  #pragma unroll
+            for (int g = 0; g < 2; ++g)
+  #pragma unroll
+              for (int t = 0; t < 4; ++t) {
+                const int64_t cj = j0 + 16 * t + 4 * fg;
+                if (rv[g] && cj < p.N)
+                  *reinterpret_cast<float4 *>(p.transformed + (int64_t)b * MN + ri[g] * p.N + cj) =
+                      make_float4(w[g][t][0], w[g][t][1], w[g][t][2], w[g][t][3]);
+              }
+          }
+          if (uniform) {
+            uint32_t m = 0u;
+  #pragma unroll
+            for (int g = 0; g < 2; ++g)
+  #pragma unroll
+              for (int t = 0; t < 4; ++t) {
+                const int64_t cj = j0 + 16 * t + 4 * fg;
+                if (rv[g] && cj < p.N) {
+  #pragma unroll
+                  for (int e = 0; e < 4; ++e) {
+                    const uint32_t a = __float_as_uint(w[g][t][e]) & 0x7fffffffu;
+                    m = a > m ? a : m;
+                  }
                 }
               }
+            m = wave_max_u32(m);
+            if (u_gb != run_blk) {
+              if (run_blk >= 0 && lane == 0 && run_max)
+                atomicMax(&p.amax[((int64_t)b * nblk + run_blk) * kAmaxSlots + slot], run_max);
+              run_blk = u_gb;
+              run_max = 0u;
             }
-          m = wave_max_u32(m);
-          if (u_gb != run_blk) {
-            if (run_blk >= 0 && lane == 0 && run_max)
-              atomicMax(&p.amax[((int64_t)b * nblk + run_blk) * kAmaxSlots + slot], run_max);
-            run_blk = u_gb;
-            run_max = 0u;
+            run_max = m > run_max ? m : run_max;
+          } else {
+            // a block edge cuts the tile: per element
+  #pragma unroll
+            for (int g = 0; g < 2; ++g)
+  #pragma unroll
+              for (int t = 0; t < 4; ++t) {
+                const int64_t cj = j0 + 16 * t + 4 * fg;
+                if (!(rv[g] && cj < p.N)) continue;
+  #pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  const uint32_t a = __float_as_uint(w[g][t][e]) & 0x7fffffffu;
+                  const int64_t gb = (ri[g] / p.br) * p.nbc + (cj + e) / p.bc;
+                  if (a) atomicMax(&p.amax[((int64_t)b * nblk + gb) * kAmaxSlots + slot], a);
+                }
+              }
           }
-          run_max = m > run_max ? m : run_max;
-        } else {
-          // a block edge cuts the tile: per element
-#pragma unroll
+        } else {  // EPI_QUANT with finished block maxima
+          float u_inv = 0.f, u_s = 0.f;
+          if (uniform) {
+            const float a = __uint_as_float(p.amax[(int64_t)b * nblk + u_gb]);
+            u_inv = e4m3_multiplier(a);
+            u_s = e4m3_scale(a);
+          }
+  #pragma unroll
           for (int g = 0; g < 2; ++g)
-#pragma unroll
+  #pragma unroll
             for (int t = 0; t < 4; ++t) {
               const int64_t cj = j0 + 16 * t + 4 * fg;
               if (!(rv[g] && cj < p.N)) continue;
-#pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                const uint32_t a = __float_as_uint(w[g][t][e]) & 0x7fffffffu;
-                const int64_t gb = (ri[g] / p.br) * p.nbc + (cj + e) / p.bc;
-                if (a) atomicMax(&p.amax[((int64_t)b * nblk + gb) * kAmaxSlots + slot], a);
+              float inv[4] = {u_inv, u_inv, u_inv, u_inv}, sc[4] = {u_s, u_s, u_s, u_s};
+              if (!uniform) {
+  #pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  const float a = __uint_as_float(p.amax[(int64_t)b * nblk + (ri[g] / p.br) * p.nbc + (cj + e) / p.bc]);
+                  inv[e] = e4m3_multiplier(a);
+                  sc[e] = e4m3_scale(a);
+                }
               }
+              const uint32_t packed = e4m3_encode4(w[g][t][0] * inv[0], w[g][t][1] * inv[1], w[g][t][2] * inv[2],
+                                                   w[g][t][3] * inv[3]);
+              float res[4];
+              if (EF) {
+                float q[4];
+                e4m3_decode4(packed, q);
+  #pragma unroll
+                for (int e = 0; e < 4; ++e) res[e] = w[g][t][e] - q[e] * sc[e];
+              }
+              const int64_t off = (int64_t)b * MN + ri[g] * p.N + cj;
+              *reinterpret_cast<uint32_t *>(p.codes + off) = packed;
+              if (EF) *reinterpret_cast<float4 *>(p.ef + off) = make_float4(res[0], res[1], res[2], res[3]);
             }
         }
-      } else {  // EPI_QUANT with finished block maxima
-        float u_inv = 0.f, u_s = 0.f;
-        if (uniform) {
-          const float a = __uint_as_float(p.amax[(int64_t)b * nblk + u_gb]);
-          u_inv = e4m3_multiplier(a);
-          u_s = e4m3_scale(a);
-        }
-#pragma unroll
-        for (int g = 0; g < 2; ++g)
-#pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            const int64_t cj = j0 + 16 * t + 4 * fg;
-            if (!(rv[g] && cj < p.N)) continue;
-            float inv[4] = {u_inv, u_inv, u_inv, u_inv}, sc[4] = {u_s, u_s, u_s, u_s};
-            if (!uniform) {
-#pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                const float a = __uint_as_float(p.amax[(int64_t)b * nblk + (ri[g] / p.br) * p.nbc + (cj + e) / p.bc]);
-                inv[e] = e4m3_multiplier(a);
-                sc[e] = e4m3_scale(a);
-              }
-            }
-            const uint32_t packed = e4m3_encode4(w[g][t][0] * inv[0], w[g][t][1] * inv[1], w[g][t][2] * inv[2],
-                                                 w[g][t][3] * inv[3]);
-            float res[4];
-            if (EF) {
-              float q[4];
-              e4m3_decode4(packed, q);
-#pragma unroll
-              for (int e = 0; e < 4; ++e) res[e] = w[g][t][e] - q[e] * sc[e];
-            }
-            const int64_t off = (int64_t)b * MN + ri[g] * p.N + cj;
-            *reinterpret_cast<uint32_t *>(p.codes + off) = packed;
-            if (EF) *reinterpret_cast<float4 *>(p.ef + off) = make_float4(res[0], res[1], res[2], res[3]);
-          }
       }
-    }
-    __syncthreads();
+    if (ct + 2 < ntiles) load_w(j0 + 128, cur, curR);
+  };
+  for (int ct = 0; ct < ntiles; ct += 2) {
+    tile(ct, dA, rA);
+    if (ct + 1 < ntiles) tile(ct + 1, dB, rB);
   }
   if (EPI == EPI_AMAX && wave_live && run_blk >= 0 && lane == 0 && run_max)
     atomicMax(&p.amax[((int64_t)b * p.nbr * p.nbc + run_blk) * kAmaxSlots + slot], run_max);
@@ -546,6 +554,16 @@ gift_status launch_lr_proj(gift_ctx *ctx, const TileJob &j) {
   return check_launch("lr_proj_kernel");
 }
 
+gift_status launch_lr_psum(gift_ctx *ctx, const float *partials, float *out, int parts, int64_t per_rank,
+                           int32_t batch, int kernel_family) {
+  const int64_t total = per_rank * batch;
+  const int64_t blocks = std::min<int64_t>((total / 4 + 255) / 256, 4096);
+  ProfileScope prof(ctx, kernel_family);
+  hipLaunchKernelGGL(lr_psum_kernel, dim3((unsigned)std::max<int64_t>(blocks, 1)), dim3(256), 0, ctx->stream,
+                     partials, out, parts, per_rank, total);
+  return check_launch("lr_psum_kernel");
+}
+
 bool lr_update_eligible(const TileJob &j) {
   if (!j.split3 || j.amax == nullptr || j.nseg < 1 || j.nseg > 2 || j.N % 4 != 0) return false;
   const int64_t K = j.seg[0].K;
@@ -587,7 +605,8 @@ gift_status launch_lr_update(gift_ctx *ctx, const TileJob &j) {
   a.nbr = j.geom.nbr;
   a.nbc = j.geom.nbc;
   ProfileScope prof(ctx, j.kernel_family);
-  const dim3 grid((unsigned)((j.N + kUpdCols - 1) / kUpdCols), (unsigned)((j.M + kUpdRows - 1) / kUpdRows),
+  const int64_t cols = 64 * upd_tiles(j.nseg * (int)((j.seg[0].K + 31) / 32));
+  const dim3 grid((unsigned)((j.N + cols - 1) / cols), (unsigned)((j.M + kUpdRows - 1) / kUpdRows),
                   (unsigned)j.batch);
   const bool quant = j.codes != nullptr;
   const bool ef = j.ef != nullptr;
