@@ -685,6 +685,17 @@ gift_status gift_encode(gift_ctx *ctx, const gift_factor *f, const float *grads,
   // QUANT pass: the streaming kernel reads the raw sub-slots itself (on the
   // stored W~ + R with a transform, on W without); otherwise a finalize
   // launch reduces them first
+  if (recompute && lr_quant_reads_raw(job)) {
+    // the quantize pass reduces the raw sub-slots itself and writes the scales
+    TileJob q = job;
+    q.from_raw = true;
+    q.clear = prev_set;
+    q.clear_words = (int64_t)prev_dirty;
+    q.kernel_family = GIFT_KERNEL_UPDATE_QUANT;
+    if ((st = launch_tile(ctx, q)) != GIFT_OK) return st;
+    amax_slots_done(ctx, raw_words);
+    return GIFT_OK;
+  }
   const float *qsrc = gemm ? wt : grads;
   if (!recompute && qsrc && stream_eligible(m, n, g, qsrc, codes, ef, nullptr)) {
     TileJob q = job;

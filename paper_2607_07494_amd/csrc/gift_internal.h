@@ -190,6 +190,8 @@ gift_status launch_tile(gift_ctx *ctx, const TileJob &job);
 // k_lowrank.hip: the encode's projection and rank-r update with split bf16
 // operands; lr_proj_parts = split-K partials of the projection
 bool lr_update_eligible(const TileJob &job);
+// its quantize pass can take the AMAX pass's raw sub-slots (job.from_raw)
+bool lr_quant_reads_raw(const TileJob &job);
 gift_status launch_lr_update(gift_ctx *ctx, const TileJob &job);
 bool lr_proj_eligible(const TileJob &job);
 gift_status launch_lr_proj(gift_ctx *ctx, const TileJob &job);

@@ -253,6 +253,16 @@ struct LUArgs {
   float *ef;            // residual (read; QUANT also writes it)
   int64_t br, bc;
   int nbr, nbc;
+  int codes_wide;       // N % 16 == 0 and 16-byte aligned codes: 16-byte stores
+  // QUANT straight from the AMAX pass's raw sub-slots (every wave tile inside
+  // one scale block): block maxima reduced in the kernel, scales written by
+  // the wave holding a block's first element, clear_words words at clear
+  // zeroed on the way
+  const uint32_t *raw;
+  float *scales;
+  uint32_t *clear;
+  int64_t clear_words;
+  int shared, batch;
 };
 
 template <int EPI, bool EF, int NSEG, int KC>
@@ -264,6 +274,10 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
   constexpr int SLOTS = TILES * TSLOTS;         // the workgroup's whole column range
   constexpr int PER = SLOTS / kUpdThreads;      // = TILES * NCH
   __shared__ uint4 chi[SLOTS], clo[SLOTS];
+  // QUANT: a wave's 32 x 64 tile of codes, written in the matrix-core layout
+  // (4 bytes per lane and 16-column group) and read back as 16 consecutive
+  // codes per lane, so the global stores are 16 bytes wide
+  __shared__ uint32_t cstage[EPI == EPI_QUANT ? kUpdThreads / 64 : 1][32 * 16];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int fr = lane & 15, fg = lane >> 4;
   const int b = blockIdx.z;
@@ -275,6 +289,13 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
   const bool wave_live = i0 < p.M;
   const int slot = (int)((((int64_t)blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x) * 4 + wave) %
                    kAmaxSlots;
+  if (EPI == EPI_QUANT && p.clear_words) {
+    const int64_t nthreads = (int64_t)gridDim.x * gridDim.y * gridDim.z * kUpdThreads;
+    const int64_t gt = (((int64_t)blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x) * kUpdThreads + tid;
+    for (int64_t i = gt; i < p.clear_words; i += nthreads) p.clear[i] = 0u;
+  }
+  int64_t q_blk = -1;      // block whose maximum q_amax holds (QUANT from raw slots)
+  float q_amax = 0.f;
   int64_t ri[2];
   bool rv[2];
 #pragma unroll
@@ -449,7 +470,25 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
         } else {  // EPI_QUANT with finished block maxima
           float u_inv = 0.f, u_s = 0.f;
           if (uniform) {
-            const float a = __uint_as_float(p.amax[(int64_t)b * nblk + u_gb]);
+            float a;
+            if (p.raw) {
+              if (u_gb != q_blk) {
+                // lane l reads sub-slot l of the block (of every rank when shared)
+                const int r0 = p.shared ? 0 : b, r1 = p.shared ? p.batch : b + 1;
+                uint32_t m = 0u;
+                for (int r = r0; r < r1; ++r) {
+                  const uint32_t v = p.raw[((int64_t)r * nblk + u_gb) * kAmaxSlots + lane];
+                  m = v > m ? v : m;
+                }
+                q_amax = __uint_as_float(wave_max_u32(m));
+                q_blk = u_gb;
+                if (lane == 0 && i0 == (int64_t)bi_lo * p.br && j0 == (int64_t)bj_lo * p.bc)
+                  p.scales[(int64_t)b * nblk + u_gb] = e4m3_scale(q_amax);
+              }
+              a = q_amax;
+            } else {
+              a = __uint_as_float(p.amax[(int64_t)b * nblk + u_gb]);
+            }
             u_inv = e4m3_multiplier(a);
             u_s = e4m3_scale(a);
           }
@@ -478,9 +517,32 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
                 for (int e = 0; e < 4; ++e) res[e] = w[g][t][e] - q[e] * sc[e];
               }
               const int64_t off = (int64_t)b * MN + ri[g] * p.N + cj;
-              *reinterpret_cast<uint32_t *>(p.codes + off) = packed;
+              cstage[wave][(16 * g + fr) * 16 + 4 * t + fg] = packed;
               if (EF) *reinterpret_cast<float4 *>(p.ef + off) = make_float4(res[0], res[1], res[2], res[3]);
             }
+          // the wave reads back only what its own lanes wrote: the fences
+          // order these LDS accesses (no workgroup barrier)
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int c = lane + 64 * h;           // 16-byte chunk: row c / 4, column quarter c % 4
+            const int row = c >> 2, qt = c & 3;
+            const int64_t gi = i0 + row;
+            const int64_t cj = j0 + 16 * qt;
+            const uint4 v = *reinterpret_cast<const uint4 *>(&cstage[wave][row * 16 + 4 * qt]);
+            if (gi < p.M) {
+              uint8_t *dst = p.codes + (int64_t)b * MN + gi * p.N + cj;
+              if (p.codes_wide && cj + 16 <= p.N) {
+                *reinterpret_cast<uint4 *>(dst) = v;
+              } else {
+                const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                  if (cj + 4 * q < p.N) *reinterpret_cast<uint32_t *>(dst + 4 * q) = wv[q];
+              }
+            }
+          }
         }
       }
     if (ct + 2 < ntiles) load_w(j0 + 128, cur, curR);
@@ -564,6 +626,12 @@ gift_status launch_lr_psum(gift_ctx *ctx, const float *partials, float *out, int
   return check_launch("lr_psum_kernel");
 }
 
+bool lr_quant_reads_raw(const TileJob &j) {
+  // every 32 x 64 wave tile inside one scale block
+  const int64_t br = j.geom.br > 0 ? j.geom.br : j.M, bc = j.geom.bc > 0 ? j.geom.bc : j.N;
+  return (br % 32 == 0 || br >= j.M) && (bc % 64 == 0 || bc >= j.N) && kAmaxSlots == 64;
+}
+
 bool lr_update_eligible(const TileJob &j) {
   if (!j.split3 || j.amax == nullptr || j.nseg < 1 || j.nseg > 2 || j.N % 4 != 0) return false;
   const int64_t K = j.seg[0].K;
@@ -604,6 +672,13 @@ gift_status launch_lr_update(gift_ctx *ctx, const TileJob &j) {
   a.bc = j.geom.bc > 0 ? j.geom.bc : j.N;
   a.nbr = j.geom.nbr;
   a.nbc = j.geom.nbc;
+  a.codes_wide = j.codes && j.N % 16 == 0 && al16(j.codes) ? 1 : 0;
+  a.raw = j.codes && j.from_raw ? j.amax : nullptr;
+  a.scales = j.scales;
+  a.clear = a.raw ? j.clear : nullptr;
+  a.clear_words = a.raw ? j.clear_words : 0;
+  a.shared = j.shared ? 1 : 0;
+  a.batch = j.batch;
   ProfileScope prof(ctx, j.kernel_family);
   const int64_t cols = 64 * upd_tiles(j.nseg * (int)((j.seg[0].K + 31) / 32));
   const dim3 grid((unsigned)((j.N + cols - 1) / cols), (unsigned)((j.M + kUpdRows - 1) / kUpdRows),
