@@ -28,6 +28,20 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
+# Source file of each kernel family: a measured HBM traffic figure (profiles/,
+# rocprofv3 FETCH_SIZE / WRITE_SIZE) is reported only while this file is
+# unchanged since the counters were taken.
+FAMILY_SOURCE = {
+    "syrk": "paper_2607_07494_amd/csrc/k_syrk.hip",
+    "amax": "paper_2607_07494_amd/csrc/k_stream.hip",
+    "quant": "paper_2607_07494_amd/csrc/k_stream.hip",
+    "reduce": "paper_2607_07494_amd/csrc/k_stream.hip",
+    "project": "paper_2607_07494_amd/csrc/k_lowrank.hip",
+    "update_amax": "paper_2607_07494_amd/csrc/k_lowrank.hip",
+    "update_quant": "paper_2607_07494_amd/csrc/k_lowrank.hip",
+}
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm-traffic.md")
+
 HBM_PEAK_GBS = 8000.0
 FP32_MFMA_TFLOPS = 157.3
 BF16_MFMA_TFLOPS = 2500.0
@@ -50,6 +64,29 @@ def parse():
                     help="only run the library's plain copy kernel on 256 MiB (5 launches), "
                          "the known-size reference for the HBM byte counters")
     return ap.parse_args()
+
+
+def source_sha256(rel):
+    import hashlib
+    with open(os.path.join(ROOT, rel), "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()
+
+
+def measured_traffic(family, workload):
+    """HBM bytes per launch of `family` on `workload` from the committed
+    counter summary, or None when there is none or the kernel's source has
+    changed since it was taken.  Lines look like
+    `traffic: family=F workload=W bytes_per_launch=B sha256=H`."""
+    if family not in FAMILY_SOURCE or not os.path.exists(TRAFFIC_FILE):
+        return None
+    sha = source_sha256(FAMILY_SOURCE[family])
+    for line in open(TRAFFIC_FILE):
+        if not line.startswith("traffic:"):
+            continue
+        kv = dict(item.split("=", 1) for item in line.split()[1:])
+        if kv.get("family") == family and kv.get("workload") == workload and kv.get("sha256") == sha:
+            return float(kv["bytes_per_launch"])
+    return None
 
 
 def copy_calibration():
@@ -92,6 +129,7 @@ class Job:
         self.factor = None
         self.sides = sides_flag if mat.gift else 0
         self.acts = self.dgrads = None
+        self.owns_factor = False   # the matrix whose refresh updates a shared factor
 
 
 def build_workload(args, torch, gift, synth, dev):
@@ -119,7 +157,11 @@ def build_workload(args, torch, gift, synth, dev):
                                                     dim, dev, dtype=wl.act_dtype)
         return xcache[key]
 
-    per_layer_acts = {}
+    # K-FAC's input factor A = E[a a^T] belongs to a layer input: matrices that
+    # read the same input (gate and up) have the same A and, with the input
+    # side alone, the same transform, so they share one factor (refreshed
+    # once).  With the output side each matrix keeps its own factor.
+    per_layer_acts, shared = {}, {}
     for jb in jobs:
         if not jb.gift_branch:
             continue
@@ -129,8 +171,12 @@ def build_workload(args, torch, gift, synth, dev):
         jb.acts = per_layer_acts[akey]
         if jb.sides & gift.SIDE_OUTPUT:
             jb.dgrads = stream(jb.m, 2).clone()
-        jb.factor = gift.Factor(ctx_holder["ctx"], jb.m, jb.n, wl.rank, jb.sides,
-                                seed=synth.seed_for(wl.cfg, 50, jb.layer, jb.mat.kind))
+        fkey = (akey, jb.m, jb.n) if jb.sides == gift.SIDE_INPUT else (akey, jb.mat.kind)
+        if fkey not in shared:
+            shared[fkey] = gift.Factor(ctx_holder["ctx"], jb.m, jb.n, wl.rank, jb.sides,
+                                       seed=synth.seed_for(wl.cfg, 50, jb.layer, jb.mat.kind))
+            jb.owns_factor = True
+        jb.factor = shared[fkey]
     del xcache
     return wl, jobs
 
@@ -168,9 +214,9 @@ def algorithmic_work(wl, jobs, args):
         mn = float(m) * n
         add("project", 2 * mn * (ra + rg), 4 * mn * ((ra > 0) + (rg > 0)))
         add("update_store", 2 * mn * (ra + rg), 8 * mn)
-        # factor refresh (amortised by the cadence)
+        # factor refresh (amortised by the cadence), once per distinct factor
         for dim, on in ((n, ra), (m, rg)):
-            if not on:
+            if not on or not jb.owns_factor:
                 continue
             T = wl.T
             k = min(dim, 2 * r)
@@ -234,7 +280,7 @@ def main():
           f"{sum(j.N * j.m * j.n for j in jobs) * 4 / 1e9:.2f} GB of rank gradients", file=sys.stderr,
           flush=True)
 
-    fjobs = [jb for jb in jobs if jb.factor is not None]
+    fjobs = [jb for jb in jobs if jb.owns_factor]
 
     def step(iters):
         if fjobs:
@@ -311,7 +357,13 @@ def main():
     else:
         roof = {"bound": "hbm", "achieved": round(by / dom_launches / (avg_ms * 1e-3) / 1e9, 2),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(frac_b, 4)}
-    roof.update({"kernel": dom, "avg_launch_ms": round(avg_ms, 5), "traffic": None})
+    wl_key = f"config{wl.cfg}-{args.sides}"
+    traffic = measured_traffic(dom, wl_key)
+    roof.update({"kernel": dom, "avg_launch_ms": round(avg_ms, 5),
+                 "traffic": round(traffic / 1e9, 4) if traffic is not None else None})
+    if traffic is not None:
+        roof["traffic_unit"] = "GB per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
+        roof["algorithmic_gb_per_launch"] = round((by / dom_launches) / 1e9, 4)
     tf_fams = ("project", "update_amax", "update_quant", "update_store")
     tf_ms = sum(fam_ms[k][1] for k in tf_fams if k in fam_ms)
     tf_flops = sum(work[k][0] for k in tf_fams if k in work)
@@ -330,6 +382,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{wl.name} (config {wl.cfg})", "ranks": wl.N, "rank": wl.rank,
                    "sides": args.sides, "tokens": wl.T, "matrices": len(jobs),
+                   "factors": sum(1 for jb in jobs if jb.owns_factor),
                    "grad_gb": round(grad_bytes / 1e9, 3), "factor_refresh_every": wl.refresh,
                    "subspace_iters": args.iters},
         "transform_tflops": round(tf_flops / (tf_ms * 1e-3) / 1e12, 3) if tf_ms else None,
@@ -340,7 +393,7 @@ def main():
         print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     for jb in jobs:
-        if jb.factor is not None:
+        if jb.owns_factor:
             jb.factor.close()
     ctx.close()
     print(json.dumps(line), flush=True)
