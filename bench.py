@@ -11,8 +11,13 @@ MLP 2816, vocab 32000; 8 simulated ranks; GIFT on gate/up/down with rank 64,
 Euclidean with a shared scale on q/k/v/o, embedding and LM head; factor
 refresh every step from 16384 bf16 tokens).
 
-Prints one JSON line (metric = BASELINE metric: gradient GB/s through
-encode+decode).  ``--gpus N`` with N > 1 is not supported: this codec runs
+Independent matrices are spread over several HIP streams (one library
+context each): a matrix's encode, rank sum and decode stay in order on its
+stream, the factor refresh runs first on the main stream and the GIFT
+encodes wait for it.
+
+Prints one JSON line (metric: gradient GB/s through encode+decode; transform
+TFLOP/s; % of roofline).  ``--gpus N`` with N > 1 is not supported: this codec runs
 its N data-parallel ranks locally on one GPU.
 """
 
@@ -58,6 +63,9 @@ def parse():
     ap.add_argument("--cold-iters", type=int, default=6, help="subspace iterations of the first refresh")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--streams", type=int, default=4,
+                    help="HIP streams (one library context each); matrices are dealt round-robin, "
+                         "each matrix's encode -> rank sum -> decode stays on its stream")
     ap.add_argument("--breakdown-steps", type=int, default=2,
                     help="untimed steps with every kernel family bracketed by events")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -281,57 +289,89 @@ def main():
           flush=True)
 
     fjobs = [jb for jb in jobs if jb.owns_factor]
+    # independent matrices on several streams (default priority), one library
+    # context per stream; the factor refresh stays on the main stream and the
+    # GIFT encodes wait for it
+    main = torch.cuda.current_stream()
+    nstreams = max(args.streams, 1)
+    streams = [main] + [torch.cuda.Stream() for _ in range(nstreams - 1)]
+    ctxs = [ctx] + [gift.Context(stream=st.cuda_stream) for st in streams[1:]]
+    for i, jb in enumerate(jobs):
+        jb.sid = i % nstreams
 
-    def step(iters):
+    def join_into_main():
+        for st in streams[1:]:
+            ev = torch.cuda.Event()
+            ev.record(st)
+            main.wait_event(ev)
+
+    def step(iters, serial=False):
+        join_into_main()           # the refresh rewrites factors the last step's encodes read
         if fjobs:
             gift.factor_update_batch(ctx, [jb.factor for jb in fjobs], [jb.acts for jb in fjobs],
                                      [jb.dgrads for jb in fjobs], iters=iters)
+        refreshed = torch.cuda.Event()
+        refreshed.record(main)
+        for st in streams[1:]:
+            st.wait_event(refreshed)
         for jb in jobs:
-            gift.encode(ctx, jb.factor, jb.grads, jb.codes, jb.scales, jb.br, jb.bc,
+            c = ctxs[0 if serial else jb.sid]
+            gift.encode(c, jb.factor, jb.grads, jb.codes, jb.scales, jb.br, jb.bc,
                         gift.SCALE_LOCAL if jb.gift_branch else gift.SCALE_SHARED)
-        for jb in jobs:
-            gift.reduce_local(ctx, jb.codes, jb.scales, jb.mean, jb.br, jb.bc)
-        for jb in jobs:
+            gift.reduce_local(c, jb.codes, jb.scales, jb.mean, jb.br, jb.bc)
             if jb.gift_branch:
-                gift.decode(ctx, jb.factor, jb.mean, jb.out)
+                gift.decode(c, jb.factor, jb.mean, jb.out)
 
     for w in range(max(args.warmup, 1)):
         step(args.cold_iters if w == 0 else args.iters)
+        join_into_main()
         torch.cuda.synchronize()
         print(f"[bench] warmup step {w} done", file=sys.stderr, flush=True)
 
-    # untimed breakdown: every kernel family bracketed by events
-    ctx.profile_reset()
-    ctx.profile_select(None)
-    ctx.profile(True)
+    def profile_all(enable, families=None, reset=False):
+        for c in ctxs:
+            if reset:
+                c.profile_reset()
+            c.profile_select(families)
+            c.profile(enable)
+
+    def read_all(name):
+        tot_l, tot_ms = 0, 0.0
+        for c in ctxs:
+            launches, ms = c.profile_read(name)
+            tot_l += launches
+            tot_ms += ms
+        return tot_l, tot_ms
+
+    # untimed breakdown on the main stream alone (isolated kernel times): every
+    # kernel family bracketed by events; the largest is the dominant family
+    profile_all(True, None, reset=True)
     nb = max(args.breakdown_steps, 1)
     for s in range(nb):
-        step(args.iters)
+        step(args.iters, serial=True)
     fam_ms = {}
     for name in gift.KERNELS:
-        launches, ms = ctx.profile_read(name)
+        launches, ms = read_all(name)
         if launches:
             fam_ms[name] = (launches / nb, ms / nb)
-    ctx.profile(False)
+    profile_all(False)
     dom = max(fam_ms, key=lambda k: fam_ms[k][1])
 
     # timed region: events only around the dominant family's launches
-    ctx.profile_reset()
-    ctx.profile_select([dom])
-    ctx.profile(True)
+    profile_all(True, [dom], reset=True)
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    start.record()
+    start.record(main)
     for s in range(args.steps):
         step(args.iters)
-    stop.record()
+    join_into_main()
+    stop.record(main)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = start.elapsed_time(stop) / args.steps
-    dom_launches, dom_ms_total = ctx.profile_read(dom)
-    ctx.profile(False)
-    ctx.profile_select(None)
+    dom_launches, dom_ms_total = read_all(dom)
+    profile_all(False)
     print(f"[bench] timed {args.steps} steps: {ms_step:.3f} ms/step (wall {wall:.2f} s)",
           file=sys.stderr, flush=True)
 
@@ -382,19 +422,23 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{wl.name} (config {wl.cfg})", "ranks": wl.N, "rank": wl.rank,
                    "sides": args.sides, "tokens": wl.T, "matrices": len(jobs),
-                   "factors": sum(1 for jb in jobs if jb.owns_factor),
+                   "factors": sum(1 for jb in jobs if jb.owns_factor), "streams": nstreams,
                    "grad_gb": round(grad_bytes / 1e9, 3), "factor_refresh_every": wl.refresh,
                    "subspace_iters": args.iters},
         "transform_tflops": round(tf_flops / (tf_ms * 1e-3) / 1e12, 3) if tf_ms else None,
         "roofline": roof,
         "kernels": kernels,
+        "kernels_note": "per-family time per step from an untimed pass with every launch on one stream",
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    torch.cuda.synchronize()
     for jb in jobs:
         if jb.owns_factor:
             jb.factor.close()
+    for c in ctxs[1:]:
+        c.close()
     ctx.close()
     print(json.dumps(line), flush=True)
 
