@@ -296,8 +296,15 @@ def main():
     nstreams = max(args.streams, 1)
     streams = [main] + [torch.cuda.Stream() for _ in range(nstreams - 1)]
     ctxs = [ctx] + [gift.Context(stream=st.cuda_stream) for st in streams[1:]]
-    for i, jb in enumerate(jobs):
+    # Euclidean matrices first, on the side streams, where they run beside the
+    # factor refresh; then the GIFT matrices on every stream after it
+    eu = [jb for jb in jobs if not jb.gift_branch]
+    gj = [jb for jb in jobs if jb.gift_branch]
+    for i, jb in enumerate(eu):
+        jb.sid = 1 + i % (nstreams - 1) if nstreams > 1 else 0
+    for i, jb in enumerate(gj):
         jb.sid = i % nstreams
+    order = eu + gj
 
     def join_into_main():
         for st in streams[1:]:
@@ -312,10 +319,13 @@ def main():
                                      [jb.dgrads for jb in fjobs], iters=iters)
         refreshed = torch.cuda.Event()
         refreshed.record(main)
-        for st in streams[1:]:
-            st.wait_event(refreshed)
-        for jb in jobs:
-            c = ctxs[0 if serial else jb.sid]
+        waited = set()
+        for jb in order:
+            sid = 0 if serial else jb.sid
+            if jb.gift_branch and sid not in waited and sid != 0:
+                streams[sid].wait_event(refreshed)     # GIFT encodes need the refreshed factors
+                waited.add(sid)
+            c = ctxs[sid]
             gift.encode(c, jb.factor, jb.grads, jb.codes, jb.scales, jb.br, jb.bc,
                         gift.SCALE_LOCAL if jb.gift_branch else gift.SCALE_SHARED)
             gift.reduce_local(c, jb.codes, jb.scales, jb.mean, jb.br, jb.bc)
