@@ -13,8 +13,10 @@ refresh every step from 16384 bf16 tokens).
 
 Independent matrices are spread over several HIP streams (one library
 context each): a matrix's encode, rank sum and decode stay in order on its
-stream, the factor refresh runs first on the main stream and the GIFT
-encodes wait for it.
+stream.  The factor refresh runs once per factor shape (the smallest group on
+the main stream, the others on further streams), and a GIFT matrix's encode
+waits only for its own group's refresh; the Euclidean matrices run beside the
+refresh.
 
 Prints one JSON line (metric: gradient GB/s through encode+decode; transform
 TFLOP/s; % of roofline).  ``--gpus N`` with N > 1 is not supported: this codec runs
@@ -290,21 +292,40 @@ def main():
 
     fjobs = [jb for jb in jobs if jb.owns_factor]
     # independent matrices on several streams (default priority), one library
-    # context per stream; the factor refresh stays on the main stream and the
-    # GIFT encodes wait for it
+    # context per stream.  The factor refresh runs per factor shape (one call
+    # per group, the smallest first on the main stream, the others on the
+    # next streams), so a GIFT matrix waits only for its own group's refresh.
     main = torch.cuda.current_stream()
     nstreams = max(args.streams, 1)
     streams = [main] + [torch.cuda.Stream() for _ in range(nstreams - 1)]
     ctxs = [ctx] + [gift.Context(stream=st.cuda_stream) for st in streams[1:]]
-    # Euclidean matrices first, on the side streams, where they run beside the
-    # factor refresh; then the GIFT matrices on every stream after it
+
+    def fkey(jb):
+        return (jb.n, jb.m if jb.sides & gift.SIDE_OUTPUT else 0)
+
+    groups = {}
+    for jb in fjobs:
+        groups.setdefault(fkey(jb), []).append(jb)
+    gorder = sorted(groups, key=lambda k: sum(jb.n * jb.n + (jb.m * jb.m if k[1] else 0)
+                                             for jb in groups[k]))
+    gsid = {k: (i if i < nstreams else 0) for i, k in enumerate(gorder)}
+    for jb in jobs:
+        jb.group = fkey(jb) if jb.gift_branch else None
+    # Euclidean matrices first, on streams that host no refresh (they run
+    # beside it); then each group's GIFT matrices, a group's matrices avoiding
+    # the streams of the groups refreshed after it
     eu = [jb for jb in jobs if not jb.gift_branch]
-    gj = [jb for jb in jobs if jb.gift_branch]
+    free = [s for s in range(nstreams) if s not in gsid.values()] or list(range(1, nstreams)) or [0]
     for i, jb in enumerate(eu):
-        jb.sid = 1 + i % (nstreams - 1) if nstreams > 1 else 0
-    for i, jb in enumerate(gj):
-        jb.sid = i % nstreams
-    order = eu + gj
+        jb.sid = free[i % len(free)]
+    order = list(eu)
+    for gi, k in enumerate(gorder):
+        later = {gsid[k2] for k2 in gorder[gi + 1:]}
+        ok = [s for s in range(nstreams) if s not in later] or [0]
+        gjobs = [jb for jb in jobs if jb.gift_branch and jb.group == k]
+        for i, jb in enumerate(gjobs):
+            jb.sid = ok[i % len(ok)]
+        order += gjobs
 
     def join_into_main():
         for st in streams[1:]:
@@ -314,17 +335,26 @@ def main():
 
     def step(iters, serial=False):
         join_into_main()           # the refresh rewrites factors the last step's encodes read
-        if fjobs:
-            gift.factor_update_batch(ctx, [jb.factor for jb in fjobs], [jb.acts for jb in fjobs],
-                                     [jb.dgrads for jb in fjobs], iters=iters)
-        refreshed = torch.cuda.Event()
-        refreshed.record(main)
+        joined = torch.cuda.Event()
+        joined.record(main)
+        ready = {}
+        for k in gorder:
+            sid = 0 if serial else gsid[k]
+            if sid != 0:
+                streams[sid].wait_event(joined)
+            g = groups[k]
+            gift.factor_update_batch(ctxs[sid], [jb.factor for jb in g], [jb.acts for jb in g],
+                                     [jb.dgrads for jb in g], iters=iters)
+            ready[k] = (sid, torch.cuda.Event())
+            ready[k][1].record(streams[sid])
         waited = set()
         for jb in order:
             sid = 0 if serial else jb.sid
-            if jb.gift_branch and sid not in waited and sid != 0:
-                streams[sid].wait_event(refreshed)     # GIFT encodes need the refreshed factors
-                waited.add(sid)
+            if jb.gift_branch:
+                rsid, ev = ready[jb.group]
+                if rsid != sid and (sid, jb.group) not in waited:
+                    streams[sid].wait_event(ev)    # GIFT encodes need the refreshed factor
+                    waited.add((sid, jb.group))
             c = ctxs[sid]
             gift.encode(c, jb.factor, jb.grads, jb.codes, jb.scales, jb.br, jb.bc,
                         gift.SCALE_LOCAL if jb.gift_branch else gift.SCALE_SHARED)
