@@ -301,11 +301,122 @@ __device__ __forceinline__ void chol_inv_body(const float *part, int ks, int k, 
   }
 }
 
+// ---------------------------------------------------------------------------
+// The same factorisation for k <= 128 with the matrices in registers.
+// Thread (ty, tx) of a 32 x 32 grid (1024 threads) owns the 4 x 4 block at
+// rows 4 ty.., columns 4 tx.. of G when tx >= ty (upper triangle) and of
+// X = L^-1 when tx <= ty (lower triangle).  Column step j, with d =
+// max(G_jj, floor) and rs = 1 / sqrt(d):
+//   the half-wave of block row j / 4 reads G_jj from the lane of the
+//   diagonal block, scales its rows j of G and X by rs, keeps the scaled X
+//   row (final) and broadcasts both through LDS:
+//     l_b = G_jb rs = R_jb = L_bj (b >= j),   x_b = X_jb rs (b <= j);
+//   after one barrier every thread updates its blocks with FMAs only:
+//     G_ab -= l_a l_b                     (Cholesky trailing update)
+//     X_ab -= l_a x_b   for a > j         (Gauss-Jordan on [L | I])
+// Two broadcast buffers alternate, so one barrier per column suffices.
+// Rows of G at or above j are never read again, so the G update runs over
+// whole blocks (stale broadcast entries only reach those rows); the X update
+// is restricted to rows below j, whose broadcast entries are current.
+// ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kSmallThreads) void chol_inv_lds_kernel(const SmallJob *jobs) {
-  __shared__ double W[kLdsK * (kLdsK + 1)];
-  __shared__ double dg[kLdsK], idg[kLdsK], sink[64];
+  __shared__ double lb[2][kLdsK], xb[2][kLdsK];   // broadcast rows of R and X
+  __shared__ double dsum[32];
   const SmallJob J = jobs[blockIdx.x];
-  chol_inv_body(J.part, J.ks, J.k, W, J.k + 1, dg, idg, sink, J.out);
+  const int k = J.k, ks = J.ks;
+  const int tid = threadIdx.x, tx = tid & 31, ty = tid >> 5;
+  const int64_t kk = (int64_t)k * k;
+  const bool own_g = tx >= ty, own_x = tx <= ty;
+  double G[4][4], X[4][4];
+  // G = sum of the split-K partials (rows / columns past k stay zero)
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      G[u][w] = 0.0;
+      X[u][w] = (4 * ty + u == 4 * tx + w && 4 * ty + u < k) ? 1.0 : 0.0;
+    }
+  if (own_g) {
+    for (int z = 0; z < ks; ++z) {
+      const float *P = J.part + z * kk;
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const int a = 4 * ty + u, b = 4 * tx + w;
+          G[u][w] += (a < k && b < k) ? (double)P[a * k + b] : 0.0;
+        }
+    }
+  }
+  // pivot floor from the trace (every thread sums the 32 block sums in order)
+  if (tx == ty) dsum[ty] = G[0][0] + G[1][1] + G[2][2] + G[3][3];
+  __syncthreads();
+  double tr = 0.0;
+  for (int i = 0; i < 32; ++i) tr += dsum[i];
+  const double floor = 1e-12 * (tr > 0.0 ? tr : 0.0) / (k > 0 ? k : 1) + 1e-300;
+  const int half = (tid & 32);   // lane offset of this thread's half-wave
+
+  for (int j = 0; j < k; ++j) {
+    const int buf = j & 1, jr = j >> 2, ju = j & 3;
+    if (ty == jr) {   // one half-wave: pivot, scaling, broadcast
+      double gd = 0.0;
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (u == ju) gd = G[u][u];
+      // G_jj from the diagonal block's lane (tx = jr) of this half-wave
+      const int src = half + jr;
+      const int lo = __builtin_amdgcn_readlane(__double2loint(gd), src);
+      const int hi = __builtin_amdgcn_readlane(__double2hiint(gd), src);
+      const double d0 = __hiloint2double(hi, lo);
+      const double d = d0 > floor ? d0 : floor;
+      const double rs = 1.0 / sqrt(d);
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const int col = 4 * tx + w;
+        double gv = 0.0, xv = 0.0;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (u == ju) {
+            X[u][w] *= rs;   // row j of X is final from here on
+            gv = G[u][w];
+            xv = X[u][w];
+          }
+        lb[buf][col] = own_g && col >= j ? gv * rs : 0.0;
+        xb[buf][col] = own_x ? xv : 0.0;
+      }
+    }
+    __syncthreads();
+    double la[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) la[u] = lb[buf][4 * ty + u];
+    if (own_g && 4 * ty + 3 > j) {
+      double lc[4];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) lc[w] = lb[buf][4 * tx + w];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) G[u][w] -= la[u] * lc[w];
+    }
+    if (own_x && 4 * ty + 3 > j) {
+      double xc[4];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) xc[w] = xb[buf][4 * tx + w];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (4 * ty + u > j)
+#pragma unroll
+          for (int w = 0; w < 4; ++w) X[u][w] -= la[u] * xc[w];
+    }
+  }
+  // R^-1 = X^T (upper triangular), row-major: element (i, c) = X[c][i]
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const int c = 4 * ty + u, i = 4 * tx + w;
+      if (c < k && i < k) J.out[i * k + c] = own_x ? (float)X[u][w] : 0.f;
+    }
 }
 
 constexpr int kCholGlobalThreads = 512;   // 64-bit addresses need the register room
