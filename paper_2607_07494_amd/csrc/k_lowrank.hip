@@ -46,12 +46,28 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 __device__ __forceinline__ float4 ld4(const float *p) { return *reinterpret_cast<const float4 *>(p); }
 __device__ __forceinline__ float4 zero4() { return make_float4(0.f, 0.f, 0.f, 0.f); }
-// 16 bytes at p when ok, else zeros (a branch around the load, never a
-// select between addresses)
+// 16 bytes at p when ok, else zeros.  p must be a valid address either way:
+// the load itself is unconditional and the zeros come from a select, because
+// a load under a branch makes every later wait for loads a full one.
 __device__ __forceinline__ float4 ld4_if(bool ok, const float *p) {
-  float4 v = zero4();
-  if (ok) v = ld4(p);
-  return v;
+  const float4 v = ld4(p);
+  return ok ? v : zero4();
+}
+
+// Stores the compiler does not track.  On this target a store and a load in
+// flight share one counter, and the compiler, seeing both kinds pending,
+// turns every wait for a load into a wait for everything; with these stores
+// its waits cover its own loads only.  The hardware counter still counts the
+// stores, so those waits can only last longer, never too short.  The s_nop
+// gives a wide store the wait state it needs before its data registers may
+// be rewritten.
+__device__ __forceinline__ void st_u32_untracked(void *p, uint32_t v) {
+  asm volatile("global_store_dword %0, %1, off\n\ts_nop 1" ::"v"(p), "v"(v) : "memory");
+}
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void st_u128_untracked(void *p, uint4 v) {
+  const u32x4_t w = {v.x, v.y, v.z, v.w};
+  asm volatile("global_store_dwordx4 %0, %1, off\n\ts_nop 1" ::"v"(p), "v"(w) : "memory");
 }
 
 // hi / lo bf16 pairs of two float32 values (round to nearest even)
@@ -139,14 +155,15 @@ __global__ __launch_bounds__(kProjThreads) void lr_proj_kernel(const LPArgs p) {
       const int ch = s / (4 * C), c = (s >> 2) % C, g = s & 3;
       const int64_t k = ks + 32 * ch + 4 * g;
       const bool ok = s < SLOTS;
-      yr[u][0] = ld4_if(ok && k < k1, yb + (int64_t)c * p.K + k);
-      yr[u][1] = ld4_if(ok && k + 16 < k1, yb + (int64_t)c * p.K + k + 16);
+      const float *yc = yb + (int64_t)c * p.K;
+      yr[u][0] = ld4_if(ok && k < k1, yc + (k < k1 ? k : k0));
+      yr[u][1] = ld4_if(ok && k + 16 < k1, yc + (k + 16 < k1 ? k + 16 : k0));
     }
 #pragma unroll
     for (int ch = 0; ch < 2; ++ch) {
       const int64_t k = ks + 32 * ch + 4 * fg;
-      xr[ch][0] = ld4_if(rv && k < k1, xrow + k);
-      xr[ch][1] = ld4_if(rv && k + 16 < k1, xrow + k + 16);
+      xr[ch][0] = ld4_if(rv && k < k1, xrow + (k < k1 ? k : k0));
+      xr[ch][1] = ld4_if(rv && k + 16 < k1, xrow + (k + 16 < k1 ? k + 16 : k0));
     }
   };
   auto stage_y = [&](int buf) {
@@ -265,8 +282,9 @@ struct LUArgs {
   int shared, batch;
 };
 
-template <int EPI, bool EF, int NSEG, int KC>
+template <int EPI, bool EF, int NSEG, int KC, bool FULL = false>
 __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) {
+  static_assert(!FULL || EPI != EPI_STORE, "FULL is an AMAX / QUANT variant");
   constexpr int NCH = NSEG * KC;                // 32-step chunks over all segments
   constexpr int TSLOTS = NCH * 64 * 4;          // (chunk, column, fg) entries of a 64-column tile
   constexpr int TILES = upd_tiles(NCH);
@@ -292,7 +310,7 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
   if (EPI == EPI_QUANT && p.clear_words) {
     const int64_t nthreads = (int64_t)gridDim.x * gridDim.y * gridDim.z * kUpdThreads;
     const int64_t gt = (((int64_t)blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x) * kUpdThreads + tid;
-    for (int64_t i = gt; i < p.clear_words; i += nthreads) p.clear[i] = 0u;
+    for (int64_t i = gt; i < p.clear_words; i += nthreads) st_u32_untracked(p.clear + i, 0u);
   }
   int64_t q_blk = -1;      // block whose maximum q_amax holds (QUANT from raw slots)
   float q_amax = 0.f;
@@ -307,25 +325,51 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
   // W (and residual) values of the wave's 32 x 64 tile: lane holds row
   // ri[g], columns j0 + 16 t + 4 fg .. + 3; two register sets alternate
   typedef float4 WTile[2][4];
+  // Unconditional buffer loads over this rank's M x N slice (a guarded load
+  // would make every later wait a full one): rows past M fall outside the
+  // range and read zeros; columns past N read the next row or zeros, and the
+  // epilogue leaves them out.
+  const __amdgpu_buffer_rsrc_t rsD =
+      __builtin_amdgcn_make_buffer_rsrc((void *)(p.D + (int64_t)b * MN), (short)0, (int)(MN * 4), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsE = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)(EF ? p.ef + (int64_t)b * MN : p.D), (short)0, EF ? (int)(MN * 4) : 0, 0x00020000);
+  uint32_t roff[2];
+#pragma unroll
+  for (int g = 0; g < 2; ++g) roff[g] = rv[g] ? (uint32_t)(ri[g] * p.N * 4) : 0x80000000u;
   auto load_w = [&](int64_t j0, WTile &dd, WTile &re) {
 #pragma unroll
     for (int g = 0; g < 2; ++g)
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        const int64_t cj = j0 + 16 * t + 4 * fg;
-        const bool ok = rv[g] && cj < p.N;
-        const int64_t off = (int64_t)b * MN + ri[g] * p.N + cj;
-        dd[g][t] = ld4_if(ok, p.D + off);
-        if (EF) re[g][t] = ld4_if(ok, p.ef + off);
+        const uint32_t off = roff[g] + (uint32_t)((j0 + 16 * t + 4 * fg) * 4);
+        dd[g][t] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rsD, (int)off, 0, 0));
+        if (EF) re[g][t] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rsE, (int)off, 0, 0));
       }
   };
-  WTile dA, dB, rA, rB;
-  load_w(c_begin, dA, rA);
-  if (ntiles > 1) load_w(c_begin + 64, dB, rB);
-
-  // the column operand of the workgroup's whole column range, split into
-  // LDS once: entry s -> (tile, chunk, column, fg), two float4 each
-#pragma unroll 4
+  // Prologue loads in the order they are needed, all unconditional so that
+  // each wait covers only what it must: the column operand of the whole
+  // column range and the row fragments' first partials, then the first two
+  // W tiles (in flight while the operands are split into LDS).
+  // FULL QUANT: the finished maximum of each tile's block from the AMAX
+  // pass's raw sub-slots (lane l reads sub-slot l; every rank's when shared)
+  uint32_t t_raw[TILES];
+  if (FULL && EPI == EPI_QUANT) {
+    const int64_t nblk = (int64_t)p.nbr * p.nbc;
+    const int64_t bi = (i0 < p.M ? i0 : p.M - 1) / p.br;
+#pragma unroll
+    for (int ct = 0; ct < TILES; ++ct) {
+      const int64_t gb = bi * p.nbc + (c_begin + 64 * ct) / p.bc;
+      uint32_t m = p.raw[((int64_t)b * nblk + gb) * kAmaxSlots + lane];
+      if (p.shared)
+        for (int r = 0; r < p.batch; ++r) {
+          const uint32_t v = p.raw[((int64_t)r * nblk + gb) * kAmaxSlots + lane];
+          m = v > m ? v : m;
+        }
+      t_raw[ct] = m;
+    }
+  }
+  float4 cv[PER][2];
+#pragma unroll
   for (int u = 0; u < PER; ++u) {
     const int s = tid + u * kUpdThreads;
     const int ct = s / TSLOTS, rem = s % TSLOTS;
@@ -334,15 +378,39 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
     const int64_t k = 32 * (ch % KC) + 4 * g;
     const int64_t j = c_begin + 64 * ct + c;
     const float *q = sg.col + (int64_t)b * sg.col_bs + (j < p.N ? j : 0) * sg.col_ld;
-    const float4 v0 = ld4_if(j < p.N && k < sg.K, q + k);
-    const float4 v1 = ld4_if(j < p.N && k + 16 < sg.K, q + k + 16);
+    cv[u][0] = ld4_if(j < p.N && k < sg.K, q + (k < sg.K ? k : 0));
+    cv[u][1] = ld4_if(j < p.N && k + 16 < sg.K, q + (k + 16 < sg.K ? k + 16 : 0));
+  }
+  float4 rv0[2][NCH], rv1[2][NCH];
+#pragma unroll
+  for (int g = 0; g < 2; ++g)
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch) {
+      const LUSeg &sg = p.seg[ch / KC];
+      const int64_t k = 32 * (ch % KC) + 4 * fg;
+      const float *q = sg.row + (int64_t)b * sg.row_parts * sg.row_bs + (rv[g] ? ri[g] : 0) * sg.row_ld;
+      rv0[g][ch] = ld4_if(rv[g] && k < sg.K, q + (k < sg.K ? k : 0));
+      rv1[g][ch] = ld4_if(rv[g] && k + 16 < sg.K, q + (k + 16 < sg.K ? k + 16 : 0));
+    }
+  WTile dA, dB, rA, rB;
+  load_w(c_begin, dA, rA);
+  load_w(c_begin + 64, dB, rB);   // past the range when ntiles == 1: not used
+  __builtin_amdgcn_sched_barrier(0);   // keep every prologue load ahead of the first wait
+
+  // the column operand split into LDS: entry s -> (tile, chunk, column, fg)
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int s = tid + u * kUpdThreads;
+    const int ct = s / TSLOTS, rem = s % TSLOTS;
+    const int ch = rem / 256, c = (rem >> 2) & 63, g = rem & 3;
     uint4 h, l;
-    split8(v0, v1, h, l);
+    split8(cv[u][0], cv[u][1], h, l);
     chi[ct * TSLOTS + ch * 256 + lds_slot(c, g)] = h;
     clo[ct * TSLOTS + ch * 256 + lds_slot(c, g)] = l;
   }
 
-  // row-side fragments of the wave's 32 rows, split once for all tiles
+  // row-side fragments of the wave's 32 rows (split-K partials summed in
+  // order), split once for all tiles
   uint4 rh[2][NCH], rl[2][NCH];
 #pragma unroll
   for (int g = 0; g < 2; ++g)
@@ -350,20 +418,15 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
     for (int ch = 0; ch < NCH; ++ch) {
       const LUSeg &sg = p.seg[ch / KC];
       const int64_t k = 32 * (ch % KC) + 4 * fg;
-      float4 v0 = zero4(), v1 = zero4();
-      if (rv[g]) {
-        const float *base = sg.row + (int64_t)b * sg.row_parts * sg.row_bs + ri[g] * sg.row_ld;
-        for (int zp = 0; zp < sg.row_parts; ++zp) {
+      float4 v0 = rv0[g][ch], v1 = rv1[g][ch];
+      if (sg.row_parts > 1) {
+        const float *base = sg.row + (int64_t)b * sg.row_parts * sg.row_bs + (rv[g] ? ri[g] : 0) * sg.row_ld;
+        for (int zp = 1; zp < sg.row_parts; ++zp) {
           const float *q = base + (int64_t)zp * sg.row_bs;
-          const float4 a = ld4_if(k < sg.K, q + k);
-          const float4 c = ld4_if(k + 16 < sg.K, q + k + 16);
-          if (zp == 0) {
-            v0 = a;
-            v1 = c;
-          } else {
-            v0.x += a.x; v0.y += a.y; v0.z += a.z; v0.w += a.w;
-            v1.x += c.x; v1.y += c.y; v1.z += c.z; v1.w += c.w;
-          }
+          const float4 a = ld4_if(rv[g] && k < sg.K, q + (k < sg.K ? k : 0));
+          const float4 c = ld4_if(rv[g] && k + 16 < sg.K, q + (k + 16 < sg.K ? k + 16 : 0));
+          v0.x += a.x; v0.y += a.y; v0.z += a.z; v0.w += a.w;
+          v1.x += c.x; v1.y += c.y; v1.z += c.z; v1.w += c.w;
         }
       }
       split8(v0, v1, rh[g][ch], rl[g][ch]);
@@ -373,6 +436,14 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
 
   uint32_t run_max = 0u;
   int64_t run_blk = -1;
+  // FULL: every wave tile lies in one scale block and the workgroup's whole
+  // column range is processed without branches, so the compiler can wait for
+  // one register set of W while the next one stays in flight.  AMAX keeps the
+  // tiles' maxima here and merges them into the block slots after the loop
+  // (no store in the loop)
+  uint32_t tmax[TILES];
+#pragma unroll
+  for (int t = 0; t < TILES; ++t) tmax[t] = 0u;
   // one 64-column tile, no barrier: products from LDS, epilogue on `cur`,
   // then the loads of tile ct + 2 into the same register set
   auto tile = [&](int ct, WTile &cur, WTile &curR) {
@@ -416,7 +487,23 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
         const bool uniform = (int64_t)(bi_lo + 1) * p.br > rlast && (int64_t)(bj_lo + 1) * p.bc > clast;
         const int64_t u_gb = (int64_t)bi_lo * p.nbc + bj_lo;
         const int64_t nblk = (int64_t)p.nbr * p.nbc;
-        if (EPI == EPI_AMAX) {
+        if (FULL && EPI == EPI_AMAX) {
+          uint32_t m = 0u;
+  #pragma unroll
+          for (int g = 0; g < 2; ++g)
+  #pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              const int64_t cj = j0 + 16 * t + 4 * fg;
+              if (rv[g] && cj < p.N) {
+  #pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  const uint32_t a = __float_as_uint(w[g][t][e]) & 0x7fffffffu;
+                  m = a > m ? a : m;
+                }
+              }
+            }
+          tmax[ct] = wave_max_u32(m);
+        } else if (EPI == EPI_AMAX) {
           if (p.transformed) {
   #pragma unroll
             for (int g = 0; g < 2; ++g)
@@ -469,7 +556,13 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
           }
         } else {  // EPI_QUANT with finished block maxima
           float u_inv = 0.f, u_s = 0.f;
-          if (uniform) {
+          if (FULL) {
+            const float a = __uint_as_float(wave_max_u32(t_raw[ct]));
+            u_inv = e4m3_multiplier(a);
+            u_s = e4m3_scale(a);
+            if (lane == 0 && i0 == (int64_t)bi_lo * p.br && j0 == (int64_t)bj_lo * p.bc)
+              st_u32_untracked(p.scales + (int64_t)b * nblk + u_gb, __float_as_uint(u_s));
+          } else if (uniform) {
             float a;
             if (p.raw) {
               if (u_gb != q_blk) {
@@ -483,7 +576,7 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
                 q_amax = __uint_as_float(wave_max_u32(m));
                 q_blk = u_gb;
                 if (lane == 0 && i0 == (int64_t)bi_lo * p.br && j0 == (int64_t)bj_lo * p.bc)
-                  p.scales[(int64_t)b * nblk + u_gb] = e4m3_scale(q_amax);
+                  st_u32_untracked(p.scales + (int64_t)b * nblk + u_gb, __float_as_uint(e4m3_scale(q_amax)));
               }
               a = q_amax;
             } else {
@@ -499,7 +592,7 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
               const int64_t cj = j0 + 16 * t + 4 * fg;
               if (!(rv[g] && cj < p.N)) continue;
               float inv[4] = {u_inv, u_inv, u_inv, u_inv}, sc[4] = {u_s, u_s, u_s, u_s};
-              if (!uniform) {
+              if (!FULL && !uniform) {
   #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                   const float a = __uint_as_float(p.amax[(int64_t)b * nblk + (ri[g] / p.br) * p.nbc + (cj + e) / p.bc]);
@@ -518,7 +611,9 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
               }
               const int64_t off = (int64_t)b * MN + ri[g] * p.N + cj;
               cstage[wave][(16 * g + fr) * 16 + 4 * t + fg] = packed;
-              if (EF) *reinterpret_cast<float4 *>(p.ef + off) = make_float4(res[0], res[1], res[2], res[3]);
+              if (EF)
+                st_u128_untracked(p.ef + off, make_uint4(__float_as_uint(res[0]), __float_as_uint(res[1]),
+                                                         __float_as_uint(res[2]), __float_as_uint(res[3])));
             }
           // the wave reads back only what its own lanes wrote: the fences
           // order these LDS accesses (no workgroup barrier)
@@ -533,23 +628,52 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
             const uint4 v = *reinterpret_cast<const uint4 *>(&cstage[wave][row * 16 + 4 * qt]);
             if (gi < p.M) {
               uint8_t *dst = p.codes + (int64_t)b * MN + gi * p.N + cj;
-              if (p.codes_wide && cj + 16 <= p.N) {
-                *reinterpret_cast<uint4 *>(dst) = v;
+              if (FULL || (p.codes_wide && cj + 16 <= p.N)) {
+                st_u128_untracked(dst, v);
               } else {
                 const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
-                  if (cj + 4 * q < p.N) *reinterpret_cast<uint32_t *>(dst + 4 * q) = wv[q];
+                  if (cj + 4 * q < p.N) st_u32_untracked(dst + 4 * q, wv[q]);
               }
             }
           }
         }
       }
-    if (ct + 2 < ntiles) load_w(j0 + 128, cur, curR);
+    if (FULL ? ct + 2 < TILES : ct + 2 < ntiles) load_w(j0 + 128, cur, curR);
   };
-  for (int ct = 0; ct < ntiles; ct += 2) {
-    tile(ct, dA, rA);
-    if (ct + 1 < ntiles) tile(ct + 1, dB, rB);
+  if (FULL) {
+    // every tile of the range, also past N in the last range of an AMAX pass
+    // (its maxima leave those columns out; QUANT runs FULL only when N fills
+    // every range): no branch between the waits
+#pragma unroll
+    for (int ct = 0; ct < TILES; ct += 2) {
+      tile(ct, dA, rA);
+      tile(ct + 1, dB, rB);
+    }
+    // one atomic per run of tiles in the same block
+    if (EPI == EPI_AMAX && wave_live && lane == 0) {
+      const int64_t nblk = (int64_t)p.nbr * p.nbc;
+      const int64_t brow = (i0 / p.br) * p.nbc;
+#pragma unroll
+      for (int ct = 0; ct < TILES; ++ct) {
+        if (ct >= ntiles) break;
+        const int64_t gb = brow + (c_begin + 64 * ct) / p.bc;
+        if (run_blk != gb) {
+          if (run_blk >= 0 && run_max)
+            atomicMax(&p.amax[((int64_t)b * nblk + run_blk) * kAmaxSlots + slot], run_max);
+          run_blk = gb;
+          run_max = tmax[ct];
+        } else {
+          run_max = tmax[ct] > run_max ? tmax[ct] : run_max;
+        }
+      }
+    }
+  } else {
+    for (int ct = 0; ct < ntiles; ct += 2) {
+      tile(ct, dA, rA);
+      if (ct + 1 < ntiles) tile(ct + 1, dB, rB);
+    }
   }
   if (EPI == EPI_AMAX && wave_live && run_blk >= 0 && lane == 0 && run_max)
     atomicMax(&p.amax[((int64_t)b * p.nbr * p.nbc + run_blk) * kAmaxSlots + slot], run_max);
@@ -634,6 +758,7 @@ bool lr_quant_reads_raw(const TileJob &j) {
 
 bool lr_update_eligible(const TileJob &j) {
   if (!j.split3 || j.amax == nullptr || j.nseg < 1 || j.nseg > 2 || j.N % 4 != 0) return false;
+  if (j.M * j.N >= (1LL << 29)) return false;   // one rank's slice within a 32-bit buffer range
   const int64_t K = j.seg[0].K;
   if (K <= 0 || K > 128 || K % 4 != 0) return false;
   for (int s = 0; s < j.nseg; ++s) {
@@ -686,8 +811,22 @@ gift_status launch_lr_update(gift_ctx *ctx, const TileJob &j) {
   const bool quant = j.codes != nullptr;
   const bool ef = j.ef != nullptr;
   const int kc = (int)((j.seg[0].K + 31) / 32);
+  // every wave tile inside one scale block, no optional W~ output, and for
+  // QUANT the raw block maxima and whole column ranges: the variant whose
+  // tile loop has no branch between its waits
+  const bool full = lr_quant_reads_raw(j) && j.transformed == nullptr &&
+                    (!quant || (a.raw != nullptr && a.codes_wide && j.N % cols == 0));
   auto go = [&](auto epi_c, auto ef_c, auto nseg_c, auto kc_c) {
-    hipLaunchKernelGGL((lr_update_kernel<decltype(epi_c)::value, decltype(ef_c)::value, decltype(nseg_c)::value,
+    constexpr int E = decltype(epi_c)::value;
+    if constexpr (E == EPI_AMAX || E == EPI_QUANT) {
+      if (full) {
+        hipLaunchKernelGGL((lr_update_kernel<E, decltype(ef_c)::value, decltype(nseg_c)::value,
+                                             decltype(kc_c)::value, true>),
+                           grid, dim3(kUpdThreads), 0, ctx->stream, a);
+        return;
+      }
+    }
+    hipLaunchKernelGGL((lr_update_kernel<E, decltype(ef_c)::value, decltype(nseg_c)::value,
                                          decltype(kc_c)::value>),
                        grid, dim3(kUpdThreads), 0, ctx->stream, a);
   };

@@ -229,24 +229,38 @@ def test_transform_encode_decode_parity(ctx, N, m, n, r, sides, br, bc):
     f.close()
 
 
-@pytest.mark.parametrize("N,m,n,r,sides,br,bc,use_ef", [
-    (8, 320, 384, 64, gift.SIDE_INPUT, 0, 128, False),
-    (2, 136, 256, 128, gift.SIDE_INPUT, 0, 0, True),
-    (3, 260, 520, 32, gift.SIDE_BOTH, 0, 0, False),
-    (2, 100, 200, 16, gift.SIDE_INPUT, 7, 12, True),
+@pytest.mark.parametrize("N,m,n,r,sides,br,bc,use_ef,shared", [
+    (8, 320, 384, 64, gift.SIDE_INPUT, 0, 128, False, False),
+    (2, 136, 256, 128, gift.SIDE_INPUT, 0, 0, True, False),
+    (3, 260, 520, 32, gift.SIDE_BOTH, 0, 0, False, False),
+    (2, 100, 200, 16, gift.SIDE_INPUT, 7, 12, True, False),
+    # whole 256-column ranges (n % 256 == 0, r = 64): the branch-free encode
+    # kernels, per-tensor and per-128/64-column blocks, ragged rows, error
+    # feedback and the shared scale
+    (4, 200, 512, 64, gift.SIDE_INPUT, 0, 128, False, False),
+    (2, 300, 1024, 64, gift.SIDE_INPUT, 0, 0, False, False),
+    (3, 96, 256, 64, gift.SIDE_INPUT, 0, 64, True, False),
+    (4, 160, 512, 64, gift.SIDE_INPUT, 0, 0, False, True),
+    (2, 64, 768, 64, gift.SIDE_INPUT, 32, 256, True, True),
 ])
-def test_recomputed_transform_matches_stored(ctx, N, m, n, r, sides, br, bc, use_ef):
+def test_recomputed_transform_matches_stored(ctx, N, m, n, r, sides, br, bc, use_ef, shared):
     """Without a `transformed` buffer the quantize pass computes W~ again
     instead of reading it back: codes, scales and residuals must equal those
     of an encode that stores W~."""
-    say(f"recompute N={N} m={m} n={n} r={r} sides={sides} block=({br},{bc}) ef={use_ef}")
+    say(f"recompute N={N} m={m} n={n} r={r} sides={sides} block=({br},{bc}) ef={use_ef} shared={shared}")
     grads = gradient_set(900 + m, 901 + n, N, m, n)
     f, _, _ = make_factor(ctx, m, n, r, sides, seed=3 * m + n)
     R0 = gradient_set(902, 903, N, m, n) * np.float32(0.01) if use_ef else None
     Ra = torch.from_numpy(R0).to(DEV) if use_ef else None
     Rb = torch.from_numpy(R0).to(DEV) if use_ef else None
-    ca, sa, _ = gpu_encode(ctx, f, grads, br, bc, False, want_t=True, ef=Ra)
-    cb, sb, _ = gpu_encode(ctx, f, grads, br, bc, False, want_t=False, ef=Rb)
+    if shared:
+        grads[1] *= 3.0
+    ca, sa, ta = gpu_encode(ctx, f, grads, br, bc, shared, want_t=True, ef=Ra)
+    cb, sb, _ = gpu_encode(ctx, f, grads, br, bc, shared, want_t=False, ef=Rb)
+    # the stored path itself against the oracle's quantizer on its W~
+    ref_codes, ref_scales = codec.quantize_transformed(ta, br, bc, shared)
+    np.testing.assert_array_equal(sa, ref_scales)
+    np.testing.assert_array_equal(ca, ref_codes)
     np.testing.assert_array_equal(sa, sb)
     np.testing.assert_array_equal(ca, cb)
     if use_ef:
