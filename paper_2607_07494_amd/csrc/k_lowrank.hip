@@ -147,6 +147,9 @@ __global__ __launch_bounds__(kProjThreads) void lr_proj_kernel(const LPArgs p) {
   const float *xrow = p.X + (int64_t)b * p.x_bs + (rv ? ri : 0) * p.K;
   const float *yb = p.Y + (int64_t)b * p.y_bs;
 
+  // Loads of one stage at clamped (valid) addresses with no select: the
+  // zeros for slots past the range are applied where the values are used,
+  // so the loads of the next stage stay in flight under this stage's MFMAs.
   float4 yr[PER][2], xr[2][2];
   auto load = [&](int64_t ks) {
 #pragma unroll
@@ -154,26 +157,26 @@ __global__ __launch_bounds__(kProjThreads) void lr_proj_kernel(const LPArgs p) {
       const int s = tid + u * kProjThreads;
       const int ch = s / (4 * C), c = (s >> 2) % C, g = s & 3;
       const int64_t k = ks + 32 * ch + 4 * g;
-      const bool ok = s < SLOTS;
       const float *yc = yb + (int64_t)c * p.K;
-      yr[u][0] = ld4_if(ok && k < k1, yc + (k < k1 ? k : k0));
-      yr[u][1] = ld4_if(ok && k + 16 < k1, yc + (k + 16 < k1 ? k + 16 : k0));
+      yr[u][0] = ld4(yc + (k < k1 ? k : k0));
+      yr[u][1] = ld4(yc + (k + 16 < k1 ? k + 16 : k0));
     }
 #pragma unroll
     for (int ch = 0; ch < 2; ++ch) {
       const int64_t k = ks + 32 * ch + 4 * fg;
-      xr[ch][0] = ld4_if(rv && k < k1, xrow + (k < k1 ? k : k0));
-      xr[ch][1] = ld4_if(rv && k + 16 < k1, xrow + (k + 16 < k1 ? k + 16 : k0));
+      xr[ch][0] = ld4(xrow + (k < k1 ? k : k0));
+      xr[ch][1] = ld4(xrow + (k + 16 < k1 ? k + 16 : k0));
     }
   };
-  auto stage_y = [&](int buf) {
+  auto stage_y = [&](int buf, int64_t ks) {
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int s = tid + u * kProjThreads;
       if (s >= SLOTS) continue;
       const int ch = s / (4 * C), c = (s >> 2) % C, g = s & 3;
+      const int64_t k = ks + 32 * ch + 4 * g;
       uint4 h, l;
-      split8(yr[u][0], yr[u][1], h, l);
+      split8(k < k1 ? yr[u][0] : zero4(), k + 16 < k1 ? yr[u][1] : zero4(), h, l);
       yhi[buf][ch * 4 * C + lds_slot(c, g)] = h;
       ylo[buf][ch * 4 * C + lds_slot(c, g)] = l;
     }
@@ -184,16 +187,20 @@ __global__ __launch_bounds__(kProjThreads) void lr_proj_kernel(const LPArgs p) {
   for (int t = 0; t < NT; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
   if (nst > 0) {
     load(k0);
-    stage_y(0);
+    stage_y(0, k0);
   }
   __syncthreads();
   for (int st = 0; st < nst; ++st) {
     const int buf = st & 1;
+    const int64_t ks = k0 + (int64_t)st * kProjStage;
     uint4 xh[2], xl[2];
 #pragma unroll
-    for (int ch = 0; ch < 2; ++ch) split8(xr[ch][0], xr[ch][1], xh[ch], xl[ch]);
+    for (int ch = 0; ch < 2; ++ch) {
+      const int64_t k = ks + 32 * ch + 4 * fg;
+      split8(rv && k < k1 ? xr[ch][0] : zero4(), rv && k + 16 < k1 ? xr[ch][1] : zero4(), xh[ch], xl[ch]);
+    }
     const bool more = st + 1 < nst;
-    if (more) load(k0 + (int64_t)(st + 1) * kProjStage);
+    if (more) load(ks + kProjStage);
 #pragma unroll
     for (int ch = 0; ch < 2; ++ch)
 #pragma unroll
@@ -201,7 +208,7 @@ __global__ __launch_bounds__(kProjThreads) void lr_proj_kernel(const LPArgs p) {
         const int e = ch * 4 * C + lds_slot(16 * t + fr, fg);
         acc[t] = mfma3(yhi[buf][e], ylo[buf][e], xh[ch], xl[ch], acc[t]);
       }
-    if (more) stage_y(buf ^ 1);
+    if (more) stage_y(buf ^ 1, ks + kProjStage);
     __syncthreads();
   }
   if (!rv) return;

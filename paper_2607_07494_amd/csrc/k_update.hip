@@ -69,6 +69,18 @@ struct UArgs {
 
 __device__ __forceinline__ float4 ld4(const float *p) { return *reinterpret_cast<const float4 *>(p); }
 
+// A 16-byte store the compiler does not track.  A store and a load in flight
+// share one counter on this target, and with both kinds pending the compiler
+// turns every wait for a load into a wait for everything; with this store its
+// waits cover its own loads only (the hardware counter still counts the
+// store, so they can only last longer).  The s_nop gives the wide store the
+// wait state it needs before its data registers may be rewritten.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void st4_untracked(float *p, float x, float y, float z, float w) {
+  const u32x4_t v = {__float_as_uint(x), __float_as_uint(y), __float_as_uint(z), __float_as_uint(w)};
+  asm volatile("global_store_dwordx4 %0, %1, off\n\ts_nop 1" ::"v"(p), "v"(v) : "memory");
+}
+
 __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -141,27 +153,34 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const UArgs p) {
       const int col = slot / (KT / 4), kq = slot % (KT / 4);
       const int s = (4 * kq) / (16 * K16), kk = 4 * kq - s * 16 * K16;
       const int64_t cj = j0 + col;
-      creg[u] = cj < p.N ? ld4(p.seg[s].col + (int64_t)b * p.seg[s].col_bs + cj * p.seg[s].col_ld + kk)
-                         : make_float4(0.f, 0.f, 0.f, 0.f);
+      // clamped address, unconditional load; columns past N are zeroed when
+      // the tile goes to LDS
+      creg[u] = ld4(p.seg[s].col + (int64_t)b * p.seg[s].col_bs + (cj < p.N ? cj : 0) * p.seg[s].col_ld + kk);
     }
   };
-  auto store_cols = [&](int buf) {
+  auto store_cols = [&](int buf, int64_t j0) {
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int slot = tid + u * kThreads;
       const int col = slot / (KT / 4), kq = slot % (KT / 4);
-      *reinterpret_cast<float4 *>(&lds[buf][col * ROW + 4 * kq]) = creg[u];
+      *reinterpret_cast<float4 *>(&lds[buf][col * ROW + 4 * kq]) =
+          j0 + col < p.N ? creg[u] : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   };
+  // W (and residual) by unconditional buffer loads over this rank's slice:
+  // rows past M read zeros, columns past N are left out by the epilogue
+  const __amdgpu_buffer_rsrc_t rsD =
+      __builtin_amdgcn_make_buffer_rsrc((void *)(p.D + (int64_t)b * MN), (short)0, (int)(MN * 4), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsE = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)(EF ? p.ef + (int64_t)b * MN : p.D), (short)0, EF ? (int)(MN * 4) : 0, 0x00020000);
+  const uint32_t roff = rv ? (uint32_t)(ri * p.N * 4) : 0x80000000u;
   float4 d[4], rr[4];
   auto load_w = [&](int64_t j0) {
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      const int64_t cj = j0 + 16 * t + 4 * fg;
-      const bool ok = rv && cj < p.N;
-      const int64_t off = (int64_t)b * MN + ri * p.N + cj;
-      d[t] = ok ? ld4(p.D + off) : make_float4(0.f, 0.f, 0.f, 0.f);
-      if (EF) rr[t] = ok ? ld4(p.ef + off) : make_float4(0.f, 0.f, 0.f, 0.f);
+      const uint32_t off = roff + (uint32_t)((j0 + 16 * t + 4 * fg) * 4);
+      d[t] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rsD, (int)off, 0, 0));
+      if (EF) rr[t] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rsE, (int)off, 0, 0));
     }
   };
 
@@ -169,7 +188,7 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const UArgs p) {
   int64_t run_blk = -1;
   load_cols(c_begin);
   load_w(c_begin);
-  store_cols(0);
+  store_cols(0, c_begin);
   __syncthreads();
   for (int ct = 0; ct < ntiles; ++ct) {
     const int buf = ct & 1;
@@ -208,7 +227,7 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const UArgs p) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[t].w, bb.w, acc[t], 0, 0, 0);
       }
-    if (more) store_cols(buf ^ 1);
+    if (more) store_cols(buf ^ 1, j0 + 64);
 
     if (wave_live) {
       // lane holds W~[ri][j0 + 16t + 4fg + v] = d + acc[t][v] (+ residual)
@@ -230,9 +249,7 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const UArgs p) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           const int64_t cj = j0 + 16 * t + 4 * fg;
-          if (rv && cj < p.N)
-            *reinterpret_cast<float4 *>(p.C + (int64_t)b * MN + ri * p.N + cj) =
-                make_float4(w[t][0], w[t][1], w[t][2], w[t][3]);
+          if (rv && cj < p.N) st4_untracked(p.C + (int64_t)b * MN + ri * p.N + cj, w[t][0], w[t][1], w[t][2], w[t][3]);
         }
       } else {
         // scale-block geometry of this wave tile (wave-uniform, two divisions)
@@ -549,6 +566,7 @@ int proj_parts(int64_t M, int64_t K, int C, int32_t batch) {
 
 bool update_kernel_eligible(const TileJob &j) {
   if (j.N % 4 != 0 || j.nseg < 1 || j.nseg > 2) return false;
+  if (j.M * j.N >= (1LL << 29)) return false;   // one rank's slice within a 32-bit buffer range
   const int64_t K = j.seg[0].K;
   if (K != 16 && K != 32 && K != 64 && K != 128) return false;
   for (int s = 0; s < j.nseg; ++s) {
