@@ -46,6 +46,8 @@ FAMILY_SOURCE = {
     "project": "paper_2607_07494_amd/csrc/k_lowrank.hip",
     "update_amax": "paper_2607_07494_amd/csrc/k_lowrank.hip",
     "update_quant": "paper_2607_07494_amd/csrc/k_lowrank.hip",
+    "update_store": "paper_2607_07494_amd/csrc/k_update.hip",
+    "decode_project": "paper_2607_07494_amd/csrc/k_update.hip",
 }
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm-traffic.md")
 
@@ -222,7 +224,7 @@ def algorithmic_work(wl, jobs, args):
         add("update_quant", 0, 5 * e)
         add("reduce", 0, float(m) * n * (N + 4))
         mn = float(m) * n
-        add("project", 2 * mn * (ra + rg), 4 * mn * ((ra > 0) + (rg > 0)))
+        add("decode_project", 2 * mn * (ra + rg), 4 * mn * ((ra > 0) + (rg > 0)))
         add("update_store", 2 * mn * (ra + rg), 8 * mn)
         # factor refresh (amortised by the cadence), once per distinct factor
         for dim, on in ((n, ra), (m, rg)):
@@ -235,6 +237,8 @@ def algorithmic_work(wl, jobs, args):
             sub = 8 * dim * k * k + q * (2 * dim * dim * k + 8 * dim * k * k) + \
                 2 * dim * dim * k + 2 * dim * k * k + 2 * dim * k * r
             add("factor", refresh * sub, 0)
+            # the k x k Cholesky factorisations and the eigensolver are
+            # latency-bound single-workgroup kernels: timed, no roofline
     return fam
 
 
@@ -444,7 +448,7 @@ def main():
     if traffic is not None:
         roof["traffic_unit"] = "GB per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
         roof["algorithmic_gb_per_launch"] = round((by / dom_launches) / 1e9, 4)
-    tf_fams = ("project", "update_amax", "update_quant", "update_store")
+    tf_fams = ("project", "update_amax", "update_quant", "decode_project", "update_store")
     tf_ms = sum(fam_ms[k][1] for k in tf_fams if k in fam_ms)
     tf_flops = sum(work[k][0] for k in tf_fams if k in work)
     line = {

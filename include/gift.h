@@ -92,9 +92,12 @@ typedef enum {
   GIFT_KERNEL_UPDATE_STORE = 5,  /* rank-r update of the inverse transform    */
   GIFT_KERNEL_REDUCE = 6,        /* dequantize-accumulate over ranks          */
   GIFT_KERNEL_SYRK = 7,          /* factor statistics X^T X / T               */
-  GIFT_KERNEL_FACTOR = 8,        /* subspace iteration, Rayleigh-Ritz, misc   */
+  GIFT_KERNEL_FACTOR = 8,        /* subspace-iteration products and setup     */
   GIFT_KERNEL_SMALL = 9,         /* small helpers (zeroing, coefficient setup) */
-  GIFT_KERNEL_COUNT = 10
+  GIFT_KERNEL_CHOL = 10,         /* CholeskyQR's k x k Cholesky and R^-1      */
+  GIFT_KERNEL_EIG = 11,          /* Rayleigh-Ritz k x k eigensolver           */
+  GIFT_KERNEL_DECODE_PROJECT = 12, /* the inverse transform's projections     */
+  GIFT_KERNEL_COUNT = 13
 } gift_kernel;
 
 /* ABI version of the loaded library (GIFT_ABI_VERSION it was built with). */

@@ -273,10 +273,11 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
     j.cbs = m * A.r;
     j.ksplit = pparts;
     j.split3 = !inverse;
-    j.kernel_family = GIFT_KERNEL_PROJECT;
+    j.kernel_family = inverse ? GIFT_KERNEL_DECODE_PROJECT : GIFT_KERNEL_PROJECT;
     if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
     if (presum &&
-        (st = launch_lr_psum(ctx, P, Psum, pparts, m * A.r, N, GIFT_KERNEL_PROJECT)) != GIFT_OK)
+        (st = launch_lr_psum(ctx, P, Psum, pparts, m * A.r, N,
+                            inverse ? GIFT_KERNEL_DECODE_PROJECT : GIFT_KERNEL_PROJECT)) != GIFT_OK)
       return st;
   }
   if (useG) {  // Qm = W^T U_G  (Q^T, n x r)
@@ -291,7 +292,7 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
     j.C = Qm;
     j.ldc = G.r;
     j.cbs = n * G.r;
-    j.kernel_family = GIFT_KERNEL_PROJECT;
+    j.kernel_family = inverse ? GIFT_KERNEL_DECODE_PROJECT : GIFT_KERNEL_PROJECT;
     if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
   }
   if (useA && useG) {
@@ -307,7 +308,7 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
       j.C = Km;
       j.ldc = A.r;
       j.cbs = (int64_t)G.r * A.r;
-      j.kernel_family = GIFT_KERNEL_PROJECT;
+      j.kernel_family = inverse ? GIFT_KERNEL_DECODE_PROJECT : GIFT_KERNEL_PROJECT;
       if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
     }
     {  // L2 = (P + U_G C_G K) C_A
@@ -327,7 +328,7 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
       j.dbs = m * A.r;
       j.beta = 1.f;
       j.colscale = inverse ? A.c_inv : A.c_fwd;
-      j.kernel_family = GIFT_KERNEL_PROJECT;
+      j.kernel_family = inverse ? GIFT_KERNEL_DECODE_PROJECT : GIFT_KERNEL_PROJECT;
       if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
     }
   }

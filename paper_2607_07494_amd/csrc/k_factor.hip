@@ -496,36 +496,43 @@ __device__ __forceinline__ void rr_emit(const double *W, const double *norms, in
   }
 }
 
-// LDS eigensolver, k <= 128: 64 pairs x 8 lanes (512 threads).  Lane l8 of
-// pair group g holds rows ((e + g) mod nb) * 8 + l8 of both columns in slot
-// e (nb = ceil(k / 8) blocks of 8 rows), so the eight pairs of a wave read
-// four different quarters of the LDS banks at every slot.
-constexpr int kEigThreads = 512;
+// LDS eigensolver, k <= 128: 64 pairs x 16 lanes (1024 threads).  Lane l16
+// of pair group g holds rows ((e + g) mod nb) * 16 + l16 of both columns in
+// slot e (nb = ceil(k / 16) blocks of 16 rows), so the four pairs of a wave
+// read four different row blocks at every slot.  Sweeps stop after the first
+// one whose largest rotated |<p,q>| / (|p| |q|) is at most kJacobiLast: the
+// next sweep would leave only about its square (far below the float32 noise
+// of B) and rotate nothing the codec can see.
+constexpr int kEigThreads = 1024;
+constexpr double kJacobiLast = 1e-6;
 __global__ __launch_bounds__(kEigThreads) void rr_eig_lds_kernel(const SmallJob *jobs,
                                                                  int max_sweeps) {
   __shared__ double W[kLdsK * kLdsK];
-  __shared__ double zpad[8], sink[8];   // loads of masked slots / their stores
+  __shared__ double zpad[16], sink[16];   // loads of masked slots / their stores
   __shared__ double norms[kLdsK];
   __shared__ int perm[kLdsK];
-  __shared__ int any_rot;
+  __shared__ int any_rot, any_big;
   const SmallJob J = jobs[blockIdx.x];
   const int k = J.k, tid = threadIdx.x;
-  if (tid < 8) zpad[tid] = 0.0;
-  load_sym<16>(J.part, J.ks, k, W);
+  if (tid < 16) zpad[tid] = 0.0;
+  load_sym<8>(J.part, J.ks, k, W);
   __syncthreads();
   const int kp = (k + 1) & ~1, npairs = kp / 2;
-  const int pi = tid >> 3, l8 = tid & 7, gw = (tid >> 3) & 7;
-  const int nb = (k + 7) >> 3;
-  int rows[16];
-  bool rv[16];
+  const int pi = tid >> 4, l16 = tid & 15, gw = (tid >> 4) & 3;
+  const int nb = (k + 15) >> 4;
+  int rows[8];
+  bool rv[8];
 #pragma unroll
-  for (int e = 0; e < 16; ++e) {
-    rows[e] = e < nb ? ((e + gw) % nb) * 8 + l8 : 0;
+  for (int e = 0; e < 8; ++e) {
+    rows[e] = e < nb ? ((e + gw) % nb) * 16 + l16 : 0;
     rv[e] = e < nb && rows[e] < k;
   }
-  const double tol2 = kJacobiTol * kJacobiTol;
+  const double tol2 = kJacobiTol * kJacobiTol, last2 = kJacobiLast * kJacobiLast;
   for (int sweep = 0; sweep < max_sweeps; ++sweep) {
-    if (tid == 0) any_rot = 0;
+    if (tid == 0) {
+      any_rot = 0;
+      any_big = 0;
+    }
     __syncthreads();
     for (int round = 0; round < kp - 1; ++round) {
       int p = 0, q = 0;
@@ -535,51 +542,54 @@ __global__ __launch_bounds__(kEigThreads) void rr_eig_lds_kernel(const SmallJob 
         valid = q < k;
       }
       double *cp = W + p * k, *cq = W + q * k;
-      double a[16], b[16];
+      double a[8], b[8];
       double alpha = 0.0, beta = 0.0, gamma = 0.0;
       // unconditional loads: a masked slot reads zeros from zpad (guarded
       // loads would each wait for the one before)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
+      for (int e = 0; e < 8; ++e) {
         const bool ok = valid && rv[e];
-        a[e] = *(ok ? cp + rows[e] : zpad + l8);
-        b[e] = *(ok ? cq + rows[e] : zpad + l8);
+        a[e] = *(ok ? cp + rows[e] : zpad + l16);
+        b[e] = *(ok ? cq + rows[e] : zpad + l16);
       }
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
+      for (int e = 0; e < 8; ++e) {
         alpha += a[e] * a[e];
         beta += b[e] * b[e];
         gamma += a[e] * b[e];
       }
-      alpha = octet_sum(alpha);
-      beta = octet_sum(beta);
-      gamma = octet_sum(gamma);
+      alpha = row16_sum(alpha);
+      beta = row16_sum(beta);
+      gamma = row16_sum(gamma);
       // |gamma| > tol sqrt(alpha beta), squared (alpha, beta >= 0)
       if (valid && gamma != 0.0 && gamma * gamma > tol2 * (alpha * beta)) {
         double c, s;
         jacobi_cs(alpha, beta, gamma, c, s);
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          *(rv[e] ? cp + rows[e] : sink + l8) = c * a[e] - s * b[e];
-          *(rv[e] ? cq + rows[e] : sink + l8) = s * a[e] + c * b[e];
+        for (int e = 0; e < 8; ++e) {
+          *(rv[e] ? cp + rows[e] : sink + l16) = c * a[e] - s * b[e];
+          *(rv[e] ? cq + rows[e] : sink + l16) = s * a[e] + c * b[e];
         }
-        if (l8 == 0) any_rot = 1;
+        if (l16 == 0) {
+          any_rot = 1;
+          if (gamma * gamma > last2 * (alpha * beta)) any_big = 1;
+        }
       }
       __syncthreads();
     }
-    const int rotated = any_rot;
+    const int rotated = any_rot, big = any_big;
     __syncthreads();
-    if (!rotated) break;
+    if (!rotated || !big) break;
   }
-  for (int c = pi; c < k; c += kEigThreads / 8) {
+  for (int c = pi; c < k; c += kEigThreads / 16) {
     double s = 0.0;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const double v = *(rv[e] ? W + c * k + rows[e] : zpad + l8);
+    for (int e = 0; e < 8; ++e) {
+      const double v = *(rv[e] ? W + c * k + rows[e] : zpad + l16);
       s += v * v;
     }
-    s = octet_sum(s);
-    if (l8 == 0) norms[c] = sqrt(s);
+    s = row16_sum(s);
+    if (l16 == 0) norms[c] = sqrt(s);
   }
   __syncthreads();
   rr_emit(W, norms, perm, k, J.out, J.theta);
@@ -1072,7 +1082,7 @@ gift_status factor_refresh_batch(gift_ctx *ctx, const std::vector<SideJob> &jobs
     return launch_tile(ctx, j);
   };
   auto small_launch = [&](bool eig) -> gift_status {
-    ProfileScope prof(ctx, GIFT_KERNEL_FACTOR);
+    ProfileScope prof(ctx, eig ? GIFT_KERNEL_EIG : GIFT_KERNEL_CHOL);
     const SmallJob *tab = eig ? d_eig : d_chol;
     if (n_lds > 0) {
       if (eig)

@@ -24,6 +24,7 @@ SCALE_LOCAL, SCALE_SHARED = 0, 1
 KERNELS = {
     "amax": 0, "quant": 1, "project": 2, "update_amax": 3, "update_quant": 4,
     "update_store": 5, "reduce": 6, "syrk": 7, "factor": 8, "small": 9,
+    "chol": 10, "eig": 11, "decode_project": 12,
 }
 
 _STATUS = {OK: "GIFT_OK", EINVAL: "GIFT_EINVAL", ESHAPE: "GIFT_ESHAPE", ENOMEM: "GIFT_ENOMEM",
