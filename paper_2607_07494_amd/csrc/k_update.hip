@@ -39,7 +39,7 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
 constexpr int kMaxK16 = 8;      // K <= 128 per segment
-constexpr int kColsPerUnit = 256;
+constexpr int kColsPerUnit = 128;
 
 struct USeg {
   const float *row;   // [batch][parts][M][K] (row_bs = 0: shared)
@@ -122,27 +122,33 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const UArgs p) {
   const int ntiles = (int)((p.N - c_begin + 63) / 64 < kColsPerUnit / 64 ? (p.N - c_begin + 63) / 64
                                                                           : kColsPerUnit / 64);
 
-  // row-side operand fragments of the strip, kept for all column tiles
+  // row-side operand fragments of the strip, kept for all column tiles: the
+  // split-K partials are summed in order, one partial's fragments loaded
+  // together (one round trip per partial, not one per fragment and partial)
   float4 bfr[NSEG][K16];
+  const int64_t rc = rv ? ri : 0;   // rows past M read row 0 and are zeroed
 #pragma unroll
-  for (int s = 0; s < NSEG; ++s)
+  for (int s = 0; s < NSEG; ++s) {
+    const int np = p.seg[s].row_parts;
+    const float *base = p.seg[s].row + (int64_t)b * np * p.seg[s].row_bs + rc * p.seg[s].row_ld + 4 * fg;
 #pragma unroll
-    for (int q = 0; q < K16; ++q) {
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (rv) {
-        const int np = p.seg[s].row_parts;
-        const float *base = p.seg[s].row + (int64_t)b * np * p.seg[s].row_bs + ri * p.seg[s].row_ld + 16 * q + 4 * fg;
-        v = ld4(base);
-        for (int z = 1; z < np; ++z) {
-          const float4 u = ld4(base + (int64_t)z * p.seg[s].row_bs);
-          v.x += u.x;
-          v.y += u.y;
-          v.z += u.z;
-          v.w += u.w;
-        }
+    for (int q = 0; q < K16; ++q) bfr[s][q] = ld4(base + 16 * q);
+    for (int z = 1; z < np; ++z) {
+      float4 u[K16];
+#pragma unroll
+      for (int q = 0; q < K16; ++q) u[q] = ld4(base + (int64_t)z * p.seg[s].row_bs + 16 * q);
+#pragma unroll
+      for (int q = 0; q < K16; ++q) {
+        bfr[s][q].x += u[q].x;
+        bfr[s][q].y += u[q].y;
+        bfr[s][q].z += u[q].z;
+        bfr[s][q].w += u[q].w;
       }
-      bfr[s][q] = v;
     }
+#pragma unroll
+    for (int q = 0; q < K16; ++q)
+      if (!rv) bfr[s][q] = make_float4(0.f, 0.f, 0.f, 0.f);
+  }
 
   // cooperative load of a column tile's operand: slot -> (column, k quad)
   float4 creg[PER];
