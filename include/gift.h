@@ -217,6 +217,26 @@ gift_status gift_encode(gift_ctx *ctx, const gift_factor *f, const float *grads,
                         int32_t block_cols, gift_scale_mode mode, float *ef,
                         uint8_t *codes, float *scales, float *transformed);
 
+/* gift_encode plus per-rank counters of codes that sit at either end of the
+ * FP8 range (Sec. V-C: the per-layer numerical-vulnerability profile
+ * that selects the layers for the geometry-aware branch; the score is the sum
+ * of the two ratios, i.e. of a rank's two counts over m*n):
+ *   hits[2j]   += codes of rank j with magnitude 448, the largest finite E4M3
+ *                 value (saturated values and every block's maximum itself);
+ *   hits[2j+1] += nonzero values of rank j whose code is +-0 (after scaling
+ *                 at most half the smallest subnormal, 2^-10).
+ * The counted values are those the codes encode (W~, + R with error
+ * feedback); NaN values count in neither.  hits: device, 4-byte aligned,
+ * uint32 [N][2], accumulated across calls (the caller zeroes it); counts past
+ * 2^32 - 1 wrap.  Everything else as gift_encode; the counting is done by the
+ * quantize kernels as they pack (no extra pass over the tensors).
+ * Errors: as gift_encode; GIFT_EINVAL for a NULL or misaligned hits. */
+gift_status gift_encode_hits(gift_ctx *ctx, const gift_factor *f, const float *grads,
+                             int32_t N, int64_t m, int64_t n, int32_t block_rows,
+                             int32_t block_cols, gift_scale_mode mode, float *ef,
+                             uint8_t *codes, float *scales, float *transformed,
+                             uint32_t *hits);
+
 /* Average the N ranks in transformed coordinates (eq. dp_grad_avg):
  *   mean[e] = fl32(acc / N),  acc = fl32(acc + fl32(val(codes[j][e]) * s_j)) for
  *   j = 0..N-1 in order (no fused multiply-add), s_j the scale of e's block.

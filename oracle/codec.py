@@ -35,6 +35,12 @@ design notes of the repository):
   the algorithm's sum-then-dequantize up to float rounding.
 * Blocks: ``block_rows x block_cols`` tiles of each rank's matrix, partial
   edge blocks allowed; 0 means the whole dimension.
+* Boundary hits (Sec. V-C ranks layers by the frequency of FP8 values at
+  the top and bottom of the format's range but leaves both undefined): an
+  upper hit is a code of magnitude 448, the largest finite E4M3 value (under
+  amax scaling every block's maximum lands there, and so does every
+  saturated value); a lower hit is a nonzero value whose code is +-0, i.e.
+  that underflowed.  NaN values count in neither.
 """
 
 from __future__ import annotations
@@ -253,6 +259,26 @@ def quantize_transformed(Wt: np.ndarray, block_rows: int = 0, block_cols: int = 
     s, inv = scales_from_amax(amax)
     codes = quantize_blocks(Wt, inv, block_rows, block_cols)
     return codes, s.astype(np.float32)
+
+
+def boundary_hits(Wt: np.ndarray, codes: np.ndarray) -> np.ndarray:
+    """Per-rank boundary hits of an encode (Sec. V-C's vulnerability profile).
+
+    ``Wt`` is the ``[N, m, n]`` float32 tensor the codes encode (the
+    transformed gradient, plus the residual with error feedback), ``codes``
+    its ``[N, m, n]`` E4M3 codes.  Returns ``[N, 2]`` int64: column 0 counts
+    codes whose value has magnitude 448 (the format's largest finite value),
+    column 1 counts nonzero values of ``Wt`` encoded as a zero.
+    """
+    Wt = np.asarray(Wt, dtype=np.float32)
+    val = e4m3.dequantize(np.asarray(codes, dtype=np.uint8))
+    N = Wt.shape[0]
+    out = np.zeros((N, 2), dtype=np.int64)
+    for j in range(N):
+        v = val[j]
+        out[j, 0] = int(np.count_nonzero(np.abs(v) == 448.0))
+        out[j, 1] = int(np.count_nonzero((v == 0.0) & (Wt[j] != 0.0)))
+    return out
 
 
 def dequantize_blocks(codes: np.ndarray, scales: np.ndarray, block_rows: int = 0,

@@ -65,4 +65,33 @@ __device__ __forceinline__ float e4m3_multiplier(float a) {
   return inv;
 }
 
+// Boundary hits of four codes (Sec. V-C's vulnerability profile): `up`
+// counts codes of magnitude 448 (the largest finite value: saturated values
+// and the block maximum itself), `lo` counts nonzero inputs whose code is +-0
+// (at most half the smallest subnormal after scaling).  NaN inputs count in
+// neither.
+__device__ __forceinline__ void e4m3_count_hits4(uint32_t packed, float x0, float x1, float x2, float x3,
+                                                 uint32_t &up, uint32_t &lo) {
+  const float x[4] = {x0, x1, x2, x3};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const uint32_t mag = (packed >> (8 * e)) & 0x7fu;
+    up += mag == 0x7eu;
+    lo += (mag == 0u) & (x[e] != 0.0f);
+  }
+}
+
+// Wave sums of the two counters added to hits[0], hits[1] by lane 0.
+__device__ __forceinline__ void e4m3_flush_hits(uint32_t *hits, uint32_t up, uint32_t lo) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    up += (uint32_t)__shfl_xor((int)up, o);
+    lo += (uint32_t)__shfl_xor((int)lo, o);
+  }
+  if ((threadIdx.x & 63) == 0) {
+    if (up) atomicAdd(hits, up);
+    if (lo) atomicAdd(hits + 1, lo);
+  }
+}
+
 }  // namespace gift

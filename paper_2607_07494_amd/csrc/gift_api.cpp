@@ -616,10 +616,10 @@ gift_status gift_factor_import(gift_ctx *ctx, gift_factor *f, int32_t side, cons
   return side_import(ctx, *s, U, c_fwd, c_inv, sigma2);
 }
 
-gift_status gift_encode(gift_ctx *ctx, const gift_factor *f, const float *grads, int32_t N,
-                        int64_t m, int64_t n, int32_t block_rows, int32_t block_cols,
-                        gift_scale_mode mode, float *ef, uint8_t *codes, float *scales,
-                        float *transformed) {
+static gift_status encode_impl(gift_ctx *ctx, const gift_factor *f, const float *grads, int32_t N,
+                               int64_t m, int64_t n, int32_t block_rows, int32_t block_cols,
+                               gift_scale_mode mode, float *ef, uint8_t *codes, float *scales,
+                               float *transformed, uint32_t *hits) {
   if (!ctx) return set_error(GIFT_EINVAL, "gift_encode: ctx is NULL");
   if (!grads || !codes || !scales) return set_error(GIFT_EINVAL, "gift_encode: NULL tensor");
   if (mode != GIFT_SCALE_LOCAL && mode != GIFT_SCALE_SHARED)
@@ -683,6 +683,7 @@ gift_status gift_encode(gift_ctx *ctx, const gift_factor *f, const float *grads,
   if ((st = launch_tile(ctx, job)) != GIFT_OK) return st;
   job.transformed = nullptr;
   job.codes = codes;
+  job.hits = hits;   // every quantize route counts the boundary hits as it packs
   // QUANT pass: the streaming kernel reads the raw sub-slots itself (on the
   // stored W~ + R with a transform, on W without); otherwise a finalize
   // launch reduces them first
@@ -719,6 +720,25 @@ gift_status gift_encode(gift_ctx *ctx, const gift_factor *f, const float *grads,
   if ((st = launch_tile(ctx, job)) != GIFT_OK) return st;
   amax_slots_done(ctx, 0);
   return GIFT_OK;
+}
+
+gift_status gift_encode(gift_ctx *ctx, const gift_factor *f, const float *grads, int32_t N,
+                        int64_t m, int64_t n, int32_t block_rows, int32_t block_cols,
+                        gift_scale_mode mode, float *ef, uint8_t *codes, float *scales,
+                        float *transformed) {
+  return encode_impl(ctx, f, grads, N, m, n, block_rows, block_cols, mode, ef, codes, scales, transformed,
+                     nullptr);
+}
+
+gift_status gift_encode_hits(gift_ctx *ctx, const gift_factor *f, const float *grads, int32_t N,
+                             int64_t m, int64_t n, int32_t block_rows, int32_t block_cols,
+                             gift_scale_mode mode, float *ef, uint8_t *codes, float *scales,
+                             float *transformed, uint32_t *hits) {
+  if (!hits) return set_error(GIFT_EINVAL, "gift_encode_hits: hits is NULL");
+  if (reinterpret_cast<uintptr_t>(hits) & 3)
+    return set_error(GIFT_EINVAL, "gift_encode_hits: hits must be 4-byte aligned");
+  return encode_impl(ctx, f, grads, N, m, n, block_rows, block_cols, mode, ef, codes, scales, transformed,
+                     hits);
 }
 
 gift_status gift_reduce_local(gift_ctx *ctx, const uint8_t *codes, const float *scales, int32_t N,

@@ -168,6 +168,7 @@ struct TileJob {
   //       float bits); QUANT pass -> finished values [batch, nbr, nbc]
   uint32_t *amax = nullptr;
   uint8_t *codes = nullptr;
+  uint32_t *hits = nullptr;   // QUANT: boundary-hit counters [batch][2] (upper, lower), accumulated
   float *scales = nullptr;
   float *transformed = nullptr;
   float *ef = nullptr;

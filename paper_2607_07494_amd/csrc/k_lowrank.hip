@@ -273,6 +273,7 @@ struct LUArgs {
   const float *D;       // [batch][M][N]
   uint32_t *amax;       // AMAX: raw sub-slots; QUANT: finished maxima [batch][nbr][nbc]
   uint8_t *codes;
+  uint32_t *hits;       // QUANT: boundary-hit counters [batch][2] or null
   float *transformed;   // AMAX: optional W~ (+ R) out
   float *ef;            // residual (read; QUANT also writes it)
   int64_t br, bc;
@@ -443,6 +444,7 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
 
   uint32_t run_max = 0u;
   int64_t run_blk = -1;
+  uint32_t hit_up = 0u, hit_lo = 0u;   // QUANT boundary hits of this lane
   // FULL: every wave tile lies in one scale block and the workgroup's whole
   // column range is processed without branches, so the compiler can wait for
   // one register set of W while the next one stays in flight.  AMAX keeps the
@@ -609,6 +611,7 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
               }
               const uint32_t packed = e4m3_encode4(w[g][t][0] * inv[0], w[g][t][1] * inv[1], w[g][t][2] * inv[2],
                                                    w[g][t][3] * inv[3]);
+              if (p.hits) e4m3_count_hits4(packed, w[g][t][0], w[g][t][1], w[g][t][2], w[g][t][3], hit_up, hit_lo);
               float res[4];
               if (EF) {
                 float q[4];
@@ -684,6 +687,7 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
   }
   if (EPI == EPI_AMAX && wave_live && run_blk >= 0 && lane == 0 && run_max)
     atomicMax(&p.amax[((int64_t)b * p.nbr * p.nbc + run_blk) * kAmaxSlots + slot], run_max);
+  if (EPI == EPI_QUANT && p.hits) e4m3_flush_hits(p.hits + 2 * (int64_t)b, hit_up, hit_lo);
 }
 
 bool al16(const void *q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; }
@@ -798,6 +802,7 @@ gift_status launch_lr_update(gift_ctx *ctx, const TileJob &j) {
   a.D = j.D;
   a.amax = j.amax;
   a.codes = j.codes;
+  a.hits = j.codes ? j.hits : nullptr;
   a.transformed = j.transformed;
   a.ef = j.ef;
   a.br = j.geom.br > 0 ? j.geom.br : j.M;

@@ -33,6 +33,7 @@ struct SArgs {
   const float *ef_in;  // residual [N][m][n] or null (read)
   float *ef;           // residual out (quantize) or null
   uint8_t *codes;      // [N][m][n]
+  uint32_t *hits;      // quantize: boundary-hit counters [N][2] or null
   float *scales;       // [N][nbr][nbc]
   uint32_t *amax;      // [N][nbr][nbc]
   float *transformed;  // optional W~ out (amax pass)
@@ -212,6 +213,7 @@ __global__ __launch_bounds__(kThreads) void stream_quant_kernel(const SArgs p) {
     sc = e4m3_scale(a);
   };
   load_scale();
+  uint32_t hit_up = 0u, hit_lo = 0u;
   const float *xb = p.x + (int64_t)w.b * mn;
   const float *eb = (EF && ADD) ? p.ef_in + (int64_t)w.b * mn : nullptr;
   uint8_t *cb = p.codes + (int64_t)w.b * mn;
@@ -244,6 +246,7 @@ __global__ __launch_bounds__(kThreads) void stream_quant_kernel(const SArgs p) {
       const int64_t off = (int64_t)row * p.n + w.cj;
       const uint32_t packed = e4m3_encode4(x.x * inv, x.y * inv, x.z * inv, x.w * inv);
       *reinterpret_cast<uint32_t *>(cb + off) = packed;
+      if (p.hits) e4m3_count_hits4(packed, x.x, x.y, x.z, x.w, hit_up, hit_lo);
       if (EF) {
         float q[4];
         e4m3_decode4(packed, q);
@@ -254,6 +257,7 @@ __global__ __launch_bounds__(kThreads) void stream_quant_kernel(const SArgs p) {
   };
   Set sa, sb;
   row_pipeline<kGroup>(w.r0, w.r1, sa, sb, load, proc);
+  if (p.hits) e4m3_flush_hits(p.hits + 2 * (int64_t)w.b, hit_up, hit_lo);
 }
 
 // Rank sum with CPL columns per lane (4: one 32-bit code word per rank and
@@ -399,6 +403,7 @@ gift_status launch_stream_codec(gift_ctx *ctx, const TileJob &j) {
   a.ef_in = j.ef;
   a.ef = j.codes ? j.ef : nullptr;
   a.codes = j.codes;
+  a.hits = j.codes ? j.hits : nullptr;
   a.scales = j.scales;
   a.amax = j.amax;
   a.transformed = j.transformed;

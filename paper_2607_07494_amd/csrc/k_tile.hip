@@ -56,6 +56,7 @@ struct KArgs {
   const float *colscale;
   uint32_t *amax;
   uint8_t *codes;
+  uint32_t *hits;        // QUANT: boundary-hit counters [batch][2] or null
   float *scales;
   float *transformed;
   float *ef;
@@ -331,6 +332,7 @@ __global__ __launch_bounds__(kThreads) void tile_kernel(const KArgs p) {
   uint32_t run_max = 0u;
   int run_lb = -1;
   int64_t run_gb = -1;
+  uint32_t hit_up = 0u, hit_lo = 0u;   // QUANT boundary hits of this thread
 
 #pragma unroll
   for (int ps = 0; ps < NPASS; ++ps) {
@@ -436,6 +438,10 @@ __global__ __launch_bounds__(kThreads) void tile_kernel(const KArgs p) {
           const float y = w[e] * inv;
           const uint32_t code = e4m3_encode(y);
           packed |= code << (8 * e);
+          if (p.hits) {
+            hit_up += (code & 0x7fu) == 0x7eu;
+            hit_lo += ((code & 0x7fu) == 0u) & (w[e] != 0.0f);
+          }
           if (p.ef) resid[e] = w[e] - e4m3_decode(code) * sc;
         }
         uint8_t *cp = p.codes + off;
@@ -459,6 +465,7 @@ __global__ __launch_bounds__(kThreads) void tile_kernel(const KArgs p) {
     }
   }
 
+  if (EPI == EPI_QUANT && p.hits) e4m3_flush_hits(p.hits + 2 * (int64_t)b, hit_up, hit_lo);
   if (EPI == EPI_AMAX) {
     if (run_lb >= 0) {
       if (lb.nlb <= kMaxLocalBlocks) atomicMax(&lds_amax[run_lb], run_max);
@@ -549,6 +556,7 @@ KArgs make_args(const TileJob &j) {
   a.colscale = j.colscale;
   a.amax = j.amax;
   a.codes = j.codes;
+  a.hits = j.codes ? j.hits : nullptr;
   a.scales = j.scales;
   a.transformed = j.transformed;
   a.ef = j.ef;

@@ -59,6 +59,7 @@ struct UArgs {
   float *C;             // STORE output [batch][M][N]
   uint32_t *amax;       // [batch][nbr][nbc]
   uint8_t *codes;
+  uint32_t *hits;       // QUANT: boundary-hit counters [batch][2] or null
   float *scales;
   float *transformed;
   float *ef;
@@ -192,6 +193,7 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const UArgs p) {
 
   uint32_t run_max = 0u;
   int64_t run_blk = -1;
+  uint32_t hit_up = 0u, hit_lo = 0u;   // QUANT boundary hits of this lane
   load_cols(c_begin);
   load_w(c_begin);
   store_cols(0, c_begin);
@@ -334,6 +336,10 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const UArgs p) {
               }
               const uint32_t code = e4m3_encode(w[t][e] * inv);
               packed |= code << (8 * e);
+              if (p.hits) {
+                hit_up += (code & 0x7fu) == 0x7eu;
+                hit_lo += ((code & 0x7fu) == 0u) & (w[t][e] != 0.0f);
+              }
               if (EF) res[e] = w[t][e] - e4m3_decode(code) * sc;
             }
             const int64_t off = (int64_t)b * MN + ri * p.N + cj;
@@ -347,6 +353,7 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const UArgs p) {
   }
   if (EPI == EPI_AMAX && wave_live && run_blk >= 0 && lane == 0 && run_max)
     atomicMax(&p.amax[((int64_t)b * p.nbr * p.nbc + run_blk) * kAmaxSlots + slot], run_max);
+  if (EPI == EPI_QUANT && p.hits) e4m3_flush_hits(p.hits + 2 * (int64_t)b, hit_up, hit_lo);
 }
 
 struct PArgs {
@@ -612,6 +619,7 @@ gift_status launch_update(gift_ctx *ctx, const TileJob &j) {
   a.C = j.C;
   a.amax = j.amax;
   a.codes = j.codes;
+  a.hits = j.codes ? j.hits : nullptr;
   a.scales = j.scales;
   a.transformed = j.transformed;
   a.ef = j.ef;

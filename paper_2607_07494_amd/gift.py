@@ -66,6 +66,7 @@ def _load():
         "gift_factor_export": ([P, P, I32, P, P, P, P], I32),
         "gift_factor_import": ([P, P, I32, P, P, P, P], I32),
         "gift_encode": ([P, P, P, I32, I64, I64, I32, I32, I32, P, P, P, P], I32),
+        "gift_encode_hits": ([P, P, P, I32, I64, I64, I32, I32, I32, P, P, P, P, P], I32),
         "gift_reduce_local": ([P, P, P, I32, I64, I64, I32, I32, P], I32),
         "gift_decode": ([P, P, P, I64, I64, P], I32),
     }
@@ -282,15 +283,25 @@ def statistics(ctx: Context, x, A):
 
 
 def encode(ctx: Context, factor, grads, codes, scales, block_rows: int = 0, block_cols: int = 0,
-           mode: int = SCALE_LOCAL, ef=None, transformed=None):
-    """``gift_encode``: grads [N, m, n] f32 -> codes [N, m, n] u8, scales [N, nbr, nbc] f32."""
+           mode: int = SCALE_LOCAL, ef=None, transformed=None, hits=None):
+    """``gift_encode``: grads [N, m, n] f32 -> codes [N, m, n] u8, scales [N, nbr, nbc] f32.
+
+    With ``hits`` (an int32 [N, 2] tensor, bit pattern of the uint32 counters)
+    this is ``gift_encode_hits``: the per-rank upper / lower boundary hits are
+    added to it.
+    """
     import torch
     N, m, n = grads.shape
-    _check(LIB.gift_encode(ctx.handle, factor.handle if factor is not None else None,
-                           _ptr(grads, torch.float32, "grads"), N, m, n, block_rows, block_cols,
-                           mode, _ptr(ef, torch.float32, "ef"), _ptr(codes, torch.uint8, "codes"),
-                           _ptr(scales, torch.float32, "scales"),
-                           _ptr(transformed, torch.float32, "transformed")))
+    args = [ctx.handle, factor.handle if factor is not None else None,
+            _ptr(grads, torch.float32, "grads"), N, m, n, block_rows, block_cols,
+            mode, _ptr(ef, torch.float32, "ef"), _ptr(codes, torch.uint8, "codes"),
+            _ptr(scales, torch.float32, "scales"), _ptr(transformed, torch.float32, "transformed")]
+    if hits is None:
+        _check(LIB.gift_encode(*args))
+        return
+    if tuple(hits.shape) != (N, 2):
+        raise ValueError(f"hits must have shape ({N}, 2), not {tuple(hits.shape)}")
+    _check(LIB.gift_encode_hits(*args, _ptr(hits, torch.int32, "hits")))
 
 
 def reduce_local(ctx: Context, codes, scales, mean, block_rows: int = 0, block_cols: int = 0):

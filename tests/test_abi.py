@@ -70,6 +70,19 @@ def test_encode_validation(ctx):
     assert enc(h, None, FAKE, 1, 2_000_000, 4, 0, 0, 0, None, FAKE, FAKE, None) == gift.ESHAPE
 
 
+def test_encode_hits_validation(ctx):
+    h = ctx.handle
+    enc = LIB.gift_encode_hits
+    assert enc(h, None, FAKE, 1, 4, 4, 0, 0, 0, None, FAKE, FAKE, None, None) == gift.EINVAL
+    assert "hits is NULL" in _err()
+    assert enc(h, None, FAKE, 1, 4, 4, 0, 0, 0, None, FAKE, FAKE, None,
+               ctypes.c_void_p(0x1002)) == gift.EINVAL
+    assert "aligned" in _err()
+    # with valid counters the encode's own checks apply
+    assert enc(h, None, FAKE, 0, 4, 4, 0, 0, 0, None, FAKE, FAKE, None, FAKE) == gift.ESHAPE
+    assert enc(h, None, None, 1, 4, 4, 0, 0, 0, None, FAKE, FAKE, None, FAKE) == gift.EINVAL
+
+
 def test_reduce_and_decode_validation(ctx):
     h = ctx.handle
     assert LIB.gift_reduce_local(h, FAKE, FAKE, 0, 4, 4, 0, 0, FAKE) == gift.ESHAPE

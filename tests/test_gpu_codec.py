@@ -268,6 +268,64 @@ def test_recomputed_transform_matches_stored(ctx, N, m, n, r, sides, br, bc, use
     f.close()
 
 
+@pytest.mark.parametrize("N,m,n,r,sides,br,bc,use_ef,shared", [
+    (3, 48, 80, 0, 0, 0, 0, False, False),                        # Euclidean, streaming
+    (2, 37, 51, 0, 0, 5, 0, True, False),                         # Euclidean, ragged: tile
+    (2, 64, 96, 0, 0, 0, 32, False, True),
+    (4, 200, 512, 64, gift.SIDE_INPUT, 0, 128, False, False),     # branch-free split-bf16
+    (2, 64, 768, 64, gift.SIDE_INPUT, 32, 256, True, True),
+    (2, 100, 200, 16, gift.SIDE_INPUT, 7, 12, True, False),       # split-bf16, ragged blocks
+    (3, 260, 520, 32, gift.SIDE_BOTH, 0, 0, False, False),
+    (2, 96, 128, 6, gift.SIDE_INPUT, 0, 32, False, False),        # stored W~, streaming quantize
+    (2, 96, 130, 6, gift.SIDE_OUTPUT, 0, 0, True, False),         # ragged columns
+])
+def test_boundary_hits(ctx, N, m, n, r, sides, br, bc, use_ef, shared):
+    """Per-rank counts of codes at +-448 and of nonzero values encoded to
+    zero, against the oracle's count on the W~ (+ R) the encode stored; a
+    second call (without the stored W~) adds the same counts."""
+    say(f"hits N={N} m={m} n={n} r={r} sides={sides} block=({br},{bc}) ef={use_ef} shared={shared}")
+    grads = gradient_set(1200 + m, 1201 + n, N, m, n)
+    grads[:, 3, :] *= np.float32(1e-7)     # a row that underflows (kept by S_A)
+    grads[:, :, 5] *= np.float32(1e-7)     # a column that underflows (kept by S_G)
+    grads[:, 1, :4] = 0.0                  # zeros are never lower hits
+    if shared:
+        grads[1] *= 5.0
+    f = make_factor(ctx, m, n, r, sides, seed=m + 7 * n)[0] if r else None
+    R0 = None
+    if use_ef:
+        R0 = gradient_set(1202, 1203, N, m, n) * np.float32(0.01)
+        R0[:, 3, :] = 0.0
+        R0[:, :, 5] = 0.0
+    hits = torch.zeros((N, 2), dtype=torch.int32, device=DEV)
+    ef = torch.from_numpy(R0).to(DEV) if use_ef else None
+    codes, scales, tr = _encode_hits(ctx, f, grads, br, bc, shared, ef, hits, True)
+    want = codec.boundary_hits(tr, codes)
+    got = hits.cpu().numpy().astype(np.int64)
+    np.testing.assert_array_equal(got, want)
+    if not shared:
+        assert np.all(got[:, 0] >= (scales > 0).reshape(N, -1).sum(axis=1))
+    if sides != gift.SIDE_BOTH:
+        assert np.all(got[:, 1] > 0)
+    ef = torch.from_numpy(R0).to(DEV) if use_ef else None
+    _encode_hits(ctx, f, grads, br, bc, shared, ef, hits, False)
+    np.testing.assert_array_equal(hits.cpu().numpy().astype(np.int64), 2 * want)
+    if f is not None:
+        f.close()
+
+
+def _encode_hits(ctx, f, grads, br, bc, shared, ef, hits, want_t):
+    N, m, n = grads.shape
+    nbr, nbc = gift.scale_grid(m, n, br, bc)
+    codes = torch.empty((N, m, n), dtype=torch.uint8, device=DEV)
+    scales = torch.empty((N, nbr, nbc), dtype=torch.float32, device=DEV)
+    tr = torch.empty((N, m, n), dtype=torch.float32, device=DEV) if want_t else None
+    gift.encode(ctx, f, t(grads), codes, scales, br, bc,
+                gift.SCALE_SHARED if shared else gift.SCALE_LOCAL, ef=ef, transformed=tr, hits=hits)
+    torch.cuda.synchronize()
+    return (codes.cpu().numpy(), scales.cpu().numpy(),
+            tr.cpu().numpy() if tr is not None else None)
+
+
 def test_identity_factor_is_euclidean(ctx):
     say("identity factor")
     grads = gradient_set(11, 12, 2, 48, 80)

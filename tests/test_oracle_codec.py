@@ -219,6 +219,55 @@ def test_scale_edge_cases():
     assert inv[3] == np.finfo(np.float32).max
 
 
+# ---------------------------------------------------------------- boundary hits
+
+def test_boundary_hits_hand_example():
+    # One block whose amax is 448, so the multiplier is exactly 1 and the
+    # values are quantized as they stand.  In E4M3 the neighbours of 448 are
+    # 416 (odd mantissa) and nothing above, so |y| >= 432 (the midpoint, tie
+    # to the even 448) encodes to 448; the smallest subnormal is 2^-9, so
+    # |y| <= 2^-10 (the midpoint, tie to the even zero) encodes to zero.
+    t = 2.0 ** -10
+    x = np.array([448, 432, 431.99, 447, -440, t, -t, t * 1.0001, 1e-30, 0.0, -0.0,
+                  416, -2.0 ** -9, 1.0], dtype=np.float32)
+    codes, s = codec.quantize_transformed(x.reshape(1, 1, -1))
+    assert s[0, 0, 0] == 1.0
+    hits = codec.boundary_hits(x.reshape(1, 1, -1), codes)
+    assert hits.tolist() == [[4, 3]]
+
+
+def test_boundary_hits_threshold_closed_form():
+    rng = _rng(41)
+    N, m, n = 3, 24, 40
+    mag = np.exp(rng.uniform(np.log(1e-6), np.log(448.0), size=(N, m, n)))
+    x = (mag * rng.choice([-1.0, 1.0], size=mag.shape)).astype(np.float32)
+    x[:, 0, 0] = 448.0                     # every rank's amax: multiplier 1
+    x[0, 1, :8] = 0.0
+    x[1, 2, :5] = np.float32(2.0 ** -10)    # the lower tie
+    x[2, 3, :5] = np.float32(432.0)         # the upper tie
+    codes, s = codec.quantize_transformed(x)
+    assert np.all(s == 1.0)
+    a = np.abs(x)
+    up = (a >= 432.0).reshape(N, -1).sum(axis=1)
+    lo = ((a > 0) & (a <= 2.0 ** -10)).reshape(N, -1).sum(axis=1)
+    hits = codec.boundary_hits(x, codes)
+    assert hits[:, 0].tolist() == up.tolist()
+    assert hits[:, 1].tolist() == lo.tolist()
+    assert np.all(up >= 1) and lo[1] >= 5
+
+
+def test_boundary_hits_every_block_max_is_an_upper_hit():
+    grads = gradient_set(5000, 5100, 3, 64, 96)
+    grads[2, :, 48:] = 0.0
+    codes, s, Wt = codec.encode(grads, block_rows=32, block_cols=48)
+    hits = codec.boundary_hits(Wt, codes)
+    nonzero_blocks = (s > 0).reshape(3, -1).sum(axis=1)
+    assert np.all(hits[:, 0] >= nonzero_blocks)
+    # zero inputs are never lower hits; a shared scale can only add lower hits
+    codes_sh = codec.quantize_transformed(Wt, 32, 48, shared=True)[0]
+    assert np.all(codec.boundary_hits(Wt, codes_sh)[:, 1] >= hits[:, 1])
+
+
 # ---------------------------------------------------------------- rank sum
 
 def test_reduce_exact_on_representable_inputs():
