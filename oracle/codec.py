@@ -24,6 +24,13 @@ design notes of the repository):
   transform).  ``S`` plays the role of ``L_A``: any
   square root of ``A`` turns the metric ellipsoid into a ball
   (eq. design_sphere_proof).
+* Cholesky-form variants (eq. design_chol with Table II's full-A, diag-A and
+  block-A-b): ``L`` is the Cholesky factor of ``A + delta I`` with ``delta =
+  damping * tr(A)/dim`` (the regularisation the equation asks for without
+  fixing it); diag-A and block-A-b keep only the diagonal, or the ``b x b``
+  diagonal blocks (the last one ragged), of ``A + delta I`` and factor those.
+  No ``sigma`` normalisation: the amax scale absorbs a common factor.  A zero
+  trace gives the identity.
 * Scale (Algorithm 1's ``Scale``; the amax rule quoted from COAT in Sec. I):
   ``s = fl32(amax/448)`` is the stored (dequantization) scale and values are
   quantized as ``fl32(x * fl32(448/amax))``; amax = 0 gives s = 0 and a zero
@@ -48,6 +55,7 @@ from __future__ import annotations
 from dataclasses import dataclass
 
 import numpy as np
+import scipy.linalg
 
 from . import e4m3
 
@@ -152,33 +160,148 @@ def identity_factor(dim: int) -> Factor:
 
 
 # --------------------------------------------------------------------------
+# Cholesky-form factors (eq. design_chol; Sec. V-B, Table II: full, diagonal
+# and block-diagonal approximations of A)
+# --------------------------------------------------------------------------
+
+@dataclass
+class CholFactor:
+    """One side's Cholesky transform ``A + delta I = L L^T`` (eq. design_chol).
+
+    ``L`` is block-diagonal with ``b x b`` diagonal blocks (``b = dim``: the
+    full factor; ``b = 1``: the diagonal of A), each block the Cholesky factor
+    of the matching diagonal block of ``A + delta I``.  Stored per block as
+    ``R = L_k^T`` (upper triangular) and ``R^-1 = L_k^-T``, ``[nblk, b, b]``;
+    the last block, when ``dim`` is not a multiple of ``b``, holds its
+    ``kv x kv`` part in the top-left corner and the identity elsewhere.
+    """
+
+    R: np.ndarray        # [nblk, b, b]
+    Rinv: np.ndarray     # [nblk, b, b]
+    dim: int
+
+    @property
+    def block(self) -> int:
+        return self.R.shape[1]
+
+    @property
+    def rank(self) -> int:   # a Cholesky factor is never the identity transform
+        return self.dim
+
+    def to_f32(self) -> "CholFactor":
+        f = lambda a: np.asarray(a, dtype=np.float32).astype(np.float64)
+        return CholFactor(f(self.R), f(self.Rinv), self.dim)
+
+    def _dense(self, blocks: np.ndarray) -> np.ndarray:
+        b = self.block
+        out = np.zeros((self.dim, self.dim))
+        for k in range(blocks.shape[0]):
+            kv = min(b, self.dim - k * b)
+            out[k * b:k * b + kv, k * b:k * b + kv] = blocks[k, :kv, :kv]
+        return out
+
+    def lower(self) -> np.ndarray:
+        """Dense ``L`` (dim x dim, lower triangular)."""
+        return self._dense(self.R).T
+
+    def right_fwd(self) -> np.ndarray:
+        """``L^-T``: the input side's forward map ``W -> W L^-T``."""
+        return self._dense(self.Rinv)
+
+    def left_fwd(self) -> np.ndarray:
+        """``L^-1``: the output side's forward map ``W -> L^-1 W``."""
+        return self._dense(self.Rinv).T
+
+    def right_inv(self) -> np.ndarray:
+        """``L^T``: the input side's inverse map ``M -> M L^T``."""
+        return self._dense(self.R)
+
+    def left_inv(self) -> np.ndarray:
+        """``L``: the output side's inverse map ``M -> L M``."""
+        return self._dense(self.R).T
+
+
+def chol_shift(A: np.ndarray, damping: float) -> float:
+    """Regularisation ``delta = damping * tr(A) / dim`` of eq. design_chol."""
+    A = np.asarray(A, dtype=np.float64)
+    return float(damping * np.trace(A) / A.shape[0])
+
+
+def chol_factor(A: np.ndarray, block: int = 0, damping: float = 1e-6) -> CholFactor:
+    """Block-diagonal Cholesky factor of ``A + delta I`` (eq. design_chol).
+
+    ``block = 0`` or ``>= dim`` is the full factor (Table II's full-A),
+    ``1`` the diagonal (diag-A), ``b`` the ``b x b`` diagonal blocks
+    (block-A-b).  A zero trace gives the identity.  Each block is factored by
+    ``numpy.linalg.cholesky`` and inverted by a triangular solve.
+    """
+    A = np.asarray(A, dtype=np.float64)
+    dim = A.shape[0]
+    b = dim if block <= 0 or block >= dim else int(block)
+    nblk = -(-dim // b)
+    R = np.zeros((nblk, b, b))
+    Rinv = np.zeros((nblk, b, b))
+    tr = float(np.trace(A))
+    delta = chol_shift(A, damping)
+    for k in range(nblk):
+        kv = min(b, dim - k * b)
+        R[k] = np.eye(b)
+        Rinv[k] = np.eye(b)
+        if tr <= 0.0:
+            continue
+        blk = A[k * b:k * b + kv, k * b:k * b + kv]
+        blk = 0.5 * (blk + blk.T) + delta * np.eye(kv)
+        Lk = np.linalg.cholesky(blk)
+        R[k, :kv, :kv] = Lk.T
+        Rinv[k, :kv, :kv] = scipy.linalg.solve_triangular(Lk.T, np.eye(kv), lower=False)
+    return CholFactor(R, Rinv, dim)
+
+
+def _right_fwd(f):
+    return f.right_fwd() if isinstance(f, CholFactor) else f.inverse_root()
+
+
+def _left_fwd(f):
+    return f.left_fwd() if isinstance(f, CholFactor) else f.inverse_root()
+
+
+def _right_inv(f):
+    return f.right_inv() if isinstance(f, CholFactor) else f.root()
+
+
+def _left_inv(f):
+    return f.left_inv() if isinstance(f, CholFactor) else f.root()
+
+
+# --------------------------------------------------------------------------
 # Transform and inverse (eq. design_full_transform / design_input_side_transform,
 # eq. design_full_inverse_transform / design_input_side_inverse)
 # --------------------------------------------------------------------------
 
-def forward(W: np.ndarray, fA: Factor | None = None, fG: Factor | None = None) -> np.ndarray:
-    """``W~ = S_G^-1 W S_A^-1`` in float64 (a missing side is the identity).
+def forward(W: np.ndarray, fA=None, fG=None) -> np.ndarray:
+    """``W~ = L_G^-1 W L_A^-T`` in float64 (a missing side is the identity).
 
-    ``W`` is ``[m, n]`` or ``[N, m, n]``.  With ``S_A^-1`` symmetric this is
-    ``W L_A^-T`` of eq. design_input_side_transform with ``L_A = S_A``.
+    ``W`` is ``[m, n]`` or ``[N, m, n]``.  For a low-rank ``Factor`` both maps
+    are the symmetric ``S^-1`` (``L = S``); for a ``CholFactor`` they are the
+    triangular ``L^-1`` and ``L^-T`` of eq. design_full_transform.
     """
     W = np.asarray(W, dtype=np.float64)
     out = W
     if fA is not None and fA.rank > 0:
-        out = out @ fA.inverse_root()
+        out = out @ _right_fwd(fA)
     if fG is not None and fG.rank > 0:
-        out = fG.inverse_root() @ out
+        out = _left_fwd(fG) @ out
     return out
 
 
-def inverse(M: np.ndarray, fA: Factor | None = None, fG: Factor | None = None) -> np.ndarray:
-    """``W^ = S_G M S_A`` in float64 (eq. design_full_inverse_transform)."""
+def inverse(M: np.ndarray, fA=None, fG=None) -> np.ndarray:
+    """``W^ = L_G M L_A^T`` in float64 (eq. design_full_inverse_transform)."""
     M = np.asarray(M, dtype=np.float64)
     out = M
     if fA is not None and fA.rank > 0:
-        out = out @ fA.root()
+        out = out @ _right_inv(fA)
     if fG is not None and fG.rank > 0:
-        out = fG.root() @ out
+        out = _left_inv(fG) @ out
     return out
 
 

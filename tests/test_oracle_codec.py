@@ -219,6 +219,91 @@ def test_scale_edge_cases():
     assert inv[3] == np.finfo(np.float32).max
 
 
+# ---------------------------------------------------------------- Cholesky-form variants
+
+def _psd(dim, seed, decay=1.2):
+    x = factor_inputs(seed, 4 * dim, dim, decay=decay)[0].astype(np.float64)
+    return codec.factor_statistics(x)
+
+
+def test_chol_full_gives_the_inverse_metric_norm():
+    # ||W L^-T||_F^2 = tr(W (A + dI)^-1 W^T): the gradient's norm under the
+    # inverse of the input-side metric (eq. design_input_side_sphere dualised);
+    # a transposed factor (W L^-1) or a dropped shift fails it
+    A = _psd(24, 3)
+    damp = 1e-3
+    f = codec.chol_factor(A, 0, damp)
+    Areg = A + codec.chol_shift(A, damp) * np.eye(24)
+    W = _rng(5).standard_normal((9, 24))
+    Wt = codec.forward(W, f)
+    want = np.trace(W @ np.linalg.inv(Areg) @ W.T)
+    assert np.isclose((Wt ** 2).sum(), want, rtol=1e-10)
+    L = f.lower()
+    assert np.allclose(np.triu(L, 1), 0.0) and np.all(np.diag(L) > 0)
+    assert np.allclose(L @ L.T, Areg, rtol=1e-12, atol=1e-12 * np.abs(Areg).max())
+
+
+def test_chol_two_sided_is_the_kronecker_whitening():
+    # ||L_G^-1 W L_A^-T||^2 = vec(W)^T (A^-1 kron G^-1) vec(W) (eq. design_vec_whiten)
+    A, G = _psd(7, 11), _psd(5, 12)
+    fA, fG = codec.chol_factor(A, 0, 1e-2), codec.chol_factor(G, 0, 1e-2)
+    Ar = A + codec.chol_shift(A, 1e-2) * np.eye(7)
+    Gr = G + codec.chol_shift(G, 1e-2) * np.eye(5)
+    W = _rng(6).standard_normal((5, 7))
+    Wt = codec.forward(W, fA, fG)
+    v = W.reshape(-1, order="F")
+    want = v @ np.kron(np.linalg.inv(Ar), np.linalg.inv(Gr)) @ v
+    assert np.isclose((Wt ** 2).sum(), want, rtol=1e-10)
+    assert np.allclose(codec.inverse(Wt, fA, fG), W, rtol=1e-10, atol=1e-12)
+
+
+def test_chol_diag_is_column_scaling():
+    A = _psd(20, 4)
+    damp = 1e-4
+    f = codec.chol_factor(A, 1, damp)
+    d = np.diag(A) + damp * np.trace(A) / 20
+    W = _rng(7).standard_normal((6, 20))
+    assert np.allclose(codec.forward(W, f), W / np.sqrt(d), rtol=1e-13)
+    assert np.allclose(codec.forward(W.T, None, f), W.T / np.sqrt(d)[:, None], rtol=1e-13)
+    assert f.R.shape == (20, 1, 1)
+
+
+def test_chol_block_matches_full_on_block_diagonal_matrices():
+    # a block-diagonal A (blocks of 4, a ragged block of 2) has a
+    # block-diagonal Cholesky factor, so block-A-4 equals full-A on it
+    dim, b = 10, 4
+    A = np.zeros((dim, dim))
+    for k in range(0, dim, b):
+        kv = min(b, dim - k)
+        A[k:k + kv, k:k + kv] = _psd(kv, 20 + k) + 0.1 * np.eye(kv)
+    fb, ff = codec.chol_factor(A, b, 1e-3), codec.chol_factor(A, 0, 1e-3)
+    assert fb.R.shape == (3, 4, 4)
+    assert np.allclose(fb.R[2, 2:, 2:], np.eye(2)) and np.allclose(fb.R[2, :2, 2:], 0)
+    assert np.allclose(fb.lower(), ff.lower(), rtol=1e-12, atol=1e-14)
+    W = _rng(8).standard_normal((3, dim))
+    assert np.allclose(codec.forward(W, fb), codec.forward(W, ff), rtol=1e-12)
+    # on a general A the blocks see only their own diagonal blocks of A
+    G = _psd(dim, 30)
+    g = codec.chol_factor(G, b, 1e-3)
+    Gr = G + codec.chol_shift(G, 1e-3) * np.eye(dim)
+    for k in range(0, dim, b):
+        kv = min(b, dim - k)
+        Lk = g.lower()[k:k + kv, k:k + kv]
+        assert np.allclose(Lk @ Lk.T, Gr[k:k + kv, k:k + kv], rtol=1e-12)
+    assert np.allclose(codec.chol_factor(G, dim, 1e-3).R, codec.chol_factor(G, 0, 1e-3).R)
+    assert np.allclose(codec.chol_factor(G, 50, 1e-3).R, codec.chol_factor(G, 0, 1e-3).R)
+
+
+def test_chol_round_trip_and_identity_cases():
+    A = _psd(16, 9)
+    for b in (0, 1, 5, 16):
+        f = codec.chol_factor(A, b, 1e-6)
+        W = _rng(b).standard_normal((4, 16))
+        assert np.allclose(codec.inverse(codec.forward(W, f), f), W, rtol=1e-9, atol=1e-12)
+    z = codec.chol_factor(np.zeros((6, 6)), 4, 1e-3)
+    assert np.all(z.R == np.eye(4)) and np.all(z.Rinv == np.eye(4))
+
+
 # ---------------------------------------------------------------- boundary hits
 
 def test_boundary_hits_hand_example():
