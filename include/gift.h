@@ -97,7 +97,8 @@ typedef enum {
   GIFT_KERNEL_CHOL = 10,         /* CholeskyQR's k x k Cholesky and R^-1      */
   GIFT_KERNEL_EIG = 11,          /* Rayleigh-Ritz k x k eigensolver           */
   GIFT_KERNEL_DECODE_PROJECT = 12, /* the inverse transform's projections     */
-  GIFT_KERNEL_COUNT = 13
+  GIFT_KERNEL_CHOL_TRANSFORM = 13, /* Cholesky-form transform products         */
+  GIFT_KERNEL_COUNT = 14
 } gift_kernel;
 
 /* ABI version of the loaded library (GIFT_ABI_VERSION it was built with). */
@@ -144,6 +145,28 @@ gift_status gift_ctx_profile_reset(gift_ctx *ctx);
 gift_status gift_factor_create(gift_ctx *ctx, int64_t m, int64_t n, int32_t rank,
                                int32_t sides, float damping, uint64_t seed,
                                gift_factor **out);
+
+/* Create a Cholesky-form factor (Sec. IV-A, eq. design_chol with the
+ * transforms of eq. design_full_transform / design_input_side_transform and
+ * their inverses; Table II's full-A, diag-A and block-A-b variants):
+ *   A + delta I = L_A L_A^T,  delta = damping * tr(A) / n  (G likewise, dim m),
+ *   encode W~ = L_G^-1 W L_A^-T,  decode W^ = L_G M L_A^T.
+ * block: 0 (or >= dim) = the full Cholesky factor; 1 = the diagonal of A
+ * (L = diag(sqrt(a_ii + delta))); b >= 2 = the Cholesky factors of the b x b
+ * diagonal blocks of A + delta I (the last block ragged when b does not
+ * divide dim), L block-diagonal.  A side's effective block is
+ * b_eff = min(block or dim, dim); it is stored as nblk = ceil(dim / b_eff)
+ * blocks of b_eff x b_eff (gift_factor_export_chol).
+ * damping must be > 0 (every pivot is then at least delta); a zero trace
+ * gives the identity.  gift_factor_update refreshes it from the statistics
+ * (iters is ignored); gift_encode, gift_encode_hits and gift_decode apply it
+ * (float32 products; the FP8 step is the Euclidean encode of W~).  The new
+ * factor is the identity.  Blocks above 128 are factored by one workgroup
+ * each: the full factor of a large dim is a slow refresh.
+ * Errors: GIFT_EINVAL (NULL, bad sides, damping not finite and > 0),
+ * GIFT_ESHAPE (m, n out of range, block < 0, block_eff > 8192). */
+gift_status gift_factor_create_chol(gift_ctx *ctx, int64_t m, int64_t n, int32_t block,
+                                    int32_t sides, float damping, gift_factor **out);
 
 /* Destroy a factor (synchronizes the context stream first). NULL ok.  A
  * factor must be destroyed before the context it was created on. */
@@ -194,7 +217,8 @@ gift_status gift_factor_update_batch(gift_ctx *ctx, int32_t count, gift_factor *
  *   c_fwd [r], c_inv [r], sigma2 [1].
  * side must be GIFT_SIDE_INPUT or GIFT_SIDE_OUTPUT and present in the factor.
  * Import replaces the side's transform (the next update warm-starts from
- * U).  Enqueued on the context stream. */
+ * U).  Enqueued on the context stream.  GIFT_EINVAL for a Cholesky-form
+ * factor (gift_factor_export_chol / gift_factor_import_chol). */
 gift_status gift_factor_export(gift_ctx *ctx, const gift_factor *f, int32_t side,
                                float *U, float *c_fwd, float *c_inv, float *sigma2);
 gift_status gift_factor_import(gift_ctx *ctx, gift_factor *f, int32_t side,
@@ -208,7 +232,8 @@ gift_status gift_factor_import(gift_ctx *ctx, gift_factor *f, int32_t side,
  *   ef           error-feedback residual [N, m, n] float32 in transformed
  *                coordinates (Algorithm 1: U~ = U + R; R <- U~ - Deq(Q(U~))),
  *                or NULL for none.  Zero it before the first step;
- *   codes        [N, m, n] uint8 out: E4M3 codes of W~_j = S_G^-1 W_j S_A^-1 (+R);
+ *   codes        [N, m, n] uint8 out: E4M3 codes of W~_j = S_G^-1 W_j S_A^-1 (+R)
+ *                (L_G^-1 W_j L_A^-T for a Cholesky-form factor);
  *   scales       [N, nbr, nbc] float32 out;
  *   transformed  optional [N, m, n] float32 out: W~ (+R) before quantization.
  * Output buffers must not overlap the inputs. */
@@ -216,6 +241,17 @@ gift_status gift_encode(gift_ctx *ctx, const gift_factor *f, const float *grads,
                         int32_t N, int64_t m, int64_t n, int32_t block_rows,
                         int32_t block_cols, gift_scale_mode mode, float *ef,
                         uint8_t *codes, float *scales, float *transformed);
+
+/* Copy one side of a Cholesky-form factor out of / into it (device
+ * pointers): R and Rinv are [nblk, b_eff, b_eff] float32, block k holding
+ * R_k = L_k^T (upper triangular) and its inverse; the last block's kv x kv
+ * part (kv = dim - (nblk - 1) b_eff) sits top-left, the identity elsewhere.
+ * Import replaces the side (both arrays are read as given).  Errors:
+ * GIFT_EINVAL for a low-rank factor, a side the factor lacks or NULL arrays. */
+gift_status gift_factor_export_chol(gift_ctx *ctx, const gift_factor *f, int32_t side, float *R,
+                                    float *Rinv);
+gift_status gift_factor_import_chol(gift_ctx *ctx, gift_factor *f, int32_t side, const float *R,
+                                    const float *Rinv);
 
 /* gift_encode plus per-rank counters of codes that sit at either end of the
  * FP8 range (Sec. V-C: the per-layer numerical-vulnerability profile

@@ -22,7 +22,8 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libgift.so")
 ARCH = "gfx950"
 
-SOURCES = ["gift_api.cpp", "k_tile.hip", "k_reduce.hip", "k_factor.hip", "k_syrk.hip", "k_update.hip", "k_stream.hip", "k_lowrank.hip"]
+SOURCES = ["gift_api.cpp", "k_tile.hip", "k_reduce.hip", "k_factor.hip", "k_syrk.hip", "k_update.hip", "k_stream.hip",
+           "k_lowrank.hip", "k_chol.hip"]
 
 
 def hipcc() -> str:

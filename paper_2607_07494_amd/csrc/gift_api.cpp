@@ -53,15 +53,15 @@ gift_status bind_device(gift_ctx *ctx) {
   return GIFT_OK;
 }
 
-gift_status workspace(gift_ctx *ctx, size_t bytes, void **out) {
+gift_status grow_buffer(gift_ctx *ctx, Workspace &w, size_t bytes, void **out) {
   bytes = (bytes + 255) & ~(size_t)255;
   if (bytes == 0) bytes = 256;
-  if (bytes > ctx->ws.bytes) {
-    if (ctx->ws.ptr) {
+  if (bytes > w.bytes) {
+    if (w.ptr) {
       GIFT_HIP_TRY(hipStreamSynchronize(ctx->stream));
-      GIFT_HIP_TRY(hipFree(ctx->ws.ptr));
-      ctx->ws.ptr = nullptr;
-      ctx->ws.bytes = 0;
+      GIFT_HIP_TRY(hipFree(w.ptr));
+      w.ptr = nullptr;
+      w.bytes = 0;
     }
     void *p = nullptr;
     hipError_t e = hipMalloc(&p, bytes);
@@ -69,12 +69,14 @@ gift_status workspace(gift_ctx *ctx, size_t bytes, void **out) {
       (void)hipGetLastError();
       return set_error(GIFT_ENOMEM, "workspace: hipMalloc of " + std::to_string(bytes) + " bytes failed");
     }
-    ctx->ws.ptr = p;
-    ctx->ws.bytes = bytes;
+    w.ptr = p;
+    w.bytes = bytes;
   }
-  *out = ctx->ws.ptr;
+  *out = w.ptr;
   return GIFT_OK;
 }
+
+gift_status workspace(gift_ctx *ctx, size_t bytes, void **out) { return grow_buffer(ctx, ctx->ws, bytes, out); }
 
 gift_status amax_slots(gift_ctx *ctx, size_t words, uint32_t **cur, uint32_t **other,
                        size_t *other_dirty) {
@@ -161,6 +163,7 @@ namespace {
 constexpr int64_t kMaxRows = 65535LL * 16;     // grid.y limit of the 16-row tiles
 constexpr int64_t kMaxCols = (1LL << 31) - 1;
 constexpr int32_t kMaxRanks = 65535;            // grid.z limit
+constexpr int64_t kMaxCholBlock = 8192;        // one workgroup factors a block
 constexpr int32_t kMaxRank = 512;               // subspace block k = 2r <= 1024
 
 gift_status drain_profile(gift_ctx *ctx) {
@@ -401,6 +404,7 @@ void gift_ctx_destroy(gift_ctx *ctx) {
     for (hipEvent_t e : ctx->event_pool) (void)hipEventDestroy(e);
     if (ctx->ws.ptr) (void)hipFree(ctx->ws.ptr);
     if (ctx->slots.ptr) (void)hipFree(ctx->slots.ptr);
+    if (ctx->xform.ptr) (void)hipFree(ctx->xform.ptr);
   }
   delete ctx;
 }
@@ -516,6 +520,79 @@ gift_status gift_factor_create(gift_ctx *ctx, int64_t m, int64_t n, int32_t rank
   return GIFT_OK;
 }
 
+gift_status gift_factor_create_chol(gift_ctx *ctx, int64_t m, int64_t n, int32_t block, int32_t sides,
+                                    float damping, gift_factor **out) {
+  if (!ctx || !out) return set_error(GIFT_EINVAL, "gift_factor_create_chol: NULL argument");
+  if (sides < GIFT_SIDE_INPUT || sides > GIFT_SIDE_BOTH)
+    return set_error(GIFT_EINVAL, "gift_factor_create_chol: sides must be INPUT, OUTPUT or BOTH");
+  if (!(damping > 0.f) || isinf(damping))
+    return set_error(GIFT_EINVAL, "gift_factor_create_chol: damping must be finite and > 0");
+  gift_status st = check_matrix_dims(m, n);
+  if (st != GIFT_OK) return st;
+  if (block < 0) return set_error(GIFT_ESHAPE, "gift_factor_create_chol: block must be >= 0");
+  const bool on[2] = {side_in(sides, GIFT_SIDE_INPUT), side_in(sides, GIFT_SIDE_OUTPUT)};
+  const int64_t dims[2] = {n, m};
+  int64_t beff[2] = {0, 0};
+  for (int i = 0; i < 2; ++i) {
+    if (!on[i]) continue;
+    beff[i] = block == 0 || block >= dims[i] ? dims[i] : block;
+    if (beff[i] > kMaxCholBlock)
+      return set_error(GIFT_ESHAPE, "gift_factor_create_chol: block (or the full dim) exceeds 8192");
+  }
+  if ((st = bind_device(ctx)) != GIFT_OK) return st;
+  gift_factor *f = new (std::nothrow) gift_factor();
+  if (!f) return set_error(GIFT_ENOMEM, "gift_factor_create_chol: out of host memory");
+  f->ctx = ctx;
+  f->m = m;
+  f->n = n;
+  f->sides = sides;
+  f->damping = damping;
+  f->chol = true;
+  f->block = block;
+  f->A.dim = n;
+  f->G.dim = m;
+  CholSide *list[2] = {&f->CA, &f->CG};
+  size_t total = 0;
+  for (int i = 0; i < 2; ++i) {
+    CholSide &s = *list[i];
+    s.dim = dims[i];
+    if (!on[i]) continue;
+    s.b = (int32_t)beff[i];
+    s.nblk = (int32_t)((dims[i] + beff[i] - 1) / beff[i]);
+    const size_t blocks = (size_t)s.nblk * s.b * s.b;
+    total += 2 * a256(sizeof(float) * blocks) + a256(sizeof(float) * (size_t)s.dim * s.dim) +
+             a256(2 * sizeof(float));
+  }
+  hipError_t e = hipMalloc(&f->alloc, total);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    delete f;
+    return set_error(GIFT_ENOMEM, "gift_factor_create_chol: device allocation failed");
+  }
+  char *p = static_cast<char *>(f->alloc);
+  auto take = [&](size_t bytes) {
+    float *q = reinterpret_cast<float *>(p);
+    p += a256(bytes);
+    return q;
+  };
+  for (int i = 0; i < 2; ++i) {
+    CholSide &s = *list[i];
+    if (s.b == 0) continue;
+    const size_t blocks = (size_t)s.nblk * s.b * s.b;
+    s.R = take(sizeof(float) * blocks);
+    s.Rinv = take(sizeof(float) * blocks);
+    s.A = take(sizeof(float) * (size_t)s.dim * s.dim);
+    s.shift = take(2 * sizeof(float));
+    if ((st = chol_side_identity(ctx, s)) != GIFT_OK) {
+      (void)hipFree(f->alloc);
+      delete f;
+      return st;
+    }
+  }
+  *out = f;
+  return GIFT_OK;
+}
+
 void gift_factor_destroy(gift_factor *f) {
   if (!f) return;
   if (f->alloc) {
@@ -561,6 +638,13 @@ gift_status gift_factor_update_batch(gift_ctx *ctx, int32_t count, gift_factor *
       if (factors[j] == f) return set_error(GIFT_EINVAL, "gift_factor_update: a factor appears twice");
     const void *a = acts ? acts[i] : nullptr;
     const void *d = out_grads ? out_grads[i] : nullptr;
+    if (f->chol) {
+      if (f->CA.b > 0 && !a)
+        return set_error(GIFT_EINVAL, "gift_factor_update: acts is NULL for an input-side factor");
+      if (f->CG.b > 0 && !d)
+        return set_error(GIFT_EINVAL, "gift_factor_update: out_grads is NULL for an output-side factor");
+      continue;
+    }
     if (f->A.r > 0) {
       if (!a) return set_error(GIFT_EINVAL, "gift_factor_update: acts is NULL for an input-side factor");
       jobs.push_back(SideJob{&f->A, a, f->seed, f->damping});
@@ -570,10 +654,21 @@ gift_status gift_factor_update_batch(gift_ctx *ctx, int32_t count, gift_factor *
       jobs.push_back(SideJob{&f->G, d, f->seed + 1, f->damping});
     }
   }
-  if (jobs.empty()) return GIFT_OK;
+  bool any_chol = false;
+  for (int32_t i = 0; i < count; ++i) any_chol = any_chol || factors[i]->chol;
+  if (jobs.empty() && !any_chol) return GIFT_OK;
   gift_status st = bind_device(ctx);
   if (st != GIFT_OK) return st;
-  return factor_refresh_batch(ctx, jobs, T, dtype, iters);
+  if (!jobs.empty() && (st = factor_refresh_batch(ctx, jobs, T, dtype, iters)) != GIFT_OK) return st;
+  for (int32_t i = 0; i < count; ++i) {
+    gift_factor *f = factors[i];
+    if (!f->chol) continue;
+    if (f->CA.b > 0 && (st = chol_side_update(ctx, f->CA, acts[i], T, dtype, f->damping)) != GIFT_OK)
+      return st;
+    if (f->CG.b > 0 && (st = chol_side_update(ctx, f->CG, out_grads[i], T, dtype, f->damping)) != GIFT_OK)
+      return st;
+  }
+  return GIFT_OK;
 }
 
 gift_status gift_factor_update(gift_ctx *ctx, gift_factor *f, const void *acts,
@@ -591,9 +686,45 @@ static gift_status pick_side(const gift_factor *f, int32_t side, const Side **s)
   return GIFT_OK;
 }
 
+static gift_status pick_chol_side(const gift_factor *f, int32_t side, const CholSide **s) {
+  if (!f->chol) return set_error(GIFT_EINVAL, "not a Cholesky-form factor");
+  if (side == GIFT_SIDE_INPUT) *s = &f->CA;
+  else if (side == GIFT_SIDE_OUTPUT) *s = &f->CG;
+  else return set_error(GIFT_EINVAL, "side must be GIFT_SIDE_INPUT or GIFT_SIDE_OUTPUT");
+  if ((*s)->b == 0) return set_error(GIFT_EINVAL, "the factor does not have this side");
+  return GIFT_OK;
+}
+
+gift_status gift_factor_export_chol(gift_ctx *ctx, const gift_factor *f, int32_t side, float *R,
+                                    float *Rinv) {
+  if (!ctx || !f || !R || !Rinv) return set_error(GIFT_EINVAL, "gift_factor_export_chol: NULL argument");
+  const CholSide *s = nullptr;
+  gift_status st = pick_chol_side(f, side, &s);
+  if (st != GIFT_OK) return st;
+  if ((st = bind_device(ctx)) != GIFT_OK) return st;
+  const size_t bytes = sizeof(float) * (size_t)s->nblk * s->b * s->b;
+  GIFT_HIP_TRY(hipMemcpyAsync(R, s->R, bytes, hipMemcpyDeviceToDevice, ctx->stream));
+  GIFT_HIP_TRY(hipMemcpyAsync(Rinv, s->Rinv, bytes, hipMemcpyDeviceToDevice, ctx->stream));
+  return GIFT_OK;
+}
+
+gift_status gift_factor_import_chol(gift_ctx *ctx, gift_factor *f, int32_t side, const float *R,
+                                    const float *Rinv) {
+  if (!ctx || !f || !R || !Rinv) return set_error(GIFT_EINVAL, "gift_factor_import_chol: NULL argument");
+  const CholSide *s = nullptr;
+  gift_status st = pick_chol_side(f, side, &s);
+  if (st != GIFT_OK) return st;
+  if ((st = bind_device(ctx)) != GIFT_OK) return st;
+  const size_t bytes = sizeof(float) * (size_t)s->nblk * s->b * s->b;
+  GIFT_HIP_TRY(hipMemcpyAsync(s->R, R, bytes, hipMemcpyDeviceToDevice, ctx->stream));
+  GIFT_HIP_TRY(hipMemcpyAsync(s->Rinv, Rinv, bytes, hipMemcpyDeviceToDevice, ctx->stream));
+  return GIFT_OK;
+}
+
 gift_status gift_factor_export(gift_ctx *ctx, const gift_factor *f, int32_t side, float *U,
                                float *c_fwd, float *c_inv, float *sigma2) {
   if (!ctx || !f || !sigma2) return set_error(GIFT_EINVAL, "gift_factor_export: NULL argument");
+  if (f->chol) return set_error(GIFT_EINVAL, "gift_factor_export: a Cholesky-form factor (use _chol)");
   const Side *s = nullptr;
   gift_status st = pick_side(f, side, &s);
   if (st != GIFT_OK) return st;
@@ -606,6 +737,7 @@ gift_status gift_factor_export(gift_ctx *ctx, const gift_factor *f, int32_t side
 gift_status gift_factor_import(gift_ctx *ctx, gift_factor *f, int32_t side, const float *U,
                                const float *c_fwd, const float *c_inv, const float *sigma2) {
   if (!ctx || !f || !sigma2) return set_error(GIFT_EINVAL, "gift_factor_import: NULL argument");
+  if (f->chol) return set_error(GIFT_EINVAL, "gift_factor_import: a Cholesky-form factor (use _chol)");
   const Side *cs = nullptr;
   gift_status st = pick_side(f, side, &cs);
   if (st != GIFT_OK) return st;
@@ -632,6 +764,19 @@ static gift_status encode_impl(gift_ctx *ctx, const gift_factor *f, const float 
   if (f && (f->m != m || f->n != n))
     return set_error(GIFT_ESHAPE, "gift_encode: factor was created for another shape");
   if ((st = bind_device(ctx)) != GIFT_OK) return st;
+  if (f && f->chol) {
+    // W~ = L_G^-1 W L_A^-T into the transform buffer, then the Euclidean
+    // encode of W~ (whose own workspace holds everything else)
+    const size_t total = (size_t)N * m * n;
+    const bool two = chol_transform_needs_tmp(f);
+    void *buf = nullptr;
+    if ((st = grow_buffer(ctx, ctx->xform, sizeof(float) * total * (two ? 2 : 1), &buf)) != GIFT_OK) return st;
+    float *wt = static_cast<float *>(buf);
+    if ((st = launch_chol_transform(ctx, f, grads, wt, N, false, two ? wt + total : nullptr)) != GIFT_OK)
+      return st;
+    return encode_impl(ctx, nullptr, wt, N, m, n, block_rows, block_cols, mode, ef, codes, scales, transformed,
+                       hits);
+  }
   const BlockGeom g = block_geom(m, n, block_rows, block_cols);
   const int64_t nblk = (int64_t)g.nbr * g.nbc;
   const size_t fin_bytes = a256(sizeof(uint32_t) * (size_t)N * nblk);
@@ -766,6 +911,15 @@ gift_status gift_decode(gift_ctx *ctx, const gift_factor *f, const float *mean, 
   if (f && (f->m != m || f->n != n))
     return set_error(GIFT_ESHAPE, "gift_decode: factor was created for another shape");
   if ((st = bind_device(ctx)) != GIFT_OK) return st;
+  if (f && f->chol) {
+    float *tmp = nullptr;
+    if (chol_transform_needs_tmp(f)) {
+      void *buf = nullptr;
+      if ((st = grow_buffer(ctx, ctx->xform, sizeof(float) * (size_t)m * n, &buf)) != GIFT_OK) return st;
+      tmp = static_cast<float *>(buf);
+    }
+    return launch_chol_transform(ctx, f, mean, out, 1, true, tmp);
+  }
   LowRankPlan plan;
   size_t bytes = 0;
   if (f && (st = plan_low_rank(ctx, f, mean, 1, m, n, true, nullptr, &bytes, &plan)) != GIFT_OK)

@@ -46,6 +46,7 @@ struct gift_ctx {
   // encode starts with is all zero; the kernel that consumes a set's maxima
   // also clears what the previous encode left in the other set.
   gift::Workspace slots;
+  gift::Workspace xform;           // transformed copies of the Cholesky-form transforms
   size_t slot_words = 0;           // capacity of one set
   int slot_set = 0;                // set of the next encode
   size_t slot_dirty[2] = {0, 0};   // words of each set still to clear
@@ -78,6 +79,20 @@ struct Side {
   bool fill_tail = false;   // Qt rows r..k-1 still need start-block rows
 };
 
+// One side's Cholesky-form transform: A + delta I ~ L L^T with L
+// block-diagonal (b x b blocks; b = dim is the full factor, b = 1 the
+// diagonal), stored per block as R = L_k^T and R^-1 (upper triangular,
+// [nblk][b][b]; the last block's kv x kv part top-left, identity elsewhere).
+struct CholSide {
+  int64_t dim = 0;
+  int32_t b = 0;          // 0: side absent
+  int32_t nblk = 0;
+  float *R = nullptr;
+  float *Rinv = nullptr;
+  float *A = nullptr;     // [dim, dim] statistics of the last update
+  float *shift = nullptr; // [2]: delta, tr(A)
+};
+
 }  // namespace gift
 
 struct gift_factor {
@@ -88,6 +103,9 @@ struct gift_factor {
   uint64_t seed = 0;
   gift::Side A;   // input side (dim n)
   gift::Side G;   // output side (dim m)
+  bool chol = false;    // Cholesky-form factor (CA / CG) instead of the low-rank one
+  int32_t block = 0;    // requested block size of a Cholesky-form factor
+  gift::CholSide CA, CG;
   void *alloc = nullptr;
 };
 
@@ -257,5 +275,28 @@ gift_status side_import(gift_ctx *ctx, Side &s, const float *U, const float *c_f
 gift_status side_export(gift_ctx *ctx, const Side &s, float *U, float *c_fwd,
                         float *c_inv, float *sigma2);
 gift_status side_set_identity(gift_ctx *ctx, Side &s);
+
+// k_factor.hip: Cholesky and inverse of `count` k x k blocks G (contiguous
+// [count][k][k], symmetric positive definite): R [count][k][k] with
+// G = R^T R (upper triangular) and Rinv = R^-1, float64 inside.  `scratch`
+// holds chol_blocks_scratch(k, count) bytes of device memory.
+size_t chol_blocks_scratch(int k, int count);
+gift_status launch_chol_blocks(gift_ctx *ctx, const float *G, int k, int count, float *R, float *Rinv,
+                               void *scratch);
+
+// k_chol.hip: Cholesky-form factors and transforms
+// Refresh one side from its [T, dim] statistics input.
+gift_status chol_side_update(gift_ctx *ctx, CholSide &s, const void *x, int64_t T, gift_dtype dtype,
+                             float damping);
+// Identity transform (R = R^-1 = I).
+gift_status chol_side_identity(gift_ctx *ctx, CholSide &s);
+// out[N, m, n] = L_G^-1 in L_A^-T (forward) or L_G in L_A^T (inverse) for the
+// sides the factor has; in and out must not overlap.  tmp: [N, m, n] floats
+// when chol_transform_needs_tmp(f) (two sides, not both diagonal), else unused.
+bool chol_transform_needs_tmp(const gift_factor *f);
+gift_status launch_chol_transform(gift_ctx *ctx, const gift_factor *f, const float *in, float *out,
+                                  int32_t N, bool inverse, float *tmp);
+// Grow-only device buffer (synchronizes the stream before it frees the old one).
+gift_status grow_buffer(gift_ctx *ctx, Workspace &w, size_t bytes, void **out);
 
 }  // namespace gift

@@ -86,6 +86,7 @@ struct SmallJob {
   double *W;             // [k][k+1] float64 scratch when k > kLdsK
   double *aux;           // [2k + 64] float64 scratch when k > kLdsK
   int ks, k;
+  float *rout;           // optional R [k][k] (Cholesky, upper triangular)
 };
 
 __device__ __forceinline__ uint32_t philox_word0(uint32_t c0, uint32_t c1, uint32_t c2,
@@ -208,7 +209,7 @@ __device__ __forceinline__ void sum_partials(const float *part, int ks, int64_t 
 // X_ic stored at W[c][i]; R^-1 = X^T, row-major float32.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ void chol_inv_body(const float *part, int ks, int k, double *W, int S, double *dg,
-                                              double *idg, double *sink, float *Rinv) {
+                                              double *idg, double *sink, float *Rinv, float *Rout) {
   const int tid = threadIdx.x, nt = blockDim.x;
   const int64_t kk = (int64_t)k * k;
   sum_partials<8>(part, ks, kk, [&](int64_t t, double v) {
@@ -299,6 +300,12 @@ __device__ __forceinline__ void chol_inv_body(const float *part, int ks, int k, 
     const int i = (int)(t / k), c = (int)(t - (int64_t)i * k);
     Rinv[t] = c >= i ? (float)W[i * S + c] : 0.f;
   }
+  // R: its strict upper part sits transposed in the lower triangle of W
+  if (Rout)
+    for (int64_t t = tid; t < kk; t += nt) {
+      const int i = (int)(t / k), c = (int)(t - (int64_t)i * k);
+      Rout[t] = c > i ? (float)W[c * S + i] : (c == i ? (float)dg[i] : 0.f);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -381,8 +388,10 @@ __global__ __launch_bounds__(kSmallThreads) void chol_inv_lds_kernel(const Small
             gv = G[u][w];
             xv = X[u][w];
           }
-        lb[buf][col] = own_g && col >= j ? gv * rs : 0.0;
+        const double lv = own_g && col >= j ? gv * rs : 0.0;   // R_j,col
+        lb[buf][col] = lv;
         xb[buf][col] = own_x ? xv : 0.0;
+        if (J.rout && col < k) J.rout[(int64_t)j * k + col] = (float)lv;
       }
     }
     __syncthreads();
@@ -424,7 +433,7 @@ __global__ __launch_bounds__(kCholGlobalThreads) void chol_inv_global_kernel(con
   const SmallJob J = jobs[blockIdx.x];
   __shared__ double dg[1];  // unused: diagonals live in aux
   (void)dg;
-  chol_inv_body(J.part, J.ks, J.k, J.W, J.k + 1, J.aux, J.aux + J.k, J.aux + 2 * J.k, J.out);
+  chol_inv_body(J.part, J.ks, J.k, J.W, J.k + 1, J.aux, J.aux + J.k, J.aux + 2 * J.k, J.out, J.rout);
 }
 
 // Givens rotation of the one-sided Jacobi step for columns with squared
@@ -1150,6 +1159,51 @@ gift_status factor_refresh_batch(gift_ctx *ctx, const std::vector<SideJob> &jobs
       jb.side->fill_tail = false;
     }
   return GIFT_OK;
+}
+
+size_t chol_blocks_scratch(int k, int count) {
+  auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  size_t b = a256(sizeof(SmallJob) * (size_t)count);
+  if (k > kLdsK)
+    b += a256(sizeof(double) * (size_t)count * k * (k + 1)) + a256(sizeof(double) * (size_t)count * (2 * k + 64));
+  return b;
+}
+
+gift_status launch_chol_blocks(gift_ctx *ctx, const float *G, int k, int count, float *R, float *Rinv,
+                               void *scratch) {
+  if (count <= 0 || k <= 0) return GIFT_OK;
+  auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  char *p = static_cast<char *>(scratch);
+  SmallJob *d_tab = reinterpret_cast<SmallJob *>(p);
+  p += a256(sizeof(SmallJob) * (size_t)count);
+  double *W = nullptr, *aux = nullptr;
+  if (k > kLdsK) {
+    W = reinterpret_cast<double *>(p);
+    p += a256(sizeof(double) * (size_t)count * k * (k + 1));
+    aux = reinterpret_cast<double *>(p);
+  }
+  const int64_t kk = (int64_t)k * k;
+  std::vector<SmallJob> h(count);
+  for (int z = 0; z < count; ++z) {
+    SmallJob &J = h[z];
+    J.part = G + z * kk;
+    J.out = Rinv + z * kk;
+    J.rout = R + z * kk;
+    J.theta = nullptr;
+    J.W = W ? W + (int64_t)z * k * (k + 1) : nullptr;
+    J.aux = aux ? aux + (int64_t)z * (2 * k + 64) : nullptr;
+    J.ks = 1;
+    J.k = k;
+  }
+  // from pageable memory: staged before hipMemcpyAsync returns
+  GIFT_HIP_TRY(hipMemcpyAsync(d_tab, h.data(), sizeof(SmallJob) * (size_t)count, hipMemcpyHostToDevice,
+                              ctx->stream));
+  ProfileScope prof(ctx, GIFT_KERNEL_CHOL);
+  if (k <= kLdsK)
+    hipLaunchKernelGGL(chol_inv_lds_kernel, dim3(count), dim3(kSmallThreads), 0, ctx->stream, d_tab);
+  else
+    hipLaunchKernelGGL(chol_inv_global_kernel, dim3(count), dim3(kCholGlobalThreads), 0, ctx->stream, d_tab);
+  return check_launch("chol_blocks");
 }
 
 }  // namespace gift

@@ -24,7 +24,7 @@ SCALE_LOCAL, SCALE_SHARED = 0, 1
 KERNELS = {
     "amax": 0, "quant": 1, "project": 2, "update_amax": 3, "update_quant": 4,
     "update_store": 5, "reduce": 6, "syrk": 7, "factor": 8, "small": 9,
-    "chol": 10, "eig": 11, "decode_project": 12,
+    "chol": 10, "eig": 11, "decode_project": 12, "chol_transform": 13,
 }
 
 _STATUS = {OK: "GIFT_OK", EINVAL: "GIFT_EINVAL", ESHAPE: "GIFT_ESHAPE", ENOMEM: "GIFT_ENOMEM",
@@ -65,6 +65,9 @@ def _load():
         "gift_factor_update_batch": ([P, I32, P, P, P, I64, I32, I32], I32),
         "gift_factor_export": ([P, P, I32, P, P, P, P], I32),
         "gift_factor_import": ([P, P, I32, P, P, P, P], I32),
+        "gift_factor_create_chol": ([P, I64, I64, I32, I32, F, PP], I32),
+        "gift_factor_export_chol": ([P, P, I32, P, P], I32),
+        "gift_factor_import_chol": ([P, P, I32, P, P], I32),
         "gift_encode": ([P, P, P, I32, I64, I64, I32, I32, I32, P, P, P, P], I32),
         "gift_encode_hits": ([P, P, P, I32, I64, I64, I32, I32, I32, P, P, P, P, P], I32),
         "gift_reduce_local": ([P, P, P, I32, I64, I64, I32, I32, P], I32),
@@ -232,6 +235,47 @@ class Factor:
             self.close()
         except Exception:
             pass
+
+
+class CholFactor(Factor):
+    """Cholesky-form factor (``gift_factor_create_chol``): block 0 = full
+    factor, 1 = diagonal, b = b x b diagonal blocks of A + delta I."""
+
+    def __init__(self, ctx: Context, m: int, n: int, block: int = 0, sides: int = SIDE_INPUT,
+                 damping: float = 1e-6):
+        self.ctx, self.m, self.n, self.block, self.sides = ctx, m, n, block, sides
+        self.rank = 0
+        self._h = ctypes.c_void_p()
+        if not ctx.handle:
+            raise GiftError(EINVAL, "the context is closed")
+        _check(LIB.gift_factor_create_chol(ctx.handle, m, n, block, sides, damping,
+                                           ctypes.byref(self._h)))
+        ctx._factors.add(self)
+
+    def block_shape(self, side: int):
+        """``(nblk, b_eff)`` of one side's stored blocks."""
+        dim = self.n if side == SIDE_INPUT else self.m
+        b = dim if self.block <= 0 or self.block >= dim else self.block
+        return -(-dim // b), b
+
+    def export(self, side: int):
+        import torch
+        nblk, b = self.block_shape(side)
+        dev = torch.device("cuda", torch.cuda.current_device())
+        R = torch.empty((nblk, b, b), dtype=torch.float32, device=dev)
+        Ri = torch.empty((nblk, b, b), dtype=torch.float32, device=dev)
+        _check(LIB.gift_factor_export_chol(self.ctx.handle, self._h, side, _ptr(R), _ptr(Ri)))
+        return R, Ri
+
+    def import_(self, side: int, R, Rinv):
+        import torch
+        nblk, b = self.block_shape(side)
+        for t, nm in ((R, "R"), (Rinv, "Rinv")):
+            if tuple(t.shape) != (nblk, b, b):
+                raise ValueError(f"{nm} must have shape {(nblk, b, b)}")
+        _check(LIB.gift_factor_import_chol(self.ctx.handle, self._h, side,
+                                           _ptr(R, torch.float32, "R"),
+                                           _ptr(Rinv, torch.float32, "Rinv")))
 
 
 def _stats_dtype(x):

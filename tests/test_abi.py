@@ -70,6 +70,22 @@ def test_encode_validation(ctx):
     assert enc(h, None, FAKE, 1, 2_000_000, 4, 0, 0, 0, None, FAKE, FAKE, None) == gift.ESHAPE
 
 
+def test_create_chol_validation(ctx):
+    h = ctx.handle
+    out = ctypes.c_void_p()
+    cr = LIB.gift_factor_create_chol
+    assert cr(None, 8, 8, 0, 1, 1e-3, ctypes.byref(out)) == gift.EINVAL
+    assert cr(h, 8, 8, 0, 4, 1e-3, ctypes.byref(out)) == gift.EINVAL
+    assert cr(h, 8, 8, 0, 1, 0.0, ctypes.byref(out)) == gift.EINVAL
+    assert "damping" in _err()
+    assert cr(h, 8, 8, 0, 1, float("inf"), ctypes.byref(out)) == gift.EINVAL
+    assert cr(h, 8, 8, -2, 1, 1e-3, ctypes.byref(out)) == gift.ESHAPE
+    assert cr(h, 8, 9000, 0, 1, 1e-3, ctypes.byref(out)) == gift.ESHAPE   # full factor over 8192
+    assert cr(h, 0, 8, 0, 1, 1e-3, ctypes.byref(out)) == gift.ESHAPE
+    assert LIB.gift_factor_export_chol(h, None, 1, FAKE, FAKE) == gift.EINVAL
+    assert LIB.gift_factor_import_chol(h, None, 1, FAKE, FAKE) == gift.EINVAL
+
+
 def test_encode_hits_validation(ctx):
     h = ctx.handle
     enc = LIB.gift_encode_hits
