@@ -48,6 +48,7 @@ FAMILY_SOURCE = {
     "update_quant": "paper_2607_07494_amd/csrc/k_lowrank.hip",
     "update_store": "paper_2607_07494_amd/csrc/k_update.hip",
     "decode_project": "paper_2607_07494_amd/csrc/k_update.hip",
+    "chol_transform": "paper_2607_07494_amd/csrc/k_chol.hip",
 }
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm-traffic.md")
 
@@ -74,6 +75,13 @@ def parse():
                          "each matrix's encode -> rank sum -> decode stays on its stream")
     ap.add_argument("--breakdown-steps", type=int, default=2,
                     help="untimed steps with every kernel family bracketed by events")
+    ap.add_argument("--fidelity", action="store_true",
+                    help="only run the transform-variant fidelity study (one-step FP8 round trip "
+                         "of one layer's gradient per transform, Tables I-II's metrics) and print "
+                         "its table")
+    ap.add_argument("--fid-shape", type=int, nargs=2, default=[1024, 2816], metavar=("M", "N"),
+                    help="layer of the fidelity study (d_out d_in; default the MLP down projection)")
+    ap.add_argument("--fid-tokens", type=int, default=8192)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run the library's plain copy kernel on 256 MiB (5 launches), "
                          "the known-size reference for the HBM byte counters")
@@ -273,6 +281,120 @@ def cpu_baseline(wl, seconds):
                       f"{per:.2f} s each"}
 
 
+# Transform variants of the fidelity study: (label, kind, size, sides); kind
+# "chol" takes a block size (0 = the full factor, 1 = the diagonal), "lowrank"
+# a rank.
+FIDELITY_METHODS = [
+    ("Euclidean baseline", None, 0, 0),
+    ("Output-side only (full)", "chol", 0, 2),
+    ("Input-side only (full-A)", "chol", 0, 1),
+    ("K-FAC (both sides, full)", "chol", 0, 3),
+    ("Input-side diag-A", "chol", 1, 1),
+    ("Input-side block-A-32", "chol", 32, 1),
+    ("Input-side block-A-64", "chol", 64, 1),
+    ("Input-side block-A-128", "chol", 128, 1),
+    ("Input-side low-rank-A-8", "lowrank", 8, 1),
+    ("Input-side low-rank-A-16", "lowrank", 16, 1),
+    ("Input-side low-rank-A-32", "lowrank", 32, 1),
+]
+FIDELITY_REGIMES = [
+    ("gaussian tokens", {}),
+    ("spiked tokens (1/512 of the tokens x20 in inputs and output gradients)",
+     {"spike_frac": 1.0 / 512.0, "spike": 20.0}),
+]
+
+
+def recon_metrics(ghat, g):
+    """RelL2, Cos, MaxErr, MSE of a reconstruction (eq. recon_metrics)."""
+    import numpy as np
+    gh = ghat.astype(np.float64).ravel()
+    g = g.astype(np.float64).ravel()
+    d = gh - g
+    return {"RelL2": float(np.linalg.norm(d) / np.linalg.norm(g)),
+            "Cos": float(gh @ g / (np.linalg.norm(gh) * np.linalg.norm(g))),
+            "MaxErr": float(np.abs(d).max()), "MSE": float(d @ d / d.size)}
+
+
+def fidelity_study(args):
+    """One-step FP8 round trip (transform, per-tensor amax E4M3, rank sum of
+    one rank, inverse) of one layer's gradient for every transform variant,
+    factors refreshed on the GPU from the layer's own inputs; plus the time of
+    one refresh and of encode + rank sum + decode of 8 ranks of that shape."""
+    import numpy as np
+    import torch
+    import paper_2607_07494_amd as gift
+    import synth
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    ctx = gift.Context()
+    m, n = args.fid_shape
+    T = args.fid_tokens
+    N8 = 8
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    rows = []
+    for regime, kw in FIDELITY_REGIMES:
+        g, xa, xg = synth.layer_gradients(4242, 1, T, m, n, **kw)
+        print(f"[fidelity] {regime}: layer {m}x{n}, {T} tokens", file=sys.stderr, flush=True)
+        gt = torch.from_numpy(g).to(dev)
+        g8 = gt.expand(N8, m, n).contiguous()
+        at = torch.from_numpy(xa).to(dev)
+        ot = torch.from_numpy(xg).to(dev)
+        codes = torch.empty((N8, m, n), dtype=torch.uint8, device=dev)
+        scales = torch.empty((N8, 1, 1), dtype=torch.float32, device=dev)
+        mean = torch.empty((m, n), dtype=torch.float32, device=dev)
+        out = torch.empty((m, n), dtype=torch.float32, device=dev)
+        for label, kind, size, sides in FIDELITY_METHODS:
+            f = None
+            refresh_ms = 0.0
+            if kind is not None:
+                f = (gift.CholFactor(ctx, m, n, size, sides, 1e-6) if kind == "chol"
+                     else gift.Factor(ctx, m, n, size, sides, 1e-6, seed=11))
+                a_in = at if sides & gift.SIDE_INPUT else None
+                o_in = ot if sides & gift.SIDE_OUTPUT else None
+                f.update(acts=a_in, out_grads=o_in, iters=8)   # cold start
+                torch.cuda.synchronize()
+                e0, e1 = ev(), ev()
+                e0.record()
+                f.update(acts=a_in, out_grads=o_in, iters=2)   # a warm refresh
+                e1.record()
+                torch.cuda.synchronize()
+                refresh_ms = e0.elapsed_time(e1)
+            # the round trip of the one gradient
+            gift.encode(ctx, f, gt, codes[:1], scales[:1])
+            gift.reduce_local(ctx, codes[:1], scales[:1], mean)
+            gift.decode(ctx, f, mean, out)
+            torch.cuda.synchronize()
+            met = recon_metrics(out.cpu().numpy(), g[0])
+            # encode + rank sum + decode of 8 ranks
+            for _ in range(2):
+                gift.encode(ctx, f, g8, codes, scales)
+            reps = 5
+            e0, e1 = ev(), ev()
+            e0.record()
+            for _ in range(reps):
+                gift.encode(ctx, f, g8, codes, scales)
+                gift.reduce_local(ctx, codes, scales, mean)
+                gift.decode(ctx, f, mean, out)
+            e1.record()
+            torch.cuda.synchronize()
+            codec_ms = e0.elapsed_time(e1) / reps
+            row = {"regime": regime, "method": label, **met, "refresh_ms": refresh_ms,
+                   "codec_ms_8ranks": codec_ms}
+            rows.append(row)
+            print(f"[fidelity] {label}: RelL2 {met['RelL2']:.4e}  refresh {refresh_ms:.2f} ms  "
+                  f"codec {codec_ms:.3f} ms", file=sys.stderr, flush=True)
+            if f is not None:
+                f.close()
+    ctx.close()
+    print(f"| regime | method | RelL2 | Cos | MaxErr | MSE | refresh ms | encode+sum+decode ms (8 ranks) |")
+    print("|---|---|---|---|---|---|---|---|")
+    for r in rows:
+        print(f"| {r['regime'].split(' (')[0]} | {r['method']} | {r['RelL2']:.4e} | {r['Cos']:.7f} | "
+              f"{r['MaxErr']:.4e} | {r['MSE']:.4e} | {r['refresh_ms']:.2f} | {r['codec_ms_8ranks']:.3f} |")
+    print(json.dumps({"fidelity": rows, "layer": [m, n], "tokens": T}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -281,6 +403,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.fidelity:
+        fidelity_study(args)
         return
     import torch
     import paper_2607_07494_amd as gift

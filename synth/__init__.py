@@ -91,6 +91,49 @@ def gradient_set(seed_base: int, noise_seed: int, N: int, m: int, n: int,
     return out
 
 
+def layer_gradients(seed: int, N: int, T: int, m: int, n: int, decay: float = 1.2,
+                    spike_frac: float = 0.0, spike: float = 1.0,
+                    target_rms: float = PAPER_GRAD_RMS):
+    """Weight gradients of one linear layer together with the inputs behind them.
+
+    Rank ``j`` sees ``T`` tokens: layer inputs ``X_j`` ``[T, n]`` and output
+    gradients ``D_j`` ``[T, m]``, each row drawn with covariance spectrum
+    ``i^-decay`` in a Haar basis shared by all ranks (the law of
+    :func:`factor_inputs`), and its weight gradient is ``D_j^T X_j / T``.  A
+    fraction ``spike_frac`` of every rank's tokens has both rows multiplied by
+    ``spike`` (tokens with large activations and gradients), which plants a
+    few large rank-one terms in the gradient.  All gradients are rescaled by
+    one common factor to rms ``target_rms`` over the ranks.
+
+    Returns ``(grads [N, m, n] float32, acts [N*T, n] float32,
+    out_grads [N*T, m] float32)``; ``acts`` / ``out_grads`` stack the ranks'
+    tokens in rank order.
+    """
+    rng = np.random.Generator(np.random.PCG64(seed))
+    qa = haar(rng, n, n)
+    qg = haar(rng, m, m)
+    sda = np.arange(1, n + 1, dtype=np.float64) ** (-decay / 2.0)
+    sdg = np.arange(1, m + 1, dtype=np.float64) ** (-decay / 2.0)
+    acts = np.empty((N * T, n), dtype=np.float32)
+    outg = np.empty((N * T, m), dtype=np.float32)
+    grads = np.empty((N, m, n), dtype=np.float64)
+    for j in range(N):
+        X = (rng.standard_normal((T, n)) * sda) @ qa.T
+        D = (rng.standard_normal((T, m)) * sdg) @ qg.T
+        if spike_frac > 0.0:
+            k = max(1, int(round(T * spike_frac)))
+            idx = rng.choice(T, k, replace=False)
+            X[idx] *= spike
+            D[idx] *= spike
+        X = X.astype(np.float32)
+        D = D.astype(np.float32)
+        acts[j * T:(j + 1) * T] = X
+        outg[j * T:(j + 1) * T] = D
+        grads[j] = D.astype(np.float64).T @ X.astype(np.float64) / T
+    rms = float(np.sqrt(np.mean(grads * grads)))
+    return (grads * (target_rms / rms)).astype(np.float32), acts, outg
+
+
 def bf16_round(x: np.ndarray) -> np.ndarray:
     """Round float32 values to bfloat16 (nearest, ties to even); float32 out."""
     b = bf16_bits(x)

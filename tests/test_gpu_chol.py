@@ -16,7 +16,7 @@ import pytest
 import torch
 
 from oracle import codec
-from synth import factor_inputs, gradient_set
+from synth import factor_inputs, gradient_set, layer_gradients
 
 pytestmark = pytest.mark.gpu
 
@@ -222,3 +222,35 @@ def test_chol_argument_errors(ctx):
         gift.Factor.export(f, gift.SIDE_INPUT)                    # Cholesky factor
     f.close()
     lr.close()
+
+
+def test_fidelity_round_trip_matches_oracle(ctx):
+    """The transform-variant fidelity study's one-step round trip (factors
+    refreshed on the GPU from the layer's own inputs) against the oracle's
+    round trip with its own factors of the same inputs: RelL2 within 2 %."""
+    m, n, T = 96, 256, 2048
+    say(f"fidelity round trip m={m} n={n} T={T}")
+    g, xa, xg = layer_gradients(31, 1, T, m, n, spike_frac=1 / 256, spike=20.0)
+    A, G = codec.factor_statistics(xa), codec.factor_statistics(xg)
+    gt = t(g)
+    codes = torch.empty((1, m, n), dtype=torch.uint8, device=DEV)
+    scales = torch.empty((1, 1, 1), dtype=torch.float32, device=DEV)
+    mean = torch.empty((m, n), dtype=torch.float32, device=DEV)
+    out = torch.empty((m, n), dtype=torch.float32, device=DEV)
+    for block, sides in ((None, 0), (0, 1), (1, 1), (32, 1), (0, 2), (0, 3)):
+        f = fA = fG = None
+        if block is not None:
+            f = gift.CholFactor(ctx, m, n, block, sides, 1e-6)
+            f.update(acts=t(xa) if sides & 1 else None, out_grads=t(xg) if sides & 2 else None)
+            fA = codec.chol_factor(A, block, 1e-6) if sides & 1 else None
+            fG = codec.chol_factor(G, block, 1e-6) if sides & 2 else None
+        gift.encode(ctx, f, gt, codes, scales)
+        gift.reduce_local(ctx, codes, scales, mean)
+        gift.decode(ctx, f, mean, out)
+        torch.cuda.synchronize()
+        got = codec.fidelity(out.cpu().numpy(), g[0])["RelL2"]
+        want = codec.fidelity(codec.round_trip(g, fA, fG), g[0])["RelL2"]
+        say(f"  block={block} sides={sides}: RelL2 gpu {got:.5e} oracle {want:.5e}")
+        assert abs(got - want) <= 0.02 * want
+        if f is not None:
+            f.close()

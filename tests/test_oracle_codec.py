@@ -14,7 +14,7 @@ import pytest
 import scipy.linalg
 
 from oracle import codec, e4m3
-from synth import factor_inputs, gradient_set, haar
+from synth import factor_inputs, gradient_set, haar, layer_gradients
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -302,6 +302,17 @@ def test_chol_round_trip_and_identity_cases():
         assert np.allclose(codec.inverse(codec.forward(W, f), f), W, rtol=1e-9, atol=1e-12)
     z = codec.chol_factor(np.zeros((6, 6)), 4, 1e-3)
     assert np.all(z.R == np.eye(4)) and np.all(z.Rinv == np.eye(4))
+
+
+def test_layer_gradients_are_the_inputs_product():
+    # the study's generator: every rank's gradient is D_j^T X_j / T up to the
+    # one common rescale, so the factor statistics describe that gradient
+    g, xa, xg = layer_gradients(3, 2, 64, 12, 20, spike_frac=1 / 32, spike=5.0)
+    assert g.shape == (2, 12, 20) and xa.shape == (128, 20) and xg.shape == (128, 12)
+    prods = [xg[64 * j:64 * (j + 1)].astype(np.float64).T @ xa[64 * j:64 * (j + 1)] / 64 for j in range(2)]
+    c = g[0, 0, 0] / prods[0][0, 0]
+    for j in range(2):
+        assert np.allclose(g[j], c * prods[j], rtol=1e-5, atol=1e-12)
 
 
 # ---------------------------------------------------------------- boundary hits
