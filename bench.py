@@ -68,13 +68,19 @@ def parse():
     ap.add_argument("--cold-iters", type=int, default=6, help="subspace iterations of the first refresh")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
-    ap.add_argument("--issue", choices=["euclid-first", "interleave"], default="euclid-first",
-                    help="host issue order of the matrices within a step")
+    ap.add_argument("--issue", choices=["euclid-first", "interleave", "euclid-after-refresh"],
+                    default="euclid-first",
+                    help="host issue order of the matrices within a step; euclid-after-refresh "
+                         "also holds the Euclidean matrices until the largest factor group's "
+                         "refresh is done, so they do not compete with its statistics kernel")
     ap.add_argument("--streams", type=int, default=4,
                     help="HIP streams (one library context each); matrices are dealt round-robin, "
                          "each matrix's encode -> rank sum -> decode stays on its stream")
     ap.add_argument("--breakdown-steps", type=int, default=2,
                     help="untimed steps with every kernel family bracketed by events")
+    ap.add_argument("--bucket", action="store_true",
+                    help="one call per bucket of same-shape matrices stacked by rows instead of "
+                         "one per matrix (fewer, larger launches; same results)")
     ap.add_argument("--fidelity", action="store_true",
                     help="only run the transform-variant fidelity study (one-step FP8 round trip "
                          "of one layer's gradient per transform, Tables I-II's metrics) and print "
@@ -134,14 +140,21 @@ def copy_calibration():
 
 
 class Job:
-    """Device buffers of one gradient matrix."""
+    """Device buffers of one bucket: gradient matrices of one shape stacked by
+    rows in every rank's buffer (``[N, count*m, n]``), encoded in one call.
+    Each matrix keeps its own scale blocks (block rows never cross a matrix),
+    so the codes, scales, rank mean and decode equal per-matrix calls."""
 
-    def __init__(self, layer, mat, wl, sides_flag, dev, torch, gift):
+    def __init__(self, mats, wl, sides_flag, dev, torch, gift):
+        self.mats = mats
+        layer, mat = mats[0]
         self.layer, self.mat = layer, mat
-        N, m, n = wl.N, mat.m, mat.n
+        N, m, n = wl.N, sum(mt.m for _, mt in mats), mat.n
         self.N, self.m, self.n = N, m, n
         self.gift_branch = mat.gift
         self.br, self.bc = wl.block_rows, wl.block_cols
+        if len(mats) > 1 and self.br == 0:
+            self.br = mat.m        # the whole of each matrix
         nbr, nbc = gift.scale_grid(m, n, self.br, self.bc)
         self.grads = torch.empty((N, m, n), dtype=torch.float32, device=dev)
         self.codes = torch.empty((N, m, n), dtype=torch.uint8, device=dev)
@@ -154,19 +167,60 @@ class Job:
         self.owns_factor = False   # the matrix whose refresh updates a shared factor
 
 
+BUCKET_ELEMS = 1 << 26   # per rank: 256 MB of float32 gradient per bucket
+
+
+def buckets(wl, sides, gift, enable):
+    """Matrices grouped into buckets of one shape, in step order.
+
+    Euclidean matrices of one shape share buckets of up to BUCKET_ELEMS
+    elements per rank; with the input-side transform alone the GIFT matrices
+    that read the same layer input (gate, up) share a bucket, since their
+    common factor acts on rows independently; everything else is a bucket of
+    one.  Block rows must tile each matrix exactly."""
+    mats = wl.all_matrices()
+    if not enable:
+        return [[x] for x in mats]
+    aligned = lambda mt: wl.block_rows == 0 or mt.m % wl.block_rows == 0
+    out, open_eu = [], {}
+    for layer, mt in mats:
+        if not mt.gift and aligned(mt):
+            key = (mt.m, mt.n)
+            b = open_eu.get(key)
+            if b is None or (len(b) + 1) * mt.m * mt.n > BUCKET_ELEMS:
+                b = []
+                open_eu[key] = b
+                out.append(b)
+            b.append((layer, mt))
+        elif mt.gift and sides == gift.SIDE_INPUT and aligned(mt):
+            for b in out:
+                l0, m0 = b[0]
+                if m0.gift and l0 == layer and m0.act == mt.act and (m0.m, m0.n) == (mt.m, mt.n):
+                    b.append((layer, mt))
+                    break
+            else:
+                out.append([(layer, mt)])
+        else:
+            out.append([(layer, mt)])
+    return out
+
+
 def build_workload(args, torch, gift, synth, dev):
     from synth.configs import WORKLOADS
     wl = WORKLOADS[args.config]
     sides = gift.SIDE_INPUT if args.sides == "input" else gift.SIDE_BOTH
-    jobs = [Job(layer, mat, wl, sides, dev, torch, gift) for layer, mat in wl.all_matrices()]
-    # one random set per distinct shape, copied into every matrix's own buffer
+    jobs = [Job(b, wl, sides, dev, torch, gift) for b in buckets(wl, sides, gift, args.bucket)]
+    # one random set per distinct shape, copied into every matrix's rows
     cache = {}
     for jb in jobs:
-        key = (jb.m, jb.n)
-        if key not in cache:
-            cache[key] = synth.gradient_set_torch(synth.seed_for(wl.cfg, 0, 0, jb.mat.kind),
-                                                  wl.N, jb.m, jb.n, dev)
-        jb.grads.copy_(cache[key])
+        off = 0
+        for _, mt in jb.mats:
+            key = (mt.m, mt.n)
+            if key not in cache:
+                cache[key] = synth.gradient_set_torch(synth.seed_for(wl.cfg, 0, 0, mt.kind),
+                                                      wl.N, mt.m, mt.n, dev)
+            jb.grads[:, off:off + mt.m].copy_(cache[key])
+            off += mt.m
     del cache
     # factor inputs: per layer, one activation stream per layer input and one
     # output-gradient stream per GIFT matrix (copies of one draw per shape)
@@ -417,7 +471,8 @@ def main():
     ctx_holder["ctx"] = ctx
     wl, jobs = build_workload(args, torch, gift, synth, dev)
     torch.cuda.synchronize()
-    print(f"[bench] workload {wl.name}: {len(jobs)} matrices, "
+    print(f"[bench] workload {wl.name}: {sum(len(j.mats) for j in jobs)} matrices in "
+          f"{len(jobs)} buckets, "
           f"{sum(j.N * j.m * j.n for j in jobs) * 4 / 1e9:.2f} GB of rank gradients", file=sys.stderr,
           flush=True)
 
@@ -457,7 +512,7 @@ def main():
         for i, jb in enumerate(gjobs):
             jb.sid = ok[i % len(ok)]
         gift_order += gjobs
-    if args.issue == "euclid-first":
+    if args.issue in ("euclid-first", "euclid-after-refresh"):
         order = list(eu) + gift_order
     else:   # alternate, so that every stream's queue holds both kinds early
         order, a, b = [], list(eu), list(gift_order)
@@ -490,6 +545,11 @@ def main():
         waited = set()
         for jb in order:
             sid = 0 if serial else jb.sid
+            if not jb.gift_branch and args.issue == "euclid-after-refresh" and not serial and gorder:
+                rsid, ev = ready[gorder[-1]]
+                if rsid != sid and (sid, None) not in waited:
+                    streams[sid].wait_event(ev)
+                    waited.add((sid, None))
             if jb.gift_branch:
                 rsid, ev = ready[jb.group]
                 if rsid != sid and (sid, jb.group) not in waited:
@@ -603,7 +663,8 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": f"{wl.name} (config {wl.cfg})", "ranks": wl.N, "rank": wl.rank,
-                   "sides": args.sides, "tokens": wl.T, "matrices": len(jobs),
+                   "sides": args.sides, "tokens": wl.T,
+                   "matrices": sum(len(jb.mats) for jb in jobs), "buckets": len(jobs),
                    "factors": sum(1 for jb in jobs if jb.owns_factor), "streams": nstreams,
                    "grad_gb": round(grad_bytes / 1e9, 3), "factor_refresh_every": wl.refresh,
                    "subspace_iters": args.iters},

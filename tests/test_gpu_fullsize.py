@@ -1,0 +1,145 @@
+"""Full-size parity on the benchmark's own matrices and launches (Llama-300M
+gradient set: 8 ranks, rank-64 input-side factors refreshed from 16384 bf16
+tokens, per-tensor scales), checked on sampled rows.
+
+Every call is the one the benchmark times (encode without a stored W~,
+LOCAL scales for the GIFT matrices, SHARED for the Euclidean ones, rank sum,
+decode).  A second encode that also stores W~ must give the same codes and
+scales (so the stored W~ is the tensor the timed encode quantized); on
+sampled rows the oracle then checks, one row at a time: W~ against the
+float64 transform with the GPU's factor (1e-5 relative), codes bit-exact
+against the oracle's quantization of that W~ with scales bit-exact against
+the oracle's block maxima of the whole W~, the rank sum bit-exact and the
+decode within 1e-5 of the oracle's inverse of the GPU's rank mean.  Both
+factors (dims 1024 and 2816) are checked against the exact
+eigendecomposition of the oracle's statistics of the same tokens: the
+captured energy tr(U^T A U) is at least 0.999 of the top-r eigenvalue sum.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import codec
+from synth import factor_inputs_torch, gradient_set_torch, seed_for
+from synth.configs import WORKLOADS
+
+pytestmark = pytest.mark.gpu
+
+gift = pytest.importorskip("paper_2607_07494_amd.gift")
+
+DEV = "cuda"
+WL = WORKLOADS[4]
+ROWS = 48   # sampled rows per matrix (first, last and a spread between)
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def rel(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+def sample_rows(m, seed):
+    rng = np.random.default_rng(seed)
+    return np.unique(np.concatenate([[0, m - 1], rng.choice(m, ROWS - 2, replace=False)]))
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    c = gift.Context()
+    yield c
+    torch.cuda.synchronize()
+    c.close()
+
+
+def run(ctx, f, g, br, bc, mode):
+    """The timed calls, then the encode that also stores W~."""
+    N, m, n = g.shape
+    nbr, nbc = gift.scale_grid(m, n, br, bc)
+    codes = torch.empty((N, m, n), dtype=torch.uint8, device=DEV)
+    scales = torch.empty((N, nbr, nbc), dtype=torch.float32, device=DEV)
+    mean = torch.empty((m, n), dtype=torch.float32, device=DEV)
+    gift.encode(ctx, f, g, codes, scales, br, bc, mode)
+    gift.reduce_local(ctx, codes, scales, mean, br, bc)
+    out = None
+    if f is not None:
+        out = torch.empty((m, n), dtype=torch.float32, device=DEV)
+        gift.decode(ctx, f, mean, out)
+    codes2 = torch.empty_like(codes)
+    scales2 = torch.empty_like(scales)
+    tr = torch.empty((N, m, n), dtype=torch.float32, device=DEV)
+    gift.encode(ctx, f, g, codes2, scales2, br, bc, mode, transformed=tr)
+    torch.cuda.synchronize()
+    assert torch.equal(codes, codes2) and torch.equal(scales, scales2)
+    return codes, scales, mean, out, tr
+
+
+def check_quant_and_sum(codes, scales, mean, tr, rows, br, bc, shared):
+    """Scales from the whole W~, codes and rank sum on the sampled rows."""
+    trh = tr.cpu().numpy()
+    amax = codec.block_amax(trh, br, bc)
+    if shared:
+        amax = np.broadcast_to(amax.max(axis=0, keepdims=True), amax.shape).copy()
+    s_ref, inv = codec.scales_from_amax(amax)
+    sc = scales.cpu().numpy()
+    np.testing.assert_array_equal(sc, s_ref)
+    assert br == 0, "row sampling keeps whole-height scale blocks"
+    sub = trh[:, rows, :]
+    ref_codes = codec.quantize_blocks(sub, inv, 0, bc)
+    got_codes = codes[:, torch.from_numpy(rows).to(DEV), :].cpu().numpy()
+    np.testing.assert_array_equal(got_codes, ref_codes)
+    ref_mean = codec.reduce_local(got_codes, sc, 0, bc)
+    got_mean = mean[torch.from_numpy(rows).to(DEV)].cpu().numpy()
+    np.testing.assert_array_equal(got_mean, ref_mean)
+    return trh, got_mean
+
+
+def gift_matrix(ctx, kind, m, n, check_factor):
+    N, r, T = WL.N, WL.rank, WL.T
+    br, bc = WL.block_rows, WL.block_cols
+    say(f"full size GIFT {kind}: N={N} m={m} n={n} r={r} T={T}")
+    g = gradient_set_torch(seed_for(WL.cfg, 0, 0, kind), N, m, n, DEV)
+    x = factor_inputs_torch(seed_for(WL.cfg, 1, 0, n % 97), T, n, DEV, dtype=WL.act_dtype)
+    f = gift.Factor(ctx, m, n, r, gift.SIDE_INPUT, seed=seed_for(WL.cfg, 50, 0, kind))
+    f.update(acts=x, iters=6)       # the benchmark's cold refresh, then a warm one
+    f.update(acts=x, iters=1)
+    U, cf, ci, s2 = (t.cpu().numpy().astype(np.float64) for t in f.export(gift.SIDE_INPUT))
+    fA = codec.Factor(U, cf, ci, float(s2[0]))
+    if check_factor:
+        A = codec.factor_statistics(x.float().cpu().numpy())
+        lam = np.linalg.eigvalsh(A)[::-1][:r]
+        captured = np.trace(U.T @ A @ U)
+        say(f"  captured energy {captured / lam.sum():.6f}")
+        assert captured >= 0.999 * lam.sum()
+    codes, scales, mean, out, tr = run(ctx, f, g, br, bc, gift.SCALE_LOCAL)
+    rows = sample_rows(m, kind)
+    trh, got_mean = check_quant_and_sum(codes, scales, mean, tr, rows, br, bc, False)
+    gh = g[:, torch.from_numpy(rows).to(DEV), :].cpu().numpy()
+    assert rel(trh[:, rows, :], codec.forward(gh, fA)) <= 1e-5
+    got_out = out[torch.from_numpy(rows).to(DEV)].cpu().numpy()
+    assert rel(got_out, codec.inverse(got_mean, fA)) <= 1e-5
+    f.close()
+
+
+def test_fullsize_gate_matrix(ctx):
+    gift_matrix(ctx, 5, 2816, 1024, check_factor=True)
+
+
+def test_fullsize_down_matrix(ctx):
+    gift_matrix(ctx, 7, 1024, 2816, check_factor=True)
+
+
+@pytest.mark.parametrize("kind,m,n", [(1, 1024, 1024), (8, 32000, 1024)])
+def test_fullsize_euclidean_matrix(ctx, kind, m, n):
+    N, br, bc = WL.N, WL.block_rows, WL.block_cols
+    say(f"full size Euclidean: N={N} m={m} n={n} shared scale")
+    g = gradient_set_torch(seed_for(WL.cfg, 0, 0, kind), N, m, n, DEV)
+    codes, scales, mean, _, tr = run(ctx, None, g, br, bc, gift.SCALE_SHARED)
+    assert torch.equal(tr, g)
+    check_quant_and_sum(codes, scales, mean, tr, sample_rows(m, kind), br, bc, True)
