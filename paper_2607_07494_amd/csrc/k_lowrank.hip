@@ -35,6 +35,7 @@
 
 #include "fp8_e4m3.h"
 #include "gift_internal.h"
+#include "xcd_map.h"
 
 namespace gift {
 namespace {
@@ -306,10 +307,15 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
   __shared__ uint32_t cstage[EPI == EPI_QUANT ? kUpdThreads / 64 : 1][32 * 16];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int fr = lane & 15, fg = lane >> 4;
-  const int b = blockIdx.z;
-  const int64_t i0 = (int64_t)blockIdx.y * kUpdRows + wave * 32;
+  // the column units of one row block on one XCD, one after another, so
+  // the row operand they share is read from HBM once
+  const int64_t lin = ((int64_t)blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x;
+  const int64_t wg_tile = xcd_tile(lin, (int64_t)gridDim.x * gridDim.y * gridDim.z);
+  const int64_t tx = wg_tile % gridDim.x, ty = (wg_tile / gridDim.x) % gridDim.y;
+  const int b = (int)(wg_tile / ((int64_t)gridDim.x * gridDim.y));
+  const int64_t i0 = ty * kUpdRows + wave * 32;
   const int64_t MN = p.M * p.N;
-  const int64_t c_begin = (int64_t)blockIdx.x * COLS;
+  const int64_t c_begin = tx * COLS;
   const int64_t c_end = c_begin + COLS < p.N ? c_begin + COLS : p.N;
   const int ntiles = (int)((c_end - c_begin + 63) / 64);
   const bool wave_live = i0 < p.M;

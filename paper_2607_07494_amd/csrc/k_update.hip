@@ -28,6 +28,7 @@
 
 #include "fp8_e4m3.h"
 #include "gift_internal.h"
+#include "xcd_map.h"
 
 namespace gift {
 
@@ -111,13 +112,18 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const UArgs p) {
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int fr = lane & 15, fg = lane >> 4;
-  const int b = blockIdx.z;
-  const int64_t i0 = (int64_t)blockIdx.y * 64 + wave * 16;
+  // the column units of one row block on one XCD, one after another (they
+  // share the row operand)
+  const int64_t lin = ((int64_t)blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x;
+  const int64_t wg_tile = xcd_tile(lin, (int64_t)gridDim.x * gridDim.y * gridDim.z);
+  const int64_t tx = wg_tile % gridDim.x, ty = (wg_tile / gridDim.x) % gridDim.y;
+  const int b = (int)(wg_tile / ((int64_t)gridDim.x * gridDim.y));
+  const int64_t i0 = ty * 64 + wave * 16;
   const int64_t ri = i0 + fr;
   const bool rv = ri < p.M;
   const bool wave_live = i0 < p.M;
   const int64_t MN = p.M * p.N;
-  const int64_t c_begin = (int64_t)blockIdx.x * kColsPerUnit;
+  const int64_t c_begin = tx * kColsPerUnit;
   const int slot = (int)((((int64_t)blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x) * 4 + wave) %
                    kAmaxSlots;
   const int ntiles = (int)((p.N - c_begin + 63) / 64 < kColsPerUnit / 64 ? (p.N - c_begin + 63) / 64
