@@ -68,19 +68,21 @@ def parse():
     ap.add_argument("--cold-iters", type=int, default=6, help="subspace iterations of the first refresh")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
-    ap.add_argument("--issue", choices=["euclid-first", "interleave", "euclid-after-refresh"],
-                    default="euclid-first",
+    ap.add_argument("--issue", choices=["euclid-first", "interleave", "euclid-after-refresh",
+                                        "euclid-after-statistics"],
+                    default="euclid-after-statistics",
                     help="host issue order of the matrices within a step; euclid-after-refresh "
                          "also holds the Euclidean matrices until the largest factor group's "
-                         "refresh is done, so they do not compete with its statistics kernel")
+                         "refresh is done, euclid-after-statistics only until its statistics "
+                         "kernel is done (the compute-bound part that cannot share CUs)")
     ap.add_argument("--streams", type=int, default=4,
                     help="HIP streams (one library context each); matrices are dealt round-robin, "
                          "each matrix's encode -> rank sum -> decode stays on its stream")
     ap.add_argument("--breakdown-steps", type=int, default=2,
                     help="untimed steps with every kernel family bracketed by events")
-    ap.add_argument("--bucket", action="store_true",
-                    help="one call per bucket of same-shape matrices stacked by rows instead of "
-                         "one per matrix (fewer, larger launches; same results)")
+    ap.add_argument("--no-bucket", dest="bucket", action="store_false",
+                    help="one call per gradient matrix instead of one per bucket of same-shape "
+                         "matrices stacked by rows (same results)")
     ap.add_argument("--fidelity", action="store_true",
                     help="only run the transform-variant fidelity study (one-step FP8 round trip "
                          "of one layer's gradient per transform, Tables I-II's metrics) and print "
@@ -512,7 +514,11 @@ def main():
         for i, jb in enumerate(gjobs):
             jb.sid = ok[i % len(ok)]
         gift_order += gjobs
-    if args.issue in ("euclid-first", "euclid-after-refresh"):
+    stats_ev = None
+    if args.issue == "euclid-after-statistics" and gorder:
+        stats_ev = torch.cuda.Event()
+        ctxs[gsid[gorder[-1]]].set_statistics_event(stats_ev)
+    if args.issue in ("euclid-first", "euclid-after-refresh", "euclid-after-statistics"):
         order = list(eu) + gift_order
     else:   # alternate, so that every stream's queue holds both kinds early
         order, a, b = [], list(eu), list(gift_order)
@@ -549,6 +555,10 @@ def main():
                 rsid, ev = ready[gorder[-1]]
                 if rsid != sid and (sid, None) not in waited:
                     streams[sid].wait_event(ev)
+                    waited.add((sid, None))
+            if not jb.gift_branch and stats_ev is not None and not serial:
+                if gsid[gorder[-1]] != sid and (sid, None) not in waited:
+                    streams[sid].wait_event(stats_ev)
                     waited.add((sid, None))
             if jb.gift_branch:
                 rsid, ev = ready[jb.group]

@@ -121,6 +121,16 @@ gift_status gift_ctx_set_stream(gift_ctx *ctx, void *hip_stream);
  * Destroy the factors created on it first. */
 void gift_ctx_destroy(gift_ctx *ctx);
 
+/* Scheduling hook: every later gift_factor_update[_batch] call on this
+ * context records hip_event (a hipEvent_t passed as void*, created and owned
+ * by the caller) on the context stream right after its statistics kernels
+ * (A = X^T X / T of every factor side), before the rest of the refresh.
+ * Other streams can wait on it to start work once the statistics (the
+ * refresh's compute-bound part) are done.  NULL stops the recording.  For the
+ * Cholesky-form factors nothing is recorded.  Errors: GIFT_EINVAL for a NULL
+ * ctx. */
+gift_status gift_ctx_set_statistics_event(gift_ctx *ctx, void *hip_event);
+
 /* Per-kernel timing: when enabled, every launch of a selected kernel family
  * is bracketed by HIP events on the context stream (all families are selected
  * until gift_ctx_profile_select is called).  gift_ctx_profile_read

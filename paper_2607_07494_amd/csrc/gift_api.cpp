@@ -409,6 +409,12 @@ void gift_ctx_destroy(gift_ctx *ctx) {
   delete ctx;
 }
 
+gift_status gift_ctx_set_statistics_event(gift_ctx *ctx, void *hip_event) {
+  if (!ctx) return set_error(GIFT_EINVAL, "gift_ctx_set_statistics_event: ctx is NULL");
+  ctx->stats_event = static_cast<hipEvent_t>(hip_event);
+  return GIFT_OK;
+}
+
 gift_status gift_ctx_profile_enable(gift_ctx *ctx, int32_t enable) {
   if (!ctx) return set_error(GIFT_EINVAL, "gift_ctx_profile_enable: ctx is NULL");
   ctx->profile = enable != 0;

@@ -51,6 +51,7 @@ struct gift_ctx {
   int slot_set = 0;                // set of the next encode
   size_t slot_dirty[2] = {0, 0};   // words of each set still to clear
   bool slots_unknown = false;      // an encode stopped between its passes
+  hipEvent_t stats_event = nullptr;  // caller's event, recorded after each refresh's statistics
   bool profile = false;
   uint32_t profile_mask = ~0u;     // kernel families timed when profiling
   std::vector<gift::ProfileRec> prof;

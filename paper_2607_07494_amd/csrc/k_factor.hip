@@ -1026,6 +1026,7 @@ gift_status factor_refresh_batch(gift_ctx *ctx, const std::vector<SideJob> &jobs
     if ((st = launch_statistics(ctx, g.xtab, xs.data(), g.G, T, g.dim, dtype, g.Amat, g.Xc)) != GIFT_OK)
       return st;
   }
+  if (ctx->stats_event) GIFT_HIP_TRY(hipEventRecord(ctx->stats_event, stream));
 
   // 2. start blocks of every member
   {

@@ -54,6 +54,7 @@ def _load():
         "gift_ctx_create": ([P, PP], I32),
         "gift_ctx_set_stream": ([P, P], I32),
         "gift_ctx_destroy": ([P], None),
+        "gift_ctx_set_statistics_event": ([P, P], I32),
         "gift_ctx_profile_enable": ([P, I32], I32),
         "gift_ctx_profile_select": ([P, ctypes.c_uint32], I32),
         "gift_ctx_profile_read": ([P, I32, ctypes.POINTER(I64), ctypes.POINTER(ctypes.c_double)], I32),
@@ -132,6 +133,16 @@ class Context:
 
     def set_stream(self, stream):
         _check(LIB.gift_ctx_set_stream(self._h, ctypes.c_void_p(int(stream))))
+
+    def set_statistics_event(self, event):
+        """Record ``event`` (a torch.cuda.Event, or None) after the statistics
+        kernels of every later factor refresh on this context."""
+        h = None
+        if event is not None:
+            import torch  # noqa: F401
+            event.record()          # creates the underlying HIP event
+            h = ctypes.c_void_p(event.cuda_event)
+        _check(LIB.gift_ctx_set_statistics_event(self._h, h))
 
     def profile(self, enable: bool = True):
         _check(LIB.gift_ctx_profile_enable(self._h, 1 if enable else 0))

@@ -43,6 +43,7 @@ def test_null_handles_are_einval():
     assert LIB.gift_decode(None, None, FAKE, 4, 4, FAKE) == gift.EINVAL
     assert LIB.gift_factor_update(None, None, FAKE, None, 8, 0, 1) == gift.EINVAL
     assert LIB.gift_ctx_create(None, None) == gift.EINVAL
+    assert LIB.gift_ctx_set_statistics_event(None, None) == gift.EINVAL
     LIB.gift_ctx_destroy(None)
     LIB.gift_factor_destroy(None)
 

@@ -1,10 +1,13 @@
 """Full-size parity on the benchmark's own matrices and launches (Llama-300M
 gradient set: 8 ranks, rank-64 input-side factors refreshed from 16384 bf16
-tokens, per-tensor scales), checked on sampled rows.
+tokens, per-matrix scales), checked on sampled rows.
 
-Every call is the one the benchmark times (encode without a stored W~,
-LOCAL scales for the GIFT matrices, SHARED for the Euclidean ones, rank sum,
-decode).  A second encode that also stores W~ must give the same codes and
+The launches are the benchmark's: its buckets (same-shape matrices stacked by
+rows, one call per bucket, scale blocks of one matrix each): the 64-matrix
+q/k/v/o bucket, the embedding + LM-head bucket, a gate + up bucket with their
+shared factor and a down matrix.  Every call is the one the benchmark times
+(encode without a stored W~, LOCAL scales for the GIFT matrices, SHARED for
+the Euclidean ones, rank sum, decode).  A second encode that also stores W~ must give the same codes and
 scales (so the stored W~ is the tensor the timed encode quantized); on
 sampled rows the oracle then checks, one row at a time: W~ against the
 float64 transform with the GPU's factor (1e-5 relative), codes bit-exact
@@ -21,6 +24,7 @@ import pytest
 import torch
 
 from oracle import codec
+import bench
 from synth import factor_inputs_torch, gradient_set_torch, seed_for
 from synth.configs import WORKLOADS
 
@@ -81,7 +85,8 @@ def run(ctx, f, g, br, bc, mode):
 
 
 def check_quant_and_sum(codes, scales, mean, tr, rows, br, bc, shared):
-    """Scales from the whole W~, codes and rank sum on the sampled rows."""
+    """Scales from the whole W~, codes and rank sum on the sampled rows
+    (each row with the scales of its own block row)."""
     trh = tr.cpu().numpy()
     amax = codec.block_amax(trh, br, bc)
     if shared:
@@ -89,22 +94,48 @@ def check_quant_and_sum(codes, scales, mean, tr, rows, br, bc, shared):
     s_ref, inv = codec.scales_from_amax(amax)
     sc = scales.cpu().numpy()
     np.testing.assert_array_equal(sc, s_ref)
-    assert br == 0, "row sampling keeps whole-height scale blocks"
-    sub = trh[:, rows, :]
-    ref_codes = codec.quantize_blocks(sub, inv, 0, bc)
+    m = trh.shape[1]
+    blk = rows // (br if br > 0 else m)
     got_codes = codes[:, torch.from_numpy(rows).to(DEV), :].cpu().numpy()
-    np.testing.assert_array_equal(got_codes, ref_codes)
-    ref_mean = codec.reduce_local(got_codes, sc, 0, bc)
     got_mean = mean[torch.from_numpy(rows).to(DEV)].cpu().numpy()
-    np.testing.assert_array_equal(got_mean, ref_mean)
+    for k, (r, q) in enumerate(zip(rows, blk)):
+        ref_codes = codec.quantize_blocks(trh[:, r:r + 1, :], inv[:, q:q + 1, :], 0, bc)
+        np.testing.assert_array_equal(got_codes[:, k:k + 1, :], ref_codes)
+        ref_mean = codec.reduce_local(got_codes[:, k:k + 1, :], sc[:, q:q + 1, :], 0, bc)
+        np.testing.assert_array_equal(got_mean[k:k + 1], ref_mean)
     return trh, got_mean
 
 
-def gift_matrix(ctx, kind, m, n, check_factor):
+def bench_bucket(pred):
+    """The first of the benchmark's buckets whose matrices satisfy pred, with
+    its block rows and gradient set filled as the benchmark fills it."""
+    import paper_2607_07494_amd as pkg
+    for b in bench.buckets(WL, gift.SIDE_INPUT, pkg, True):
+        if pred(b):
+            break
+    else:
+        raise AssertionError("no such bucket")
+    N, n = WL.N, b[0][1].n
+    m = sum(mt.m for _, mt in b)
+    br = b[0][1].m if len(b) > 1 and WL.block_rows == 0 else WL.block_rows
+    g = torch.empty((N, m, n), dtype=torch.float32, device=DEV)
+    off, sets = 0, {}
+    for _, mt in b:
+        if mt.kind not in sets:
+            sets[mt.kind] = gradient_set_torch(seed_for(WL.cfg, 0, 0, mt.kind), N, mt.m, mt.n, DEV)
+        g[:, off:off + mt.m].copy_(sets[mt.kind])
+        off += mt.m
+    return b, g, br
+
+
+def gift_matrix(ctx, name, check_factor):
     N, r, T = WL.N, WL.rank, WL.T
-    br, bc = WL.block_rows, WL.block_cols
-    say(f"full size GIFT {kind}: N={N} m={m} n={n} r={r} T={T}")
-    g = gradient_set_torch(seed_for(WL.cfg, 0, 0, kind), N, m, n, DEV)
+    b, g, br = bench_bucket(lambda b: b[0][1].gift and b[0][1].name == name)
+    bc = WL.block_cols
+    _, m, n = g.shape
+    kind = b[0][1].kind
+    say(f"full size GIFT bucket {[mt.name for _, mt in b]}: N={N} m={m} n={n} r={r} T={T} "
+        f"block=({br},{bc})")
     x = factor_inputs_torch(seed_for(WL.cfg, 1, 0, n % 97), T, n, DEV, dtype=WL.act_dtype)
     f = gift.Factor(ctx, m, n, r, gift.SIDE_INPUT, seed=seed_for(WL.cfg, 50, 0, kind))
     f.update(acts=x, iters=6)       # the benchmark's cold refresh, then a warm one
@@ -127,19 +158,21 @@ def gift_matrix(ctx, kind, m, n, check_factor):
     f.close()
 
 
-def test_fullsize_gate_matrix(ctx):
-    gift_matrix(ctx, 5, 2816, 1024, check_factor=True)
+def test_fullsize_gate_up_bucket(ctx):
+    gift_matrix(ctx, "gate", check_factor=True)
 
 
 def test_fullsize_down_matrix(ctx):
-    gift_matrix(ctx, 7, 1024, 2816, check_factor=True)
+    gift_matrix(ctx, "down", check_factor=True)
 
 
-@pytest.mark.parametrize("kind,m,n", [(1, 1024, 1024), (8, 32000, 1024)])
-def test_fullsize_euclidean_matrix(ctx, kind, m, n):
-    N, br, bc = WL.N, WL.block_rows, WL.block_cols
-    say(f"full size Euclidean: N={N} m={m} n={n} shared scale")
-    g = gradient_set_torch(seed_for(WL.cfg, 0, 0, kind), N, m, n, DEV)
+@pytest.mark.parametrize("name", ["q", "embed"])
+def test_fullsize_euclidean_bucket(ctx, name):
+    N, bc = WL.N, WL.block_cols
+    b, g, br = bench_bucket(lambda b: not b[0][1].gift and b[0][1].name == name)
+    _, m, n = g.shape
+    say(f"full size Euclidean bucket of {len(b)} x {b[0][1].name}: N={N} m={m} n={n} "
+        f"block=({br},{bc}) shared scale")
     codes, scales, mean, _, tr = run(ctx, None, g, br, bc, gift.SCALE_SHARED)
     assert torch.equal(tr, g)
-    check_quant_and_sum(codes, scales, mean, tr, sample_rows(m, kind), br, bc, True)
+    check_quant_and_sum(codes, scales, mean, tr, sample_rows(m, b[0][1].kind), br, bc, True)
