@@ -205,6 +205,9 @@ bool encode_recomputes(const gift_factor *f, int64_t n, const float *grads, cons
   const bool useG = side_in(f->sides, GIFT_SIDE_OUTPUT) && f->G.r > 0;
   if (!useA && !useG) return false;
   if (useA && useG && f->A.r != f->G.r) return false;
+  // the split-bf16 update kernels take one rank's slice within a 32-bit
+  // buffer range; larger matrices store W~ and quantize it in a second pass
+  if (f->m * n >= (1LL << 29)) return false;
   const int K = useA ? f->A.r : f->G.r;
   if (K > 128 || K % 4 != 0 || n % 4 != 0) return false;
   return al16p(grads) && (!ef || al16p(ef)) && (!transformed || al16p(transformed)) &&
