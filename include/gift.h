@@ -98,7 +98,8 @@ typedef enum {
   GIFT_KERNEL_EIG = 11,          /* Rayleigh-Ritz k x k eigensolver           */
   GIFT_KERNEL_DECODE_PROJECT = 12, /* the inverse transform's projections     */
   GIFT_KERNEL_CHOL_TRANSFORM = 13, /* Cholesky-form transform products         */
-  GIFT_KERNEL_COUNT = 14
+  GIFT_KERNEL_MXFP4 = 14,        /* MXFP4 scale + pack (gift_encode_mxfp4)     */
+  GIFT_KERNEL_COUNT = 15
 } gift_kernel;
 
 /* ABI version of the loaded library (GIFT_ABI_VERSION it was built with). */
@@ -282,6 +283,35 @@ gift_status gift_encode_hits(gift_ctx *ctx, const gift_factor *f, const float *g
                              int32_t block_cols, gift_scale_mode mode, float *ef,
                              uint8_t *codes, float *scales, float *transformed,
                              uint32_t *hits);
+
+/* MXFP4 variant of gift_encode: the same transform (W~ = S_G^-1 W S_A^-1, or
+ * the Cholesky form; f = NULL: W itself), then OCP Microscaling FP4 instead of
+ * FP8 -- the 4-bit format the paper names as future work (Sec. I; Sec. VI,
+ * Discussion):
+ *   per rank, row and 32 consecutive columns, k = floor(log2(amax)) - 2
+ *   (>= -127; a block holding a NaN or an infinity: scale 255 = NaN, codes 0),
+ *   scales = k + 127 (E8M0), each element v * 2^-k rounded to the nearest FP4
+ *   E2M1 value (0, 0.5, 1, 1.5, 2, 3, 4, 6; ties to the even code; larger
+ *   magnitudes saturate to 6; sign of zero kept).
+ *   codes  [N, m, n/2] uint8 out, two codes per byte, element 2i in the low
+ *          nibble (4-byte aligned);  scales [N, m, n/32] uint8 out;
+ *   ef     optional residual [N, m, n] in transformed coordinates, read and
+ *          rewritten (U = W~ + R; R <- U - Dequantize(codes));
+ *   transformed  optional [N, m, n] float32 out: U before quantization.
+ * The low-rank transform's products are float32 here (stored, then quantized
+ * in a second pass).  n must be a multiple of 32 (GIFT_ESHAPE); grads, ef and
+ * transformed 16-byte aligned (GIFT_EINVAL).  Scales are per rank (no
+ * shared-scale mode).  Uses the context workspace. */
+gift_status gift_encode_mxfp4(gift_ctx *ctx, const gift_factor *f, const float *grads, int32_t N,
+                              int64_t m, int64_t n, float *ef, uint8_t *codes, uint8_t *scales,
+                              float *transformed);
+
+/* Rank mean of MXFP4-encoded ranks: mean[e] = fl32(acc / N), acc = fl32(acc +
+ * v_j[e]) for j = 0..N-1 in order, v_j = E2M1 value x 2^(scale - 127) (exact;
+ * NaN for scale 255).  codes [N, m, n/2] (4-byte aligned), scales
+ * [N, m, n/32], mean [m, n] float32 out (16-byte aligned); n % 32 == 0. */
+gift_status gift_reduce_local_mxfp4(gift_ctx *ctx, const uint8_t *codes, const uint8_t *scales,
+                                    int32_t N, int64_t m, int64_t n, float *mean);
 
 /* Average the N ranks in transformed coordinates (eq. dp_grad_avg):
  *   mean[e] = fl32(acc / N),  acc = fl32(acc + fl32(val(codes[j][e]) * s_j)) for

@@ -23,7 +23,7 @@ LIB = os.path.join(PKG, "libgift.so")
 ARCH = "gfx950"
 
 SOURCES = ["gift_api.cpp", "k_tile.hip", "k_reduce.hip", "k_factor.hip", "k_syrk.hip", "k_update.hip", "k_stream.hip",
-           "k_lowrank.hip", "k_chol.hip"]
+           "k_lowrank.hip", "k_chol.hip", "k_mx.hip"]
 
 
 def hipcc() -> str:

@@ -910,6 +910,80 @@ gift_status gift_reduce_local(gift_ctx *ctx, const uint8_t *codes, const float *
   return launch_reduce(ctx, codes, scales, N, m, n, block_geom(m, n, block_rows, block_cols), mean);
 }
 
+gift_status gift_encode_mxfp4(gift_ctx *ctx, const gift_factor *f, const float *grads, int32_t N,
+                              int64_t m, int64_t n, float *ef, uint8_t *codes, uint8_t *scales,
+                              float *transformed) {
+  if (!ctx) return set_error(GIFT_EINVAL, "gift_encode_mxfp4: ctx is NULL");
+  if (!grads || !codes || !scales) return set_error(GIFT_EINVAL, "gift_encode_mxfp4: NULL tensor");
+  if (N <= 0 || N > kMaxRanks) return set_error(GIFT_ESHAPE, "gift_encode_mxfp4: N must be in [1, 65535]");
+  gift_status st = check_matrix_dims(m, n);
+  if (st != GIFT_OK) return st;
+  if (n % 32 != 0) return set_error(GIFT_ESHAPE, "gift_encode_mxfp4: n must be a multiple of 32");
+  if (f && (f->m != m || f->n != n))
+    return set_error(GIFT_ESHAPE, "gift_encode_mxfp4: factor was created for another shape");
+  if (!al16p(grads) || (ef && !al16p(ef)) || (transformed && !al16p(transformed)) ||
+      (reinterpret_cast<uintptr_t>(codes) & 3))
+    return set_error(GIFT_EINVAL,
+                     "gift_encode_mxfp4: grads, ef and transformed must be 16-byte aligned, codes 4-byte aligned");
+  if ((st = bind_device(ctx)) != GIFT_OK) return st;
+  const int64_t total = (int64_t)N * m * n;
+  const float *src = grads;
+  if (f) {
+    if (f->chol) {
+      const bool two = chol_transform_needs_tmp(f);
+      void *buf = nullptr;
+      if ((st = grow_buffer(ctx, ctx->xform, sizeof(float) * (size_t)total * (two ? 2 : 1), &buf)) != GIFT_OK)
+        return st;
+      float *wt = static_cast<float *>(buf);
+      if ((st = launch_chol_transform(ctx, f, grads, wt, N, false, two ? wt + total : nullptr)) != GIFT_OK)
+        return st;
+      src = wt;
+    } else {
+      LowRankPlan plan;
+      size_t bytes = 0;
+      if ((st = plan_low_rank(ctx, f, grads, N, m, n, false, nullptr, &bytes, &plan)) != GIFT_OK) return st;
+      if (plan.active) {
+        void *buf = nullptr;
+        if ((st = grow_buffer(ctx, ctx->xform, sizeof(float) * (size_t)total, &buf)) != GIFT_OK) return st;
+        void *ws = nullptr;
+        if ((st = workspace(ctx, bytes, &ws)) != GIFT_OK) return st;
+        if ((st = plan_low_rank(ctx, f, grads, N, m, n, false, static_cast<char *>(ws), &bytes, &plan)) !=
+            GIFT_OK)
+          return st;
+        // W~ = W + the low-rank part, stored (float32 products)
+        TileJob job = plan.upd;
+        job.C = static_cast<float *>(buf);
+        job.ldc = n;
+        job.cbs = m * n;
+        job.D = grads;
+        job.ldd = n;
+        job.dbs = m * n;
+        job.beta = 1.f;
+        job.split3 = false;
+        job.kernel_family = GIFT_KERNEL_UPDATE_STORE;
+        if ((st = launch_tile(ctx, job)) != GIFT_OK) return st;
+        src = static_cast<float *>(buf);
+      }
+    }
+  }
+  return launch_mx_quant(ctx, src, ef, ef, transformed, codes, scales, total);
+}
+
+gift_status gift_reduce_local_mxfp4(gift_ctx *ctx, const uint8_t *codes, const uint8_t *scales, int32_t N,
+                                    int64_t m, int64_t n, float *mean) {
+  if (!ctx) return set_error(GIFT_EINVAL, "gift_reduce_local_mxfp4: ctx is NULL");
+  if (!codes || !scales || !mean) return set_error(GIFT_EINVAL, "gift_reduce_local_mxfp4: NULL tensor");
+  if (N <= 0 || N > kMaxRanks)
+    return set_error(GIFT_ESHAPE, "gift_reduce_local_mxfp4: N must be in [1, 65535]");
+  gift_status st = check_matrix_dims(m, n);
+  if (st != GIFT_OK) return st;
+  if (n % 32 != 0) return set_error(GIFT_ESHAPE, "gift_reduce_local_mxfp4: n must be a multiple of 32");
+  if ((reinterpret_cast<uintptr_t>(codes) & 3) || !al16p(mean))
+    return set_error(GIFT_EINVAL, "gift_reduce_local_mxfp4: codes must be 4-byte, mean 16-byte aligned");
+  if ((st = bind_device(ctx)) != GIFT_OK) return st;
+  return launch_mx_reduce(ctx, codes, scales, N, m * n, mean);
+}
+
 gift_status gift_decode(gift_ctx *ctx, const gift_factor *f, const float *mean, int64_t m,
                         int64_t n, float *out) {
   if (!ctx) return set_error(GIFT_EINVAL, "gift_decode: ctx is NULL");

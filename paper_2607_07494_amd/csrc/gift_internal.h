@@ -297,6 +297,14 @@ gift_status chol_side_identity(gift_ctx *ctx, CholSide &s);
 bool chol_transform_needs_tmp(const gift_factor *f);
 gift_status launch_chol_transform(gift_ctx *ctx, const gift_factor *f, const float *in, float *out,
                                   int32_t N, bool inverse, float *tmp);
+// k_mx.hip: MXFP4 (OCP MX: E2M1 elements, E8M0 scale per 32 elements of a row)
+// encode of x (+ ef_in) into packed codes [total / 2] and scales [total / 32]
+// (total a multiple of 32, x / ef / transformed 16-byte aligned, codes 4-byte
+// aligned), and the rank mean of N such ranks of per_rank elements each.
+gift_status launch_mx_quant(gift_ctx *ctx, const float *x, const float *ef_in, float *ef, float *transformed,
+                            uint8_t *codes, uint8_t *scales, int64_t total);
+gift_status launch_mx_reduce(gift_ctx *ctx, const uint8_t *codes, const uint8_t *scales, int32_t N,
+                             int64_t per_rank, float *mean);
 // Grow-only device buffer (synchronizes the stream before it frees the old one).
 gift_status grow_buffer(gift_ctx *ctx, Workspace &w, size_t bytes, void **out);
 

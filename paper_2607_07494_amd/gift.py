@@ -24,7 +24,7 @@ SCALE_LOCAL, SCALE_SHARED = 0, 1
 KERNELS = {
     "amax": 0, "quant": 1, "project": 2, "update_amax": 3, "update_quant": 4,
     "update_store": 5, "reduce": 6, "syrk": 7, "factor": 8, "small": 9,
-    "chol": 10, "eig": 11, "decode_project": 12, "chol_transform": 13,
+    "chol": 10, "eig": 11, "decode_project": 12, "chol_transform": 13, "mxfp4": 14,
 }
 
 _STATUS = {OK: "GIFT_OK", EINVAL: "GIFT_EINVAL", ESHAPE: "GIFT_ESHAPE", ENOMEM: "GIFT_ENOMEM",
@@ -72,6 +72,8 @@ def _load():
         "gift_encode": ([P, P, P, I32, I64, I64, I32, I32, I32, P, P, P, P], I32),
         "gift_encode_hits": ([P, P, P, I32, I64, I64, I32, I32, I32, P, P, P, P, P], I32),
         "gift_reduce_local": ([P, P, P, I32, I64, I64, I32, I32, P], I32),
+        "gift_encode_mxfp4": ([P, P, P, I32, I64, I64, P, P, P, P], I32),
+        "gift_reduce_local_mxfp4": ([P, P, P, I32, I64, I64, P], I32),
         "gift_decode": ([P, P, P, I64, I64, P], I32),
     }
     for name, (args, res) in sigs.items():
@@ -366,6 +368,26 @@ def reduce_local(ctx: Context, codes, scales, mean, block_rows: int = 0, block_c
     _check(LIB.gift_reduce_local(ctx.handle, _ptr(codes, torch.uint8, "codes"),
                                  _ptr(scales, torch.float32, "scales"), N, m, n, block_rows,
                                  block_cols, _ptr(mean, torch.float32, "mean")))
+
+
+def encode_mxfp4(ctx: Context, factor, grads, codes, scales, ef=None, transformed=None):
+    """``gift_encode_mxfp4``: grads [N, m, n] f32 -> codes [N, m, n/2] u8 (packed
+    E2M1), scales [N, m, n/32] u8 (E8M0)."""
+    import torch
+    N, m, n = grads.shape
+    _check(LIB.gift_encode_mxfp4(ctx.handle, factor.handle if factor is not None else None,
+                                 _ptr(grads, torch.float32, "grads"), N, m, n, _ptr(ef, torch.float32, "ef"),
+                                 _ptr(codes, torch.uint8, "codes"), _ptr(scales, torch.uint8, "scales"),
+                                 _ptr(transformed, torch.float32, "transformed")))
+
+
+def reduce_local_mxfp4(ctx: Context, codes, scales, mean):
+    """``gift_reduce_local_mxfp4``: codes [N, m, n/2], scales [N, m, n/32] -> mean [m, n] f32."""
+    import torch
+    N, m, half = codes.shape
+    _check(LIB.gift_reduce_local_mxfp4(ctx.handle, _ptr(codes, torch.uint8, "codes"),
+                                       _ptr(scales, torch.uint8, "scales"), N, m, 2 * half,
+                                       _ptr(mean, torch.float32, "mean")))
 
 
 def decode(ctx: Context, factor, mean, out):

@@ -87,6 +87,21 @@ def test_create_chol_validation(ctx):
     assert LIB.gift_factor_import_chol(h, None, 1, FAKE, FAKE) == gift.EINVAL
 
 
+def test_mxfp4_validation(ctx):
+    h = ctx.handle
+    enc = LIB.gift_encode_mxfp4
+    assert enc(None, None, FAKE, 1, 4, 32, None, FAKE, FAKE, None) == gift.EINVAL
+    assert enc(h, None, None, 1, 4, 32, None, FAKE, FAKE, None) == gift.EINVAL
+    assert enc(h, None, FAKE, 1, 4, 48, None, FAKE, FAKE, None) == gift.ESHAPE
+    assert "multiple of 32" in _err()
+    assert enc(h, None, FAKE, 0, 4, 32, None, FAKE, FAKE, None) == gift.ESHAPE
+    assert enc(h, None, ctypes.c_void_p(0x1004), 1, 4, 32, None, FAKE, FAKE, None) == gift.EINVAL
+    red = LIB.gift_reduce_local_mxfp4
+    assert red(h, FAKE, FAKE, 1, 4, 40, FAKE) == gift.ESHAPE
+    assert red(h, None, FAKE, 1, 4, 32, FAKE) == gift.EINVAL
+    assert red(h, FAKE, FAKE, 1, 4, 32, ctypes.c_void_p(0x1008)) == gift.EINVAL
+
+
 def test_encode_hits_validation(ctx):
     h = ctx.handle
     enc = LIB.gift_encode_hits
