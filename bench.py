@@ -49,6 +49,7 @@ FAMILY_SOURCE = {
     "update_store": "paper_2607_07494_amd/csrc/k_update.hip",
     "decode_project": "paper_2607_07494_amd/csrc/k_update.hip",
     "chol_transform": "paper_2607_07494_amd/csrc/k_chol.hip",
+    "mxfp4": "paper_2607_07494_amd/csrc/k_mx.hip",
 }
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm-traffic.md")
 
@@ -80,6 +81,9 @@ def parse():
                          "each matrix's encode -> rank sum -> decode stays on its stream")
     ap.add_argument("--breakdown-steps", type=int, default=2,
                     help="untimed steps with every kernel family bracketed by events")
+    ap.add_argument("--format", choices=["fp8", "mxfp4"], default="fp8",
+                    help="communication format: FP8 E4M3 (the paper's) or OCP MXFP4 (E2M1 with an "
+                         "E8M0 scale per 32 elements of a row, per-rank scales for every matrix)")
     ap.add_argument("--no-bucket", dest="bucket", action="store_false",
                     help="one call per gradient matrix instead of one per bucket of same-shape "
                          "matrices stacked by rows (same results)")
@@ -147,7 +151,7 @@ class Job:
     Each matrix keeps its own scale blocks (block rows never cross a matrix),
     so the codes, scales, rank mean and decode equal per-matrix calls."""
 
-    def __init__(self, mats, wl, sides_flag, dev, torch, gift):
+    def __init__(self, mats, wl, sides_flag, dev, torch, gift, fmt="fp8"):
         self.mats = mats
         layer, mat = mats[0]
         self.layer, self.mat = layer, mat
@@ -159,8 +163,12 @@ class Job:
             self.br = mat.m        # the whole of each matrix
         nbr, nbc = gift.scale_grid(m, n, self.br, self.bc)
         self.grads = torch.empty((N, m, n), dtype=torch.float32, device=dev)
-        self.codes = torch.empty((N, m, n), dtype=torch.uint8, device=dev)
-        self.scales = torch.empty((N, nbr, nbc), dtype=torch.float32, device=dev)
+        if fmt == "mxfp4":
+            self.codes = torch.empty((N, m, n // 2), dtype=torch.uint8, device=dev)
+            self.scales = torch.empty((N, m, n // 32), dtype=torch.uint8, device=dev)
+        else:
+            self.codes = torch.empty((N, m, n), dtype=torch.uint8, device=dev)
+            self.scales = torch.empty((N, nbr, nbc), dtype=torch.float32, device=dev)
         self.mean = torch.empty((m, n), dtype=torch.float32, device=dev)
         self.out = torch.empty((m, n), dtype=torch.float32, device=dev) if mat.gift else None
         self.factor = None
@@ -211,7 +219,7 @@ def build_workload(args, torch, gift, synth, dev):
     from synth.configs import WORKLOADS
     wl = WORKLOADS[args.config]
     sides = gift.SIDE_INPUT if args.sides == "input" else gift.SIDE_BOTH
-    jobs = [Job(b, wl, sides, dev, torch, gift) for b in buckets(wl, sides, gift, args.bucket)]
+    jobs = [Job(b, wl, sides, dev, torch, gift, args.format) for b in buckets(wl, sides, gift, args.bucket)]
     # one random set per distinct shape, copied into every matrix's rows
     cache = {}
     for jb in jobs:
@@ -272,26 +280,40 @@ def algorithmic_work(wl, jobs, args):
         fam[name] = (f + flops, b + bytes_)
 
     refresh = 1.0 / wl.refresh
+    mxb = 0.5 + 1.0 / 32.0     # MXFP4 bytes per element: a 4-bit code and 1/32 of a scale
     for jb in jobs:
         N, m, n = jb.N, jb.m, jb.n
         e = float(N) * m * n
-        if not jb.gift_branch:
+        mn = float(m) * n
+        ra = r if jb.gift_branch and jb.sides & 1 else 0
+        rg = r if jb.gift_branch and jb.sides & 2 else 0
+        proj_flops = 2 * e * (ra + rg) + (4 * N * rg * ra * m if ra and rg else 0)
+        proj_bytes = 4 * e * ((ra > 0) + (rg > 0))
+        if args.format == "mxfp4":
+            add("mxfp4", 0, (4 + mxb) * e)
+            add("reduce", 0, mn * (N * mxb + 4))
+            if jb.gift_branch:
+                # projections, then W~ = W + the low-rank part stored (float32
+                # products, 8 B/elem, the decode's STORE family) before the
+                # MXFP4 pass; the decode as in FP8
+                add("project", proj_flops, proj_bytes)
+                add("update_store", 2 * (e + mn) * (ra + rg), 8 * (e + mn))
+                add("decode_project", 2 * mn * (ra + rg), 4 * mn * ((ra > 0) + (rg > 0)))
+        elif not jb.gift_branch:
             add("amax", 0, 4 * e)
             add("quant", 0, 5 * e)
-            add("reduce", 0, float(m) * n * (N + 4))
+            add("reduce", 0, mn * (N + 4))
+        else:
+            # encode: projections (2r flops/elem per side), the rank-r update
+            # fused with the block maxima, then scale + FP8 pack of W~
+            add("project", proj_flops, proj_bytes)
+            add("update_amax", 2 * e * (ra + rg), 4 * e)
+            add("update_quant", 0, 5 * e)
+            add("reduce", 0, mn * (N + 4))
+            add("decode_project", 2 * mn * (ra + rg), 4 * mn * ((ra > 0) + (rg > 0)))
+            add("update_store", 2 * mn * (ra + rg), 8 * mn)
+        if not jb.gift_branch:
             continue
-        ra = r if jb.sides & 1 else 0
-        rg = r if jb.sides & 2 else 0
-        # encode: projections (2r flops/elem per side), the rank-r update fused
-        # with the block maxima, then scale + FP8 pack of W~ (no products)
-        add("project", 2 * e * (ra + rg) + (2 * N * rg * ra * m if ra and rg else 0)
-            + (2 * N * m * rg * ra if ra and rg else 0), 4 * e * ((ra > 0) + (rg > 0)))
-        add("update_amax", 2 * e * (ra + rg), 4 * e)
-        add("update_quant", 0, 5 * e)
-        add("reduce", 0, float(m) * n * (N + 4))
-        mn = float(m) * n
-        add("decode_project", 2 * mn * (ra + rg), 4 * mn * ((ra > 0) + (rg > 0)))
-        add("update_store", 2 * mn * (ra + rg), 8 * mn)
         # factor refresh (amortised by the cadence), once per distinct factor
         for dim, on in ((n, ra), (m, rg)):
             if not on or not jb.owns_factor:
@@ -374,6 +396,7 @@ def recon_metrics(ghat, g):
 def fidelity_study(args):
     """One-step FP8 round trip (transform, per-tensor amax E4M3, rank sum of
     one rank, inverse) of one layer's gradient for every transform variant,
+    and the same with MXFP4 (per-32-element E8M0 scales) in place of FP8,
     factors refreshed on the GPU from the layer's own inputs; plus the time of
     one refresh and of encode + rank sum + decode of 8 ranks of that shape."""
     import numpy as np
@@ -398,6 +421,8 @@ def fidelity_study(args):
         ot = torch.from_numpy(xg).to(dev)
         codes = torch.empty((N8, m, n), dtype=torch.uint8, device=dev)
         scales = torch.empty((N8, 1, 1), dtype=torch.float32, device=dev)
+        mxc = torch.empty((1, m, n // 2), dtype=torch.uint8, device=dev)
+        mxs = torch.empty((1, m, n // 32), dtype=torch.uint8, device=dev)
         mean = torch.empty((m, n), dtype=torch.float32, device=dev)
         out = torch.empty((m, n), dtype=torch.float32, device=dev)
         for label, kind, size, sides in FIDELITY_METHODS:
@@ -422,6 +447,11 @@ def fidelity_study(args):
             gift.decode(ctx, f, mean, out)
             torch.cuda.synchronize()
             met = recon_metrics(out.cpu().numpy(), g[0])
+            gift.encode_mxfp4(ctx, f, gt, mxc, mxs)
+            gift.reduce_local_mxfp4(ctx, mxc, mxs, mean)
+            gift.decode(ctx, f, mean, out)
+            torch.cuda.synchronize()
+            met_mx = recon_metrics(out.cpu().numpy(), g[0])
             # encode + rank sum + decode of 8 ranks
             for _ in range(2):
                 gift.encode(ctx, f, g8, codes, scales)
@@ -436,7 +466,7 @@ def fidelity_study(args):
             torch.cuda.synchronize()
             codec_ms = e0.elapsed_time(e1) / reps
             row = {"regime": regime, "method": label, **met, "refresh_ms": refresh_ms,
-                   "codec_ms_8ranks": codec_ms}
+                   "codec_ms_8ranks": codec_ms, "mxfp4": met_mx}
             rows.append(row)
             print(f"[fidelity] {label}: RelL2 {met['RelL2']:.4e}  refresh {refresh_ms:.2f} ms  "
                   f"codec {codec_ms:.3f} ms", file=sys.stderr, flush=True)
@@ -448,6 +478,13 @@ def fidelity_study(args):
     for r in rows:
         print(f"| {r['regime'].split(' (')[0]} | {r['method']} | {r['RelL2']:.4e} | {r['Cos']:.7f} | "
               f"{r['MaxErr']:.4e} | {r['MSE']:.4e} | {r['refresh_ms']:.2f} | {r['codec_ms_8ranks']:.3f} |")
+    print()
+    print("| regime | method | MXFP4 RelL2 | Cos | MaxErr | MSE |")
+    print("|---|---|---|---|---|---|")
+    for r in rows:
+        x = r["mxfp4"]
+        print(f"| {r['regime'].split(' (')[0]} | {r['method']} | {x['RelL2']:.4e} | {x['Cos']:.7f} | "
+              f"{x['MaxErr']:.4e} | {x['MSE']:.4e} |")
     print(json.dumps({"fidelity": rows, "layer": [m, n], "tokens": T}), flush=True)
 
 
@@ -566,9 +603,13 @@ def main():
                     streams[sid].wait_event(ev)    # GIFT encodes need the refreshed factor
                     waited.add((sid, jb.group))
             c = ctxs[sid]
-            gift.encode(c, jb.factor, jb.grads, jb.codes, jb.scales, jb.br, jb.bc,
-                        gift.SCALE_LOCAL if jb.gift_branch else gift.SCALE_SHARED)
-            gift.reduce_local(c, jb.codes, jb.scales, jb.mean, jb.br, jb.bc)
+            if args.format == "mxfp4":
+                gift.encode_mxfp4(c, jb.factor, jb.grads, jb.codes, jb.scales)
+                gift.reduce_local_mxfp4(c, jb.codes, jb.scales, jb.mean)
+            else:
+                gift.encode(c, jb.factor, jb.grads, jb.codes, jb.scales, jb.br, jb.bc,
+                            gift.SCALE_LOCAL if jb.gift_branch else gift.SCALE_SHARED)
+                gift.reduce_local(c, jb.codes, jb.scales, jb.mean, jb.br, jb.bc)
             if jb.gift_branch:
                 gift.decode(c, jb.factor, jb.mean, jb.out)
 
@@ -675,6 +716,7 @@ def main():
         "config": {"workload": f"{wl.name} (config {wl.cfg})", "ranks": wl.N, "rank": wl.rank,
                    "sides": args.sides, "tokens": wl.T,
                    "matrices": sum(len(jb.mats) for jb in jobs), "buckets": len(jobs),
+                   "format": args.format,
                    "factors": sum(1 for jb in jobs if jb.owns_factor), "streams": nstreams,
                    "grad_gb": round(grad_bytes / 1e9, 3), "factor_refresh_every": wl.refresh,
                    "subspace_iters": args.iters},
