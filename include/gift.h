@@ -127,9 +127,10 @@ void gift_ctx_destroy(gift_ctx *ctx);
  * by the caller) on the context stream right after its statistics kernels
  * (A = X^T X / T of every factor side), before the rest of the refresh.
  * Other streams can wait on it to start work once the statistics (the
- * refresh's compute-bound part) are done.  NULL stops the recording.  For the
- * Cholesky-form factors nothing is recorded.  Errors: GIFT_EINVAL for a NULL
- * ctx. */
+ * refresh's compute-bound part) are done.  NULL stops the recording.  The
+ * event must stay valid until it is replaced or unset (the library keeps the
+ * handle, not a copy).  For the Cholesky-form factors nothing is recorded.
+ * Errors: GIFT_EINVAL for a NULL ctx. */
 gift_status gift_ctx_set_statistics_event(gift_ctx *ctx, void *hip_event);
 
 /* Per-kernel timing: when enabled, every launch of a selected kernel family

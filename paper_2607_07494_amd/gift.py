@@ -138,8 +138,10 @@ class Context:
 
     def set_statistics_event(self, event):
         """Record ``event`` (a torch.cuda.Event, or None) after the statistics
-        kernels of every later factor refresh on this context."""
+        kernels of every later factor refresh on this context.  The context
+        keeps a reference to the event so that it outlives the registration."""
         h = None
+        self._stats_event = event
         if event is not None:
             import torch  # noqa: F401
             event.record()          # creates the underlying HIP event
