@@ -51,7 +51,7 @@ FAMILY_SOURCE = {
     "chol_transform": "paper_2607_07494_amd/csrc/k_chol.hip",
     "mxfp4": "paper_2607_07494_amd/csrc/k_mx.hip",
 }
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm-traffic.md")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "llama300m-gradient-set_input_hbm-traffic-per-kernel.md")
 
 HBM_PEAK_GBS = 8000.0
 FP32_MFMA_TFLOPS = 157.3
