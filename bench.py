@@ -290,14 +290,14 @@ def algorithmic_work(wl, jobs, args):
         proj_flops = 2 * e * (ra + rg) + (4 * N * rg * ra * m if ra and rg else 0)
         proj_bytes = 4 * e * ((ra > 0) + (rg > 0))
         if args.format == "mxfp4":
-            add("mxfp4", 0, (4 + mxb) * e)
+            # the MXFP4 pass (on the GIFT branch fused with the rank-r update:
+            # 2r flops/elem), the rank sum; the projections and the decode as
+            # in FP8
+            add("mxfp4", 2 * e * (ra + rg), (4 + mxb) * e)
             add("reduce", 0, mn * (N * mxb + 4))
             if jb.gift_branch:
-                # projections, then W~ = W + the low-rank part stored (float32
-                # products, 8 B/elem, the decode's STORE family) before the
-                # MXFP4 pass; the decode as in FP8
                 add("project", proj_flops, proj_bytes)
-                add("update_store", 2 * (e + mn) * (ra + rg), 8 * (e + mn))
+                add("update_store", 2 * mn * (ra + rg), 8 * mn)
                 add("decode_project", 2 * mn * (ra + rg), 4 * mn * ((ra > 0) + (rg > 0)))
         elif not jb.gift_branch:
             add("amax", 0, 4 * e)

@@ -299,8 +299,10 @@ gift_status gift_encode_hits(gift_ctx *ctx, const gift_factor *f, const float *g
  *   ef     optional residual [N, m, n] in transformed coordinates, read and
  *          rewritten (U = W~ + R; R <- U - Dequantize(codes));
  *   transformed  optional [N, m, n] float32 out: U before quantization.
- * The low-rank transform's products are float32 here (stored, then quantized
- * in a second pass).  n must be a multiple of 32 (GIFT_ESHAPE); grads, ef and
+ * The low-rank transform is computed as in gift_encode (split-bf16 products)
+ * and packed in the same pass when the rank is a multiple of 4 and at most
+ * 128 and one rank's slice has fewer than 2^29 elements; otherwise W~ is
+ * stored with float32 products, then quantized.  n must be a multiple of 32 (GIFT_ESHAPE); grads, ef and
  * transformed 16-byte aligned (GIFT_EINVAL).  Scales are per rank (no
  * shared-scale mode).  Uses the context workspace. */
 gift_status gift_encode_mxfp4(gift_ctx *ctx, const gift_factor *f, const float *grads, int32_t N,

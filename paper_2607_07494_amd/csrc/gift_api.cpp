@@ -943,13 +943,24 @@ gift_status gift_encode_mxfp4(gift_ctx *ctx, const gift_factor *f, const float *
       size_t bytes = 0;
       if ((st = plan_low_rank(ctx, f, grads, N, m, n, false, nullptr, &bytes, &plan)) != GIFT_OK) return st;
       if (plan.active) {
-        void *buf = nullptr;
-        if ((st = grow_buffer(ctx, ctx->xform, sizeof(float) * (size_t)total, &buf)) != GIFT_OK) return st;
         void *ws = nullptr;
         if ((st = workspace(ctx, bytes, &ws)) != GIFT_OK) return st;
         if ((st = plan_low_rank(ctx, f, grads, N, m, n, false, static_cast<char *>(ws), &bytes, &plan)) !=
             GIFT_OK)
           return st;
+        // the split-bf16 update computes W~ (+ R) and packs MXFP4 in one pass
+        TileJob mj = plan.upd;
+        mj.D = grads;
+        mj.ldd = n;
+        mj.dbs = m * n;
+        mj.ef = ef;
+        mj.transformed = transformed;
+        mj.mx_codes = codes;
+        mj.mx_scales = scales;
+        mj.kernel_family = GIFT_KERNEL_MXFP4;
+        if (lr_update_eligible(mj)) return launch_lr_update(ctx, mj);
+        void *buf = nullptr;
+        if ((st = grow_buffer(ctx, ctx->xform, sizeof(float) * (size_t)total, &buf)) != GIFT_OK) return st;
         // W~ = W + the low-rank part, stored (float32 products)
         TileJob job = plan.upd;
         job.C = static_cast<float *>(buf);

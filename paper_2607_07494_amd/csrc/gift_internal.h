@@ -160,7 +160,7 @@ struct Segment {
   int64_t K = 0;
 };
 
-enum Epilogue { EPI_STORE = 0, EPI_AMAX = 1, EPI_QUANT = 2 };
+enum Epilogue { EPI_STORE = 0, EPI_AMAX = 1, EPI_QUANT = 2, EPI_MX = 3 };
 
 // Block maxima are accumulated with atomicMax into kAmaxSlots sub-slots per
 // (rank, block) -- producers pick a slot from their wave id, so no single
@@ -188,6 +188,10 @@ struct TileJob {
   uint32_t *amax = nullptr;
   uint8_t *codes = nullptr;
   uint32_t *hits = nullptr;   // QUANT: boundary-hit counters [batch][2] (upper, lower), accumulated
+  // MXFP4 in the update pass (split-bf16 kernel only): packed codes
+  // [batch][M][N/2] and E8M0 scales [batch][M][N/32]; amax stays null
+  uint8_t *mx_codes = nullptr;
+  uint8_t *mx_scales = nullptr;
   float *scales = nullptr;
   float *transformed = nullptr;
   float *ef = nullptr;

@@ -35,6 +35,7 @@
 
 #include "fp8_e4m3.h"
 #include "gift_internal.h"
+#include "mx_fp4.h"
 #include "xcd_map.h"
 
 namespace gift {
@@ -289,6 +290,8 @@ struct LUArgs {
   uint32_t *clear;
   int64_t clear_words;
   int shared, batch;
+  uint8_t *mx_codes;    // MX: packed E2M1 codes [batch][M][N/2]
+  uint8_t *mx_scales;   // MX: E8M0 scales [batch][M][N/32]
 };
 
 template <int EPI, bool EF, int NSEG, int KC, bool FULL = false>
@@ -502,7 +505,56 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
         const bool uniform = (int64_t)(bi_lo + 1) * p.br > rlast && (int64_t)(bj_lo + 1) * p.bc > clast;
         const int64_t u_gb = (int64_t)bi_lo * p.nbc + bj_lo;
         const int64_t nblk = (int64_t)p.nbr * p.nbc;
-        if (FULL && EPI == EPI_AMAX) {
+        if (EPI == EPI_MX) {
+          // MXFP4: the lanes fr, fr + 16, fr + 32, fr + 48 hold the 32
+          // columns j0 + 32 h .. of row ri[g] (8 each, in t = 2h, 2h + 1)
+          const int64_t nsb = p.N / 32;
+#pragma unroll
+          for (int g = 0; g < 2; ++g)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+              float am = 0.f;
+              int bad = 0;
+#pragma unroll
+              for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  const float a = fabsf(w[g][2 * h + tt][e]);
+                  bad |= !(a <= 3.402823466e38f);
+                  am = a > am ? a : am;
+                }
+#pragma unroll
+              for (int o = 16; o < 64; o <<= 1) {
+                const float u = __shfl_xor(am, o);
+                am = u > am ? u : am;
+                bad |= __shfl_xor(bad, o);
+              }
+              const int k = mx_scale_exp(am, bad);
+              const int64_t cb = j0 + 32 * h;
+              const bool ok = rv[g] && cb < p.N;
+#pragma unroll
+              for (int tt = 0; tt < 2; ++tt) {
+                const int t = 2 * h + tt;
+                const int64_t cj = j0 + 16 * t + 4 * fg;
+                uint32_t pk = 0u;
+                float d[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) pk |= mx_encode(w[g][t][e], k, bad, d[e]) << (4 * e);
+                if (ok) {
+                  const int64_t off = (int64_t)b * MN + ri[g] * p.N + cj;
+                  *reinterpret_cast<uint16_t *>(p.mx_codes + off / 2) = (uint16_t)pk;
+                  if (EF)
+                    *reinterpret_cast<float4 *>(p.ef + off) =
+                        make_float4(w[g][t][0] - d[0], w[g][t][1] - d[1], w[g][t][2] - d[2], w[g][t][3] - d[3]);
+                  if (p.transformed)
+                    *reinterpret_cast<float4 *>(p.transformed + off) =
+                        make_float4(w[g][t][0], w[g][t][1], w[g][t][2], w[g][t][3]);
+                }
+              }
+              if (ok && fg == 0)
+                p.mx_scales[((int64_t)b * p.M + ri[g]) * nsb + cb / 32] = bad ? (uint8_t)255 : (uint8_t)(k + 127);
+            }
+        } else if (FULL && EPI == EPI_AMAX) {
           uint32_t m = 0u;
   #pragma unroll
           for (int g = 0; g < 2; ++g)
@@ -778,7 +830,9 @@ bool lr_quant_reads_raw(const TileJob &j) {
 }
 
 bool lr_update_eligible(const TileJob &j) {
-  if (!j.split3 || j.amax == nullptr || j.nseg < 1 || j.nseg > 2 || j.N % 4 != 0) return false;
+  const bool mx = j.mx_codes != nullptr;
+  if (!j.split3 || (j.amax == nullptr && !mx) || j.nseg < 1 || j.nseg > 2 || j.N % 4 != 0) return false;
+  if (mx && (j.N % 32 != 0 || j.codes != nullptr || (reinterpret_cast<uintptr_t>(j.mx_codes) & 1))) return false;
   if (j.M * j.N >= (1LL << 29)) return false;   // one rank's slice within a 32-bit buffer range
   const int64_t K = j.seg[0].K;
   if (K <= 0 || K > 128 || K % 4 != 0) return false;
@@ -826,6 +880,8 @@ gift_status launch_lr_update(gift_ctx *ctx, const TileJob &j) {
   a.clear_words = a.raw ? j.clear_words : 0;
   a.shared = j.shared ? 1 : 0;
   a.batch = j.batch;
+  a.mx_codes = j.mx_codes;
+  a.mx_scales = j.mx_scales;
   ProfileScope prof(ctx, j.kernel_family);
   const int64_t cols = 64 * upd_tiles(j.nseg * (int)((j.seg[0].K + 31) / 32));
   const dim3 grid((unsigned)((j.N + cols - 1) / cols), (unsigned)((j.M + kUpdRows - 1) / kUpdRows),
@@ -868,7 +924,11 @@ gift_status launch_lr_update(gift_ctx *ctx, const TileJob &j) {
   using F_ = std::false_type;
   using AMAX_ = std::integral_constant<int, EPI_AMAX>;
   using QUANT_ = std::integral_constant<int, EPI_QUANT>;
-  if (!quant) {
+  using MX_ = std::integral_constant<int, EPI_MX>;
+  if (j.mx_codes) {
+    if (ef) by_seg(MX_{}, T_{});
+    else by_seg(MX_{}, F_{});
+  } else if (!quant) {
     if (ef) by_seg(AMAX_{}, T_{});
     else by_seg(AMAX_{}, F_{});
   } else {

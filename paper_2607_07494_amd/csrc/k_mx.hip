@@ -19,6 +19,7 @@
 #include <math.h>
 
 #include "gift_internal.h"
+#include "mx_fp4.h"
 
 namespace gift {
 namespace {
@@ -34,26 +35,6 @@ struct MxArgs {
 };
 
 __device__ __forceinline__ float4 ld4(const float *p) { return *reinterpret_cast<const float4 *>(p); }
-
-// E2M1 magnitude code of |y| (nearest, ties to the even code, saturating)
-__device__ __forceinline__ uint32_t e2m1_mag(float a) {
-  return a <= 0.25f ? 0u : a < 0.75f ? 1u : a <= 1.25f ? 2u : a < 1.75f ? 3u
-       : a <= 2.5f ? 4u : a < 3.5f ? 5u : a <= 5.0f ? 6u : 7u;
-}
-
-__device__ __forceinline__ float e2m1_val(uint32_t mag) {
-  // 0, 0.5, 1, 1.5, 2, 3, 4, 6
-  return mag < 2u ? 0.5f * (float)mag : (mag < 4u ? 1.0f + 0.5f * (float)(mag - 2u)
-                                                  : (mag < 6u ? 2.0f + (float)(mag - 4u) : (mag == 6u ? 4.0f : 6.0f)));
-}
-
-// floor(log2(a)) of a finite a > 0 from its bits (subnormals included)
-__device__ __forceinline__ int floor_log2(float a) {
-  const uint32_t b = __float_as_uint(a);
-  const int e = (int)(b >> 23);
-  if (e > 0) return e - 127;
-  return -149 + (31 - __clz((int)(b & 0x7fffffu)));
-}
 
 __global__ __launch_bounds__(256) void mx_quant_kernel(const MxArgs a) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -89,22 +70,11 @@ __global__ __launch_bounds__(256) void mx_quant_kernel(const MxArgs a) {
       am = u > am ? u : am;
       bad |= __shfl_xor(bad, o);
     }
-    int k = -127;
-    if (!bad && am > 0.f) {
-      k = floor_log2(am) - 2;
-      k = k < -127 ? -127 : k;
-    }
+    const int k = mx_scale_exp(am, bad);
     uint32_t packed = 0u;
     float deq[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float y = ldexpf(v[i], -k);
-      const uint32_t mag = bad ? 0u : e2m1_mag(fabsf(y));
-      const uint32_t c = bad ? 0u : (mag | (signbit(v[i]) ? 8u : 0u));
-      packed |= c << (4 * i);
-      const float d = ldexpf(e2m1_val(mag), k);
-      deq[i] = bad ? __int_as_float(0x7fc00000) : (signbit(v[i]) ? -d : d);
-    }
+    for (int i = 0; i < 8; ++i) packed |= mx_encode(v[i], k, bad, deq[i]) << (4 * i);
     *reinterpret_cast<uint32_t *>(a.codes + e / 2) = packed;
     if ((g & 3) == 0) a.scales[e / 32] = bad ? (uint8_t)255 : (uint8_t)(k + 127);
     if (a.ef) {

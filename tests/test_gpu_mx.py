@@ -119,8 +119,12 @@ def chol(ctx, m, n, block, seed):
     return f, fA
 
 
-@pytest.mark.parametrize("kind,N,m,n,r", [("lowrank", 4, 200, 512, 64), ("lowrank", 2, 96, 256, 16),
-                                          ("chol", 2, 64, 256, 32), ("chol", 3, 48, 128, 0)])
+@pytest.mark.parametrize("kind,N,m,n,r", [
+    ("lowrank", 4, 200, 512, 64),    # MXFP4 inside the split-bf16 update pass, ragged rows
+    ("lowrank", 2, 96, 256, 16),
+    ("lowrank", 2, 70, 160, 32),     # last 64-column tile half past n
+    ("lowrank", 2, 64, 128, 6),      # rank not a multiple of 4: W~ stored, then quantized
+    ("chol", 2, 64, 256, 32), ("chol", 3, 48, 128, 0)])
 def test_transform_mxfp4_round_trip(ctx, kind, N, m, n, r):
     say(f"mxfp4 {kind} N={N} m={m} n={n} r/block={r}")
     grads = gradient_set(400 + m, 401 + n, N, m, n)
