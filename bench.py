@@ -61,7 +61,9 @@ BF16_MFMA_TFLOPS = 2500.0
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default 10, or one full refresh period when the "
+                         "factors are refreshed less often than every step)")
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=4, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--sides", choices=["input", "both"], default="input")
@@ -509,6 +511,8 @@ def main():
     ctx = gift.Context()
     ctx_holder["ctx"] = ctx
     wl, jobs = build_workload(args, torch, gift, synth, dev)
+    if args.steps is None:
+        args.steps = 10 if wl.refresh <= 1 else wl.refresh
     torch.cuda.synchronize()
     print(f"[bench] workload {wl.name}: {sum(len(j.mats) for j in jobs)} matrices in "
           f"{len(jobs)} buckets, "
@@ -571,12 +575,14 @@ def main():
             ev.record(st)
             main.wait_event(ev)
 
-    def step(iters, serial=False):
+    def step(iters, serial=False, refresh=True, codec=True):
+        """One step; refresh=False reuses the factors of the last refresh
+        (the cadence's other steps), codec=False runs the refresh alone."""
         join_into_main()           # the refresh rewrites factors the last step's encodes read
         joined = torch.cuda.Event()
         joined.record(main)
         ready = {}
-        for k in gorder:
+        for k in (gorder if refresh else ()):
             sid = 0 if serial else gsid[k]
             if sid != 0:
                 streams[sid].wait_event(joined)
@@ -586,18 +592,18 @@ def main():
             ready[k] = (sid, torch.cuda.Event())
             ready[k][1].record(streams[sid])
         waited = set()
-        for jb in order:
+        for jb in (order if codec else ()):
             sid = 0 if serial else jb.sid
-            if not jb.gift_branch and args.issue == "euclid-after-refresh" and not serial and gorder:
+            if not jb.gift_branch and args.issue == "euclid-after-refresh" and not serial and ready:
                 rsid, ev = ready[gorder[-1]]
                 if rsid != sid and (sid, None) not in waited:
                     streams[sid].wait_event(ev)
                     waited.add((sid, None))
-            if not jb.gift_branch and stats_ev is not None and not serial:
+            if not jb.gift_branch and stats_ev is not None and not serial and ready:
                 if gsid[gorder[-1]] != sid and (sid, None) not in waited:
                     streams[sid].wait_event(stats_ev)
                     waited.add((sid, None))
-            if jb.gift_branch:
+            if jb.gift_branch and jb.group in ready:
                 rsid, ev = ready[jb.group]
                 if rsid != sid and (sid, jb.group) not in waited:
                     streams[sid].wait_event(ev)    # GIFT encodes need the refreshed factor
@@ -636,15 +642,19 @@ def main():
 
     # untimed breakdown on the main stream alone (isolated kernel times): every
     # kernel family bracketed by events; the largest is the dominant family
-    profile_all(True, None, reset=True)
+    # kernel family bracketed by events; the refresh and the codec passes are
+    # timed apart and the refresh is amortised over its cadence
     nb = max(args.breakdown_steps, 1)
-    for s in range(nb):
-        step(args.iters, serial=True)
     fam_ms = {}
-    for name in gift.KERNELS:
-        launches, ms = read_all(name)
-        if launches:
-            fam_ms[name] = (launches / nb, ms / nb)
+    for refresh, codec, weight in ((True, False, 1.0 / wl.refresh), (False, True, 1.0)):
+        profile_all(True, None, reset=True)
+        for s in range(nb):
+            step(args.iters, serial=True, refresh=refresh, codec=codec)
+        for name in gift.KERNELS:
+            launches, ms = read_all(name)
+            if launches:
+                l0, m0 = fam_ms.get(name, (0.0, 0.0))
+                fam_ms[name] = (l0 + weight * launches / nb, m0 + weight * ms / nb)
     profile_all(False)
     dom = max(fam_ms, key=lambda k: fam_ms[k][1])
 
@@ -655,7 +665,7 @@ def main():
     t0 = time.perf_counter()
     start.record(main)
     for s in range(args.steps):
-        step(args.iters)
+        step(args.iters, refresh=s % wl.refresh == 0)
     join_into_main()
     stop.record(main)
     enqueue = time.perf_counter() - t0   # host time to issue the timed steps
@@ -719,6 +729,7 @@ def main():
                    "format": args.format,
                    "factors": sum(1 for jb in jobs if jb.owns_factor), "streams": nstreams,
                    "grad_gb": round(grad_bytes / 1e9, 3), "factor_refresh_every": wl.refresh,
+                   "refreshes_timed": sum(1 for s in range(args.steps) if s % wl.refresh == 0),
                    "subspace_iters": args.iters},
         "transform_tflops": round(tf_flops / (tf_ms * 1e-3) / 1e12, 3) if tf_ms else None,
         "roofline": roof,

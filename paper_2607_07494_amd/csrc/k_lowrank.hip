@@ -294,8 +294,8 @@ struct LUArgs {
   uint8_t *mx_scales;   // MX: E8M0 scales [batch][M][N/32]
 };
 
-template <int EPI, bool EF, int NSEG, int KC, bool FULL = false>
-__global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) {
+template <int EPI, bool EF, int NSEG, int KC, bool FULL>
+__device__ __forceinline__ void lr_update_body(const LUArgs &p) {
   static_assert(!FULL || EPI != EPI_STORE, "FULL is an AMAX / QUANT variant");
   constexpr int NCH = NSEG * KC;                // 32-step chunks over all segments
   constexpr int TSLOTS = NCH * 64 * 4;          // (chunk, column, fg) entries of a 64-column tile
@@ -748,6 +748,27 @@ __global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) 
   if (EPI == EPI_QUANT && p.hits) e4m3_flush_hits(p.hits + 2 * (int64_t)b, hit_up, hit_lo);
 }
 
+template <int EPI, bool EF, int NSEG, int KC, bool FULL = false>
+__global__ __launch_bounds__(kUpdThreads) void lr_update_kernel(const LUArgs p) {
+  lr_update_body<EPI, EF, NSEG, KC, FULL>(p);
+}
+
+// The same kernel held to two waves per SIMD (at most 256 VGPRs + AGPRs per
+// lane).  From 128 contraction steps on (rank-128 transforms) the unbounded
+// build takes one wave per SIMD, which leaves the loads of a wave's tiles
+// with nothing to hide behind; two workgroups per CU still fit in LDS.
+// Variants (epilogue, residual, 32-step chunks, branch-free) built for two
+// waves per SIMD: 4-6 chunks without a residual, the ones that fit 256 VGPRs
+// with no scratch (the branch-free AMAX pass at 4 chunks does not).
+constexpr bool upd_two_waves(int epi, bool ef, int nch, bool full) {
+  return epi != EPI_MX && !ef && nch >= 4 && nch <= 6 && !(epi == EPI_AMAX && full && nch == 4);
+}
+template <int EPI, bool EF, int NSEG, int KC, bool FULL = false>
+__global__ __launch_bounds__(kUpdThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void lr_update_kernel_o2(
+    const LUArgs p) {
+  lr_update_body<EPI, EF, NSEG, KC, FULL>(p);
+}
+
 bool al16(const void *q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; }
 
 }  // namespace
@@ -896,17 +917,27 @@ gift_status launch_lr_update(gift_ctx *ctx, const TileJob &j) {
                     (!quant || (a.raw != nullptr && a.codes_wide && j.N % cols == 0));
   auto go = [&](auto epi_c, auto ef_c, auto nseg_c, auto kc_c) {
     constexpr int E = decltype(epi_c)::value;
+    constexpr bool EFv = decltype(ef_c)::value;
+    constexpr int NS = decltype(nseg_c)::value, KCv = decltype(kc_c)::value;
     if constexpr (E == EPI_AMAX || E == EPI_QUANT) {
       if (full) {
-        hipLaunchKernelGGL((lr_update_kernel<E, decltype(ef_c)::value, decltype(nseg_c)::value,
-                                             decltype(kc_c)::value, true>),
-                           grid, dim3(kUpdThreads), 0, ctx->stream, a);
-        return;
+        if constexpr (upd_two_waves(E, EFv, NS * KCv, true)) {
+          hipLaunchKernelGGL((lr_update_kernel_o2<E, EFv, NS, KCv, true>), grid, dim3(kUpdThreads), 0,
+                             ctx->stream, a);
+          return;
+        } else if constexpr (!upd_two_waves(E, EFv, NS * KCv, false)) {
+          hipLaunchKernelGGL((lr_update_kernel<E, EFv, NS, KCv, true>), grid, dim3(kUpdThreads), 0,
+                             ctx->stream, a);
+          return;
+        }
+        // else: the general variant at two waves per SIMD beats the
+        // branch-free one at one
       }
     }
-    hipLaunchKernelGGL((lr_update_kernel<E, decltype(ef_c)::value, decltype(nseg_c)::value,
-                                         decltype(kc_c)::value>),
-                       grid, dim3(kUpdThreads), 0, ctx->stream, a);
+    if constexpr (upd_two_waves(E, EFv, NS * KCv, false))
+      hipLaunchKernelGGL((lr_update_kernel_o2<E, EFv, NS, KCv>), grid, dim3(kUpdThreads), 0, ctx->stream, a);
+    else
+      hipLaunchKernelGGL((lr_update_kernel<E, EFv, NS, KCv>), grid, dim3(kUpdThreads), 0, ctx->stream, a);
   };
   auto by_k = [&](auto epi_c, auto ef_c, auto nseg_c) {
     switch (kc) {
