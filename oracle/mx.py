@@ -26,7 +26,9 @@ Pins (tests/test_oracle_mx.py): the E2M1 values from the bit-field formula,
 brute-force nearest-value rounding at every midpoint, scale closed forms
 (amax 6 -> X = 1, amax 8 -> X = 2, saturation between 6 and 8), zero and
 NaN blocks, and the quantization error bound (half an E2M1 grid step of the
-scaled value) below saturation, packing and exact rank sums.
+scaled value) below saturation, packing and exact rank sums; the residual by
+its exactness (deq + R == U in float32, by Sterbenz's lemma), its half-step
+bound and NaN residuals of NaN / Inf blocks.
 """
 
 from __future__ import annotations

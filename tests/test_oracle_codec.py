@@ -211,6 +211,30 @@ def test_block_grid_partial_edges():
     assert am[1, 2, 2] == Wt[1, 4, 6] and am[0, 0, 0] == Wt[0, 1, 2]
 
 
+def test_block_amax_nan_wins():
+    # A NaN anywhere in a block makes that block's maximum NaN (and with it
+    # the scale and every code of the block), so a NaN gradient cannot pass
+    # as a finite one.  A maximum that skips NaN (np.nanmax) fails this.
+    Wt = np.arange(2 * 4 * 6, dtype=np.float32).reshape(2, 4, 6) - 20.0
+    Wt[1, 3, 1] = np.nan
+    am = codec.block_amax(Wt, 2, 3)
+    assert np.isnan(am[1, 1, 0])
+    finite = ~np.isnan(am)
+    assert finite.sum() == am.size - 1
+    # the other blocks keep their plain maxima of |x|
+    assert am[1, 1, 1] == np.abs(Wt[1, 2:4, 3:6]).max()
+    assert am[0, 0, 0] == 20.0 and am[1, 0, 0] == np.abs(Wt[1, 0:2, 0:3]).max()
+    s, inv = codec.scales_from_amax(am)
+    assert np.isnan(s[1, 1, 0])
+    codes = codec.quantize_blocks(Wt, inv, 2, 3)
+    assert np.all(codes[1, 2:4, 0:3] & 0x7F == 0x7F)    # every code of the block is NaN
+    # an infinity is an ordinary maximum: inf amax, scale inf, multiplier 0
+    Wi = np.ones((1, 2, 2), np.float32)
+    Wi[0, 0, 0] = -np.inf
+    ai = codec.block_amax(Wi)
+    assert np.isposinf(ai[0, 0, 0])
+
+
 def test_scale_edge_cases():
     s, inv = codec.scales_from_amax(np.array([0.0, 448.0, np.inf, 1e-40], dtype=np.float32))
     assert s[0] == 0 and inv[0] == 0

@@ -83,3 +83,67 @@ def test_pack_and_rank_sum():
     codes[:, 0, 0] = [2, 4, 7]          # 1, 2, 6 at scale 2^0
     scales = np.full((3, 1, 1), 127, np.uint8)
     assert mx.reduce_local(codes, scales)[0, 0] == np.float32(3.0)
+
+
+def _e2m1_half_step(a):
+    """Half the distance to the next E2M1 magnitude above |a| (scaled units):
+    grid 0, 0.5, 1, 1.5, 2, 3, 4, 6, written out from the format's fields
+    (spacing 0.5 below 2, 1 from 2 to 4, 2 from 4 to 6)."""
+    a = np.abs(a)
+    return np.where(a < 2.0, 0.25, np.where(a < 4.0, 0.5, 1.0))
+
+
+def test_residual_is_exact_by_sterbenz():
+    # Error feedback keeps R = fl32(U - deq).  Below saturation deq is U
+    # rounded to the nearest grid value, which lies within a factor 2 of U
+    # (or is 0, and then R = U); above it deq = 6 X and U < 8 X (X is the
+    # block's power-of-two scale), again within a factor 2.  So by Sterbenz
+    # the subtraction is exact: deq + R == U with no rounding anywhere.
+    rng = np.random.default_rng(11)
+    U = (rng.standard_normal((3, 4, 128)) * np.exp(rng.uniform(-30, 30, (3, 4, 1)))).astype(np.float32)
+    U[0, 0, :32] = np.float32(2.0 ** -130)      # subnormal block: X = 2^-127 floor
+    U[1, 2, 32:64] = np.clip(U[1, 2, 32:64], -0.1, 0.1)
+    U[1, 2, 40] = np.float32(7.5 * 2.0 ** -3)   # block max 7.5 X with X = 2^-3: saturates
+    U[2, 1, 64:96] = 0.0
+    codes, scales = mx.quantize(U)
+    deq = mx.dequantize(codes, scales)
+    R = mx.residual(U, codes, scales)
+    assert R.dtype == np.float32
+    np.testing.assert_array_equal(deq.astype(np.float64) + R.astype(np.float64), U.astype(np.float64))
+    # the zero block leaves a zero residual; the saturated element leaves
+    # U - 6 X, at most a third of U
+    assert np.all(R[2, 1, 64:96] == 0)
+    X = np.ldexp(1.0, scales.astype(np.int64) - 127)
+    Xe = np.repeat(X, 32, axis=-1)
+    sat = np.abs(U) > 6 * Xe
+    assert sat[1, 2, 40]
+    assert np.all(np.abs(R[sat]) < np.abs(U[sat]) / 3)
+
+
+def test_residual_is_within_half_a_grid_step_below_saturation():
+    rng = np.random.default_rng(12)
+    U = (rng.uniform(-1, 1, (2, 8, 64)) * np.exp(rng.uniform(-8, 8, (2, 8, 1)))).astype(np.float32)
+    codes, scales = mx.quantize(U)
+    R = mx.residual(U, codes, scales).astype(np.float64)
+    X = np.repeat(np.ldexp(1.0, scales.astype(np.int64) - 127), 32, axis=-1)
+    y = U.astype(np.float64) / X                     # scaled value, exact (X a power of two)
+    unsat = np.abs(y) <= 6.0
+    assert unsat.mean() > 0.9
+    # |R| <= half the grid spacing at the scaled value, times X; a residual
+    # of the wrong sign or a dropped scale would break this or the identity
+    # of the previous test
+    assert np.all(np.abs(R[unsat]) <= _e2m1_half_step(y[unsat]) * X[unsat])
+    # and it is the signed remainder: deq = U - R is a grid value times X
+    grid = np.array([0, 0.5, 1, 1.5, 2, 3, 4, 6], dtype=np.float64)
+    g = np.abs((U.astype(np.float64) - R) / X)
+    assert np.all(np.min(np.abs(g[..., None] - grid), axis=-1) == 0)
+
+
+def test_residual_of_a_nan_block_is_nan():
+    U = np.ones((1, 1, 64), np.float32)
+    U[0, 0, 3] = np.nan
+    U[0, 0, 40] = np.inf
+    codes, scales = mx.quantize(U)
+    R = mx.residual(U, codes, scales)
+    assert np.all(np.isnan(R[0, 0, :32]))        # NaN scale: every element NaN
+    assert np.all(np.isnan(R[0, 0, 32:64]))      # inf block: NaN scale as well
