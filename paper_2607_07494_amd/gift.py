@@ -2,10 +2,13 @@
 
 Argument marshalling only: every computation runs in the library's HIP
 kernels.  Tensors are torch tensors on the GPU (device memory and streams are
-all torch is used for); the wrappers check dtype, device and contiguity, pass
-``data_ptr()`` and raise :class:`GiftError` with the library's message when a
-call fails.  There is no fallback: if ``libgift.so`` is missing, importing
-this module raises.
+all torch is used for); the wrappers check every tensor's shape against the
+sizes the call is given (the library sizes its loops and buffer ranges from
+those sizes, so a short tensor would be read or written out of bounds), then
+dtype, device and contiguity, pass ``data_ptr()`` and raise
+:class:`GiftError` with the library's message when a call fails.  A shape
+mismatch raises ``ValueError`` before anything is enqueued.  There is no
+fallback: if ``libgift.so`` is missing, importing this module raises.
 """
 
 from __future__ import annotations
@@ -109,6 +112,23 @@ def _ptr(t, dtype=None, name="tensor"):
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     return ctypes.c_void_p(t.data_ptr())
+
+
+def _expect(t, shape, name):
+    """Raise ValueError unless tensor ``t`` (may be None) has exactly ``shape``."""
+    if t is None:
+        return
+    got = tuple(getattr(t, "shape", ()))
+    if got != tuple(int(d) for d in shape):
+        raise ValueError(f"{name} must have shape {tuple(int(d) for d in shape)}, not {got}")
+
+
+def _dims(t, k, name):
+    """The shape of ``t``, which must be a ``k``-dimensional tensor."""
+    shape = tuple(getattr(t, "shape", ()))
+    if len(shape) != k:
+        raise ValueError(f"{name} must be {k}-dimensional, not of shape {shape}")
+    return shape
 
 
 def scale_grid(m: int, n: int, block_rows: int = 0, block_cols: int = 0):
@@ -218,6 +238,7 @@ class Factor:
         for t, nm in ((acts, "acts"), (out_grads, "out_grads")):
             if t is not None and (t.dim() != 2 or t.shape[0] != T or t.dtype != x.dtype):
                 raise ValueError(f"{nm} must be [T, dim] with the common T and dtype")
+        _check_stats_inputs(self, acts, out_grads, T)
         _check(LIB.gift_factor_update(self.ctx.handle, self._h, _ptr(acts, None, "acts"),
                                       _ptr(out_grads, None, "out_grads"), T, dt, iters))
 
@@ -236,6 +257,13 @@ class Factor:
     def import_(self, side: int, U, c_fwd, c_inv, sigma2):
         import torch
         f = torch.float32
+        if side not in (SIDE_INPUT, SIDE_OUTPUT):
+            raise ValueError("side must be SIDE_INPUT or SIDE_OUTPUT")
+        dim = self.n if side == SIDE_INPUT else self.m
+        _expect(U, (dim, self.rank), "U")
+        _expect(c_fwd, (self.rank,), "c_fwd")
+        _expect(c_inv, (self.rank,), "c_inv")
+        _expect(sigma2, (1,), "sigma2")
         _check(LIB.gift_factor_import(self.ctx.handle, self._h, side, _ptr(U, f, "U"),
                                       _ptr(c_fwd, f, "c_fwd"), _ptr(c_inv, f, "c_inv"),
                                       _ptr(sigma2, f, "sigma2")))
@@ -302,6 +330,20 @@ def _stats_dtype(x):
     raise TypeError("statistics inputs must be float32 or bfloat16")
 
 
+def _check_stats_inputs(factor, acts, out_grads, T):
+    """acts [T, n] for a factor with the input side, out_grads [T, m] for one
+    with the output side (the refresh reads T x dim values of each)."""
+    sides = getattr(factor, "sides", 0)
+    if sides & SIDE_INPUT:
+        if acts is None:
+            raise ValueError("acts is required for a factor with the input side")
+        _expect(acts, (T, factor.n), "acts")
+    if sides & SIDE_OUTPUT:
+        if out_grads is None:
+            raise ValueError("out_grads is required for a factor with the output side")
+        _expect(out_grads, (T, factor.m), "out_grads")
+
+
 def factor_update_batch(ctx: Context, factors, acts=None, out_grads=None, iters: int = 4):
     """``gift_factor_update_batch``: refresh many factors in one launch sequence.
 
@@ -322,6 +364,8 @@ def factor_update_batch(ctx: Context, factors, acts=None, out_grads=None, iters:
     for x in tensors:
         if x.dim() != 2 or x.shape[0] != T or _stats_dtype(x) != dt:
             raise ValueError("statistics inputs must be [T, dim] with a common T and dtype")
+    for f, a, g in zip(factors, acts, out_grads):
+        _check_stats_inputs(f, a, g, T)
     arr = ctypes.c_void_p * count
     fa = arr(*[f.handle.value for f in factors])
     aa = arr(*[(_ptr(x).value if x is not None else None) for x in acts])
@@ -350,7 +394,14 @@ def encode(ctx: Context, factor, grads, codes, scales, block_rows: int = 0, bloc
     added to it.
     """
     import torch
-    N, m, n = grads.shape
+    N, m, n = _dims(grads, 3, "grads")
+    if factor is not None and (factor.m, factor.n) != (m, n):
+        raise ValueError(f"the factor was created for {factor.m} x {factor.n}, not {m} x {n}")
+    _expect(codes, (N, m, n), "codes")
+    _expect(scales, (N,) + scale_grid(m, n, block_rows, block_cols), "scales")
+    _expect(ef, (N, m, n), "ef")
+    _expect(transformed, (N, m, n), "transformed")
+    _expect(hits, (N, 2), "hits")
     args = [ctx.handle, factor.handle if factor is not None else None,
             _ptr(grads, torch.float32, "grads"), N, m, n, block_rows, block_cols,
             mode, _ptr(ef, torch.float32, "ef"), _ptr(codes, torch.uint8, "codes"),
@@ -358,15 +409,15 @@ def encode(ctx: Context, factor, grads, codes, scales, block_rows: int = 0, bloc
     if hits is None:
         _check(LIB.gift_encode(*args))
         return
-    if tuple(hits.shape) != (N, 2):
-        raise ValueError(f"hits must have shape ({N}, 2), not {tuple(hits.shape)}")
     _check(LIB.gift_encode_hits(*args, _ptr(hits, torch.int32, "hits")))
 
 
 def reduce_local(ctx: Context, codes, scales, mean, block_rows: int = 0, block_cols: int = 0):
     """``gift_reduce_local``: codes [N, m, n], scales -> mean [m, n] f32."""
     import torch
-    N, m, n = codes.shape
+    N, m, n = _dims(codes, 3, "codes")
+    _expect(scales, (N,) + scale_grid(m, n, block_rows, block_cols), "scales")
+    _expect(mean, (m, n), "mean")
     _check(LIB.gift_reduce_local(ctx.handle, _ptr(codes, torch.uint8, "codes"),
                                  _ptr(scales, torch.float32, "scales"), N, m, n, block_rows,
                                  block_cols, _ptr(mean, torch.float32, "mean")))
@@ -376,7 +427,15 @@ def encode_mxfp4(ctx: Context, factor, grads, codes, scales, ef=None, transforme
     """``gift_encode_mxfp4``: grads [N, m, n] f32 -> codes [N, m, n/2] u8 (packed
     E2M1), scales [N, m, n/32] u8 (E8M0)."""
     import torch
-    N, m, n = grads.shape
+    N, m, n = _dims(grads, 3, "grads")
+    if factor is not None and (factor.m, factor.n) != (m, n):
+        raise ValueError(f"the factor was created for {factor.m} x {factor.n}, not {m} x {n}")
+    if n % 32:
+        raise ValueError("MXFP4 needs n to be a multiple of 32")
+    _expect(codes, (N, m, n // 2), "codes")
+    _expect(scales, (N, m, n // 32), "scales")
+    _expect(ef, (N, m, n), "ef")
+    _expect(transformed, (N, m, n), "transformed")
     _check(LIB.gift_encode_mxfp4(ctx.handle, factor.handle if factor is not None else None,
                                  _ptr(grads, torch.float32, "grads"), N, m, n, _ptr(ef, torch.float32, "ef"),
                                  _ptr(codes, torch.uint8, "codes"), _ptr(scales, torch.uint8, "scales"),
@@ -386,7 +445,11 @@ def encode_mxfp4(ctx: Context, factor, grads, codes, scales, ef=None, transforme
 def reduce_local_mxfp4(ctx: Context, codes, scales, mean):
     """``gift_reduce_local_mxfp4``: codes [N, m, n/2], scales [N, m, n/32] -> mean [m, n] f32."""
     import torch
-    N, m, half = codes.shape
+    N, m, half = _dims(codes, 3, "codes")
+    if (2 * half) % 32:
+        raise ValueError("MXFP4 needs n = 2 * codes.shape[2] to be a multiple of 32")
+    _expect(scales, (N, m, 2 * half // 32), "scales")
+    _expect(mean, (m, 2 * half), "mean")
     _check(LIB.gift_reduce_local_mxfp4(ctx.handle, _ptr(codes, torch.uint8, "codes"),
                                        _ptr(scales, torch.uint8, "scales"), N, m, 2 * half,
                                        _ptr(mean, torch.float32, "mean")))
@@ -395,6 +458,9 @@ def reduce_local_mxfp4(ctx: Context, codes, scales, mean):
 def decode(ctx: Context, factor, mean, out):
     """``gift_decode``: inverse transform of the rank mean [m, n] f32 into out."""
     import torch
-    m, n = mean.shape
+    m, n = _dims(mean, 2, "mean")
+    if factor is not None and (factor.m, factor.n) != (m, n):
+        raise ValueError(f"the factor was created for {factor.m} x {factor.n}, not {m} x {n}")
+    _expect(out, (m, n), "out")
     _check(LIB.gift_decode(ctx.handle, factor.handle if factor is not None else None,
                            _ptr(mean, torch.float32, "mean"), m, n, _ptr(out, torch.float32, "out")))

@@ -177,3 +177,107 @@ def test_one_hip_runtime_in_the_process():
     maps = open("/proc/self/maps").read().split("\n")
     hip = {line.split()[-1] for line in maps if "libamdhip64" in line}
     assert len(hip) == 1, hip
+
+
+# ---------------------------------------------------------------- binding shape checks
+# The wrappers check every tensor's shape before any pointer is passed: the
+# library sizes its loops and buffer ranges from m, n, N and the factor's
+# dims, so a short tensor would be an out-of-bounds device access.  These run
+# on CPU tensors (the shape check comes before the device check) and a
+# stand-in factor object, so nothing reaches the library.
+
+def _fake_factor(m, n, rank=4, sides=gift.SIDE_INPUT):
+    import types
+    return types.SimpleNamespace(m=m, n=n, rank=rank, sides=sides, handle=FAKE)
+
+
+def _z(*shape, dtype=None):
+    import torch
+    return torch.zeros(shape, dtype=dtype or torch.float32)
+
+
+def test_binding_encode_shape_checks(ctx):
+    import torch
+    g = _z(2, 6, 8)
+    u8 = torch.uint8
+    good = dict(codes=_z(2, 6, 8, dtype=u8), scales=_z(2, 1, 1))
+    bad_cases = [
+        dict(good, codes=_z(2, 6, 7, dtype=u8)),
+        dict(good, codes=_z(1, 6, 8, dtype=u8)),
+        dict(good, scales=_z(2, 1, 2)),
+        dict(good, ef=_z(2, 6, 4)),
+        dict(good, transformed=_z(2, 5, 8)),
+    ]
+    for kw in bad_cases:
+        with pytest.raises(ValueError, match="must have shape"):
+            gift.encode(ctx, None, g, **kw)
+    with pytest.raises(ValueError, match="must have shape"):   # per-block scale grid
+        gift.encode(ctx, None, g, good["codes"], _z(2, 1, 1), 0, 4)
+    with pytest.raises(ValueError, match="3-dimensional"):
+        gift.encode(ctx, None, _z(6, 8), **good)
+    with pytest.raises(ValueError, match="created for"):
+        gift.encode(ctx, _fake_factor(6, 9), g, **good)
+    with pytest.raises(ValueError, match="must have shape"):
+        gift.encode(ctx, None, g, **good, hits=torch.zeros((3, 2), dtype=torch.int32))
+
+
+def test_binding_reduce_decode_shape_checks(ctx):
+    import torch
+    codes = _z(3, 6, 8, dtype=torch.uint8)
+    with pytest.raises(ValueError, match="scales"):
+        gift.reduce_local(ctx, codes, _z(3, 1, 2), _z(6, 8))
+    with pytest.raises(ValueError, match="scales"):
+        gift.reduce_local(ctx, codes, _z(2, 1, 1), _z(6, 8))
+    with pytest.raises(ValueError, match="mean"):
+        gift.reduce_local(ctx, codes, _z(3, 1, 1), _z(6, 7))
+    with pytest.raises(ValueError, match="out"):
+        gift.decode(ctx, None, _z(6, 8), _z(8, 6))
+    with pytest.raises(ValueError, match="created for"):
+        gift.decode(ctx, _fake_factor(8, 6), _z(6, 8), _z(6, 8))
+    with pytest.raises(ValueError, match="2-dimensional"):
+        gift.decode(ctx, None, _z(1, 6, 8), _z(6, 8))
+
+
+def test_binding_mxfp4_shape_checks(ctx):
+    import torch
+    u8 = torch.uint8
+    g = _z(2, 4, 64)
+    with pytest.raises(ValueError, match="codes"):
+        gift.encode_mxfp4(ctx, None, g, _z(2, 4, 64, dtype=u8), _z(2, 4, 2, dtype=u8))
+    with pytest.raises(ValueError, match="scales"):
+        gift.encode_mxfp4(ctx, None, g, _z(2, 4, 32, dtype=u8), _z(2, 4, 1, dtype=u8))
+    with pytest.raises(ValueError, match="ef"):
+        gift.encode_mxfp4(ctx, None, g, _z(2, 4, 32, dtype=u8), _z(2, 4, 2, dtype=u8), ef=_z(2, 4, 32))
+    with pytest.raises(ValueError, match="multiple of 32"):
+        gift.encode_mxfp4(ctx, None, _z(2, 4, 48), _z(2, 4, 24, dtype=u8), _z(2, 4, 1, dtype=u8))
+    with pytest.raises(ValueError, match="scales"):
+        gift.reduce_local_mxfp4(ctx, _z(2, 4, 32, dtype=u8), _z(2, 4, 1, dtype=u8), _z(4, 64))
+    with pytest.raises(ValueError, match="mean"):
+        gift.reduce_local_mxfp4(ctx, _z(2, 4, 32, dtype=u8), _z(2, 4, 2, dtype=u8), _z(4, 32))
+
+
+def test_binding_factor_input_shape_checks(ctx):
+    import torch
+    bf = torch.bfloat16
+    fi = _fake_factor(6, 8, sides=gift.SIDE_INPUT)
+    fb = _fake_factor(6, 8, sides=gift.SIDE_BOTH)
+    # acts must be [T, n], out_grads [T, m]
+    with pytest.raises(ValueError, match="acts"):
+        gift._check_stats_inputs(fi, _z(16, 6, dtype=bf), None, 16)
+    with pytest.raises(ValueError, match="out_grads"):
+        gift._check_stats_inputs(fb, _z(16, 8, dtype=bf), _z(16, 8, dtype=bf), 16)
+    with pytest.raises(ValueError, match="out_grads is required"):
+        gift._check_stats_inputs(fb, _z(16, 8, dtype=bf), None, 16)
+    gift._check_stats_inputs(fb, _z(16, 8, dtype=bf), _z(16, 6, dtype=bf), 16)   # fine
+    with pytest.raises(ValueError, match="acts"):
+        gift.factor_update_batch(ctx, [fi, fi], [_z(16, 8, dtype=bf), _z(16, 7, dtype=bf)], None)
+    # Factor.update and import_ go through the same checks
+    f = gift.Factor.__new__(gift.Factor)
+    f.ctx, f.m, f.n, f.rank, f.sides, f._h = ctx, 6, 8, 4, gift.SIDE_BOTH, FAKE
+    with pytest.raises(ValueError, match="out_grads"):
+        f.update(acts=_z(16, 8, dtype=bf), out_grads=_z(16, 8, dtype=bf))
+    with pytest.raises(ValueError, match="U must have shape"):
+        f.import_(gift.SIDE_OUTPUT, _z(8, 4), _z(4), _z(4), _z(1))
+    with pytest.raises(ValueError, match="c_inv"):
+        f.import_(gift.SIDE_INPUT, _z(8, 4), _z(4), _z(3), _z(1))
+    f._h = ctypes.c_void_p()   # nothing to destroy
