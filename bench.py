@@ -6,10 +6,19 @@ transform), the encode of every matrix (transform + amax + FP8 E4M3 for the
 GIFT matrices, amax + FP8 for the Euclidean ones), the local rank sum and the
 inverse transform.  Inputs are resident in HBM before the timed region.
 
-Default workload: the Llama-300M-like gradient set (24 layers, hidden 1024,
-MLP 2816, vocab 32000; 8 simulated ranks; GIFT on gate/up/down with rank 64,
-Euclidean with a shared scale on q/k/v/o, embedding and LM head; factor
-refresh every step from 16384 bf16 tokens).
+Default workload: the Llama-600M-like gradient set, the largest of the five
+workloads (24 layers, hidden 1536, MLP 4096; 16 simulated ranks; the GIFT
+transform with rank 128 on every projection; per-128-column-block FP8 scales;
+factors from 32768 bf16 tokens refreshed every 50 steps, Sec. V-E).
+``--config 4`` is the Llama-300M-like set (8 ranks, rank 64 on gate/up/down,
+Euclidean with a shared scale on q/k/v/o, embedding and LM head; refresh
+every step), ``--config 1..3`` the single-matrix and MLP-pair workloads.
+
+Refresh cadence: a step refreshes the factors iff its index is a multiple of
+the cadence K.  Steps with and without a refresh are timed apart (HIP events
+around each step), and ``ms_per_step`` / ``value`` are the cadence's average
+``(t_refresh + (K - 1) t_codec) / K`` whatever ``--steps`` is;
+``ms_per_step_raw`` is the plain mean over the timed steps.
 
 Independent matrices are spread over several HIP streams (one library
 context each): a matrix's encode, rank sum and decode stay in order on its
@@ -62,10 +71,10 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None,
-                    help="timed steps (default 10, or one full refresh period when the "
-                         "factors are refreshed less often than every step)")
+                    help="timed steps (default 10; 20 when the factors are refreshed less often "
+                         "than every step: step 0 refreshes, the others reuse the factors)")
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=4, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--config", type=int, default=5, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--sides", choices=["input", "both"], default="input")
     ap.add_argument("--iters", type=int, default=1, help="subspace iterations per warm refresh")
     ap.add_argument("--cold-iters", type=int, default=6, help="subspace iterations of the first refresh")
@@ -96,6 +105,14 @@ def parse():
     ap.add_argument("--fid-shape", type=int, nargs=2, default=[1024, 2816], metavar=("M", "N"),
                     help="layer of the fidelity study (d_out d_in; default the MLP down projection)")
     ap.add_argument("--fid-tokens", type=int, default=8192)
+    ap.add_argument("--ef", action="store_true",
+                    help="error feedback on the GIFT matrices (Algorithm 1: U~ = U + R, R <- U~ - Deq(Q(U~))), "
+                         "a float32 residual per rank and element kept across steps")
+    ap.add_argument("--no-embed", action="store_true",
+                    help="leave the embedding and LM head out of the Llama-300M set")
+    ap.add_argument("--flush-mall", action="store_true",
+                    help="overwrite a 512 MiB scratch buffer before every timed step (outside the "
+                         "step's events), so that each step starts with a cold 256 MB Infinity Cache")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run the library's plain copy kernel on 256 MiB (5 launches), "
                          "the known-size reference for the HBM byte counters")
@@ -173,6 +190,7 @@ class Job:
             self.scales = torch.empty((N, nbr, nbc), dtype=torch.float32, device=dev)
         self.mean = torch.empty((m, n), dtype=torch.float32, device=dev)
         self.out = torch.empty((m, n), dtype=torch.float32, device=dev) if mat.gift else None
+        self.ef = None
         self.factor = None
         self.sides = sides_flag if mat.gift else 0
         self.acts = self.dgrads = None
@@ -220,6 +238,9 @@ def buckets(wl, sides, gift, enable):
 def build_workload(args, torch, gift, synth, dev):
     from synth.configs import WORKLOADS
     wl = WORKLOADS[args.config]
+    if args.no_embed:
+        import dataclasses
+        wl = dataclasses.replace(wl, name=wl.name + "-no-embedding", extra=())
     sides = gift.SIDE_INPUT if args.sides == "input" else gift.SIDE_BOTH
     jobs = [Job(b, wl, sides, dev, torch, gift, args.format) for b in buckets(wl, sides, gift, args.bucket)]
     # one random set per distinct shape, copied into every matrix's rows
@@ -234,6 +255,10 @@ def build_workload(args, torch, gift, synth, dev):
             jb.grads[:, off:off + mt.m].copy_(cache[key])
             off += mt.m
     del cache
+    if args.ef:
+        for jb in jobs:
+            if jb.gift_branch:
+                jb.ef = torch.zeros_like(jb.grads)
     # factor inputs: per layer, one activation stream per layer input and one
     # output-gradient stream per GIFT matrix (copies of one draw per shape)
     xcache = {}
@@ -308,9 +333,12 @@ def algorithmic_work(wl, jobs, args):
         else:
             # encode: projections (2r flops/elem per side), the rank-r update
             # fused with the block maxima, then scale + FP8 pack of W~
+            # (error feedback: the AMAX pass reads R, the QUANT pass reads
+            # and rewrites it, since both form W~ + R)
+            efb = 1.0 if jb.ef is not None else 0.0
             add("project", proj_flops, proj_bytes)
-            add("update_amax", 2 * e * (ra + rg), 4 * e)
-            add("update_quant", 0, 5 * e)
+            add("update_amax", 2 * e * (ra + rg), (4 + 4 * efb) * e)
+            add("update_quant", 0, (5 + 8 * efb) * e)
             add("reduce", 0, mn * (N + 4))
             add("decode_project", 2 * mn * (ra + rg), 4 * mn * ((ra > 0) + (rg > 0)))
             add("update_store", 2 * mn * (ra + rg), 8 * mn)
@@ -332,33 +360,63 @@ def algorithmic_work(wl, jobs, args):
     return fam
 
 
-def cpu_baseline(wl, seconds):
-    """The oracle on one GIFT matrix of the workload, timed on the host cores."""
-    import numpy as np
-    from threadpoolctl import threadpool_info
-    from oracle import codec
-    from synth import factor_inputs, gradient_set, seed_for
+def cpu_baseline(wl, jobs, seconds):
+    """The oracle on a bounded sample of the workload, timed on the host cores.
 
-    mat = next(mt for _, mt in wl.all_matrices() if mt.gift)
-    N, m, n, r = wl.N, mat.m, mat.n, wl.rank
-    grads = gradient_set(seed_for(wl.cfg, 0), seed_for(wl.cfg, 100), N, m, n)
-    X, _ = factor_inputs(seed_for(wl.cfg, 1), wl.T, n, dtype=wl.act_dtype)
+    Sample: the first ``rows`` rows of the first GIFT matrix, all N ranks
+    (the input-side transform acts on each row alone, so a row slice is a
+    proper part of the encode / rank sum / decode), plus the full factor
+    refresh of that matrix's input side (statistics from all T tokens, exact
+    eigendecomposition).  Inputs are the benchmark's own device inputs copied
+    to the host.  Each part is timed up to three times (median), bounded by
+    ``seconds``; the refresh is charged to the sample in the proportion the
+    GPU metric charges it: divided by the cadence K and by the rows that share
+    the factor.  A single-thread time of the codec sample is reported too.
+    """
+    import numpy as np
+    from threadpoolctl import threadpool_info, threadpool_limits
+    from oracle import codec
+
+    jb = next(j for j in jobs if j.gift_branch and j.owns_factor)
+    mat = jb.mats[0][1]
+    N, n, r = jb.N, jb.n, wl.rank
+    rows = min(512, mat.m)
+    grads = jb.grads[:, :rows, :].float().cpu().numpy()
+    X = jb.acts.float().cpu().numpy()
+    shared_rows = sum(j.m for j in jobs if j.factor is jb.factor)
     cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    t0 = time.perf_counter()
-    reps = 0
-    while True:
-        fA = codec.lowrank_factor(codec.factor_statistics(X), r).to_f32()
-        codec.round_trip(grads, fA, None, wl.block_rows, wl.block_cols, False)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= seconds or reps >= 3:
-            break
-    per = el / reps
-    gbs = N * m * n * 4 / per / 1e9
-    return {"value": round(gbs, 4), "unit": "GB/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"one {mat.name} matrix ({m}x{n}, N={N}, r={r}, input side, factor from "
-                      f"{wl.T} tokens): factor + encode + reduce + decode, {reps} rep(s), "
-                      f"{per:.2f} s each"}
+
+    def timed(fn, budget):
+        ts = []
+        t_start = time.perf_counter()
+        while len(ts) < 3:
+            t0 = time.perf_counter()
+            out = fn()
+            ts.append(time.perf_counter() - t0)
+            if time.perf_counter() - t_start >= budget:
+                break
+        return float(np.median(ts)), len(ts), out
+
+    t_ref, n_ref, fA = timed(lambda: codec.lowrank_factor(codec.factor_statistics(X), r).to_f32(),
+                             0.25 * seconds)
+    br, bc = wl.block_rows, wl.block_cols
+    codec_fn = lambda: codec.round_trip(grads, fA, None, br, bc, False)
+    t_codec, n_codec, _ = timed(codec_fn, 0.5 * seconds)
+    with threadpool_limits(1):
+        t1 = time.perf_counter()
+        codec_fn()
+        t_codec_1 = time.perf_counter() - t1
+    share = rows / shared_rows / wl.refresh
+    per = t_codec + share * t_ref
+    by = N * rows * n * 4
+    return {"value": round(by / per / 1e9, 5), "unit": "GB/s", "cores": int(cores), "kind": "oracle",
+            "single_thread_value": round(by / (t_codec_1 + share * t_ref) / 1e9, 5),
+            "sample": f"rows 0..{rows - 1} of one {mat.name} matrix ({mat.m}x{n}, N={N} ranks, r={r}, "
+                      f"input side, block ({br},{bc})): encode + rank sum + decode, median of {n_codec} "
+                      f"({t_codec:.2f} s; one thread {t_codec_1:.2f} s), plus the factor refresh from "
+                      f"{X.shape[0]} tokens (statistics + exact eigendecomposition, median of {n_ref}: "
+                      f"{t_ref:.2f} s) charged x {share:.2e} (the sample's rows of the {shared_rows} rows "
+                      f"sharing the factor, over the cadence {wl.refresh})"}
 
 
 # Transform variants of the fidelity study: (label, kind, size, sides); kind
@@ -512,7 +570,7 @@ def main():
     ctx_holder["ctx"] = ctx
     wl, jobs = build_workload(args, torch, gift, synth, dev)
     if args.steps is None:
-        args.steps = 10 if wl.refresh <= 1 else wl.refresh
+        args.steps = 10 if wl.refresh <= 1 else 20
     torch.cuda.synchronize()
     print(f"[bench] workload {wl.name}: {sum(len(j.mats) for j in jobs)} matrices in "
           f"{len(jobs)} buckets, "
@@ -610,11 +668,11 @@ def main():
                     waited.add((sid, jb.group))
             c = ctxs[sid]
             if args.format == "mxfp4":
-                gift.encode_mxfp4(c, jb.factor, jb.grads, jb.codes, jb.scales)
+                gift.encode_mxfp4(c, jb.factor, jb.grads, jb.codes, jb.scales, ef=jb.ef)
                 gift.reduce_local_mxfp4(c, jb.codes, jb.scales, jb.mean)
             else:
                 gift.encode(c, jb.factor, jb.grads, jb.codes, jb.scales, jb.br, jb.bc,
-                            gift.SCALE_LOCAL if jb.gift_branch else gift.SCALE_SHARED)
+                            gift.SCALE_LOCAL if jb.gift_branch else gift.SCALE_SHARED, ef=jb.ef)
                 gift.reduce_local(c, jb.codes, jb.scales, jb.mean, jb.br, jb.bc)
             if jb.gift_branch:
                 gift.decode(c, jb.factor, jb.mean, jb.out)
@@ -640,12 +698,14 @@ def main():
             tot_ms += ms
         return tot_l, tot_ms
 
-    # untimed breakdown on the main stream alone (isolated kernel times): every
-    # kernel family bracketed by events; the largest is the dominant family
-    # kernel family bracketed by events; the refresh and the codec passes are
-    # timed apart and the refresh is amortised over its cadence
+    # untimed breakdown with every launch on the main stream (isolated,
+    # non-overlapping kernel times): every kernel family bracketed by events;
+    # the refresh and the codec passes are timed apart and the refresh is
+    # amortised over its cadence.  The largest family per amortised step is
+    # the dominant kernel; its roofline comes from these isolated launches.
     nb = max(args.breakdown_steps, 1)
     fam_ms = {}
+    fam_raw = {}     # family -> (launches, ms) per isolated step of its kind
     for refresh, codec, weight in ((True, False, 1.0 / wl.refresh), (False, True, 1.0)):
         profile_all(True, None, reset=True)
         for s in range(nb):
@@ -655,27 +715,50 @@ def main():
             if launches:
                 l0, m0 = fam_ms.get(name, (0.0, 0.0))
                 fam_ms[name] = (l0 + weight * launches / nb, m0 + weight * ms / nb)
+                r0, q0 = fam_raw.get(name, (0, 0.0))
+                fam_raw[name] = (r0 + launches, q0 + ms)
     profile_all(False)
     dom = max(fam_ms, key=lambda k: fam_ms[k][1])
 
-    # timed region: events only around the dominant family's launches
+    # timed region: events around every step (refresh steps and codec-only
+    # steps are timed apart), and around the dominant family's launches
     profile_all(True, [dom], reset=True)
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    K = max(wl.refresh, 1)
+    nsteps = args.steps
+    ev_s = [torch.cuda.Event(enable_timing=True) for _ in range(nsteps)]
+    ev_e = [torch.cuda.Event(enable_timing=True) for _ in range(nsteps)]
+    flush = torch.empty(128 * 1024 * 1024, dtype=torch.float32, device=dev) if args.flush_mall else None
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    start.record(main)
-    for s in range(args.steps):
-        step(args.iters, refresh=s % wl.refresh == 0)
-    join_into_main()
-    stop.record(main)
+    for s in range(nsteps):
+        if flush is not None:
+            join_into_main()
+            flush.fill_(float(s))
+        join_into_main()
+        ev_s[s].record(main)
+        step(args.iters, refresh=s % K == 0)
+        join_into_main()
+        ev_e[s].record(main)
     enqueue = time.perf_counter() - t0   # host time to issue the timed steps
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms_step = start.elapsed_time(stop) / args.steps
+    step_ms = [ev_s[s].elapsed_time(ev_e[s]) for s in range(nsteps)]
+    ms_raw = sum(step_ms) / nsteps
+    ref_ms = [step_ms[s] for s in range(nsteps) if s % K == 0]
+    cod_ms = [step_ms[s] for s in range(nsteps) if s % K != 0]
+    import statistics
+    t_ref = statistics.median(ref_ms)
+    t_cod = statistics.median(cod_ms) if cod_ms else None
+    if K > 1 and t_cod is not None:
+        ms_step = (t_ref + (K - 1) * t_cod) / K
+    else:
+        ms_step = statistics.median(step_ms)
     dom_launches, dom_ms_total = read_all(dom)
     profile_all(False)
-    print(f"[bench] timed {args.steps} steps: {ms_step:.3f} ms/step (wall {wall:.2f} s, "
-          f"host issue {enqueue / args.steps * 1e3:.3f} ms/step)", file=sys.stderr, flush=True)
+    print(f"[bench] timed {nsteps} steps: {ms_step:.3f} ms/step at the refresh cadence {K} "
+          f"(refresh step {t_ref:.3f} ms, codec-only step "
+          f"{t_cod if t_cod is None else round(t_cod, 3)} ms, raw mean {ms_raw:.3f} ms; wall "
+          f"{wall:.2f} s, host issue {enqueue / nsteps * 1e3:.3f} ms/step)", file=sys.stderr, flush=True)
 
     grad_bytes = sum(j.N * j.m * j.n * 4 for j in jobs)
     value = grad_bytes / (ms_step * 1e-3) / 1e9
@@ -686,26 +769,34 @@ def main():
         kernels[name] = {"ms_per_step": round(ms, 4), "launches_per_step": round(launches, 2),
                          "tflops": round(fl / (ms * 1e-3) / 1e12, 3) if ms > 0 else None,
                          "gbs": round(by / (ms * 1e-3) / 1e9, 2) if ms > 0 else None}
+    # roofline of the dominant kernel from its isolated launches: algorithmic
+    # work per launch (per step / launches per step) over the average
+    # isolated launch duration
     fl, by = work.get(dom, (0.0, 0.0))
-    dom_launches /= args.steps
-    dom_ms = dom_ms_total / args.steps
-    avg_ms = dom_ms / dom_launches
+    per_step_launches, per_step_ms = fam_ms[dom]
+    iso_launches, iso_ms = fam_raw[dom]
+    avg_ms = iso_ms / iso_launches
+    fl_l, by_l = fl / per_step_launches, by / per_step_launches
     peak_f = BF16_MFMA_TFLOPS if dom == "syrk" and wl.act_dtype == "bf16" else FP32_MFMA_TFLOPS
-    frac_f = fl / (dom_ms * 1e-3) / 1e12 / peak_f if fl else 0.0
-    frac_b = by / (dom_ms * 1e-3) / 1e9 / HBM_PEAK_GBS if by else 0.0
+    frac_f = fl_l / (avg_ms * 1e-3) / 1e12 / peak_f if fl else 0.0
+    frac_b = by_l / (avg_ms * 1e-3) / 1e9 / HBM_PEAK_GBS if by else 0.0
     if frac_f >= frac_b:
-        roof = {"bound": "mfma", "achieved": round(fl / dom_launches / (avg_ms * 1e-3) / 1e12, 3),
+        roof = {"bound": "mfma", "achieved": round(fl_l / (avg_ms * 1e-3) / 1e12, 3),
                 "peak": peak_f, "unit": "TFLOP/s", "frac": round(frac_f, 4)}
     else:
-        roof = {"bound": "hbm", "achieved": round(by / dom_launches / (avg_ms * 1e-3) / 1e9, 2),
+        roof = {"bound": "hbm", "achieved": round(by_l / (avg_ms * 1e-3) / 1e9, 2),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(frac_b, 4)}
-    wl_key = f"config{wl.cfg}-{args.sides}"
+    wl_key = f"config{wl.cfg}-{args.sides}" + ("-ef" if args.ef else "")
     traffic = measured_traffic(dom, wl_key)
+    timed_avg = dom_ms_total / dom_launches if dom_launches else None
     roof.update({"kernel": dom, "avg_launch_ms": round(avg_ms, 5),
+                 "launch_source": "isolated launches (untimed pass, every launch on one stream)",
+                 "timed_region_avg_launch_ms": round(timed_avg, 5) if timed_avg else None,
+                 "algorithmic_gb_per_launch": round(by_l / 1e9, 4),
+                 "algorithmic_tflop_per_launch": round(fl_l / 1e12, 4),
                  "traffic": round(traffic / 1e9, 4) if traffic is not None else None})
     if traffic is not None:
         roof["traffic_unit"] = "GB per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
-        roof["algorithmic_gb_per_launch"] = round((by / dom_launches) / 1e9, 4)
     tf_fams = ("project", "update_amax", "update_quant", "decode_project", "update_store")
     tf_ms = sum(fam_ms[k][1] for k in tf_fams if k in fam_ms)
     tf_flops = sum(work[k][0] for k in tf_fams if k in work)
@@ -714,31 +805,39 @@ def main():
         "value": round(value, 3),
         "unit": "GB/s",
         "n_gpus": 1,
-        "steps": args.steps,
+        "steps": nsteps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
-        "host_issue_ms_per_step": round(enqueue / args.steps * 1e3, 3),
+        "ms_per_step_raw": round(ms_raw, 4),
+        "ms_refresh_step": round(t_ref, 4),
+        "ms_codec_step": round(t_cod, 4) if t_cod is not None else None,
+        "host_issue_ms_per_step": round(enqueue / nsteps * 1e3, 3),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
+        "dtype_detail": "float32 gradients, transforms and accumulation; the forward transform's "
+                        "products as three bf16 MFMA products of hi/lo splits of both float32 operands "
+                        "(within 1e-5 of float64); the inverse on FP32 MFMA; statistics from bf16 "
+                        "inputs on BF16 MFMA with float32 sums; FP8 E4M3 codes",
         "data": "synthetic",
         "config": {"workload": f"{wl.name} (config {wl.cfg})", "ranks": wl.N, "rank": wl.rank,
                    "sides": args.sides, "tokens": wl.T,
                    "matrices": sum(len(jb.mats) for jb in jobs), "buckets": len(jobs),
-                   "format": args.format,
+                   "format": args.format, "error_feedback": bool(args.ef),
                    "factors": sum(1 for jb in jobs if jb.owns_factor), "streams": nstreams,
                    "grad_gb": round(grad_bytes / 1e9, 3), "factor_refresh_every": wl.refresh,
-                   "refreshes_timed": sum(1 for s in range(args.steps) if s % wl.refresh == 0),
-                   "subspace_iters": args.iters},
+                   "refreshes_timed": len(ref_ms), "subspace_iters": args.iters,
+                   "mall_flushed": bool(args.flush_mall)},
         "transform_tflops": round(tf_flops / (tf_ms * 1e-3) / 1e12, 3) if tf_ms else None,
         "roofline": roof,
         "kernels": kernels,
-        "kernels_note": "per-family time per step from an untimed pass with every launch on one stream",
+        "kernels_note": "per-family time per step (refresh amortised over the cadence) from an untimed "
+                        "pass with every launch on one stream",
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
-        line["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(wl, jobs, args.cpu_seconds)
     torch.cuda.synchronize()
     for jb in jobs:
         if jb.owns_factor:

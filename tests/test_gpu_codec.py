@@ -202,6 +202,14 @@ TRANSFORM_CASES = [
     (2, 136, 256, 128, gift.SIDE_INPUT, 0, 0),
     (3, 260, 520, 32, gift.SIDE_BOTH, 0, 0),
     (2, 100, 200, 16, gift.SIDE_INPUT, 7, 12),
+    # two-segment (both sides) updates of 4, 6 and 8 chunks: r = 64 and 96
+    # run at two waves per SIMD (n a multiple of the column unit: the
+    # branch-free quantize variant), r = 128 at one; r = 100 on the input
+    # side leaves the last 32-step chunk partly filled
+    (2, 200, 512, 64, gift.SIDE_BOTH, 0, 128),
+    (2, 136, 384, 96, gift.SIDE_BOTH, 0, 0),
+    (2, 160, 256, 128, gift.SIDE_BOTH, 0, 128),
+    (2, 136, 256, 100, gift.SIDE_INPUT, 0, 0),
 ]
 
 
@@ -242,6 +250,11 @@ def test_transform_encode_decode_parity(ctx, N, m, n, r, sides, br, bc):
     (3, 96, 256, 64, gift.SIDE_INPUT, 0, 64, True, False),
     (4, 160, 512, 64, gift.SIDE_INPUT, 0, 0, False, True),
     (2, 64, 768, 64, gift.SIDE_INPUT, 32, 256, True, True),
+    # two-segment updates at 4, 6 and 8 chunks, and a partial last chunk
+    (2, 200, 512, 64, gift.SIDE_BOTH, 0, 128, False, False),
+    (2, 136, 384, 96, gift.SIDE_BOTH, 0, 0, False, False),
+    (2, 160, 256, 128, gift.SIDE_BOTH, 0, 128, True, False),
+    (2, 136, 256, 100, gift.SIDE_INPUT, 0, 0, False, True),
 ])
 def test_recomputed_transform_matches_stored(ctx, N, m, n, r, sides, br, bc, use_ef, shared):
     """Without a `transformed` buffer the quantize pass computes W~ again

@@ -191,3 +191,54 @@ def test_fullsize_euclidean_bucket(ctx, name):
     codes, scales, mean, _, tr = run(ctx, None, g, br, bc, gift.SCALE_SHARED)
     assert torch.equal(tr, g)
     check_quant_and_sum(codes, scales, mean, tr, sample_rows(m, b[0][1].kind), br, bc, True)
+
+
+# ---------------------------------------------------------------- both sides, Llama-600M
+# With the output side every matrix keeps its own factor pair (G belongs to
+# the matrix's outputs), so the benchmark's --sides both runs one call per
+# matrix.  W~ = S_G^-1 W S_A^-1 mixes rows, so a sampled row of W~ needs all of
+# W: the oracle applies row i of the dense S_G^-1 to each rank's whole W, then
+# S_A^-1 (eq. design_full_transform); likewise row i of the decode is
+# (row i of S_G) M S_A (eq. design_full_inverse_transform).
+
+@pytest.mark.parametrize("name", ["q", "down"])
+def test_fullsize_600m_both_sides(ctx, name):
+    wl = WL5
+    N, r, T = wl.N, wl.rank, wl.T
+    mat = next(mt for mt in wl.matrices if mt.name == name)
+    m, n, br, bc = mat.m, mat.n, wl.block_rows, wl.block_cols
+    say(f"full size two-sided {name}: N={N} m={m} n={n} r={r} T={T} block=({br},{bc})")
+    g = gradient_set_torch(seed_for(wl.cfg, 0, 0, mat.kind), N, m, n, DEV)
+    x = factor_inputs_torch(seed_for(wl.cfg, 1, 0, n % 97), T, n, DEV, dtype=wl.act_dtype)
+    d = factor_inputs_torch(seed_for(wl.cfg, 2, 0, m % 97), T, m, DEV, dtype=wl.act_dtype)
+    f = gift.Factor(ctx, m, n, r, gift.SIDE_BOTH, seed=seed_for(wl.cfg, 50, 0, mat.kind))
+    f.update(acts=x, out_grads=d, iters=6)
+    f.update(acts=x, out_grads=d, iters=1)
+    sides = {}
+    for side, inp in ((gift.SIDE_INPUT, x), (gift.SIDE_OUTPUT, d)):
+        U, cf, ci, s2 = (t_.cpu().numpy().astype(np.float64) for t_ in f.export(side))
+        fx = codec.Factor(U, cf, ci, float(s2[0]))
+        A = codec.factor_statistics(inp.float().cpu().numpy())
+        lam = np.linalg.eigvalsh(A)[::-1][:r]
+        captured = np.trace(U.T @ A @ U)
+        say(f"  side {side} (dim {A.shape[0]}): captured energy {captured / lam.sum():.6f}")
+        assert captured >= 0.999 * lam.sum()
+        sides[side] = fx
+    fA, fG = sides[gift.SIDE_INPUT], sides[gift.SIDE_OUTPUT]
+    codes, scales, mean, out, tr = run(ctx, f, g, br, bc, gift.SCALE_LOCAL)
+    rows = sample_rows(m, 7 + mat.kind)
+    trh, got_mean = check_quant_and_sum(codes, scales, mean, tr, rows, br, bc, False)
+    Lg = codec._left_fwd(fG)[rows]          # rows of S_G^-1, [len(rows), m]
+    Ra = codec._right_fwd(fA)               # S_A^-1, [n, n]
+    gh = g.cpu().numpy().astype(np.float64)
+    ref_rows = np.stack([(Lg @ gh[j]) @ Ra for j in range(N)])
+    e = rel(trh[:, rows, :], ref_rows)
+    say(f"  W~ rel. error on {len(rows)} rows: {e:.2e}")
+    assert e <= 1e-5
+    Mfull = mean.cpu().numpy().astype(np.float64)
+    ref_out = (codec._left_inv(fG)[rows] @ Mfull) @ codec._right_inv(fA)
+    got_out = out[torch.from_numpy(rows).to(DEV)].cpu().numpy()
+    e = rel(got_out, ref_out)
+    say(f"  decode rel. error on {len(rows)} rows: {e:.2e}")
+    assert e <= 1e-5
+    f.close()
