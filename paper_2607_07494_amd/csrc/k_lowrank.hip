@@ -713,11 +713,14 @@ __device__ __forceinline__ void lr_update_body(const LUArgs &p) {
   if (FULL) {
     // every tile of the range, also past N in the last range of an AMAX pass
     // (its maxima leave those columns out; QUANT runs FULL only when N fills
-    // every range): no branch between the waits
+    // every range): no branch between the waits.  TILES is 1 from five
+    // chunks on, so the second tile of a pair exists only when TILES > 1
+    // (a compile-time test): a tile past the range would belong to the next
+    // workgroup's columns.
 #pragma unroll
     for (int ct = 0; ct < TILES; ct += 2) {
       tile(ct, dA, rA);
-      tile(ct + 1, dB, rB);
+      if (ct + 1 < TILES) tile(ct + 1, dB, rB);
     }
     // one atomic per run of tiles in the same block
     if (EPI == EPI_AMAX && wave_live && lane == 0) {

@@ -205,10 +205,15 @@ TRANSFORM_CASES = [
     # two-segment (both sides) updates of 4, 6 and 8 chunks: r = 64 and 96
     # run at two waves per SIMD (n a multiple of the column unit: the
     # branch-free quantize variant), r = 128 at one; r = 100 on the input
-    # side leaves the last 32-step chunk partly filled
+    # side leaves the last 32-step chunk partly filled.  With rank 128 on
+    # both sides of a 160 x 256 matrix the inverse multiplies the error of a
+    # code that rounds the other way by up to (1 + c'_G)(1 + c'_A) ~ 550, so
+    # the end-to-end bar (the workloads' 4 to 16 ranks) needs the rank mean
+    # of more than two ranks: a float64 simulation of a 3e-6 W~ perturbation
+    # gives 4e-3 at N = 2 and 1.3e-3 at N = 8
     (2, 200, 512, 64, gift.SIDE_BOTH, 0, 128),
     (2, 136, 384, 96, gift.SIDE_BOTH, 0, 0),
-    (2, 160, 256, 128, gift.SIDE_BOTH, 0, 128),
+    (8, 160, 256, 128, gift.SIDE_BOTH, 0, 128),
     (2, 136, 256, 100, gift.SIDE_INPUT, 0, 0),
 ]
 
