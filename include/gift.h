@@ -254,6 +254,32 @@ gift_status gift_encode(gift_ctx *ctx, const gift_factor *f, const float *grads,
                         int32_t block_cols, gift_scale_mode mode, float *ef,
                         uint8_t *codes, float *scales, float *transformed);
 
+/* Size of the fixed device scratch of gift_encode_noalloc (64 MiB per device). */
+#define GIFT_NOALLOC_SCRATCH_BYTES (64ull * 1024ull * 1024ull)
+
+/* gift_encode without any device allocation, for callers that cannot
+ * allocate: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  Arguments, results and kernels are those of gift_encode
+ * (codes, scales, ef and transformed identical).  Its scratch (block-maximum
+ * sub-slots, the finalize buffer, the projections P = W U and their partial
+ * sums, a stored W~ when the transform cannot be recomputed, the Cholesky-form
+ * transform buffer) comes from one fixed array of GIFT_NOALLOC_SCRATCH_BYTES
+ * in device memory, which each device holds from the library's load there
+ * until the process ends; the call makes no hipMalloc, hipFree, event or
+ * other allocating call (the first call on a device looks the array's device
+ * address up once).  The sub-slots are cleared by a kernel at the start of
+ * every call.  Limits: a call whose scratch exceeds the array returns
+ * GIFT_ESHAPE before anything is enqueued (e.g. a low-rank encode needs about
+ * 4 N m r (parts + 1) bytes of projections; split the ranks or rows, or pass
+ * `transformed` where W~ would be stored).  Every call on one device shares
+ * the array: calls that overlap in time on one device (other streams, other
+ * contexts, other threads) race and must be ordered by the caller.  The
+ * context's device must be current.  Per-kernel timing is not recorded. */
+gift_status gift_encode_noalloc(gift_ctx *ctx, const gift_factor *f, const float *grads,
+                                int32_t N, int64_t m, int64_t n, int32_t block_rows,
+                                int32_t block_cols, gift_scale_mode mode, float *ef,
+                                uint8_t *codes, float *scales, float *transformed);
+
 /* Copy one side of a Cholesky-form factor out of / into it (device
  * pointers): R and Rinv are [nblk, b_eff, b_eff] float32, block k holding
  * R_k = L_k^T (upper triangular) and its inverse; the last block's kv x kv

@@ -19,10 +19,20 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 #include <string>
 
 #include "gift_internal.h"
+
+// Device scratch of gift_encode_noalloc, the entry point for callers that
+// cannot allocate device memory.  Every device the library runs on holds its
+// own copy from the moment the code object is loaded there until the process
+// ends.  Host code never takes this array's address directly (on the host the
+// name is only a stand-in for the symbol): noalloc_scratch() looks the device
+// address up once per device with hipGetSymbolAddress and the kernels receive
+// that pointer.
+static __device__ __align__(256) unsigned char scratch[GIFT_NOALLOC_SCRATCH_BYTES];
 
 namespace gift {
 
@@ -123,7 +133,7 @@ void amax_slots_done(gift_ctx *ctx, size_t left) {
 }
 
 ProfileScope::ProfileScope(gift_ctx *c, int k) : ctx(c), kernel(k) {
-  if (!ctx || !ctx->profile || !((ctx->profile_mask >> kernel) & 1u)) return;
+  if (!ctx || !ctx->profile || ctx->no_alloc_call || !((ctx->profile_mask >> kernel) & 1u)) return;
   hipEvent_t start = nullptr;
   auto grab = [&]() -> hipEvent_t {
     if (!ctx->event_pool.empty()) {
@@ -757,10 +767,10 @@ gift_status gift_factor_import(gift_ctx *ctx, gift_factor *f, int32_t side, cons
   return side_import(ctx, *s, U, c_fwd, c_inv, sigma2);
 }
 
-static gift_status encode_impl(gift_ctx *ctx, const gift_factor *f, const float *grads, int32_t N,
-                               int64_t m, int64_t n, int32_t block_rows, int32_t block_cols,
-                               gift_scale_mode mode, float *ef, uint8_t *codes, float *scales,
-                               float *transformed, uint32_t *hits) {
+// Host-side checks shared by the encode entry points (no HIP call).
+static gift_status encode_validate(gift_ctx *ctx, const gift_factor *f, const float *grads, int32_t N,
+                                   int64_t m, int64_t n, int32_t block_rows, int32_t block_cols,
+                                   gift_scale_mode mode, const uint8_t *codes, const float *scales) {
   if (!ctx) return set_error(GIFT_EINVAL, "gift_encode: ctx is NULL");
   if (!grads || !codes || !scales) return set_error(GIFT_EINVAL, "gift_encode: NULL tensor");
   if (mode != GIFT_SCALE_LOCAL && mode != GIFT_SCALE_SHARED)
@@ -772,19 +782,80 @@ static gift_status encode_impl(gift_ctx *ctx, const gift_factor *f, const float 
     return set_error(GIFT_ESHAPE, "gift_encode: block sizes must be >= 0");
   if (f && (f->m != m || f->n != n))
     return set_error(GIFT_ESHAPE, "gift_encode: factor was created for another shape");
+  return GIFT_OK;
+}
+
+// A fixed device region that an allocation-free encode carves its scratch
+// from (sub-slots, finalize buffer, projections, stored W~, Cholesky-form
+// transform), instead of the context's grow-only buffers.
+struct FixedScratch {
+  char *base = nullptr;
+  size_t cap = 0;
+};
+
+// Bytes of fixed scratch encode_impl carves for this call (mirrors its
+// buffer plan; no HIP call).
+static gift_status encode_fixed_bytes(gift_ctx *ctx, const gift_factor *f, const float *grads, int32_t N,
+                                      int64_t m, int64_t n, int32_t block_rows, int32_t block_cols,
+                                      const float *ef, const uint8_t *codes, const float *transformed,
+                                      size_t *out) {
+  if (f && f->chol) {
+    const bool two = chol_transform_needs_tmp(f);
+    const size_t xb = a256(sizeof(float) * (size_t)N * m * n * (two ? 2 : 1));
+    size_t rest = 0;
+    // the Euclidean encode of W~ (held 256-byte aligned in the scratch)
+    gift_status st = encode_fixed_bytes(ctx, nullptr, grads, N, m, n, block_rows, block_cols, ef, codes,
+                                        transformed, &rest);
+    if (st != GIFT_OK) return st;
+    *out = xb + rest;
+    return GIFT_OK;
+  }
+  const BlockGeom g = block_geom(m, n, block_rows, block_cols);
+  const int64_t nblk = (int64_t)g.nbr * g.nbc;
+  const size_t raw_bytes = a256(sizeof(uint32_t) * (size_t)N * nblk * kAmaxSlots);
+  const size_t fin_bytes = a256(sizeof(uint32_t) * (size_t)N * nblk);
+  LowRankPlan plan;
+  size_t proj_bytes = 0;
+  if (f) {
+    gift_status st = plan_low_rank(ctx, f, grads, N, m, n, false, nullptr, &proj_bytes, &plan);
+    if (st != GIFT_OK) return st;
+  }
+  const bool gemm = f && plan.active;
+  const bool recompute = gemm && encode_recomputes(f, n, grads, ef, codes, transformed);
+  const bool store_wt = gemm && !recompute && n % 4 == 0 && g.bc % 4 == 0;
+  const size_t wt_bytes = store_wt && !transformed ? a256(sizeof(float) * (size_t)N * m * n) : 0;
+  *out = raw_bytes + fin_bytes + proj_bytes + wt_bytes;
+  return GIFT_OK;
+}
+
+static gift_status encode_impl(gift_ctx *ctx, const gift_factor *f, const float *grads, int32_t N,
+                               int64_t m, int64_t n, int32_t block_rows, int32_t block_cols,
+                               gift_scale_mode mode, float *ef, uint8_t *codes, float *scales,
+                               float *transformed, uint32_t *hits, const FixedScratch *fx) {
+  gift_status st = encode_validate(ctx, f, grads, N, m, n, block_rows, block_cols, mode, codes, scales);
+  if (st != GIFT_OK) return st;
   if ((st = bind_device(ctx)) != GIFT_OK) return st;
   if (f && f->chol) {
     // W~ = L_G^-1 W L_A^-T into the transform buffer, then the Euclidean
     // encode of W~ (whose own workspace holds everything else)
     const size_t total = (size_t)N * m * n;
     const bool two = chol_transform_needs_tmp(f);
+    const size_t xbytes = sizeof(float) * total * (two ? 2 : 1);
     void *buf = nullptr;
-    if ((st = grow_buffer(ctx, ctx->xform, sizeof(float) * total * (two ? 2 : 1), &buf)) != GIFT_OK) return st;
+    FixedScratch rest;
+    if (fx) {
+      if (a256(xbytes) > fx->cap) return set_error(GIFT_ESHAPE, "gift_encode: fixed scratch too small");
+      buf = fx->base;
+      rest.base = fx->base + a256(xbytes);
+      rest.cap = fx->cap - a256(xbytes);
+    } else if ((st = grow_buffer(ctx, ctx->xform, xbytes, &buf)) != GIFT_OK) {
+      return st;
+    }
     float *wt = static_cast<float *>(buf);
     if ((st = launch_chol_transform(ctx, f, grads, wt, N, false, two ? wt + total : nullptr)) != GIFT_OK)
       return st;
     return encode_impl(ctx, nullptr, wt, N, m, n, block_rows, block_cols, mode, ef, codes, scales, transformed,
-                       hits);
+                       hits, fx ? &rest : nullptr);
   }
   const BlockGeom g = block_geom(m, n, block_rows, block_cols);
   const int64_t nblk = (int64_t)g.nbr * g.nbc;
@@ -805,9 +876,25 @@ static gift_status encode_impl(gift_ctx *ctx, const gift_factor *f, const float 
   const size_t raw_words = (size_t)N * nblk * kAmaxSlots;
   uint32_t *amax_raw = nullptr, *prev_set = nullptr;
   size_t prev_dirty = 0;
-  if ((st = amax_slots(ctx, raw_words, &amax_raw, &prev_set, &prev_dirty)) != GIFT_OK) return st;
   void *ws = nullptr;
-  if ((st = workspace(ctx, fin_bytes + proj_bytes + wt_bytes, &ws)) != GIFT_OK) return st;
+  if (fx) {
+    // the fixed region holds the sub-slots (cleared here: the last call on
+    // this device left its maxima in them), then the rest
+    const size_t raw_bytes = a256(sizeof(uint32_t) * raw_words);
+    if (raw_bytes + fin_bytes + proj_bytes + wt_bytes > fx->cap)
+      return set_error(GIFT_ESHAPE, "gift_encode: fixed scratch too small");
+    amax_raw = reinterpret_cast<uint32_t *>(fx->base);
+    ws = fx->base + raw_bytes;
+    if ((st = launch_zero_u32(ctx, amax_raw, (int64_t)raw_words)) != GIFT_OK) return st;
+  } else {
+    if ((st = amax_slots(ctx, raw_words, &amax_raw, &prev_set, &prev_dirty)) != GIFT_OK) return st;
+    if ((st = workspace(ctx, fin_bytes + proj_bytes + wt_bytes, &ws)) != GIFT_OK) return st;
+  }
+  // book-keeping of the context's alternating sub-slot sets (not used by a
+  // fixed region, which is cleared at the start of every call)
+  auto slots_done = [&](size_t left) {
+    if (!fx) amax_slots_done(ctx, left);
+  };
   uint32_t *amax_fin = static_cast<uint32_t *>(ws);
   float *wt = transformed;
   if (wt_bytes) wt = reinterpret_cast<float *>(static_cast<char *>(ws) + fin_bytes + proj_bytes);
@@ -849,7 +936,7 @@ static gift_status encode_impl(gift_ctx *ctx, const gift_factor *f, const float 
     q.clear_words = (int64_t)prev_dirty;
     q.kernel_family = GIFT_KERNEL_UPDATE_QUANT;
     if ((st = launch_tile(ctx, q)) != GIFT_OK) return st;
-    amax_slots_done(ctx, raw_words);
+    slots_done(raw_words);
     return GIFT_OK;
   }
   const float *qsrc = gemm ? wt : grads;
@@ -863,7 +950,7 @@ static gift_status encode_impl(gift_ctx *ctx, const gift_factor *f, const float 
     q.clear_words = (int64_t)prev_dirty;
     q.kernel_family = gemm ? GIFT_KERNEL_UPDATE_QUANT : GIFT_KERNEL_QUANT;
     if ((st = launch_stream_codec(ctx, q)) != GIFT_OK) return st;
-    amax_slots_done(ctx, raw_words);
+    slots_done(raw_words);
     return GIFT_OK;
   }
   if ((st = launch_finalize_amax(ctx, amax_raw, N, nblk, job.shared, amax_fin, scales, prev_set,
@@ -872,16 +959,75 @@ static gift_status encode_impl(gift_ctx *ctx, const gift_factor *f, const float 
   job.amax = amax_fin;
   job.kernel_family = gemm ? GIFT_KERNEL_UPDATE_QUANT : GIFT_KERNEL_QUANT;
   if ((st = launch_tile(ctx, job)) != GIFT_OK) return st;
-  amax_slots_done(ctx, 0);
+  slots_done(0);
   return GIFT_OK;
 }
+
+namespace {
+// Device address of this device's `scratch` array, looked up once per device
+// (hipGetSymbolAddress with the device current) and kept.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+gift_status noalloc_scratch(gift_ctx *ctx, char **out) {
+  int dev = -1;
+  GIFT_HIP_TRY(hipGetDevice(&dev));
+  if (dev != ctx->device)
+    return set_error(GIFT_EINVAL, "gift_encode_noalloc: the context's device must be the current device");
+  if (dev < 0 || dev >= kMaxDevices)
+    return set_error(GIFT_EUNSUPPORTED, "gift_encode_noalloc: device index above 63");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_error(e, "gift_encode_noalloc: hipGetSymbolAddress(scratch)");
+    if (!p) return set_error(GIFT_EHIP, "gift_encode_noalloc: no device address for the scratch array");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = static_cast<char *>(g_scratch_ptr[dev]);
+  return GIFT_OK;
+}
+
+// Marks the context for the duration of an allocation-free call (no
+// profiling events are created or recorded).
+struct NoAllocCall {
+  gift_ctx *ctx;
+  explicit NoAllocCall(gift_ctx *c) : ctx(c) { ctx->no_alloc_call = true; }
+  ~NoAllocCall() { ctx->no_alloc_call = false; }
+};
+}  // namespace
 
 gift_status gift_encode(gift_ctx *ctx, const gift_factor *f, const float *grads, int32_t N,
                         int64_t m, int64_t n, int32_t block_rows, int32_t block_cols,
                         gift_scale_mode mode, float *ef, uint8_t *codes, float *scales,
                         float *transformed) {
   return encode_impl(ctx, f, grads, N, m, n, block_rows, block_cols, mode, ef, codes, scales, transformed,
-                     nullptr);
+                     nullptr, nullptr);
+}
+
+gift_status gift_encode_noalloc(gift_ctx *ctx, const gift_factor *f, const float *grads, int32_t N,
+                                int64_t m, int64_t n, int32_t block_rows, int32_t block_cols,
+                                gift_scale_mode mode, float *ef, uint8_t *codes, float *scales,
+                                float *transformed) {
+  gift_status st = encode_validate(ctx, f, grads, N, m, n, block_rows, block_cols, mode, codes, scales);
+  if (st != GIFT_OK) return st;
+  size_t need = 0;
+  if ((st = encode_fixed_bytes(ctx, f, grads, N, m, n, block_rows, block_cols, ef, codes, transformed,
+                               &need)) != GIFT_OK)
+    return st;
+  if (need > (size_t)GIFT_NOALLOC_SCRATCH_BYTES)
+    return set_error(GIFT_ESHAPE, "gift_encode_noalloc: this encode needs " + std::to_string(need) +
+                                      " bytes of scratch, more than the fixed " +
+                                      std::to_string((size_t)GIFT_NOALLOC_SCRATCH_BYTES) +
+                                      " (split the call into fewer ranks or rows, or pass `transformed`)");
+  if ((st = bind_device(ctx)) != GIFT_OK) return st;
+  FixedScratch fx;
+  if ((st = noalloc_scratch(ctx, &fx.base)) != GIFT_OK) return st;
+  fx.cap = (size_t)GIFT_NOALLOC_SCRATCH_BYTES;
+  NoAllocCall mark(ctx);
+  return encode_impl(ctx, f, grads, N, m, n, block_rows, block_cols, mode, ef, codes, scales, transformed,
+                     nullptr, &fx);
 }
 
 gift_status gift_encode_hits(gift_ctx *ctx, const gift_factor *f, const float *grads, int32_t N,
@@ -892,7 +1038,7 @@ gift_status gift_encode_hits(gift_ctx *ctx, const gift_factor *f, const float *g
   if (reinterpret_cast<uintptr_t>(hits) & 3)
     return set_error(GIFT_EINVAL, "gift_encode_hits: hits must be 4-byte aligned");
   return encode_impl(ctx, f, grads, N, m, n, block_rows, block_cols, mode, ef, codes, scales, transformed,
-                     hits);
+                     hits, nullptr);
 }
 
 gift_status gift_reduce_local(gift_ctx *ctx, const uint8_t *codes, const float *scales, int32_t N,

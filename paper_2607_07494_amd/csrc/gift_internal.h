@@ -58,6 +58,9 @@ struct gift_ctx {
   int64_t prof_launches[GIFT_KERNEL_COUNT] = {};
   double prof_ms[GIFT_KERNEL_COUNT] = {};
   std::vector<hipEvent_t> event_pool;
+  // set for the duration of an allocation-free call: no profiling events
+  // are created or recorded
+  bool no_alloc_call = false;
 };
 
 namespace gift {

@@ -74,6 +74,7 @@ def _load():
         "gift_factor_import_chol": ([P, P, I32, P, P], I32),
         "gift_encode": ([P, P, P, I32, I64, I64, I32, I32, I32, P, P, P, P], I32),
         "gift_encode_hits": ([P, P, P, I32, I64, I64, I32, I32, I32, P, P, P, P, P], I32),
+        "gift_encode_noalloc": ([P, P, P, I32, I64, I64, I32, I32, I32, P, P, P, P], I32),
         "gift_reduce_local": ([P, P, P, I32, I64, I64, I32, I32, P], I32),
         "gift_encode_mxfp4": ([P, P, P, I32, I64, I64, P, P, P, P], I32),
         "gift_reduce_local_mxfp4": ([P, P, P, I32, I64, I64, P], I32),
@@ -410,6 +411,29 @@ def encode(ctx: Context, factor, grads, codes, scales, block_rows: int = 0, bloc
         _check(LIB.gift_encode(*args))
         return
     _check(LIB.gift_encode_hits(*args, _ptr(hits, torch.int32, "hits")))
+
+
+NOALLOC_SCRATCH_BYTES = 64 * 1024 * 1024
+
+
+def encode_noalloc(ctx: Context, factor, grads, codes, scales, block_rows: int = 0, block_cols: int = 0,
+                   mode: int = SCALE_LOCAL, ef=None, transformed=None):
+    """``gift_encode_noalloc``: :func:`encode` with its scratch in the library's
+    fixed per-device array (no device allocation; calls on one device must
+    not overlap)."""
+    import torch
+    N, m, n = _dims(grads, 3, "grads")
+    if factor is not None and (factor.m, factor.n) != (m, n):
+        raise ValueError(f"the factor was created for {factor.m} x {factor.n}, not {m} x {n}")
+    _expect(codes, (N, m, n), "codes")
+    _expect(scales, (N,) + scale_grid(m, n, block_rows, block_cols), "scales")
+    _expect(ef, (N, m, n), "ef")
+    _expect(transformed, (N, m, n), "transformed")
+    _check(LIB.gift_encode_noalloc(ctx.handle, factor.handle if factor is not None else None,
+                                   _ptr(grads, torch.float32, "grads"), N, m, n, block_rows, block_cols,
+                                   mode, _ptr(ef, torch.float32, "ef"), _ptr(codes, torch.uint8, "codes"),
+                                   _ptr(scales, torch.float32, "scales"),
+                                   _ptr(transformed, torch.float32, "transformed")))
 
 
 def reduce_local(ctx: Context, codes, scales, mean, block_rows: int = 0, block_cols: int = 0):

@@ -281,3 +281,15 @@ def test_binding_factor_input_shape_checks(ctx):
     with pytest.raises(ValueError, match="c_inv"):
         f.import_(gift.SIDE_INPUT, _z(8, 4), _z(4), _z(3), _z(1))
     f._h = ctypes.c_void_p()   # nothing to destroy
+
+
+def test_encode_noalloc_host_validation(ctx):
+    h = ctx.handle
+    enc = LIB.gift_encode_noalloc
+    assert enc(h, None, None, 1, 4, 4, 0, 0, 0, None, FAKE, FAKE, None) == gift.EINVAL
+    assert enc(h, None, FAKE, 0, 4, 4, 0, 0, 0, None, FAKE, FAKE, None) == gift.ESHAPE
+    assert enc(h, None, FAKE, 1, 4, 4, 0, 0, 9, None, FAKE, FAKE, None) == gift.EINVAL
+    # 1 x 1 scale blocks on 4 x 300 x 256: 78.6 MB of sub-slots, over the
+    # fixed 64 MiB; rejected on the host before any HIP call
+    assert enc(h, None, FAKE, 4, 300, 256, 1, 1, 0, None, FAKE, FAKE, None) == gift.ESHAPE
+    assert "scratch" in _err() and str(64 * 1024 * 1024) in _err()
