@@ -60,7 +60,7 @@ FAMILY_SOURCE = {
     "chol_transform": "paper_2607_07494_amd/csrc/k_chol.hip",
     "mxfp4": "paper_2607_07494_amd/csrc/k_mx.hip",
 }
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "llama300m-gradient-set_input_hbm-traffic-per-kernel.md")
+TRAFFIC_GLOB = os.path.join(ROOT, "profiles", "*_hbm-traffic-per-kernel.md")
 
 HBM_PEAK_GBS = 8000.0
 FP32_MFMA_TFLOPS = 157.3
@@ -113,6 +113,10 @@ def parse():
     ap.add_argument("--flush-mall", action="store_true",
                     help="overwrite a 512 MiB scratch buffer before every timed step (outside the "
                          "step's events), so that each step starts with a cold 256 MB Infinity Cache")
+    ap.add_argument("--calibrate", action="store_true",
+                    help="only measure the achievable peaks the roofline is compared with: the "
+                         "library's float32 copy kernel over 1 GiB (HBM read + write) and matrix-core "
+                         "loops with no memory traffic (bf16 16x16x32 and float32 16x16x4 MFMA)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run the library's plain copy kernel on 256 MiB (5 launches), "
                          "the known-size reference for the HBM byte counters")
@@ -130,15 +134,17 @@ def measured_traffic(family, workload):
     counter summary, or None when there is none or the kernel's source has
     changed since it was taken.  Lines look like
     `traffic: family=F workload=W bytes_per_launch=B sha256=H`."""
-    if family not in FAMILY_SOURCE or not os.path.exists(TRAFFIC_FILE):
+    import glob
+    if family not in FAMILY_SOURCE:
         return None
     sha = source_sha256(FAMILY_SOURCE[family])
-    for line in open(TRAFFIC_FILE):
-        if not line.startswith("traffic:"):
-            continue
-        kv = dict(item.split("=", 1) for item in line.split()[1:])
-        if kv.get("family") == family and kv.get("workload") == workload and kv.get("sha256") == sha:
-            return float(kv["bytes_per_launch"])
+    for path in sorted(glob.glob(TRAFFIC_GLOB)):
+        for line in open(path):
+            if not line.startswith("traffic:"):
+                continue
+            kv = dict(item.split("=", 1) for item in line.split()[1:])
+            if kv.get("family") == family and kv.get("workload") == workload and kv.get("sha256") == sha:
+                return float(kv["bytes_per_launch"])
     return None
 
 
@@ -162,6 +168,56 @@ def copy_calibration():
     ctx.close()
     print(json.dumps({"copy_calibration": {"bytes_read": count * 4, "bytes_written": count * 4,
                                            "launches": 5}}), flush=True)
+
+
+def calibrate():
+    """Achievable peaks on this GPU, reported beside the vendor figures."""
+    import ctypes
+    import torch
+    import paper_2607_07494_amd as gift
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    ctx = gift.Context()
+    out = {}
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    for mib in (1024, 4096):
+        count = mib * 1024 * 1024 // 4
+        src = torch.rand(count, device=dev).reshape(-1, 4096)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            gift.decode(ctx, None, src, dst)
+        e0, e1 = ev(), ev()
+        reps = 10
+        e0.record()
+        for _ in range(reps):
+            gift.decode(ctx, None, src, dst)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        out[f"copy_{mib}mib_gbs"] = round(2 * count * 4 / (ms * 1e-3) / 1e9, 1)
+        del src, dst
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2607_07494_amd", "libgift_calib.so"))
+    lib.gift_calib_mfma.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_int]
+    chains = lib.gift_calib_chains()
+    blocks = 256 * 8                       # 8 waves per SIMD
+    buf = torch.empty(blocks * 256, dtype=torch.float32, device=dev)
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    for kind, name, flops_per, iters in ((0, "mfma_bf16_tflops", 16384, 2000), (1, "mfma_f32_tflops", 2048, 1000)):
+        for _ in range(2):
+            assert lib.gift_calib_mfma(stream, kind, ctypes.c_void_p(buf.data_ptr()), blocks, 50) == 0
+        e0, e1 = ev(), ev()
+        e0.record()
+        assert lib.gift_calib_mfma(stream, kind, ctypes.c_void_p(buf.data_ptr()), blocks, iters) == 0
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        flops = blocks * 4.0 * iters * chains * flops_per
+        out[name] = round(flops / (ms * 1e-3) / 1e12, 1)
+    ctx.close()
+    out.update({"hbm_spec_gbs": HBM_PEAK_GBS, "mfma_bf16_spec_tflops": BF16_MFMA_TFLOPS,
+                "mfma_f32_spec_tflops": FP32_MFMA_TFLOPS})
+    print(json.dumps({"calibration": out}), flush=True)
 
 
 class Job:
@@ -556,6 +612,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.calibrate:
+        calibrate()
         return
     if args.fidelity:
         fidelity_study(args)

@@ -22,6 +22,9 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libgift.so")
 ARCH = "gfx950"
 
+CALIB_SOURCE = "calib.hip"
+CALIB_LIB = os.path.join(PKG, "libgift_calib.so")
+
 SOURCES = ["gift_api.cpp", "k_tile.hip", "k_reduce.hip", "k_factor.hip", "k_syrk.hip", "k_update.hip", "k_stream.hip",
            "k_lowrank.hip", "k_chol.hip", "k_mx.hip"]
 
@@ -47,27 +50,76 @@ def compile_flags():
     ]
 
 
+# Sources whose compiler resource report is kept (kernel-resource-usage
+# remarks), for the spill check below.
+RESOURCE_REPORT = {"k_lowrank.hip"}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
     cmd = [hipcc(), "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj] + compile_flags()
+    if src in RESOURCE_REPORT:
+        cmd.append("-Rpass-analysis=kernel-resource-usage")
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{res.stdout}\n{res.stderr}")
+    if src in RESOURCE_REPORT:
+        with open(obj + ".resources.txt", "w") as fh:
+            fh.write(res.stderr)
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    """Compile all sources and link ``libgift.so``; returns the library path."""
-    os.makedirs(BUILD, exist_ok=True)
-    workers = min(len(SOURCES), max(1, (os.cpu_count() or 2) // 2), 8)
-    with concurrent.futures.ThreadPoolExecutor(workers) as pool:
-        objs = list(pool.map(_compile, SOURCES))
-    tmp = LIB + ".tmp"
+def two_wave_scratch():
+    """{kernel: scratch bytes per lane} of the two-waves-per-SIMD update
+    variants (lr_update_kernel_o2), from the compiler's resource report."""
+    import re
+    path = os.path.join(BUILD, "k_lowrank.hip.o.resources.txt")
+    out, name = {}, None
+    for line in open(path):
+        m = re.search(r"Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+            continue
+        m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
+        if m and name and "lr_update_kernel_o2" in name:
+            out[name] = int(m.group(1))
+    return out
+
+
+def check_two_wave_spills(verbose: bool = False):
+    """The two-wave update variants exist to hold two waves per SIMD with no
+    scratch; a toolchain or code change that makes one spill would slow the
+    rank-128 encode without changing its results, so the build fails."""
+    scratch = two_wave_scratch()
+    if not scratch:
+        raise RuntimeError("no resource report for the two-wave update kernels")
+    bad = {k: v for k, v in scratch.items() if v > 0}
+    if bad:
+        raise RuntimeError("two-wave update kernels spill to scratch: " +
+                           ", ".join(f"{k} ({v} B/lane)" for k, v in sorted(bad.items())))
+    if verbose:
+        print(f"{len(scratch)} two-wave update kernels, no scratch")
+
+
+def _link(objs, out):
+    tmp = out + ".tmp"
     cmd = [hipcc(), "-shared", f"--offload-arch={ARCH}", "-fPIC", "-o", tmp] + objs
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"link failed:\n{res.stdout}\n{res.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, out)
+
+
+def build(verbose: bool = False) -> str:
+    """Compile all sources and link ``libgift.so`` (and the benchmark's peak
+    calibration kernels, ``libgift_calib.so``); returns the library path."""
+    os.makedirs(BUILD, exist_ok=True)
+    workers = min(len(SOURCES) + 1, max(1, (os.cpu_count() or 2) // 2), 8)
+    with concurrent.futures.ThreadPoolExecutor(workers) as pool:
+        objs = list(pool.map(_compile, SOURCES + [CALIB_SOURCE]))
+    _link(objs[:-1], LIB)
+    _link(objs[-1:], CALIB_LIB)
+    check_two_wave_spills(verbose)
     if verbose:
         print(f"built {LIB}")
     return LIB
