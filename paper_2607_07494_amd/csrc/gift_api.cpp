@@ -88,6 +88,50 @@ gift_status grow_buffer(gift_ctx *ctx, Workspace &w, size_t bytes, void **out) {
 
 gift_status workspace(gift_ctx *ctx, size_t bytes, void **out) { return grow_buffer(ctx, ctx->ws, bytes, out); }
 
+gift_status upload_table(gift_ctx *ctx, int kind, const void *owner, const void *host, size_t bytes,
+                         void **dev) {
+  TableSlot &t = ctx->tables[std::make_pair(kind, owner)];
+  if (t.valid && t.last.size() == bytes && memcmp(t.last.data(), host, bytes) == 0) {
+    *dev = t.dev.ptr;
+    return GIFT_OK;
+  }
+  t.valid = false;
+  void *d = nullptr;
+  gift_status st = grow_buffer(ctx, t.dev, bytes, &d);
+  if (st != GIFT_OK) return st;
+  if (t.copied) {
+    // the pinned buffer is rewritten below: its last copy must have run
+    hipError_t q = hipEventQuery(t.copied);
+    if (q == hipErrorNotReady) {
+      GIFT_HIP_TRY(hipEventSynchronize(t.copied));
+    } else if (q != hipSuccess) {
+      return hip_error(q, "upload_table: hipEventQuery");
+    }
+  } else {
+    GIFT_HIP_TRY(hipEventCreateWithFlags(&t.copied, hipEventDisableTiming));
+  }
+  if (t.pinned_bytes < bytes) {
+    if (t.pinned) GIFT_HIP_TRY(hipHostFree(t.pinned));
+    t.pinned = nullptr;
+    t.pinned_bytes = 0;
+    void *p = nullptr;
+    hipError_t e = hipHostMalloc(&p, bytes, 0);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return set_error(GIFT_ENOMEM, "upload_table: hipHostMalloc of " + std::to_string(bytes) + " bytes failed");
+    }
+    t.pinned = p;
+    t.pinned_bytes = bytes;
+  }
+  memcpy(t.pinned, host, bytes);
+  GIFT_HIP_TRY(hipMemcpyAsync(d, t.pinned, bytes, hipMemcpyHostToDevice, ctx->stream));
+  GIFT_HIP_TRY(hipEventRecord(t.copied, ctx->stream));
+  t.last.assign(static_cast<const char *>(host), static_cast<const char *>(host) + bytes);
+  t.valid = true;
+  *dev = d;
+  return GIFT_OK;
+}
+
 gift_status amax_slots(gift_ctx *ctx, size_t words, uint32_t **cur, uint32_t **other,
                        size_t *other_dirty) {
   if (words > ctx->slot_words || ctx->slots_unknown) {
@@ -418,6 +462,11 @@ void gift_ctx_destroy(gift_ctx *ctx) {
     if (ctx->ws.ptr) (void)hipFree(ctx->ws.ptr);
     if (ctx->slots.ptr) (void)hipFree(ctx->slots.ptr);
     if (ctx->xform.ptr) (void)hipFree(ctx->xform.ptr);
+    for (auto &kv : ctx->tables) {
+      if (kv.second.dev.ptr) (void)hipFree(kv.second.dev.ptr);
+      if (kv.second.pinned) (void)hipHostFree(kv.second.pinned);
+      if (kv.second.copied) (void)hipEventDestroy(kv.second.copied);
+    }
   }
   delete ctx;
 }
@@ -632,11 +681,11 @@ gift_status gift_statistics(gift_ctx *ctx, const void *x, int64_t T, int64_t dim
   if (st != GIFT_OK) return st;
   const bool widen = dtype == GIFT_BF16 && !statistics_direct(dtype, dim);
   void *ws = nullptr;
-  if ((st = workspace(ctx, 256 + (widen ? sizeof(float) * (size_t)T * dim : 0), &ws)) != GIFT_OK) return st;
-  const void **d_tab = static_cast<const void **>(ws);
-  float *Xc = widen ? reinterpret_cast<float *>(static_cast<char *>(ws) + 256) : nullptr;
-  GIFT_HIP_TRY(hipMemcpyAsync(d_tab, &x, sizeof(void *), hipMemcpyHostToDevice, ctx->stream));
-  return launch_statistics(ctx, d_tab, &x, 1, T, dim, dtype, A, Xc);
+  if ((st = workspace(ctx, widen ? sizeof(float) * (size_t)T * dim : 256, &ws)) != GIFT_OK) return st;
+  float *Xc = widen ? static_cast<float *>(ws) : nullptr;
+  void *d_tab = nullptr;
+  if ((st = upload_table(ctx, TAB_STATS, nullptr, &x, sizeof(void *), &d_tab)) != GIFT_OK) return st;
+  return launch_statistics(ctx, static_cast<const void *const *>(d_tab), &x, 1, T, dim, dtype, A, Xc);
 }
 
 gift_status gift_factor_update_batch(gift_ctx *ctx, int32_t count, gift_factor *const *factors,

@@ -4,7 +4,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <map>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "gift.h"
@@ -36,6 +38,20 @@ struct ProfileRec {
   hipEvent_t start, stop;
 };
 
+// A small device table (pointer and job tables of a launch sequence) with
+// the host image it was last uploaded from.  Uploads go through pinned host
+// memory owned by the context and happen only when the contents change, so
+// a compute call with unchanged tables makes no host-to-device copy.
+struct TableSlot {
+  Workspace dev;
+  void *pinned = nullptr;
+  size_t pinned_bytes = 0;
+  std::vector<char> last;
+  hipEvent_t copied = nullptr;   // the last copy out of `pinned`
+  bool valid = false;
+};
+enum TableKind { TAB_REFRESH = 0, TAB_STATS = 1, TAB_CHOL_STATS = 2, TAB_CHOL_BLOCKS = 3 };
+
 }  // namespace gift
 
 struct gift_ctx {
@@ -61,6 +77,8 @@ struct gift_ctx {
   // set for the duration of an allocation-free call: no profiling events
   // are created or recorded
   bool no_alloc_call = false;
+  // device tables by (kind, owner), see TableSlot
+  std::map<std::pair<int, const void *>, gift::TableSlot> tables;
 };
 
 namespace gift {
@@ -314,5 +332,10 @@ gift_status launch_mx_reduce(gift_ctx *ctx, const uint8_t *codes, const uint8_t 
                              int64_t per_rank, float *mean);
 // Grow-only device buffer (synchronizes the stream before it frees the old one).
 gift_status grow_buffer(gift_ctx *ctx, Workspace &w, size_t bytes, void **out);
+// Device copy of a small host table for (kind, owner): the cached copy when
+// the bytes equal the last upload, else an asynchronous upload through the
+// context's pinned buffer (waiting first for that buffer's previous copy).
+gift_status upload_table(gift_ctx *ctx, int kind, const void *owner, const void *host, size_t bytes,
+                         void **dev);
 
 }  // namespace gift

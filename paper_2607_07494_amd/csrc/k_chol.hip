@@ -188,12 +188,14 @@ gift_status chol_side_update(gift_ctx *ctx, CholSide &s, const void *x, int64_t 
   // statistics A = X^T X / T into the side's own buffer
   const bool widen = dtype == GIFT_BF16 && !statistics_direct(dtype, dim);
   void *ws = nullptr;
-  gift_status st = workspace(ctx, 256 + (widen ? sizeof(float) * (size_t)T * dim : 0), &ws);
+  gift_status st = workspace(ctx, widen ? sizeof(float) * (size_t)T * dim : 256, &ws);
   if (st != GIFT_OK) return st;
-  const void **d_tab = static_cast<const void **>(ws);
-  float *Xc = widen ? reinterpret_cast<float *>(static_cast<char *>(ws) + 256) : nullptr;
-  GIFT_HIP_TRY(hipMemcpyAsync(d_tab, &x, sizeof(void *), hipMemcpyHostToDevice, ctx->stream));
-  if ((st = launch_statistics(ctx, d_tab, &x, 1, T, dim, dtype, s.A, Xc)) != GIFT_OK) return st;
+  float *Xc = widen ? static_cast<float *>(ws) : nullptr;
+  void *d_tab = nullptr;
+  if ((st = upload_table(ctx, TAB_CHOL_STATS, &s, &x, sizeof(void *), &d_tab)) != GIFT_OK) return st;
+  if ((st = launch_statistics(ctx, static_cast<const void *const *>(d_tab), &x, 1, T, dim, dtype, s.A, Xc)) !=
+      GIFT_OK)
+    return st;
   {
     ProfileScope prof(ctx, GIFT_KERNEL_SMALL);
     hipLaunchKernelGGL(chol_shift_kernel, dim3(1), dim3(kShiftThreads), 0, ctx->stream, s.A, dim, damping,

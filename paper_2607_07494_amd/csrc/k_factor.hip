@@ -956,8 +956,8 @@ gift_status factor_refresh_batch(gift_ctx *ctx, const std::vector<SideJob> &jobs
   const void **d_xt = reinterpret_cast<const void **>(b + o_xt);
   hipStream_t stream = ctx->stream;
 
-  // host copies of the tables (copied from pageable memory: staged before
-  // hipMemcpyAsync returns)
+  // host image of the tables, uploaded (through the context's pinned
+  // buffer) only when it differs from the last refresh's on this context
   std::vector<char> host(tables_bytes, 0);
   Member *h_mem = reinterpret_cast<Member *>(host.data() + o_mem);
   SmallJob *h_chol = reinterpret_cast<SmallJob *>(host.data() + o_chol);
@@ -1017,7 +1017,16 @@ gift_status factor_refresh_batch(gift_ctx *ctx, const std::vector<SideJob> &jobs
       h_xt[g.first + m] = g.jobs[m].x;
     }
   }
-  GIFT_HIP_TRY(hipMemcpyAsync(b, host.data(), tables_bytes, hipMemcpyHostToDevice, stream));
+  {
+    void *tb = nullptr;
+    if ((st = upload_table(ctx, TAB_REFRESH, nullptr, host.data(), tables_bytes, &tb)) != GIFT_OK) return st;
+    char *t = static_cast<char *>(tb);
+    d_mem = reinterpret_cast<Member *>(t + o_mem);
+    d_chol = reinterpret_cast<SmallJob *>(t + o_chol);
+    d_eig = reinterpret_cast<SmallJob *>(t + o_eig);
+    d_xt = reinterpret_cast<const void **>(t + o_xt);
+    for (Group &g : groups) g.xtab = d_xt + g.first;
+  }
 
   // 1. statistics A_g = X_g^T X_g / T
   for (Group &g : groups) {
@@ -1164,7 +1173,7 @@ gift_status factor_refresh_batch(gift_ctx *ctx, const std::vector<SideJob> &jobs
 
 size_t chol_blocks_scratch(int k, int count) {
   auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  size_t b = a256(sizeof(SmallJob) * (size_t)count);
+  size_t b = 256;
   if (k > kLdsK)
     b += a256(sizeof(double) * (size_t)count * k * (k + 1)) + a256(sizeof(double) * (size_t)count * (2 * k + 64));
   return b;
@@ -1175,8 +1184,6 @@ gift_status launch_chol_blocks(gift_ctx *ctx, const float *G, int k, int count, 
   if (count <= 0 || k <= 0) return GIFT_OK;
   auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
   char *p = static_cast<char *>(scratch);
-  SmallJob *d_tab = reinterpret_cast<SmallJob *>(p);
-  p += a256(sizeof(SmallJob) * (size_t)count);
   double *W = nullptr, *aux = nullptr;
   if (k > kLdsK) {
     W = reinterpret_cast<double *>(p);
@@ -1196,9 +1203,11 @@ gift_status launch_chol_blocks(gift_ctx *ctx, const float *G, int k, int count, 
     J.ks = 1;
     J.k = k;
   }
-  // from pageable memory: staged before hipMemcpyAsync returns
-  GIFT_HIP_TRY(hipMemcpyAsync(d_tab, h.data(), sizeof(SmallJob) * (size_t)count, hipMemcpyHostToDevice,
-                              ctx->stream));
+  // the job table of these blocks (the factors written, R, identify it)
+  void *tab = nullptr;
+  gift_status st = upload_table(ctx, TAB_CHOL_BLOCKS, R, h.data(), sizeof(SmallJob) * (size_t)count, &tab);
+  if (st != GIFT_OK) return st;
+  const SmallJob *d_tab = static_cast<const SmallJob *>(tab);
   ProfileScope prof(ctx, GIFT_KERNEL_CHOL);
   if (k <= kLdsK)
     hipLaunchKernelGGL(chol_inv_lds_kernel, dim3(count), dim3(kSmallThreads), 0, ctx->stream, d_tab);
