@@ -304,10 +304,15 @@ __device__ __forceinline__ void lr_update_body(const LUArgs &p) {
   constexpr int SLOTS = TILES * TSLOTS;         // the workgroup's whole column range
   constexpr int PER = SLOTS / kUpdThreads;      // = TILES * NCH
   __shared__ uint4 chi[SLOTS], clo[SLOTS];
-  // QUANT: a wave's 32 x 64 tile of codes, written in the matrix-core layout
-  // (4 bytes per lane and 16-column group) and read back as 16 consecutive
-  // codes per lane, so the global stores are 16 bytes wide
-  __shared__ uint32_t cstage[EPI == EPI_QUANT ? kUpdThreads / 64 : 1][32 * 16];
+  // QUANT: a wave's codes of two consecutive 32 x 64 tiles (one, when the
+  // range holds one tile), written in the matrix-core layout (4 bytes per
+  // lane and 16-column group) and read back as 16 consecutive codes per
+  // lane: the global stores are 16 bytes wide and each row's 128 codes of a
+  // tile pair leave in one instruction, whole 128-byte lines (a half line
+  // would make the cache fetch the other half from HBM before merging it)
+  constexpr bool PAIR = TILES >= 2;
+  constexpr int CW = PAIR ? 32 : 16;            // staged words per row
+  __shared__ uint32_t cstage[EPI == EPI_QUANT ? kUpdThreads / 64 : 1][32 * CW];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int fr = lane & 15, fg = lane >> 4;
   // the column units of one row block on one XCD, one after another, so
@@ -678,31 +683,37 @@ __device__ __forceinline__ void lr_update_body(const LUArgs &p) {
                 for (int e = 0; e < 4; ++e) res[e] = w[g][t][e] - q[e] * sc[e];
               }
               const int64_t off = (int64_t)b * MN + ri[g] * p.N + cj;
-              cstage[wave][(16 * g + fr) * 16 + 4 * t + fg] = packed;
+              cstage[wave][(16 * g + fr) * CW + (PAIR ? 16 * (ct & 1) : 0) + 4 * t + fg] = packed;
               if (EF)
                 st_u128_untracked(p.ef + off, make_uint4(__float_as_uint(res[0]), __float_as_uint(res[1]),
                                                          __float_as_uint(res[2]), __float_as_uint(res[3])));
             }
-          // the wave reads back only what its own lanes wrote: the fences
-          // order these LDS accesses (no workgroup barrier)
-          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+          // a pair is stored after its second tile, or after a last tile
+          // without a partner (its missing half lies past N)
+          if (!PAIR || (ct & 1) || ct + 1 == ntiles) {
+            // the wave reads back only what its own lanes wrote: the fences
+            // order these LDS accesses (no workgroup barrier)
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+            const int64_t jp = PAIR ? j0 - 64 * (ct & 1) : j0;   // first column staged
+            constexpr int QPR = CW / 4;                          // 16-byte chunks per row
 #pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const int c = lane + 64 * h;           // 16-byte chunk: row c / 4, column quarter c % 4
-            const int row = c >> 2, qt = c & 3;
-            const int64_t gi = i0 + row;
-            const int64_t cj = j0 + 16 * qt;
-            const uint4 v = *reinterpret_cast<const uint4 *>(&cstage[wave][row * 16 + 4 * qt]);
-            if (gi < p.M) {
-              uint8_t *dst = p.codes + (int64_t)b * MN + gi * p.N + cj;
-              if (FULL || (p.codes_wide && cj + 16 <= p.N)) {
-                st_u128_untracked(dst, v);
-              } else {
-                const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+            for (int h = 0; h < 32 * QPR / 64; ++h) {
+              const int c = lane + 64 * h;         // 16-byte chunk: row c / QPR, chunk c % QPR
+              const int row = c / QPR, qt = c % QPR;
+              const int64_t gi = i0 + row;
+              const int64_t cj = jp + 16 * qt;
+              const uint4 v = *reinterpret_cast<const uint4 *>(&cstage[wave][row * CW + 4 * qt]);
+              if (gi < p.M) {
+                uint8_t *dst = p.codes + (int64_t)b * MN + gi * p.N + cj;
+                if (FULL || (p.codes_wide && cj + 16 <= p.N)) {
+                  st_u128_untracked(dst, v);
+                } else {
+                  const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-                for (int q = 0; q < 4; ++q)
-                  if (cj + 4 * q < p.N) st_u32_untracked(dst + 4 * q, wv[q]);
+                  for (int q = 0; q < 4; ++q)
+                    if (cj + 4 * q < p.N) st_u32_untracked(dst + 4 * q, wv[q]);
+                }
               }
             }
           }
