@@ -777,7 +777,13 @@ def main():
                 r0, q0 = fam_raw.get(name, (0, 0.0))
                 fam_raw[name] = (r0 + launches, q0 + ms)
     profile_all(False)
-    dom = max(fam_ms, key=lambda k: fam_ms[k][1])
+    # the dominant kernel: the family with the most time per step among
+    # those with a roofline (algorithmic bytes or flops); the refresh's
+    # one-workgroup-per-factor k x k kernels (chol, eig) are latency-bound
+    work = algorithmic_work(wl, jobs, args)
+    with_roof = [k for k in fam_ms if sum(work.get(k, (0.0, 0.0))) > 0]
+    dom = max(with_roof or list(fam_ms), key=lambda k: fam_ms[k][1])
+    latency_ms = {k: round(fam_ms[k][1], 4) for k in fam_ms if k not in with_roof}
 
     # timed region: events around every step (refresh steps and codec-only
     # steps are timed apart), and around the dominant family's launches
@@ -821,7 +827,6 @@ def main():
 
     grad_bytes = sum(j.N * j.m * j.n * 4 for j in jobs)
     value = grad_bytes / (ms_step * 1e-3) / 1e9
-    work = algorithmic_work(wl, jobs, args)
     kernels = {}
     for name, (launches, ms) in fam_ms.items():
         fl, by = work.get(name, (0.0, 0.0))
@@ -893,6 +898,7 @@ def main():
         "kernels": kernels,
         "kernels_note": "per-family time per step (refresh amortised over the cadence) from an untimed "
                         "pass with every launch on one stream",
+        "latency_bound_ms_per_step": latency_ms,
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
