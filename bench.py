@@ -22,7 +22,8 @@ around each step), and ``ms_per_step`` / ``value`` are the cadence's average
 
 Independent matrices are spread over several HIP streams (one library
 context each): a matrix's encode, rank sum and decode stay in order on its
-stream.  The factor refresh runs once per factor shape (the smallest group on
+stream, and each stream decodes its same-shape matrices in one grouped call
+after their rank sums.  The factor refresh runs once per factor shape (the smallest group on
 the main stream, the others on further streams), and a GIFT matrix's encode
 waits only for its own group's refresh; the Euclidean matrices run beside the
 refresh.
@@ -105,6 +106,9 @@ def parse():
     ap.add_argument("--fid-shape", type=int, nargs=2, default=[1024, 2816], metavar=("M", "N"),
                     help="layer of the fidelity study (d_out d_in; default the MLP down projection)")
     ap.add_argument("--fid-tokens", type=int, default=8192)
+    ap.add_argument("--decode", choices=["batch", "each"], default="batch",
+                    help="batch: each stream decodes its same-shape buckets in one gift_decode_batch call "
+                         "after their rank sums; each: one gift_decode per bucket right after its rank sum")
     ap.add_argument("--ef", action="store_true",
                     help="error feedback on the GIFT matrices (Algorithm 1: U~ = U + R, R <- U~ - Deq(Q(U~))), "
                          "a float32 residual per rank and element kept across steps")
@@ -709,6 +713,7 @@ def main():
             ready[k] = (sid, torch.cuda.Event())
             ready[k][1].record(streams[sid])
         waited = set()
+        pending = {}   # (stream, shape) -> buckets whose decode is grouped
         for jb in (order if codec else ()):
             sid = 0 if serial else jb.sid
             if not jb.gift_branch and args.issue == "euclid-after-refresh" and not serial and ready:
@@ -734,7 +739,16 @@ def main():
                             gift.SCALE_LOCAL if jb.gift_branch else gift.SCALE_SHARED, ef=jb.ef)
                 gift.reduce_local(c, jb.codes, jb.scales, jb.mean, jb.br, jb.bc)
             if jb.gift_branch:
-                gift.decode(c, jb.factor, jb.mean, jb.out)
+                if args.decode == "batch":
+                    # (buckets are issued in layer order, so the streams run a
+                    # mix of shapes at any time; each stream decodes its
+                    # buckets of a shape together once it has summed them all)
+                    pending.setdefault((sid, jb.m, jb.n), []).append(jb)
+                else:
+                    gift.decode(c, jb.factor, jb.mean, jb.out)
+        for (sid, _, _), jbs in pending.items():
+            gift.decode_batch(ctxs[sid], [jb.factor for jb in jbs], [jb.mean for jb in jbs],
+                              [jb.out for jb in jbs])
 
     for w in range(max(args.warmup, 1)):
         step(args.cold_iters if w == 0 else args.iters)
@@ -892,7 +906,7 @@ def main():
                    "factors": sum(1 for jb in jobs if jb.owns_factor), "streams": nstreams,
                    "grad_gb": round(grad_bytes / 1e9, 3), "factor_refresh_every": wl.refresh,
                    "refreshes_timed": len(ref_ms), "subspace_iters": args.iters,
-                   "mall_flushed": bool(args.flush_mall)},
+                   "mall_flushed": bool(args.flush_mall), "decode": args.decode},
         "transform_tflops": round(tf_flops / (tf_ms * 1e-3) / 1e12, 3) if tf_ms else None,
         "roofline": roof,
         "kernels": kernels,

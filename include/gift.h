@@ -358,6 +358,24 @@ gift_status gift_reduce_local(gift_ctx *ctx, const uint8_t *codes, const float *
 gift_status gift_decode(gift_ctx *ctx, const gift_factor *f, const float *mean,
                         int64_t m, int64_t n, float *out);
 
+/* gift_decode of many matrices of one shape in one call (the inverse
+ * transform of eq. design_input_side_inverse for every matrix of a gradient
+ * bucket set, Algorithm 1's last step): out[i] = decode(factors[i], means[i]).
+ * factors, means and outs are HOST arrays of count device handles /
+ * pointers; every mean and out is [m, n] float32, outs distinct and not
+ * aliasing their means.  When every factor is a low-rank input-side factor
+ * of one rank r in {16, 32, 64, 128} (and the buffers are 16-byte aligned),
+ * each pass runs as one launch over all matrices with the kernels,
+ * split-K partials and summation order of gift_decode, so the results equal
+ * count separate gift_decode calls bit for bit; the per-matrix operand
+ * pointers come from a device table the context uploads (through its pinned
+ * buffer) only when they change.  Otherwise the call runs count gift_decode
+ * calls.  Uses the context workspace (count * parts * m * r floats of
+ * projections).  Errors: as gift_decode; GIFT_EINVAL for NULL arrays, a
+ * count outside [0, 65535] or an output listed twice. */
+gift_status gift_decode_batch(gift_ctx *ctx, int32_t count, const gift_factor *const *factors,
+                              const float *const *means, float *const *outs, int64_t m, int64_t n);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1230,4 +1230,90 @@ gift_status gift_decode(gift_ctx *ctx, const gift_factor *f, const float *mean, 
   return launch_tile(ctx, job);
 }
 
+gift_status gift_decode_batch(gift_ctx *ctx, int32_t count, const gift_factor *const *factors,
+                              const float *const *means, float *const *outs, int64_t m, int64_t n) {
+  if (!ctx) return set_error(GIFT_EINVAL, "gift_decode_batch: ctx is NULL");
+  if (count < 0 || count > kMaxRanks)
+    return set_error(GIFT_EINVAL, "gift_decode_batch: count must be in [0, 65535]");
+  if (count == 0) return GIFT_OK;
+  if (!factors || !means || !outs) return set_error(GIFT_EINVAL, "gift_decode_batch: NULL array");
+  gift_status st = check_matrix_dims(m, n);
+  if (st != GIFT_OK) return st;
+  for (int32_t i = 0; i < count; ++i) {
+    if (!means[i] || !outs[i]) return set_error(GIFT_EINVAL, "gift_decode_batch: NULL tensor");
+    if (means[i] == outs[i]) return set_error(GIFT_EINVAL, "gift_decode_batch: out must not alias mean");
+    if (factors[i] && (factors[i]->m != m || factors[i]->n != n))
+      return set_error(GIFT_ESHAPE, "gift_decode_batch: factor was created for another shape");
+    for (int32_t j = 0; j < i; ++j)
+      if (outs[j] == outs[i]) return set_error(GIFT_EINVAL, "gift_decode_batch: an output appears twice");
+  }
+  if ((st = bind_device(ctx)) != GIFT_OK) return st;
+  // one launch per pass for input-side low-rank factors of one rank: the
+  // kernels, split-K partials and summation order of gift_decode, with the
+  // batch index running over the matrices
+  const gift_factor *f0 = factors[0];
+  bool grouped = count > 1 && f0 && !f0->chol && f0->A.r > 0 && f0->G.r == 0 && n % 4 == 0 &&
+                 m * n < (1LL << 29);
+  const int32_t r = grouped ? f0->A.r : 0;
+  if (grouped && r != 16 && r != 32 && r != 64 && r != 128) grouped = false;
+  for (int32_t i = 0; grouped && i < count; ++i) {
+    const gift_factor *f = factors[i];
+    grouped = f && !f->chol && f->A.r == r && f->G.r == 0 && al16p(means[i]) && al16p(outs[i]);
+  }
+  TileJob pj, uj;
+  int pparts = 1;
+  if (grouped) {
+    pparts = proj_parts(m, n, r, 1);
+    pj.nseg = 1;
+    pj.seg[0].a = Operand{means[0], n, 0, true};
+    pj.seg[0].b = Operand{f0->A.Ut, n, 0, true};
+    pj.seg[0].K = n;
+    pj.M = m;
+    pj.N = r;
+    pj.batch = count;
+    pj.ldc = r;
+    pj.cbs = m * r;
+    pj.ksplit = pparts;
+    pj.kernel_family = GIFT_KERNEL_DECODE_PROJECT;
+    grouped = proj_staged_eligible(pj);
+  }
+  if (!grouped) {
+    for (int32_t i = 0; i < count; ++i)
+      if ((st = gift_decode(ctx, factors[i], means[i], m, n, outs[i])) != GIFT_OK) return st;
+    return GIFT_OK;
+  }
+  void *ws = nullptr;
+  if ((st = workspace(ctx, sizeof(float) * (size_t)count * pparts * m * r, &ws)) != GIFT_OK) return st;
+  float *P = static_cast<float *>(ws);
+  std::vector<DecodePtrs> host(count);
+  for (int32_t i = 0; i < count; ++i)
+    host[i] = DecodePtrs{means[i], factors[i]->A.Ut, factors[i]->A.Uci, outs[i]};
+  void *tab = nullptr;
+  if ((st = upload_table(ctx, TAB_DECODE, f0, host.data(), sizeof(DecodePtrs) * (size_t)count, &tab)) != GIFT_OK)
+    return st;
+  const DecodePtrs *d_tab = static_cast<const DecodePtrs *>(tab);
+  pj.C = P;
+  pj.decode_tab = d_tab;
+  if ((st = launch_proj(ctx, pj)) != GIFT_OK) return st;
+  uj.nseg = 1;
+  uj.seg[0].a = Operand{P, r, m * r, true, pparts};
+  uj.seg[0].b = Operand{f0->A.Uci, r, 0, true};
+  uj.seg[0].K = r;
+  uj.M = m;
+  uj.N = n;
+  uj.batch = count;
+  uj.C = outs[0];
+  uj.ldc = n;
+  uj.cbs = m * n;
+  uj.D = means[0];
+  uj.ldd = n;
+  uj.dbs = m * n;
+  uj.beta = 1.f;
+  uj.kernel_family = GIFT_KERNEL_UPDATE_STORE;
+  uj.decode_tab = d_tab;
+  if (!update_kernel_eligible(uj))
+    return set_error(GIFT_EUNSUPPORTED, "gift_decode_batch: internal: update kernel not applicable");
+  return launch_update(ctx, uj);
+}
+
 }  // extern "C"

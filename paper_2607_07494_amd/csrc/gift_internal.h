@@ -50,7 +50,16 @@ struct TableSlot {
   hipEvent_t copied = nullptr;   // the last copy out of `pinned`
   bool valid = false;
 };
-enum TableKind { TAB_REFRESH = 0, TAB_STATS = 1, TAB_CHOL_STATS = 2, TAB_CHOL_BLOCKS = 3 };
+enum TableKind { TAB_REFRESH = 0, TAB_STATS = 1, TAB_CHOL_STATS = 2, TAB_CHOL_BLOCKS = 3, TAB_DECODE = 4 };
+
+// Per-matrix operands of a grouped decode (one batch entry per matrix): the
+// rank mean, the factor's U^T and U diag(c'), and the output.
+struct DecodePtrs {
+  const float *mean;
+  const float *ut;
+  const float *uci;
+  float *out;
+};
 
 }  // namespace gift
 
@@ -229,6 +238,10 @@ struct TileJob {
   // matrix cores (k_lowrank.hip) where the shapes allow; float32 otherwise
   bool split3 = false;
   int kernel_family = GIFT_KERNEL_FACTOR;
+  // grouped decode (k_update.hip kernels only): batch entry b takes its
+  // mean / U^T (projection) and U diag(c') / mean / output (update) from
+  // decode_tab[b] (device) instead of base + b * stride
+  const DecodePtrs *decode_tab = nullptr;
 };
 
 gift_status launch_tile(gift_ctx *ctx, const TileJob &job);
@@ -250,6 +263,9 @@ gift_status launch_lr_psum(gift_ctx *ctx, const float *partials, float *out, int
 bool update_kernel_eligible(const TileJob &job);
 gift_status launch_update(gift_ctx *ctx, const TileJob &job);
 bool proj_kernel_eligible(const TileJob &job);
+// launch_proj takes the LDS-staged projection kernel (the one that reads a
+// grouped decode's table) for this job
+bool proj_staged_eligible(const TileJob &job);
 // k_stream.hip: streaming Euclidean amax / quantize and rank sum
 bool stream_eligible(int64_t m, int64_t n, const BlockGeom &g, const void *x, const void *codes,
                      const void *a, const void *b);

@@ -67,6 +67,7 @@ struct UArgs {
   int64_t br, bc;
   int nbr, nbc;
   int shared;
+  const DecodePtrs *tab;  // grouped decode: per-entry column operand, D and C
 };
 
 __device__ __forceinline__ float4 ld4(const float *p) { return *reinterpret_cast<const float4 *>(p); }
@@ -168,7 +169,8 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const UArgs p) {
       const int64_t cj = j0 + col;
       // clamped address, unconditional load; columns past N are zeroed when
       // the tile goes to LDS
-      creg[u] = ld4(p.seg[s].col + (int64_t)b * p.seg[s].col_bs + (cj < p.N ? cj : 0) * p.seg[s].col_ld + kk);
+      const float *colb = p.tab ? p.tab[b].uci : p.seg[s].col + (int64_t)b * p.seg[s].col_bs;
+      creg[u] = ld4(colb + (cj < p.N ? cj : 0) * p.seg[s].col_ld + kk);
     }
   };
   auto store_cols = [&](int buf, int64_t j0) {
@@ -182,8 +184,10 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const UArgs p) {
   };
   // W (and residual) by unconditional buffer loads over this rank's slice:
   // rows past M read zeros, columns past N are left out by the epilogue
+  const float *Db = p.tab ? p.tab[b].mean : p.D + (int64_t)b * MN;
+  float *Cb = p.tab ? p.tab[b].out : (p.C ? p.C + (int64_t)b * MN : nullptr);
   const __amdgpu_buffer_rsrc_t rsD =
-      __builtin_amdgcn_make_buffer_rsrc((void *)(p.D + (int64_t)b * MN), (short)0, (int)(MN * 4), 0x00020000);
+      __builtin_amdgcn_make_buffer_rsrc((void *)Db, (short)0, (int)(MN * 4), 0x00020000);
   const __amdgpu_buffer_rsrc_t rsE = __builtin_amdgcn_make_buffer_rsrc(
       (void *)(EF ? p.ef + (int64_t)b * MN : p.D), (short)0, EF ? (int)(MN * 4) : 0, 0x00020000);
   const uint32_t roff = rv ? (uint32_t)(ri * p.N * 4) : 0x80000000u;
@@ -263,7 +267,7 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const UArgs p) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           const int64_t cj = j0 + 16 * t + 4 * fg;
-          if (rv && cj < p.N) st4_untracked(p.C + (int64_t)b * MN + ri * p.N + cj, w[t][0], w[t][1], w[t][2], w[t][3]);
+          if (rv && cj < p.N) st4_untracked(Cb + ri * p.N + cj, w[t][0], w[t][1], w[t][2], w[t][3]);
         }
       } else {
         // scale-block geometry of this wave tile (wave-uniform, two divisions)
@@ -372,6 +376,7 @@ struct PArgs {
   float *out;         // [batch][M][C], or [batch][C][M] when out_t
   int64_t out_ld, out_bs;
   int out_t;
+  const DecodePtrs *tab;  // grouped decode: per-entry X (mean) and Y (U^T)
 };
 
 // KS waves of a workgroup share one 16-row strip and split K; 4 / KS strips
@@ -490,8 +495,8 @@ __global__ __launch_bounds__(kThreads) void proj_staged_kernel(const PArgs p, in
   const int64_t kper = ((p.K + parts - 1) / parts + KC - 1) / KC * KC;
   const int64_t k0 = z * kper, k1 = k0 + kper < p.K ? k0 + kper : p.K;
   const int nchunks = k1 > k0 ? (int)((k1 - k0 + KC - 1) / KC) : 0;
-  const float *xrow = p.X + (int64_t)b * p.x_bs + ri * p.x_ld;
-  const float *yb = p.Y + (int64_t)b * p.y_bs;
+  const float *xrow = (p.tab ? p.tab[b].mean : p.X + (int64_t)b * p.x_bs) + ri * p.x_ld;
+  const float *yb = p.tab ? p.tab[b].ut : p.Y + (int64_t)b * p.y_bs;
   float4 yreg[PER], xn[4];
   auto load_y = [&](int64_t kc) {
 #pragma unroll
@@ -583,6 +588,8 @@ int proj_parts(int64_t M, int64_t K, int C, int32_t batch) {
   return parts;
 }
 
+bool proj_staged_eligible(const TileJob &j) { return proj_kernel_eligible(j) && staged_eligible(j); }
+
 bool update_kernel_eligible(const TileJob &j) {
   if (j.N % 4 != 0 || j.nseg < 1 || j.nseg > 2) return false;
   if (j.M * j.N >= (1LL << 29)) return false;   // one rank's slice within a 32-bit buffer range
@@ -634,6 +641,7 @@ gift_status launch_update(gift_ctx *ctx, const TileJob &j) {
   a.nbr = j.geom.nbr;
   a.nbc = j.geom.nbc;
   a.shared = j.shared ? 1 : 0;
+  a.tab = j.decode_tab;
   ProfileScope prof(ctx, j.kernel_family);
   dim3 grid((unsigned)((j.N + kColsPerUnit - 1) / kColsPerUnit), (unsigned)((j.M + 63) / 64),
             (unsigned)j.batch);
@@ -705,6 +713,7 @@ gift_status launch_proj(gift_ctx *ctx, const TileJob &j) {
   a.out_ld = j.ldc;
   a.out_bs = j.cbs;
   a.out_t = tr ? 1 : 0;
+  a.tab = j.decode_tab;
   ProfileScope prof(ctx, j.kernel_family);
   if (staged_eligible(j)) {
     const int parts = j.ksplit > 1 ? j.ksplit : 1;

@@ -79,6 +79,7 @@ def _load():
         "gift_encode_mxfp4": ([P, P, P, I32, I64, I64, P, P, P, P], I32),
         "gift_reduce_local_mxfp4": ([P, P, P, I32, I64, I64, P], I32),
         "gift_decode": ([P, P, P, I64, I64, P], I32),
+        "gift_decode_batch": ([P, I32, P, P, P, I64, I64], I32),
     }
     for name, (args, res) in sigs.items():
         fn = getattr(lib, name)
@@ -488,3 +489,26 @@ def decode(ctx: Context, factor, mean, out):
     _expect(out, (m, n), "out")
     _check(LIB.gift_decode(ctx.handle, factor.handle if factor is not None else None,
                            _ptr(mean, torch.float32, "mean"), m, n, _ptr(out, torch.float32, "out")))
+
+
+def decode_batch(ctx: Context, factors, means, outs):
+    """``gift_decode_batch``: ``outs[i] = decode(factors[i], means[i])`` for
+    matrices of one shape, one launch per pass when the factors allow."""
+    import torch
+    count = len(means)
+    if len(factors) != count or len(outs) != count:
+        raise ValueError("factors, means and outs must have one entry per matrix")
+    if count == 0:
+        return
+    m, n = _dims(means[0], 2, "means[0]")
+    for i in range(count):
+        _expect(means[i], (m, n), f"means[{i}]")
+        _expect(outs[i], (m, n), f"outs[{i}]")
+        f = factors[i]
+        if f is not None and (f.m, f.n) != (m, n):
+            raise ValueError(f"factor {i} was created for {f.m} x {f.n}, not {m} x {n}")
+    arr = ctypes.c_void_p * count
+    fa = arr(*[(f.handle.value if f is not None else None) for f in factors])
+    ma = arr(*[_ptr(t, torch.float32, "means").value for t in means])
+    oa = arr(*[_ptr(t, torch.float32, "outs").value for t in outs])
+    _check(LIB.gift_decode_batch(ctx.handle, count, fa, ma, oa, m, n))

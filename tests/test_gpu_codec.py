@@ -413,3 +413,39 @@ def test_error_feedback_two_steps(ctx, N, m, n, r, sides, br, bc):
         R_prev = R_new
     if f is not None:
         f.close()
+
+
+@pytest.mark.parametrize("label,m,n,ranks,sides,nulls", [
+    ("grouped r=128", 300, 512, [128, 128, 128], gift.SIDE_INPUT, []),
+    ("grouped r=64, ragged rows", 333, 256, [64] * 5, gift.SIDE_INPUT, []),
+    ("grouped r=16", 520, 384, [16, 16], gift.SIDE_INPUT, []),
+    ("mixed ranks: per-matrix calls", 300, 256, [32, 64], gift.SIDE_INPUT, []),
+    ("two-sided: per-matrix calls", 200, 256, [32, 32], gift.SIDE_BOTH, []),
+    ("identity entry: per-matrix calls", 300, 256, [64, 64, 64], gift.SIDE_INPUT, [1]),
+])
+def test_decode_batch_equals_separate_decodes(ctx, label, m, n, ranks, sides, nulls):
+    """gift_decode_batch over matrices of one shape gives exactly what one
+    gift_decode per matrix gives (the grouped launch runs the same kernels,
+    split-K partials and summation order), also after the factors change."""
+    say(f"decode batch: {label} m={m} n={n} ranks={ranks}")
+    fs = [None if i in nulls else make_factor(ctx, m, n, r, sides, seed=17 * i + m)[0]
+          for i, r in enumerate(ranks)]
+    means = [t(gradient_set(700 + i, 710 + i, 1, m, n)[0]) for i in range(len(ranks))]
+    for rep in range(2):
+        outs = [torch.full((m, n), float("nan"), device=DEV) for _ in ranks]
+        refs = [torch.empty((m, n), device=DEV) for _ in ranks]
+        gift.decode_batch(ctx, fs, means, outs)
+        for f, mean, ref in zip(fs, means, refs):
+            gift.decode(ctx, f, mean, ref)
+        torch.cuda.synchronize()
+        for o, ref in zip(outs, refs):
+            assert torch.equal(o, ref)
+        # a refreshed factor set (new pointers' contents, same table)
+        for f, r in zip(fs, ranks):
+            if f is not None and sides == gift.SIDE_INPUT:
+                fA = codec.lowrank_factor(codec.factor_statistics(factor_inputs(900 + rep, 4 * n, n)[0]), r).to_f32()
+                f.import_(gift.SIDE_INPUT, t(fA.U.astype(np.float32)), t(fA.c_fwd.astype(np.float32)),
+                          t(fA.c_inv.astype(np.float32)), t(np.array([fA.sigma2], np.float32)))
+    for f in fs:
+        if f is not None:
+            f.close()
