@@ -71,7 +71,8 @@ def _compile(src: str) -> str:
 
 def two_wave_scratch():
     """{kernel: scratch bytes per lane} of the two-waves-per-SIMD update
-    variants (lr_update_kernel_o2), from the compiler's resource report."""
+    variants (lr_update_kernel_o2, lr_sweep_kernel), from the compiler's
+    resource report."""
     import re
     path = os.path.join(BUILD, "k_lowrank.hip.o.resources.txt")
     out, name = {}, None
@@ -81,7 +82,7 @@ def two_wave_scratch():
             name = m.group(1)
             continue
         m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
-        if m and name and "lr_update_kernel_o2" in name:
+        if m and name and ("lr_update_kernel_o2" in name or "lr_sweep_kernel" in name):
             out[name] = int(m.group(1))
     return out
 

@@ -315,6 +315,14 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
     L2 = reinterpret_cast<float *>(ws + off);
     off += a256(sizeof(float) * N * m * A.r);
   }
+  // the forward update of the input side alone: its column operand as the
+  // sweep kernel's LDS image
+  const size_t img_bytes = !inverse && useA && !useG ? lr_col_image_bytes(n, A.r) : 0;
+  void *img = nullptr;
+  if (img_bytes) {
+    img = ws + off;
+    off += a256(img_bytes);
+  }
   *used = off;
   if (ws == nullptr) return GIFT_OK;  // sizing pass
   gift_status st;
@@ -412,11 +420,14 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
     } else if (presum) {  // P (C_A U_A^T), P already summed
       s.a = Operand{Psum, A.r, m * A.r, true, 1};
       s.b = Operand{A.Uc, A.r, 0, true};
+      u.col_img = img;
     } else {  // P (C_A U_A^T), P summed from its partials
       s.a = Operand{P, A.r, m * A.r, true, pparts};
       s.b = Operand{inverse ? A.Uci : A.Uc, A.r, 0, true};
+      if (!inverse) u.col_img = img;
     }
     s.K = A.r;
+    if (u.col_img && (st = launch_lr_col_image(ctx, A.Uc, A.r, n, (int)A.r, img)) != GIFT_OK) return st;
   }
   return GIFT_OK;
 }

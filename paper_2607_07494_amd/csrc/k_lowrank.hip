@@ -292,6 +292,8 @@ struct LUArgs {
   int shared, batch;
   uint8_t *mx_codes;    // MX: packed E2M1 codes [batch][M][N/2]
   uint8_t *mx_scales;   // MX: E8M0 scales [batch][M][N/32]
+  int upw;              // sweep variant: 128 x 128 units per workgroup
+  const void *col_img;  // sweep variant: the column operand's LDS image
 };
 
 template <int EPI, bool EF, int NSEG, int KC, bool FULL>
@@ -783,6 +785,304 @@ __global__ __launch_bounds__(kUpdThreads) __attribute__((amdgpu_waves_per_eu(2, 
   lr_update_body<EPI, EF, NSEG, KC, FULL>(p);
 }
 
+#define GIFT_LDS __attribute__((address_space(3)))
+
+// s_waitcnt vmcnt(N) alone (expcnt and lgkmcnt at their maxima): at most N
+// vector memory operations of this wave still outstanding
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt is six bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// The column-operand image: entry (tile T, chunk ch, column c, fg g) holds
+// the hi and lo fragments of col[64 T + c][32 ch + 4 g .. + 3] and
+// [32 ch + 16 + 4 g .. + 3] (split8), hi at T 2 TS + ch 256 + lds_slot(c, g)
+// and lo TS entries after it, TS = 256 K / 32: the LDS layout of one tile.
+__global__ __launch_bounds__(256) void lr_col_image_kernel(const float *col, int64_t ld, int64_t entries, int nch,
+                                                           uint4 *img) {
+  const int TS = nch * 256;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < entries; i += (int64_t)gridDim.x * 256) {
+    const int g = (int)(i & 3), c = (int)((i >> 2) & 63);
+    const int64_t r = i >> 8;
+    const int ch = (int)(r % nch);
+    const int64_t T = r / nch;
+    const float *q = col + (64 * T + c) * ld + 32 * ch + 4 * g;
+    uint4 h, l;
+    split8(ld4(q), ld4(q + 16), h, l);
+    uint4 *o = img + T * 2 * TS + ch * 256 + lds_slot(c, g);
+    o[0] = h;
+    o[TS] = l;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Sweep variant of the encode's two passes, for the input-side transform
+// alone at rank 32 NCH (no residual, N a multiple of 128, every 32 x 64 wave
+// tile inside one scale block, per-rank scales, no boundary-hit counts): a
+// workgroup walks a run of
+// `upw` consecutive 128 x 128 units of the batch, ordered (rank, row block,
+// column pair), 64 columns at a time.  Per tile it multiplies from one half
+// of a double-buffered LDS ring while the next tile's column operand is
+// copied into the other half straight from its pre-split image (no registers,
+// no conversions) and W of the tile after next is loading into the register
+// set just consumed; the row operand (the rows of P) is loaded and split once
+// per row block.  The products are those of lr_update_body in the same order
+// and the image holds the same splits, so W~, the block maxima and the codes
+// are bit-identical to it.
+// ---------------------------------------------------------------------------
+
+template <int EPI, int NCH>
+__device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
+  static_assert(EPI == EPI_AMAX || EPI == EPI_QUANT, "sweep: AMAX or QUANT");
+  constexpr int TS = NCH * 256;     // (chunk, column, fg) entries of one 64-column tile
+  constexpr int CPW = 2 * TS / 64 / 4;   // 1-KiB pieces of a tile's image per wave
+  // the two halves of the ring as separate arrays, so that the compiler's
+  // wait analysis tells the copies into one from reads of the other: hi
+  // fragments at [0, TS), lo at [TS, 2 TS)
+  __shared__ __attribute__((aligned(1024))) uint4 ring0[2 * TS], ring1[2 * TS];
+  __shared__ uint32_t cstage[EPI == EPI_QUANT ? kUpdThreads / 64 : 1][32 * 32];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int fr = lane & 15, fg = lane >> 4;
+  const int64_t MN = p.M * p.N;
+  const int M32 = (int)p.M, N32 = (int)p.N;
+  const int ucols = N32 / 128;
+  const int per_rank = (M32 + kUpdRows - 1) / kUpdRows * ucols;
+  const int total = per_rank * p.batch;               // < 2^31 (launcher)
+  const int u0 = (int)blockIdx.x * p.upw;
+  const int Q = 2 * ((u0 + p.upw < total ? u0 + p.upw : total) - u0);   // tiles of the run, >= 2
+  const int slot = (int)(((int64_t)blockIdx.x * 4 + wave) % kAmaxSlots);
+  const int64_t nblk = (int64_t)p.nbr * p.nbc;
+  const int br = (int)p.br, bc = (int)p.bc;
+  const LUSeg &sg = p.seg[0];
+  if (EPI == EPI_QUANT && p.clear_words) {
+    const int64_t nthreads = (int64_t)gridDim.x * kUpdThreads;
+    for (int64_t i = (int64_t)blockIdx.x * kUpdThreads + tid; i < p.clear_words; i += nthreads)
+      st_u32_untracked(p.clear + i, 0u);
+  }
+  // tile q of the run: rank b, row block rb, first column j0 (wave-uniform)
+  auto coord = [&](int q, int &b, int &rb, int &j0) {
+    const int u = u0 + (q >> 1);
+    b = u / per_rank;
+    const int r = u - b * per_rank;
+    rb = r / ucols;
+    j0 = (r - rb * ucols) * 128 + 64 * (q & 1);
+  };
+  typedef float4 WTile[2][4];
+  // W of tile q (rows past M fall outside the buffer range and read zeros)
+  auto load_w = [&](int q, WTile &dd) {
+    int b, rb, j0;
+    coord(q, b, rb, j0);
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc((void *)(p.D + (int64_t)b * MN), (short)0, (int)(MN * 4), 0x00020000);
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      const int r = rb * kUpdRows + wave * 32 + 16 * g + fr;
+      const uint32_t ro = r < M32 ? (uint32_t)r * (uint32_t)N32 * 4u : 0x80000000u;
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        dd[g][t] = __builtin_bit_cast(
+            float4, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)(ro + (uint32_t)(j0 + 16 * t + 4 * fg) * 4u), 0, 0));
+    }
+  };
+  // column operand of tile q: its image (hi and lo fragments in LDS order,
+  // 2 TS x 16 bytes per 64 columns) copied HBM -> LDS with no registers;
+  // each wave copies CPW consecutive 1-KiB pieces
+  const __amdgpu_buffer_rsrc_t rsI = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)p.col_img, (short)0, (int)((int64_t)(N32 / 64) * 2 * TS * 16), 0x00020000);
+  auto copy_c = [&](int q, uint4 *ring) {
+    int b, rb, j0;
+    coord(q, b, rb, j0);
+    const uint32_t src = (uint32_t)(j0 / 64) * (uint32_t)(2 * TS * 16) + (uint32_t)(wave * CPW * 1024 + lane * 16);
+#pragma unroll
+    for (int i = 0; i < CPW; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsI, (GIFT_LDS void *)(ring + (wave * CPW + i) * 64), 16,
+                                               (int)(src + (uint32_t)i * 1024u), 0, 0, 0);
+  };
+  // row operand of the wave's 32 rows of row block rb of rank b
+  float4 rw[2][NCH][2];
+  auto load_r = [&](int b, int rb) {
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      const int r = rb * kUpdRows + wave * 32 + 16 * g + fr;
+      const bool ok = r < M32;
+      const float *q = sg.row + (int64_t)b * sg.row_bs + (int64_t)(ok ? r : 0) * sg.row_ld + 4 * fg;
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) {
+        rw[g][ch][0] = ld4_if(ok, q + 32 * ch);
+        rw[g][ch][1] = ld4_if(ok, q + 32 * ch + 16);
+      }
+    }
+  };
+  uint4 rh[2][NCH], rl[2][NCH];
+  auto split_r = [&]() {
+#pragma unroll
+    for (int g = 0; g < 2; ++g)
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) split8(rw[g][ch][0], rw[g][ch][1], rh[g][ch], rl[g][ch]);
+  };
+  // QUANT: raw sub-slot `lane` of tile q's block
+  auto load_raw = [&](int q) -> uint32_t {
+    int b, rb, j0;
+    coord(q, b, rb, j0);
+    const int i0 = rb * kUpdRows + wave * 32;   // a wave past M reads the last block row (not used)
+    const int64_t gb = (int64_t)b * nblk + (int64_t)((i0 < M32 ? i0 : M32 - 1) / br) * p.nbc + j0 / bc;
+    return p.raw[gb * kAmaxSlots + lane];
+  };
+
+  int cur_b, cur_rb;
+  {
+    int j0;
+    coord(0, cur_b, cur_rb, j0);
+  }
+  WTile dA, dB;
+  uint32_t rawA = 0u, rawB = 0u;
+  load_r(cur_b, cur_rb);
+  copy_c(0, ring0);
+  load_w(0, dA);
+  load_w(1, dB);
+  if (EPI == EPI_QUANT) {
+    rawA = load_raw(0);
+    rawB = load_raw(1);
+  }
+  __builtin_amdgcn_sched_barrier(0);   // every prologue load ahead of the first wait
+  split_r();
+  // this wave's copies into ring0 done (the 16 W and 0 / 2 raw loads issued
+  // after them may still be in flight), then everyone's
+  wait_vm<EPI == EPI_QUANT ? 18 : 16>();
+  __syncthreads();
+
+  uint32_t run_max = 0u;
+  int64_t run_blk = -1;
+  int64_t q_blk = -1;
+  float q_inv = 0.f;
+  // tile q (h = q & 1, a constant at each call)
+  auto tile = [&](int q, const int h, WTile &cur, uint32_t &raw) {
+    int b, rb, j0;
+    coord(q, b, rb, j0);
+    uint4 *const rd = h ? ring1 : ring0;
+    // the next tile's column operand into the other half (all waves left
+    // it at the end of the previous tile)
+    copy_c(q + 1 < Q ? q + 1 : Q - 1, h ? ring0 : ring1);
+    __builtin_amdgcn_sched_barrier(0);
+    if (h == 0 && (b != cur_b || rb != cur_rb)) {   // a new row block (workgroup-uniform)
+      cur_b = b;
+      cur_rb = rb;
+      load_r(b, rb);
+      split_r();
+    }
+    const int i0 = rb * kUpdRows + wave * 32;
+    floatx4 acc[2][4];
+#pragma unroll
+    for (int g = 0; g < 2; ++g)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) acc[g][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int e = ch * 256 + lds_slot(16 * t + fr, fg);
+        const uint4 ah = rd[e], al = rd[TS + e];
+#pragma unroll
+        for (int g = 0; g < 2; ++g) acc[g][t] = mfma3(ah, al, rh[g][ch], rl[g][ch], acc[g][t]);
+      }
+    if (i0 < M32) {
+      bool rv[2];
+#pragma unroll
+      for (int g = 0; g < 2; ++g) rv[g] = i0 + 16 * g + fr < M32;
+      float w[2][4][4];
+#pragma unroll
+      for (int g = 0; g < 2; ++g)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          w[g][t][0] = cur[g][t].x + acc[g][t][0];
+          w[g][t][1] = cur[g][t].y + acc[g][t][1];
+          w[g][t][2] = cur[g][t].z + acc[g][t][2];
+          w[g][t][3] = cur[g][t].w + acc[g][t][3];
+        }
+      const int bi = i0 / br, bj = j0 / bc;
+      const int64_t gb = (int64_t)b * nblk + (int64_t)bi * p.nbc + bj;
+      if (EPI == EPI_AMAX) {
+        uint32_t m = 0u;
+#pragma unroll
+        for (int g = 0; g < 2; ++g)
+          if (rv[g]) {
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const uint32_t a = __float_as_uint(w[g][t][e]) & 0x7fffffffu;
+                m = a > m ? a : m;
+              }
+          }
+        m = wave_max_u32(m);
+        if (gb != run_blk) {
+          if (run_blk >= 0 && lane == 0 && run_max) atomicMax(&p.amax[run_blk * kAmaxSlots + slot], run_max);
+          run_blk = gb;
+          run_max = 0u;
+        }
+        run_max = m > run_max ? m : run_max;
+      } else {
+        if (gb != q_blk) {
+          const float a = __uint_as_float(wave_max_u32(raw));
+          q_inv = e4m3_multiplier(a);
+          q_blk = gb;
+          if (lane == 0 && i0 == bi * br && j0 == bj * bc)
+            st_u32_untracked(p.scales + gb, __float_as_uint(e4m3_scale(a)));
+        }
+#pragma unroll
+        for (int g = 0; g < 2; ++g)
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const uint32_t packed = e4m3_encode4(w[g][t][0] * q_inv, w[g][t][1] * q_inv, w[g][t][2] * q_inv,
+                                                 w[g][t][3] * q_inv);
+            cstage[wave][(16 * g + fr) * 32 + 16 * h + 4 * t + fg] = packed;
+          }
+        if (h == 1) {
+          // the pair's codes, whole 128-byte lines; the wave reads back only
+          // what its own lanes wrote, and one wave's LDS accesses complete in
+          // order: wavefront-scope fences keep the compiler from reordering
+          // them without waiting for this wave's loads in flight
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+          uint8_t *cb = p.codes + (int64_t)b * MN + (int64_t)(j0 - 64);
+#pragma unroll
+          for (int h = 0; h < 4; ++h) {
+            const int c = lane + 64 * h;        // 16-byte chunk: row c / 8, chunk c % 8
+            const int row = c >> 3, qt = c & 7;
+            const uint4 v = *reinterpret_cast<const uint4 *>(&cstage[wave][row * 32 + 4 * qt]);
+            if (i0 + row < M32) st_u128_untracked(cb + (int64_t)(i0 + row) * N32 + 16 * qt, v);
+          }
+        }
+      }
+    }
+    // the tile after next (the last tile again at the end of the run: an
+    // unconditional load keeps every wait exact), then the next tile's
+    // column operand into the other half of the ring
+    const int qn = q + 2 < Q ? q + 2 : Q - 1;
+    __builtin_amdgcn_sched_barrier(0);
+    load_w(qn, cur);
+    if (EPI == EPI_QUANT) raw = load_raw(qn);
+    // this wave's copies of the next tile done (only the 8 W and 0 / 1 raw
+    // loads above may still be in flight: loads complete in order), then
+    // everyone's
+    wait_vm<EPI == EPI_QUANT ? 9 : 8>();
+    __syncthreads();
+  };
+  for (int q = 0; q < Q; q += 2) {
+    tile(q, 0, dA, rawA);
+    tile(q + 1, 1, dB, rawB);
+  }
+  if (EPI == EPI_AMAX && run_blk >= 0 && lane == 0 && run_max)
+    atomicMax(&p.amax[run_blk * kAmaxSlots + slot], run_max);
+}
+
+template <int EPI, int NCH>
+__global__ __launch_bounds__(kUpdThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void lr_sweep_kernel(
+    const LUArgs p) {
+  lr_sweep_body<EPI, NCH>(p);
+}
+
 bool al16(const void *q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; }
 
 }  // namespace
@@ -846,6 +1146,21 @@ gift_status launch_lr_proj(gift_ctx *ctx, const TileJob &j) {
     default: hipLaunchKernelGGL(lr_proj_kernel<8>, grid, dim3(kProjThreads), 0, ctx->stream, a); break;
   }
   return check_launch("lr_proj_kernel");
+}
+
+size_t lr_col_image_bytes(int64_t N, int K) {
+  if (N <= 0 || N % 128 != 0 || !(K == 64 || K == 96 || K == 128)) return 0;
+  return (size_t)N * (size_t)K * 4;   // hi + lo bf16 per element
+}
+
+gift_status launch_lr_col_image(gift_ctx *ctx, const float *col, int64_t ld, int64_t N, int K, void *img) {
+  const int nch = K / 32;
+  const int64_t entries = N / 64 * nch * 256;
+  const int64_t blocks = std::min<int64_t>((entries + 255) / 256, 2048);
+  ProfileScope prof(ctx, GIFT_KERNEL_PROJECT);
+  hipLaunchKernelGGL(lr_col_image_kernel, dim3((unsigned)blocks), dim3(256), 0, ctx->stream, col, ld, entries, nch,
+                     static_cast<uint4 *>(img));
+  return check_launch("lr_col_image_kernel");
 }
 
 gift_status launch_lr_psum(gift_ctx *ctx, const float *partials, float *out, int parts, int64_t per_rank,
@@ -929,6 +1244,36 @@ gift_status launch_lr_update(gift_ctx *ctx, const TileJob &j) {
   // tile loop has no branch between its waits
   const bool full = lr_quant_reads_raw(j) && j.transformed == nullptr &&
                     (!quant || (a.raw != nullptr && a.codes_wide && j.N % cols == 0));
+  // the sweep variant: input side alone, no residual, whole 128-column
+  // units, per-rank scales, every wave tile inside one block, no hit counts
+  const int64_t sw_units = j.batch * ((j.M + kUpdRows - 1) / kUpdRows) * (j.N / 128);
+  const bool sweep = full && j.col_img != nullptr && !j.mx_codes && !ef && !(quant && j.hits) && j.nseg == 1 &&
+                     j.seg[0].a.parts == 1 && j.seg[0].b.bs == 0 &&
+                     (j.seg[0].K == 64 || j.seg[0].K == 96 || j.seg[0].K == 128) && j.N % 128 == 0 &&
+                     !j.shared && sw_units > 0 && sw_units < (1LL << 30);
+  if (sweep) {
+    // runs of four units (eight 64-column tiles) once the launch fills four
+    // rounds of resident workgroups (two per CU), shorter runs below.
+    // Measured on the Llama-600M buckets in the four-stream step: runs of
+    // 3-4 units 38.8-39.6 ms per codec step, 5-6 units 43-45 ms, runs sized
+    // for one or two rounds 46-47 ms (the same kernels in isolation differ
+    // by under 5 %)
+    const int64_t upw = sw_units >= 4 * 512 ? 4 : std::max<int64_t>(1, sw_units / 512);
+    a.upw = (int)upw;
+    a.col_img = j.col_img;
+    const dim3 sgrid((unsigned)((sw_units + upw - 1) / upw));
+    auto sgo = [&](auto epi_c) {
+      constexpr int E = decltype(epi_c)::value;
+      switch (j.seg[0].K) {
+        case 64: hipLaunchKernelGGL((lr_sweep_kernel<E, 2>), sgrid, dim3(kUpdThreads), 0, ctx->stream, a); break;
+        case 96: hipLaunchKernelGGL((lr_sweep_kernel<E, 3>), sgrid, dim3(kUpdThreads), 0, ctx->stream, a); break;
+        default: hipLaunchKernelGGL((lr_sweep_kernel<E, 4>), sgrid, dim3(kUpdThreads), 0, ctx->stream, a); break;
+      }
+    };
+    if (quant) sgo(std::integral_constant<int, EPI_QUANT>{});
+    else sgo(std::integral_constant<int, EPI_AMAX>{});
+    return check_launch("lr_sweep_kernel");
+  }
   auto go = [&](auto epi_c, auto ef_c, auto nseg_c, auto kc_c) {
     constexpr int E = decltype(epi_c)::value;
     constexpr bool EFv = decltype(ef_c)::value;
