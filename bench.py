@@ -223,6 +223,30 @@ def calibrate():
         ms = e0.elapsed_time(e1)
         flops = blocks * 4.0 * iters * chains * flops_per
         out[name] = round(flops / (ms * 1e-3) / 1e12, 1)
+    # streaming reads of 4 GiB (far past the 256 MB Infinity Cache) and of
+    # 128 MiB (held by it), cached and non-temporal loads
+    lib.gift_calib_read.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int64,
+                                    ctypes.c_void_p, ctypes.c_int]
+    rblocks = 256 * 16
+    rout = torch.empty(rblocks * 256, dtype=torch.float32, device=dev)
+    for mib in (4096, 128):
+        src = torch.zeros(mib * 1024 * 1024 // 4, dtype=torch.float32, device=dev)
+        nbytes = src.numel() * 4
+        for kind, name in ((0, "cached"), (1, "nontemporal")):
+            for _ in range(3):
+                assert lib.gift_calib_read(stream, kind, ctypes.c_void_p(src.data_ptr()), nbytes,
+                                           ctypes.c_void_p(rout.data_ptr()), rblocks) == 0
+            reps = 20
+            e0, e1 = ev(), ev()
+            e0.record()
+            for _ in range(reps):
+                assert lib.gift_calib_read(stream, kind, ctypes.c_void_p(src.data_ptr()), nbytes,
+                                           ctypes.c_void_p(rout.data_ptr()), rblocks) == 0
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / reps
+            out[f"read_{mib}mib_{name}_gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
+        del src
     ctx.close()
     out.update({"hbm_spec_gbs": HBM_PEAK_GBS, "mfma_bf16_spec_tflops": BF16_MFMA_TFLOPS,
                 "mfma_f32_spec_tflops": FP32_MFMA_TFLOPS})

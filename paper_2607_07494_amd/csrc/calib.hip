@@ -2,8 +2,9 @@
 // codec): matrix-core loops with no memory traffic, whose rate is the
 // achievable dense MFMA throughput of this GPU for the two instruction kinds
 // the codec uses (bf16 16x16x32 for the statistics and the split-bf16
-// transforms, float32 16x16x4 for the inverse transform).  Built into
-// libgift_calib.so, called by bench.py --calibrate.
+// transforms, float32 16x16x4 for the inverse transform), and a streaming
+// read, the achievable HBM read rate (the encode is almost all reads).
+// Built into libgift_calib.so, called by bench.py --calibrate.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -47,9 +48,41 @@ __global__ __launch_bounds__(256) void mfma_loop_f32(float *out, int iters) {
   out[(int64_t)blockIdx.x * blockDim.x + threadIdx.x] = s;
 }
 
+// Streaming read: every float4 of src once per launch (grid-stride, two
+// loads in flight per lane), summed so the loads are not dropped; one float
+// written per lane.  nt: non-temporal loads.
+template <bool NT>
+__global__ __launch_bounds__(256) void read_stream(const floatx4 *__restrict__ src, int64_t n4, float *out) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  floatx4 a = {0.f, 0.f, 0.f, 0.f}, b = {0.f, 0.f, 0.f, 0.f};
+  for (; i + stride < n4; i += 2 * stride) {
+    const floatx4 x = NT ? __builtin_nontemporal_load(src + i) : src[i];
+    const floatx4 y = NT ? __builtin_nontemporal_load(src + i + stride) : src[i + stride];
+    a += x;
+    b += y;
+  }
+  if (i < n4) a += src[i];
+  out[(int64_t)blockIdx.x * 256 + threadIdx.x] = a[0] + a[1] + a[2] + a[3] + b[0] + b[1] + b[2] + b[3];
+}
+
 }  // namespace
 
 extern "C" {
+
+// Reads `bytes` (a multiple of 16) at src with `blocks` workgroups of 256
+// threads (kind 0: cached loads, 1: non-temporal).  out: device float32
+// [blocks * 256].  Returns the HIP status of the launch.
+int gift_calib_read(void *stream, int kind, const void *src, int64_t bytes, float *out, int blocks) {
+  const floatx4 *p = static_cast<const floatx4 *>(src);
+  if (kind == 0)
+    hipLaunchKernelGGL(read_stream<false>, dim3(blocks), dim3(256), 0, static_cast<hipStream_t>(stream), p, bytes / 16,
+                       out);
+  else
+    hipLaunchKernelGGL(read_stream<true>, dim3(blocks), dim3(256), 0, static_cast<hipStream_t>(stream), p, bytes / 16,
+                       out);
+  return (int)hipGetLastError();
+}
 
 // Launches `blocks` workgroups of 256 threads, each wave running `iters`
 // rounds of kChains matrix-core instructions (kind 0: bf16 16x16x32, 16384

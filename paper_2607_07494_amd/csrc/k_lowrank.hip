@@ -849,7 +849,9 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
   const int ucols = N32 / 128;
   const int per_rank = (M32 + kUpdRows - 1) / kUpdRows * ucols;
   const int total = per_rank * p.batch;               // < 2^31 (launcher)
-  const int u0 = (int)blockIdx.x * p.upw;
+  // consecutive runs (the runs of one row block, which share its rows of P)
+  // on one XCD, one after another
+  const int u0 = (int)xcd_tile(blockIdx.x, gridDim.x) * p.upw;
   const int Q = 2 * ((u0 + p.upw < total ? u0 + p.upw : total) - u0);   // tiles of the run, >= 2
   const int slot = (int)(((int64_t)blockIdx.x * 4 + wave) % kAmaxSlots);
   const int64_t nblk = (int64_t)p.nbr * p.nbc;
@@ -869,16 +871,18 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
     j0 = (r - rb * ucols) * 128 + 64 * (q & 1);
   };
   typedef float4 WTile[2][4];
-  // W of tile q (rows past M fall outside the buffer range and read zeros)
+  // W of tile q (rows past M fall outside the buffer range and read zeros;
+  // so does every row of a tile past the run, q >= Q: no fetch at all)
   auto load_w = [&](int q, WTile &dd) {
+    const bool in_run = q < Q;
     int b, rb, j0;
-    coord(q, b, rb, j0);
+    coord(in_run ? q : Q - 1, b, rb, j0);
     const __amdgpu_buffer_rsrc_t rs =
         __builtin_amdgcn_make_buffer_rsrc((void *)(p.D + (int64_t)b * MN), (short)0, (int)(MN * 4), 0x00020000);
 #pragma unroll
     for (int g = 0; g < 2; ++g) {
       const int r = rb * kUpdRows + wave * 32 + 16 * g + fr;
-      const uint32_t ro = r < M32 ? (uint32_t)r * (uint32_t)N32 * 4u : 0x80000000u;
+      const uint32_t ro = in_run && r < M32 ? (uint32_t)r * (uint32_t)N32 * 4u : 0x80000000u;
 #pragma unroll
       for (int t = 0; t < 4; ++t)
         dd[g][t] = __builtin_bit_cast(
@@ -890,10 +894,12 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
   // each wave copies CPW consecutive 1-KiB pieces
   const __amdgpu_buffer_rsrc_t rsI = __builtin_amdgcn_make_buffer_rsrc(
       (void *)p.col_img, (short)0, (int)((int64_t)(N32 / 64) * 2 * TS * 16), 0x00020000);
+  // (a tile past the run, q >= Q, copies zeros from past the range: no fetch)
   auto copy_c = [&](int q, uint4 *ring) {
     int b, rb, j0;
-    coord(q, b, rb, j0);
-    const uint32_t src = (uint32_t)(j0 / 64) * (uint32_t)(2 * TS * 16) + (uint32_t)(wave * CPW * 1024 + lane * 16);
+    coord(q < Q ? q : Q - 1, b, rb, j0);
+    const uint32_t src = q < Q ? (uint32_t)(j0 / 64) * (uint32_t)(2 * TS * 16) + (uint32_t)(wave * CPW * 1024 + lane * 16)
+                               : 0x80000000u;
 #pragma unroll
     for (int i = 0; i < CPW; ++i)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rsI, (GIFT_LDS void *)(ring + (wave * CPW + i) * 64), 16,
@@ -963,7 +969,7 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
     uint4 *const rd = h ? ring1 : ring0;
     // the next tile's column operand into the other half (all waves left
     // it at the end of the previous tile)
-    copy_c(q + 1 < Q ? q + 1 : Q - 1, h ? ring0 : ring1);
+    copy_c(q + 1, h ? ring0 : ring1);
     __builtin_amdgcn_sched_barrier(0);
     if (h == 0 && (b != cur_b || rb != cur_rb)) {   // a new row block (workgroup-uniform)
       cur_b = b;
@@ -1056,13 +1062,12 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
         }
       }
     }
-    // the tile after next (the last tile again at the end of the run: an
-    // unconditional load keeps every wait exact), then the next tile's
-    // column operand into the other half of the ring
-    const int qn = q + 2 < Q ? q + 2 : Q - 1;
+    // W of the tile after next (past the run: zeros, unfetched, loaded all
+    // the same so that every wait stays exact)
+    const int qn = q + 2;
     __builtin_amdgcn_sched_barrier(0);
     load_w(qn, cur);
-    if (EPI == EPI_QUANT) raw = load_raw(qn);
+    if (EPI == EPI_QUANT) raw = load_raw(qn < Q ? qn : Q - 1);
     // this wave's copies of the next tile done (only the 8 W and 0 / 1 raw
     // loads above may still be in flight: loads complete in order), then
     // everyone's

@@ -88,7 +88,7 @@ struct Frags {
   bf16x8 a[8], b[4];
 };
 
-template <bool DIAG>
+template <bool DIAGONAL>
 __device__ __forceinline__ void syrk_tile(const SyrkArgs &p, int member, int ti, int tj,
                                           uint16_t *a0, uint16_t *a1, uint16_t *a2, uint16_t *a3,
                                           uint16_t *b0, uint16_t *b1, uint16_t *b2, uint16_t *b3) {
@@ -98,7 +98,7 @@ __device__ __forceinline__ void syrk_tile(const SyrkArgs &p, int member, int ti,
   const uint16_t *X = p.X[member];
   const int64_t T = p.T, dim = p.dim;
   const int nst = (int)((T + kStageTok - 1) / kStageTok);
-  constexpr int kLoadsPerStage = DIAG ? 2 : 4;   // load instructions per wave and stage
+  constexpr int kLoadsPerStage = DIAGONAL ? 2 : 4;   // load instructions per wave and stage
 
   // Load mapping: wave w fills 1-KiB chunks 2w and 2w + 1 of each strip; a
   // chunk is token rows 2c and 2c + 1.  Lane l writes 16-byte unit pu =
@@ -127,7 +127,7 @@ __device__ __forceinline__ void syrk_tile(const SyrkArgs &p, int member, int ti,
     for (int c2 = 0; c2 < 2; ++c2) {
       const int c = 2 * wave + c2;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (GIFT_LDS void *)(As + c * 512), 16, (int)va[c2], 0, 0, 0);
-      if (!DIAG)
+      if (!DIAGONAL)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (GIFT_LDS void *)(Bs + c * 512), 16, (int)vb[c2], 0, 0, 0);
     }
   };
@@ -164,7 +164,7 @@ __device__ __forceinline__ void syrk_tile(const SyrkArgs &p, int member, int ti,
     int ba = base_a, bb = base_b;
     asm volatile("" : "+v"(ba), "+v"(bb));   // keep 2 base registers, not 12 addresses
 #pragma unroll
-    for (int b = 0; b < 4; ++b) F.b[b] = frag(DIAG ? As : Bs, bb ^ (32 * b));
+    for (int b = 0; b < 4; ++b) F.b[b] = frag(DIAGONAL ? As : Bs, bb ^ (32 * b));
 #pragma unroll
     for (int a = 0; a < 8; ++a) F.a[a] = frag(As, ba ^ (32 * a));
   };
@@ -235,7 +235,7 @@ __device__ __forceinline__ void syrk_tile(const SyrkArgs &p, int member, int ti,
 #pragma unroll
         for (int v = 0; v < 4; ++v) A[(gi + v) * dim + gj] = acc[a][b][v] * sc;
         // mirror: (gj, gi..gi+3) is 16 contiguous bytes (dim % 8 == 0)
-        if (!DIAG)
+        if (!DIAGONAL)
           *reinterpret_cast<float4 *>(A + gj * dim + gi) =
               make_float4(acc[a][b][0] * sc, acc[a][b][1] * sc, acc[a][b][2] * sc, acc[a][b][3] * sc);
       }
