@@ -1129,7 +1129,7 @@ gift_status launch_lr_proj(gift_ctx *ctx, const TileJob &j) {
   const bool tr = lr_strip_is_b(j);
   const Operand &xs = tr ? j.seg[0].b : j.seg[0].a, &ys = tr ? j.seg[0].a : j.seg[0].b;
   const int64_t C = tr ? j.M : j.N;
-  LPArgs a;
+  LPArgs a{};
   a.X = xs.ptr;
   a.x_bs = xs.bs;
   a.Y = ys.ptr;

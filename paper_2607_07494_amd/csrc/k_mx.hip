@@ -122,7 +122,7 @@ unsigned grid_for(int64_t work, int threads) {
 
 gift_status launch_mx_quant(gift_ctx *ctx, const float *x, const float *ef_in, float *ef, float *transformed,
                             uint8_t *codes, uint8_t *scales, int64_t total) {
-  MxArgs a;
+  MxArgs a{};
   a.x = x;
   a.ef_in = ef_in;
   a.ef = ef;

@@ -108,7 +108,7 @@ gift_status launch_reduce(gift_ctx *ctx, const uint8_t *codes, const float *scal
   if (m <= 0 || n <= 0) return GIFT_OK;
   if (stream_eligible(m, n, g, mean, codes, nullptr, nullptr))
     return launch_stream_reduce(ctx, codes, scales, N, m, n, g, mean);
-  RArgs a;
+  RArgs a{};
   a.codes = codes;
   a.scales = scales;
   a.mean = mean;

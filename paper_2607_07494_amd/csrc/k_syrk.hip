@@ -276,7 +276,7 @@ gift_status launch_syrk_bf16(gift_ctx *ctx, const uint16_t *const *x_table, int 
   // 32-bit buffer offsets of one stage (32 token rows) and stage counts
   if (dim > (1LL << 24) || T > (1LL << 36))
     return set_error(GIFT_ESHAPE, "internal: statistics shape too large for the bf16 kernel");
-  SyrkArgs a;
+  SyrkArgs a{};
   a.X = x_table;
   a.A = A;
   a.T = T;

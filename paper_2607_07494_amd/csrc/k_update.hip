@@ -696,7 +696,7 @@ bool proj_kernel_eligible(const TileJob &j) {
 }
 
 gift_status launch_proj(gift_ctx *ctx, const TileJob &j) {
-  PArgs a;
+  PArgs a{};
   const bool tr = proj_strip_is_b(j);
   const Operand &xs = tr ? j.seg[0].b : j.seg[0].a;   // strip side
   const Operand &ys = tr ? j.seg[0].a : j.seg[0].b;
