@@ -292,8 +292,22 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
   const bool aligned = (reinterpret_cast<uintptr_t>(W) & 15) == 0;
   const bool pp_ok = useA && !useG && aligned && n % 4 == 0 && (A.r == 16 || A.r == 32 || A.r == 64 || A.r == 128);
   const int pparts = !pp_ok ? 1 : (inverse ? proj_parts(m, n, A.r, N) : lr_proj_parts(m, n, N));
+  // the two-sided form's products with small grids (K = U_G^T P always, and
+  // W^T U_G over few ranks: 4 to 64 tiles of 64 x 64) split their
+  // contraction over the rows into partials, summed in order: enough
+  // workgroups to fill the GPU
+  auto small_split = [](int64_t M, int64_t Nc, int64_t batch, int64_t K) -> int {
+    const int64_t tiles = (M + 63) / 64 * ((Nc + 63) / 64) * batch;
+    int ks = 1;
+    while (ks < 16 && tiles * ks < 512 && K / (2 * ks) >= 64) ks *= 2;
+    return ks;
+  };
+  // (the in-order sum reads 16-byte groups: a partial's size a multiple of 4)
+  const int qsplit = useG && (n * G.r) % 4 == 0 ? small_split(n, G.r, N, m) : 1;
+  const int ksplit_k = useA && useG && ((int64_t)G.r * A.r) % 4 == 0 ? small_split(G.r, A.r, N, m) : 1;
   size_t off = 0;
   float *P = nullptr, *Qm = nullptr, *Km = nullptr, *L2 = nullptr, *Psum = nullptr;
+  float *Qpart = nullptr, *Kpart = nullptr;
   if (useA) {
     P = reinterpret_cast<float *>(ws + off);
     off += a256(sizeof(float) * N * pparts * m * A.r);
@@ -314,6 +328,14 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
     off += a256(sizeof(float) * N * G.r * A.r);
     L2 = reinterpret_cast<float *>(ws + off);
     off += a256(sizeof(float) * N * m * A.r);
+  }
+  if (qsplit > 1) {
+    Qpart = reinterpret_cast<float *>(ws + off);
+    off += a256(sizeof(float) * N * qsplit * n * G.r);
+  }
+  if (ksplit_k > 1) {
+    Kpart = reinterpret_cast<float *>(ws + off);
+    off += a256(sizeof(float) * N * ksplit_k * G.r * A.r);
   }
   // the forward update of the input side alone: its column operand as the
   // sweep kernel's LDS image
@@ -357,11 +379,14 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
     j.M = n;
     j.N = G.r;
     j.batch = N;
-    j.C = Qm;
+    j.C = qsplit > 1 ? Qpart : Qm;
     j.ldc = G.r;
     j.cbs = n * G.r;
+    j.ksplit = qsplit;
     j.kernel_family = inverse ? GIFT_KERNEL_DECODE_PROJECT : GIFT_KERNEL_PROJECT;
     if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
+    if (qsplit > 1 && (st = launch_lr_psum(ctx, Qpart, Qm, qsplit, n * G.r, N, j.kernel_family)) != GIFT_OK)
+      return st;
   }
   if (useA && useG) {
     {  // K = U_G^T P  (r_G x r_A)
@@ -373,11 +398,15 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
       j.M = G.r;
       j.N = A.r;
       j.batch = N;
-      j.C = Km;
+      j.C = ksplit_k > 1 ? Kpart : Km;
       j.ldc = A.r;
       j.cbs = (int64_t)G.r * A.r;
+      j.ksplit = ksplit_k;
       j.kernel_family = inverse ? GIFT_KERNEL_DECODE_PROJECT : GIFT_KERNEL_PROJECT;
       if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
+      if (ksplit_k > 1 &&
+          (st = launch_lr_psum(ctx, Kpart, Km, ksplit_k, (int64_t)G.r * A.r, N, j.kernel_family)) != GIFT_OK)
+        return st;
     }
     {  // L2 = (P + U_G C_G K) C_A
       TileJob j;
