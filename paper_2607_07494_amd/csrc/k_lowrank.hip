@@ -818,9 +818,9 @@ __global__ __launch_bounds__(256) void lr_col_image_kernel(const float *col, int
 
 // ---------------------------------------------------------------------------
 // Sweep variant of the encode's two passes, for the input-side transform
-// alone at rank 32 NCH (no residual, N a multiple of 128, every 32 x 64 wave
-// tile inside one scale block, per-rank scales, no boundary-hit counts): a
-// workgroup walks a run of
+// alone at rank 32 NCH (N a multiple of 128, every 32 x 64 wave tile inside
+// one scale block, per-rank scales, no boundary-hit counts; with or without
+// the error-feedback residual): a workgroup walks a run of
 // `upw` consecutive 128 x 128 units of the batch, ordered (rank, row block,
 // column pair), 64 columns at a time.  Per tile it multiplies from one half
 // of a double-buffered LDS ring while the next tile's column operand is
@@ -832,9 +832,14 @@ __global__ __launch_bounds__(256) void lr_col_image_kernel(const float *col, int
 // are bit-identical to it.
 // ---------------------------------------------------------------------------
 
-template <int EPI, int NCH>
+template <int EPI, int NCH, bool EF>
 __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
   static_assert(EPI == EPI_AMAX || EPI == EPI_QUANT, "sweep: AMAX or QUANT");
+  // W (and the residual) of the tile after next in a second register set,
+  // or, with a residual at rank 96 or 128 (whose two sets would not fit two
+  // waves per SIMD), of the next tile in the one set (its loads then wait
+  // behind the tile's products only)
+  constexpr bool DEEP = !(EF && NCH >= 3);
   constexpr int TS = NCH * 256;     // (chunk, column, fg) entries of one 64-column tile
   constexpr int CPW = 2 * TS / 64 / 4;   // 1-KiB pieces of a tile's image per wave
   // the two halves of the ring as separate arrays, so that the compiler's
@@ -871,22 +876,27 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
     j0 = (r - rb * ucols) * 128 + 64 * (q & 1);
   };
   typedef float4 WTile[2][4];
-  // W of tile q (rows past M fall outside the buffer range and read zeros;
-  // so does every row of a tile past the run, q >= Q: no fetch at all)
-  auto load_w = [&](int q, WTile &dd) {
+  // W (and the residual) of tile q (rows past M fall outside the buffer
+  // range and read zeros; so does every row of a tile past the run, q >= Q:
+  // no fetch at all)
+  auto load_w = [&](int q, WTile &dd, WTile &re) {
     const bool in_run = q < Q;
     int b, rb, j0;
     coord(in_run ? q : Q - 1, b, rb, j0);
     const __amdgpu_buffer_rsrc_t rs =
         __builtin_amdgcn_make_buffer_rsrc((void *)(p.D + (int64_t)b * MN), (short)0, (int)(MN * 4), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rsE = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(EF ? p.ef + (int64_t)b * MN : p.D), (short)0, EF ? (int)(MN * 4) : 0, 0x00020000);
 #pragma unroll
     for (int g = 0; g < 2; ++g) {
       const int r = rb * kUpdRows + wave * 32 + 16 * g + fr;
       const uint32_t ro = in_run && r < M32 ? (uint32_t)r * (uint32_t)N32 * 4u : 0x80000000u;
 #pragma unroll
-      for (int t = 0; t < 4; ++t)
-        dd[g][t] = __builtin_bit_cast(
-            float4, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)(ro + (uint32_t)(j0 + 16 * t + 4 * fg) * 4u), 0, 0));
+      for (int t = 0; t < 4; ++t) {
+        const int off = (int)(ro + (uint32_t)(j0 + 16 * t + 4 * fg) * 4u);
+        dd[g][t] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+        if (EF) re[g][t] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rsE, off, 0, 0));
+      }
     }
   };
   // column operand of tile q: its image (hi and lo fragments in LDS order,
@@ -941,29 +951,29 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
     int j0;
     coord(0, cur_b, cur_rb, j0);
   }
-  WTile dA, dB;
+  WTile dA, dB, rA, rB;
   uint32_t rawA = 0u, rawB = 0u;
   load_r(cur_b, cur_rb);
   copy_c(0, ring0);
-  load_w(0, dA);
-  load_w(1, dB);
+  load_w(0, dA, rA);
+  if (DEEP) load_w(1, dB, rB);
   if (EPI == EPI_QUANT) {
     rawA = load_raw(0);
-    rawB = load_raw(1);
+    if (DEEP) rawB = load_raw(1);
   }
   __builtin_amdgcn_sched_barrier(0);   // every prologue load ahead of the first wait
   split_r();
   // this wave's copies into ring0 done (the 16 W and 0 / 2 raw loads issued
   // after them may still be in flight), then everyone's
-  wait_vm<EPI == EPI_QUANT ? 18 : 16>();
+  wait_vm<(DEEP ? 2 : 1) * ((EF ? 16 : 8) + (EPI == EPI_QUANT ? 1 : 0))>();
   __syncthreads();
 
   uint32_t run_max = 0u;
   int64_t run_blk = -1;
   int64_t q_blk = -1;
-  float q_inv = 0.f;
+  float q_inv = 0.f, q_s = 0.f;
   // tile q (h = q & 1, a constant at each call)
-  auto tile = [&](int q, const int h, WTile &cur, uint32_t &raw) {
+  auto tile = [&](int q, const int h, WTile &cur, WTile &curR, uint32_t &raw) {
     int b, rb, j0;
     coord(q, b, rb, j0);
     uint4 *const rd = h ? ring1 : ring0;
@@ -1005,6 +1015,12 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
           w[g][t][1] = cur[g][t].y + acc[g][t][1];
           w[g][t][2] = cur[g][t].z + acc[g][t][2];
           w[g][t][3] = cur[g][t].w + acc[g][t][3];
+          if (EF) {
+            w[g][t][0] += curR[g][t].x;
+            w[g][t][1] += curR[g][t].y;
+            w[g][t][2] += curR[g][t].z;
+            w[g][t][3] += curR[g][t].w;
+          }
         }
       const int bi = i0 / br, bj = j0 / bc;
       const int64_t gb = (int64_t)b * nblk + (int64_t)bi * p.nbc + bj;
@@ -1032,6 +1048,7 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
         if (gb != q_blk) {
           const float a = __uint_as_float(wave_max_u32(raw));
           q_inv = e4m3_multiplier(a);
+          q_s = e4m3_scale(a);
           q_blk = gb;
           if (lane == 0 && i0 == bi * br && j0 == bj * bc)
             st_u32_untracked(p.scales + gb, __float_as_uint(e4m3_scale(a)));
@@ -1043,6 +1060,15 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
             const uint32_t packed = e4m3_encode4(w[g][t][0] * q_inv, w[g][t][1] * q_inv, w[g][t][2] * q_inv,
                                                  w[g][t][3] * q_inv);
             cstage[wave][(16 * g + fr) * 32 + 16 * h + 4 * t + fg] = packed;
+            if (EF && rv[g]) {   // R = W~ - its dequantized code
+              float qv[4];
+              e4m3_decode4(packed, qv);
+              st_u128_untracked(p.ef + (int64_t)b * MN + (int64_t)(i0 + 16 * g + fr) * N32 + j0 + 16 * t + 4 * fg,
+                                make_uint4(__float_as_uint(w[g][t][0] - qv[0] * q_s),
+                                           __float_as_uint(w[g][t][1] - qv[1] * q_s),
+                                           __float_as_uint(w[g][t][2] - qv[2] * q_s),
+                                           __float_as_uint(w[g][t][3] - qv[3] * q_s)));
+            }
           }
         if (h == 1) {
           // the pair's codes, whole 128-byte lines; the wave reads back only
@@ -1064,28 +1090,29 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
     }
     // W of the tile after next (past the run: zeros, unfetched, loaded all
     // the same so that every wait stays exact)
-    const int qn = q + 2;
+    const int qn = DEEP ? q + 2 : q + 1;
     __builtin_amdgcn_sched_barrier(0);
-    load_w(qn, cur);
+    load_w(qn, cur, curR);
     if (EPI == EPI_QUANT) raw = load_raw(qn < Q ? qn : Q - 1);
-    // this wave's copies of the next tile done (only the 8 W and 0 / 1 raw
-    // loads above may still be in flight: loads complete in order), then
-    // everyone's
-    wait_vm<EPI == EPI_QUANT ? 9 : 8>();
+    // this wave's copies of the next tile done (only the 8 W (+ 8 residual)
+    // and 0 / 1 raw loads above may still be in flight: loads complete in
+    // order), then everyone's
+    wait_vm<(EF ? 16 : 8) + (EPI == EPI_QUANT ? 1 : 0)>();
     __syncthreads();
   };
   for (int q = 0; q < Q; q += 2) {
-    tile(q, 0, dA, rawA);
-    tile(q + 1, 1, dB, rawB);
+    tile(q, 0, dA, rA, rawA);
+    if (DEEP) tile(q + 1, 1, dB, rB, rawB);
+    else tile(q + 1, 1, dA, rA, rawA);
   }
   if (EPI == EPI_AMAX && run_blk >= 0 && lane == 0 && run_max)
     atomicMax(&p.amax[run_blk * kAmaxSlots + slot], run_max);
 }
 
-template <int EPI, int NCH>
+template <int EPI, int NCH, bool EF = false>
 __global__ __launch_bounds__(kUpdThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void lr_sweep_kernel(
     const LUArgs p) {
-  lr_sweep_body<EPI, NCH>(p);
+  lr_sweep_body<EPI, NCH, EF>(p);
 }
 
 bool al16(const void *q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; }
@@ -1249,10 +1276,10 @@ gift_status launch_lr_update(gift_ctx *ctx, const TileJob &j) {
   // tile loop has no branch between its waits
   const bool full = lr_quant_reads_raw(j) && j.transformed == nullptr &&
                     (!quant || (a.raw != nullptr && a.codes_wide && j.N % cols == 0));
-  // the sweep variant: input side alone, no residual, whole 128-column
-  // units, per-rank scales, every wave tile inside one block, no hit counts
+  // the sweep variant: input side alone, whole 128-column units, per-rank
+  // scales, every wave tile inside one block, no hit counts
   const int64_t sw_units = j.batch * ((j.M + kUpdRows - 1) / kUpdRows) * (j.N / 128);
-  const bool sweep = full && j.col_img != nullptr && !j.mx_codes && !ef && !(quant && j.hits) && j.nseg == 1 &&
+  const bool sweep = full && j.col_img != nullptr && !j.mx_codes && !(quant && j.hits) && j.nseg == 1 &&
                      j.seg[0].a.parts == 1 && j.seg[0].b.bs == 0 &&
                      (j.seg[0].K == 64 || j.seg[0].K == 96 || j.seg[0].K == 128) && j.N % 128 == 0 &&
                      !j.shared && sw_units > 0 && sw_units < (1LL << 30);
@@ -1267,16 +1294,22 @@ gift_status launch_lr_update(gift_ctx *ctx, const TileJob &j) {
     a.upw = (int)upw;
     a.col_img = j.col_img;
     const dim3 sgrid((unsigned)((sw_units + upw - 1) / upw));
-    auto sgo = [&](auto epi_c) {
+    auto sgo = [&](auto epi_c, auto ef_c) {
       constexpr int E = decltype(epi_c)::value;
+      constexpr bool R = decltype(ef_c)::value;
       switch (j.seg[0].K) {
-        case 64: hipLaunchKernelGGL((lr_sweep_kernel<E, 2>), sgrid, dim3(kUpdThreads), 0, ctx->stream, a); break;
-        case 96: hipLaunchKernelGGL((lr_sweep_kernel<E, 3>), sgrid, dim3(kUpdThreads), 0, ctx->stream, a); break;
-        default: hipLaunchKernelGGL((lr_sweep_kernel<E, 4>), sgrid, dim3(kUpdThreads), 0, ctx->stream, a); break;
+        case 64: hipLaunchKernelGGL((lr_sweep_kernel<E, 2, R>), sgrid, dim3(kUpdThreads), 0, ctx->stream, a); break;
+        case 96: hipLaunchKernelGGL((lr_sweep_kernel<E, 3, R>), sgrid, dim3(kUpdThreads), 0, ctx->stream, a); break;
+        default: hipLaunchKernelGGL((lr_sweep_kernel<E, 4, R>), sgrid, dim3(kUpdThreads), 0, ctx->stream, a); break;
       }
     };
-    if (quant) sgo(std::integral_constant<int, EPI_QUANT>{});
-    else sgo(std::integral_constant<int, EPI_AMAX>{});
+    if (quant) {
+      if (ef) sgo(std::integral_constant<int, EPI_QUANT>{}, std::true_type{});
+      else sgo(std::integral_constant<int, EPI_QUANT>{}, std::false_type{});
+    } else {
+      if (ef) sgo(std::integral_constant<int, EPI_AMAX>{}, std::true_type{});
+      else sgo(std::integral_constant<int, EPI_AMAX>{}, std::false_type{});
+    }
     return check_launch("lr_sweep_kernel");
   }
   auto go = [&](auto epi_c, auto ef_c, auto nseg_c, auto kc_c) {

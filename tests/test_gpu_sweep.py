@@ -112,3 +112,43 @@ def test_sweep_matches_unit_kernel_and_oracle(ctx, N, m, n, r, br, bc):
     torch.cuda.synchronize()
     assert torch.equal(codes_2, codes_s) and torch.equal(scales_2, scales_s)
     f.close()
+
+
+EF_CASES = [
+    # (N, m, n, r, block_rows, block_cols): ranks 64 (W two tiles ahead), 96 and
+    # 128 (one tile ahead), runs across row blocks and ranks
+    (10, 1000, 1664, 64, 0, 128),
+    (6, 520, 1536, 96, 0, 256),
+    (23, 800, 1664, 128, 0, 128),
+]
+
+
+@pytest.mark.parametrize("N,m,n,r,br,bc", EF_CASES)
+def test_sweep_error_feedback_matches_unit_kernel(ctx, N, m, n, r, br, bc):
+    """Two error-feedback steps (Algorithm 1, GIFT branch: encode W + R, R <-
+    W~ - dequantized codes) through the sweep kernels and through the
+    per-unit kernel (the encode that stores W~): codes, scales and the
+    residual bit-identical after each step."""
+    say(f"sweep error feedback N={N} m={m} n={n} r={r} block=({br},{bc}) run={run_length(N, m, n)}")
+    fA = codec.lowrank_factor(codec.factor_statistics(factor_inputs(17 + r, 4 * n, n)[0]), r).to_f32()
+    f = gift.Factor(ctx, m, n, r, gift.SIDE_INPUT)
+    f.import_(gift.SIDE_INPUT, t(fA.U.astype(np.float32)), t(fA.c_fwd.astype(np.float32)),
+              t(fA.c_inv.astype(np.float32)), t(np.array([fA.sigma2], np.float32)))
+    nbr, nbc = gift.scale_grid(m, n, br, bc)
+    ef_s = torch.zeros((N, m, n), dtype=torch.float32, device=DEV)
+    ef_u = torch.zeros_like(ef_s)
+    tr = torch.empty((N, m, n), dtype=torch.float32, device=DEV)
+    for step in range(2):
+        g = t(gradient_set(500 + step + m, 600 + n, N, m, n))
+        codes_s = torch.empty((N, m, n), dtype=torch.uint8, device=DEV)
+        scales_s = torch.full((N, nbr, nbc), float("nan"), dtype=torch.float32, device=DEV)
+        gift.encode(ctx, f, g, codes_s, scales_s, br, bc, gift.SCALE_LOCAL, ef=ef_s)                 # sweep
+        codes_u = torch.empty_like(codes_s)
+        scales_u = torch.full_like(scales_s, float("nan"))
+        gift.encode(ctx, f, g, codes_u, scales_u, br, bc, gift.SCALE_LOCAL, ef=ef_u, transformed=tr)  # per unit
+        torch.cuda.synchronize()
+        assert torch.equal(scales_s, scales_u), f"step {step}: scales differ"
+        assert torch.equal(codes_s, codes_u), f"step {step}: codes differ"
+        assert torch.equal(ef_s, ef_u), f"step {step}: residuals differ"
+        assert float(ef_s.abs().max()) > 0.0
+    f.close()
