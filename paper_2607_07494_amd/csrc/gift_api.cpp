@@ -337,13 +337,20 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
     Kpart = reinterpret_cast<float *>(ws + off);
     off += a256(sizeof(float) * N * ksplit_k * G.r * A.r);
   }
-  // the forward update of the input side alone: its column operand as the
-  // sweep kernel's LDS image
-  const size_t img_bytes = !inverse && useA && !useG ? lr_col_image_bytes(n, A.r) : 0;
-  void *img = nullptr;
+  // the forward update's column operands as the sweep kernel's LDS images:
+  // input side alone, C_A U_A^T (shared); both sides at one rank, Q of each
+  // rank and U_A^T (shared)
+  const bool two_img = !inverse && useA && useG && A.r == G.r && lr_col_image_bytes(n, A.r) > 0;
+  const size_t img_bytes = !inverse && useA && (!useG || two_img) ? lr_col_image_bytes(n, A.r) : 0;
+  const size_t qimg_bytes = two_img ? lr_col_image_bytes(n, G.r) : 0;
+  void *img = nullptr, *qimg = nullptr;
   if (img_bytes) {
     img = ws + off;
     off += a256(img_bytes);
+  }
+  if (qimg_bytes) {
+    qimg = ws + off;
+    off += a256(qimg_bytes * N);
   }
   *used = off;
   if (ws == nullptr) return GIFT_OK;  // sizing pass
@@ -446,6 +453,14 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
     if (useG) {  // L2 U_A^T
       s.a = Operand{L2, A.r, m * A.r, true};
       s.b = Operand{A.U, A.r, 0, true};
+      if (two_img) {
+        u.col_img = qimg;   // segment 0: Q of each rank
+        u.img_bs = (int64_t)qimg_bytes;
+        u.col_img2 = img;   // segment 1: U_A^T
+        if ((st = launch_lr_col_image(ctx, Qm, G.r, n, (int)G.r, qimg, N, n * G.r)) != GIFT_OK ||
+            (st = launch_lr_col_image(ctx, A.U, A.r, n, (int)A.r, img)) != GIFT_OK)
+          return st;
+      }
     } else if (presum) {  // P (C_A U_A^T), P already summed
       s.a = Operand{Psum, A.r, m * A.r, true, 1};
       s.b = Operand{A.Uc, A.r, 0, true};
@@ -456,7 +471,7 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
       if (!inverse) u.col_img = img;
     }
     s.K = A.r;
-    if (u.col_img && (st = launch_lr_col_image(ctx, A.Uc, A.r, n, (int)A.r, img)) != GIFT_OK) return st;
+    if (!useG && u.col_img && (st = launch_lr_col_image(ctx, A.Uc, A.r, n, (int)A.r, img)) != GIFT_OK) return st;
   }
   return GIFT_OK;
 }

@@ -242,10 +242,13 @@ struct TileJob {
   // mean / U^T (projection) and U diag(c') / mean / output (update) from
   // decode_tab[b] (device) instead of base + b * stride
   const DecodePtrs *decode_tab = nullptr;
-  // the encode's update (input side alone): the column operand split into
-  // bf16 hi / lo fragments in the LDS layout of its 64-column tiles
-  // (launch_lr_col_image), which the sweep variant copies straight into LDS
+  // the encode's update: each segment's column operand split into bf16 hi /
+  // lo fragments in the LDS layout of its 64-column tiles
+  // (launch_lr_col_image), which the sweep variant copies straight into LDS;
+  // img_bs / img_bs2: bytes between batch entries' images (0: shared)
   const void *col_img = nullptr;
+  const void *col_img2 = nullptr;
+  int64_t img_bs = 0, img_bs2 = 0;
 };
 
 gift_status launch_tile(gift_ctx *ctx, const TileJob &job);
@@ -261,9 +264,11 @@ int lr_proj_parts(int64_t M, int64_t K, int32_t batch);
 // the column-operand image of the encode's sweep update: col [N][K] (row
 // stride ld) -> bf16 hi / lo fragments of each 64-column tile, K = 64, 96 or
 // 128 and N a multiple of 128; lr_col_image_bytes = its size (0: no image
-// for this shape)
+// for this shape).  count > 1: count operands col_bs floats apart, their
+// images lr_col_image_bytes apart
 size_t lr_col_image_bytes(int64_t N, int K);
-gift_status launch_lr_col_image(gift_ctx *ctx, const float *col, int64_t ld, int64_t N, int K, void *img);
+gift_status launch_lr_col_image(gift_ctx *ctx, const float *col, int64_t ld, int64_t N, int K, void *img,
+                                int32_t count = 1, int64_t col_bs = 0);
 // out[b] = sum_z partials[b][z] (in order) for [batch][parts][per_rank] floats
 // (per_rank a multiple of 4, 16-byte aligned buffers)
 gift_status launch_lr_psum(gift_ctx *ctx, const float *partials, float *out, int parts, int64_t per_rank,

@@ -292,8 +292,11 @@ struct LUArgs {
   int shared, batch;
   uint8_t *mx_codes;    // MX: packed E2M1 codes [batch][M][N/2]
   uint8_t *mx_scales;   // MX: E8M0 scales [batch][M][N/32]
-  int upw;              // sweep variant: 128 x 128 units per workgroup
-  const void *col_img;  // sweep variant: the column operand's LDS image
+  int upw = 1;                      // sweep variant: 128 x 128 units per workgroup
+  const void *col_img = nullptr;    // sweep variant: the column operand's LDS image
+  int64_t img_bs = 0;               // bytes between batch entries' images (0: shared)
+  const void *col_img2 = nullptr;   // sweep variant, two segments: segment 1's image
+  int64_t img_bs2 = 0;              // bytes between batch entries' segment-1 images (0: shared)
 };
 
 template <int EPI, bool EF, int NSEG, int KC, bool FULL>
@@ -799,18 +802,22 @@ __device__ __forceinline__ void wait_vm() {
 // the hi and lo fragments of col[64 T + c][32 ch + 4 g .. + 3] and
 // [32 ch + 16 + 4 g .. + 3] (split8), hi at T 2 TS + ch 256 + lds_slot(c, g)
 // and lo TS entries after it, TS = 256 K / 32: the LDS layout of one tile.
-__global__ __launch_bounds__(256) void lr_col_image_kernel(const float *col, int64_t ld, int64_t entries, int nch,
-                                                           uint4 *img) {
+// count > 1: operand b at col + b col_bs, its image 2 entries uint4 after
+// operand b - 1's.
+__global__ __launch_bounds__(256) void lr_col_image_kernel(const float *col, int64_t ld, int64_t col_bs,
+                                                           int64_t entries, int64_t count, int nch, uint4 *img) {
   const int TS = nch * 256;
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < entries; i += (int64_t)gridDim.x * 256) {
-    const int g = (int)(i & 3), c = (int)((i >> 2) & 63);
-    const int64_t r = i >> 8;
+  const int64_t total = entries * count;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    const int64_t b = i / entries, ie = i - b * entries;
+    const int g = (int)(ie & 3), c = (int)((ie >> 2) & 63);
+    const int64_t r = ie >> 8;
     const int ch = (int)(r % nch);
     const int64_t T = r / nch;
-    const float *q = col + (64 * T + c) * ld + 32 * ch + 4 * g;
+    const float *q = col + b * col_bs + (64 * T + c) * ld + 32 * ch + 4 * g;
     uint4 h, l;
     split8(ld4(q), ld4(q + 16), h, l);
-    uint4 *o = img + T * 2 * TS + ch * 256 + lds_slot(c, g);
+    uint4 *o = img + b * 2 * entries + T * 2 * TS + ch * 256 + lds_slot(c, g);
     o[0] = h;
     o[TS] = l;
   }
@@ -832,22 +839,30 @@ __global__ __launch_bounds__(256) void lr_col_image_kernel(const float *col, int
 // are bit-identical to it.
 // ---------------------------------------------------------------------------
 
-template <int EPI, int NCH, bool EF>
+template <int EPI, int KC, bool EF, int NSEG>
 __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
   static_assert(EPI == EPI_AMAX || EPI == EPI_QUANT, "sweep: AMAX or QUANT");
+  static_assert(NSEG == 1 || (NSEG == 2 && !EF), "sweep: two segments without a residual");
+  constexpr int NCH = NSEG * KC;    // 32-step chunks over both segments
   // W (and the residual) of the tile after next in a second register set,
   // or, with a residual at rank 96 or 128 (whose two sets would not fit two
   // waves per SIMD), of the next tile in the one set (its loads then wait
   // behind the tile's products only)
-  constexpr bool DEEP = !(EF && NCH >= 3);
-  constexpr int TS = NCH * 256;     // (chunk, column, fg) entries of one 64-column tile
+  // With two segments (the two-sided transform's rank-2r update) the row
+  // operand of both takes 128 registers, so W also loads one tile ahead,
+  // and each ring half holds one segment's image: a tile multiplies
+  // segment 0 from one half while segment 1 is copied into the other, then
+  // segment 1 while the next tile's segment 0 is copied.
+  constexpr bool DEEP = NSEG == 1 && !(EF && KC >= 3);
+  constexpr int TS = KC * 256;      // (chunk, column, fg) entries of one segment's 64-column tile
   constexpr int CPW = 2 * TS / 64 / 4;   // 1-KiB pieces of a tile's image per wave
   // the two halves of the ring as separate arrays, so that the compiler's
   // wait analysis tells the copies into one from reads of the other: hi
   // fragments at [0, TS), lo at [TS, 2 TS)
   __shared__ __attribute__((aligned(1024))) uint4 ring0[2 * TS], ring1[2 * TS];
   __shared__ uint32_t cstage[EPI == EPI_QUANT ? kUpdThreads / 64 : 1][32 * 32];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // (the wave index in a scalar register: every wave-derived offset scalar)
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int fr = lane & 15, fg = lane >> 4;
   const int64_t MN = p.M * p.N;
   const int M32 = (int)p.M, N32 = (int)p.N;
@@ -859,9 +874,9 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
   const int u0 = (int)xcd_tile(blockIdx.x, gridDim.x) * p.upw;
   const int Q = 2 * ((u0 + p.upw < total ? u0 + p.upw : total) - u0);   // tiles of the run, >= 2
   const int slot = (int)(((int64_t)blockIdx.x * 4 + wave) % kAmaxSlots);
-  const int64_t nblk = (int64_t)p.nbr * p.nbc;
+  // block indices over the batch fit 32 bits with their sub-slots (launcher)
+  const int nblk = (int)(p.nbr * p.nbc);
   const int br = (int)p.br, bc = (int)p.bc;
-  const LUSeg &sg = p.seg[0];
   if (EPI == EPI_QUANT && p.clear_words) {
     const int64_t nthreads = (int64_t)gridDim.x * kUpdThreads;
     for (int64_t i = (int64_t)blockIdx.x * kUpdThreads + tid; i < p.clear_words; i += nthreads)
@@ -899,15 +914,17 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
       }
     }
   };
-  // column operand of tile q: its image (hi and lo fragments in LDS order,
-  // 2 TS x 16 bytes per 64 columns) copied HBM -> LDS with no registers;
-  // each wave copies CPW consecutive 1-KiB pieces
-  const __amdgpu_buffer_rsrc_t rsI = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)p.col_img, (short)0, (int)((int64_t)(N32 / 64) * 2 * TS * 16), 0x00020000);
-  // (a tile past the run, q >= Q, copies zeros from past the range: no fetch)
-  auto copy_c = [&](int q, uint4 *ring) {
+  // column operand of tile q (segment sg_i): its image (hi and lo fragments
+  // in LDS order, 2 TS x 16 bytes per 64 columns; rank b's at img_bs bytes
+  // from rank 0's) copied HBM -> LDS with no registers; each wave copies CPW
+  // consecutive 1-KiB pieces (a tile past the run, q >= Q, copies zeros from
+  // past the range: no fetch)
+  auto copy_c = [&](int q, int sg_i, uint4 *ring) {
     int b, rb, j0;
     coord(q < Q ? q : Q - 1, b, rb, j0);
+    const char *img = static_cast<const char *>(sg_i ? p.col_img2 : p.col_img) + (int64_t)b * (sg_i ? p.img_bs2 : p.img_bs);
+    const __amdgpu_buffer_rsrc_t rsI = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)img, (short)0, (int)((int64_t)(N32 / 64) * 2 * TS * 16), 0x00020000);
     const uint32_t src = q < Q ? (uint32_t)(j0 / 64) * (uint32_t)(2 * TS * 16) + (uint32_t)(wave * CPW * 1024 + lane * 16)
                                : 0x80000000u;
 #pragma unroll
@@ -915,34 +932,53 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rsI, (GIFT_LDS void *)(ring + (wave * CPW + i) * 64), 16,
                                                (int)(src + (uint32_t)i * 1024u), 0, 0, 0);
   };
-  // row operand of the wave's 32 rows of row block rb of rank b
-  float4 rw[2][NCH][2];
-  auto load_r = [&](int b, int rb) {
+  // row operand (segment sg_i) of the wave's rows 16 g .. + 15 of row
+  // block rb of rank b, loaded, then split into chunks sg_i KC .. of rh /
+  // rl (two segments: one 16-row group's loads at a time, which keeps the
+  // split fragments of both segments and one group in flight under 256
+  // registers)
+  constexpr int RWG = NSEG == 2 ? 1 : 2;
+  float4 rw[RWG][KC][2];
+  uint4 rh[2][NCH], rl[2][NCH];
+  auto load_r = [&](int b, int rb, int sg_i, int g) {
+    const LUSeg &sq = p.seg[sg_i];
+    const int r = rb * kUpdRows + wave * 32 + 16 * g + fr;
+    const bool ok = r < M32;
+    const float *q = sq.row + (int64_t)b * sq.row_bs + (int64_t)(ok ? r : 0) * sq.row_ld + 4 * fg;
 #pragma unroll
-    for (int g = 0; g < 2; ++g) {
-      const int r = rb * kUpdRows + wave * 32 + 16 * g + fr;
-      const bool ok = r < M32;
-      const float *q = sg.row + (int64_t)b * sg.row_bs + (int64_t)(ok ? r : 0) * sg.row_ld + 4 * fg;
-#pragma unroll
-      for (int ch = 0; ch < NCH; ++ch) {
-        rw[g][ch][0] = ld4_if(ok, q + 32 * ch);
-        rw[g][ch][1] = ld4_if(ok, q + 32 * ch + 16);
-      }
+    for (int ch = 0; ch < KC; ++ch) {
+      rw[g % RWG][ch][0] = ld4_if(ok, q + 32 * ch);
+      rw[g % RWG][ch][1] = ld4_if(ok, q + 32 * ch + 16);
     }
   };
-  uint4 rh[2][NCH], rl[2][NCH];
-  auto split_r = [&]() {
+  auto split_r = [&](int sg_i, int g) {
 #pragma unroll
-    for (int g = 0; g < 2; ++g)
+    for (int ch = 0; ch < KC; ++ch)
+      split8(rw[g % RWG][ch][0], rw[g % RWG][ch][1], rh[g][sg_i * KC + ch], rl[g][sg_i * KC + ch]);
+  };
+  // the row operand of row block rb of rank b, both groups of every segment
+  auto reload_r = [&](int b, int rb) {
+    if (NSEG == 1) {
+      load_r(b, rb, 0, 0);
+      load_r(b, rb, 0, 1);
+      split_r(0, 0);
+      split_r(0, 1);
+    } else {
 #pragma unroll
-      for (int ch = 0; ch < NCH; ++ch) split8(rw[g][ch][0], rw[g][ch][1], rh[g][ch], rl[g][ch]);
+      for (int s2 = 0; s2 < NSEG; ++s2)
+#pragma unroll
+        for (int g = 0; g < 2; ++g) {
+          load_r(b, rb, s2, g);
+          split_r(s2, g);
+        }
+    }
   };
   // QUANT: raw sub-slot `lane` of tile q's block
   auto load_raw = [&](int q) -> uint32_t {
     int b, rb, j0;
     coord(q, b, rb, j0);
     const int i0 = rb * kUpdRows + wave * 32;   // a wave past M reads the last block row (not used)
-    const int64_t gb = (int64_t)b * nblk + (int64_t)((i0 < M32 ? i0 : M32 - 1) / br) * p.nbc + j0 / bc;
+    const int gb = b * nblk + ((i0 < M32 ? i0 : M32 - 1) / br) * (int)p.nbc + j0 / bc;
     return p.raw[gb * kAmaxSlots + lane];
   };
 
@@ -953,8 +989,20 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
   }
   WTile dA, dB, rA, rB;
   uint32_t rawA = 0u, rawB = 0u;
-  load_r(cur_b, cur_rb);
-  copy_c(0, ring0);
+  if (NSEG == 2) {   // segment 1's rows and segment 0's first group split ahead
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      load_r(cur_b, cur_rb, 1, g);
+      split_r(1, g);
+    }
+    load_r(cur_b, cur_rb, 0, 0);
+    split_r(0, 0);
+    load_r(cur_b, cur_rb, 0, 1);
+  } else {
+    load_r(cur_b, cur_rb, 0, 0);
+    load_r(cur_b, cur_rb, 0, 1);
+  }
+  copy_c(0, 0, ring0);
   load_w(0, dA, rA);
   if (DEEP) load_w(1, dB, rB);
   if (EPI == EPI_QUANT) {
@@ -962,30 +1010,44 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
     if (DEEP) rawB = load_raw(1);
   }
   __builtin_amdgcn_sched_barrier(0);   // every prologue load ahead of the first wait
-  split_r();
+  if (NSEG == 1) split_r(0, 0);
+  split_r(0, 1);
   // this wave's copies into ring0 done (the 16 W and 0 / 2 raw loads issued
   // after them may still be in flight), then everyone's
   wait_vm<(DEEP ? 2 : 1) * ((EF ? 16 : 8) + (EPI == EPI_QUANT ? 1 : 0))>();
   __syncthreads();
 
   uint32_t run_max = 0u;
-  int64_t run_blk = -1;
-  int64_t q_blk = -1;
+  int run_blk = -1;
+  int q_blk = -1;
   float q_inv = 0.f, q_s = 0.f;
+  // two segments: one segment's products issued with the LDS reads of the
+  // next 16 columns one step ahead of their products (two reads, then six
+  // products), so that two steps' fragments at most are held in registers
+  auto pipe_one_ahead = [&]() {
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+    for (int i = 1; i < 4 * KC; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 6, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 6, 0);
+  };
   // tile q (h = q & 1, a constant at each call)
   auto tile = [&](int q, const int h, WTile &cur, WTile &curR, uint32_t &raw) {
     int b, rb, j0;
     coord(q, b, rb, j0);
-    uint4 *const rd = h ? ring1 : ring0;
-    // the next tile's column operand into the other half (all waves left
-    // it at the end of the previous tile)
-    copy_c(q + 1, h ? ring0 : ring1);
+    uint4 *const rd = NSEG == 2 || h == 0 ? ring0 : ring1;
+    // one segment: the next tile's column operand into the other half (all
+    // waves left it at the end of the previous tile); two: this tile's
+    // segment 1 into ring1
+    if (NSEG == 1) copy_c(q + 1, 0, h ? ring0 : ring1);
+    else copy_c(q, 1, ring1);
     __builtin_amdgcn_sched_barrier(0);
     if (h == 0 && (b != cur_b || rb != cur_rb)) {   // a new row block (workgroup-uniform)
       cur_b = b;
       cur_rb = rb;
-      load_r(b, rb);
-      split_r();
+      reload_r(b, rb);
     }
     const int i0 = rb * kUpdRows + wave * 32;
     floatx4 acc[2][4];
@@ -994,7 +1056,7 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
 #pragma unroll
       for (int t = 0; t < 4; ++t) acc[g][t] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int ch = 0; ch < NCH; ++ch)
+    for (int ch = 0; ch < KC; ++ch)
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         const int e = ch * 256 + lds_slot(16 * t + fr, fg);
@@ -1002,6 +1064,24 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
 #pragma unroll
         for (int g = 0; g < 2; ++g) acc[g][t] = mfma3(ah, al, rh[g][ch], rl[g][ch], acc[g][t]);
       }
+    if (NSEG == 2) {
+      // this wave's copies of segment 1 done (nothing issued after them),
+      // then everyone's; everyone is done with ring0: the next tile's
+      // segment 0 goes there under segment 1's products
+      wait_vm<0>();
+      __syncthreads();
+      copy_c(q + 1, 0, ring0);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int ch = KC; ch < NCH; ++ch)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int e = (ch - KC) * 256 + lds_slot(16 * t + fr, fg);
+          const uint4 ah = ring1[e], al = ring1[TS + e];
+#pragma unroll
+          for (int g = 0; g < 2; ++g) acc[g][t] = mfma3(ah, al, rh[g][ch], rl[g][ch], acc[g][t]);
+        }
+    }
     if (i0 < M32) {
       bool rv[2];
 #pragma unroll
@@ -1023,7 +1103,7 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
           }
         }
       const int bi = i0 / br, bj = j0 / bc;
-      const int64_t gb = (int64_t)b * nblk + (int64_t)bi * p.nbc + bj;
+      const int gb = b * nblk + bi * (int)p.nbc + bj;
       if (EPI == EPI_AMAX) {
         uint32_t m = 0u;
 #pragma unroll
@@ -1077,13 +1157,14 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
           // them without waiting for this wave's loads in flight
           __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
           __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-          uint8_t *cb = p.codes + (int64_t)b * MN + (int64_t)(j0 - 64);
+          // 16-byte chunk lane + 64 h: row lane / 8 + 8 h, chunk lane % 8
+          const int row0 = lane >> 3, qt = lane & 7;
+          const uint4 *src = reinterpret_cast<const uint4 *>(&cstage[wave][row0 * 32 + 4 * qt]);
+          uint8_t *cb = p.codes + (int64_t)b * MN + (int64_t)(i0 + row0) * N32 + (j0 - 64 + 16 * qt);
 #pragma unroll
           for (int h = 0; h < 4; ++h) {
-            const int c = lane + 64 * h;        // 16-byte chunk: row c / 8, chunk c % 8
-            const int row = c >> 3, qt = c & 7;
-            const uint4 v = *reinterpret_cast<const uint4 *>(&cstage[wave][row * 32 + 4 * qt]);
-            if (i0 + row < M32) st_u128_untracked(cb + (int64_t)(i0 + row) * N32 + 16 * qt, v);
+            const uint4 v = src[64 * h];
+            if (i0 + row0 + 8 * h < M32) st_u128_untracked(cb + (int64_t)(8 * h) * N32, v);
           }
         }
       }
@@ -1109,10 +1190,10 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
     atomicMax(&p.amax[run_blk * kAmaxSlots + slot], run_max);
 }
 
-template <int EPI, int NCH, bool EF = false>
+template <int EPI, int KC, bool EF = false, int NSEG = 1>
 __global__ __launch_bounds__(kUpdThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void lr_sweep_kernel(
     const LUArgs p) {
-  lr_sweep_body<EPI, NCH, EF>(p);
+  lr_sweep_body<EPI, KC, EF, NSEG>(p);
 }
 
 bool al16(const void *q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; }
@@ -1185,13 +1266,15 @@ size_t lr_col_image_bytes(int64_t N, int K) {
   return (size_t)N * (size_t)K * 4;   // hi + lo bf16 per element
 }
 
-gift_status launch_lr_col_image(gift_ctx *ctx, const float *col, int64_t ld, int64_t N, int K, void *img) {
+gift_status launch_lr_col_image(gift_ctx *ctx, const float *col, int64_t ld, int64_t N, int K, void *img,
+                                int32_t count, int64_t col_bs) {
+  if (lr_col_image_bytes(N, K) == 0 || count < 1) return GIFT_ESHAPE;
   const int nch = K / 32;
   const int64_t entries = N / 64 * nch * 256;
-  const int64_t blocks = std::min<int64_t>((entries + 255) / 256, 2048);
+  const int64_t blocks = std::min<int64_t>((entries * count + 255) / 256, 2048);
   ProfileScope prof(ctx, GIFT_KERNEL_PROJECT);
-  hipLaunchKernelGGL(lr_col_image_kernel, dim3((unsigned)blocks), dim3(256), 0, ctx->stream, col, ld, entries, nch,
-                     static_cast<uint4 *>(img));
+  hipLaunchKernelGGL(lr_col_image_kernel, dim3((unsigned)blocks), dim3(256), 0, ctx->stream, col, ld, col_bs, entries,
+                     (int64_t)count, nch, static_cast<uint4 *>(img));
   return check_launch("lr_col_image_kernel");
 }
 
@@ -1276,13 +1359,20 @@ gift_status launch_lr_update(gift_ctx *ctx, const TileJob &j) {
   // tile loop has no branch between its waits
   const bool full = lr_quant_reads_raw(j) && j.transformed == nullptr &&
                     (!quant || (a.raw != nullptr && a.codes_wide && j.N % cols == 0));
-  // the sweep variant: input side alone, whole 128-column units, per-rank
-  // scales, every wave tile inside one block, no hit counts
+  // the sweep variant: whole 128-column units, per-rank scales, every wave
+  // tile inside one block, no hit counts, each segment's column operand as
+  // its LDS image; one segment (the input side alone, a shared column
+  // operand, with or without the residual) or two (both sides: rank-2r
+  // update, no residual) of one rank each, K = 64, 96 or 128
   const int64_t sw_units = j.batch * ((j.M + kUpdRows - 1) / kUpdRows) * (j.N / 128);
-  const bool sweep = full && j.col_img != nullptr && !j.mx_codes && !(quant && j.hits) && j.nseg == 1 &&
-                     j.seg[0].a.parts == 1 && j.seg[0].b.bs == 0 &&
-                     (j.seg[0].K == 64 || j.seg[0].K == 96 || j.seg[0].K == 128) && j.N % 128 == 0 &&
-                     !j.shared && sw_units > 0 && sw_units < (1LL << 30);
+  const int64_t K0 = j.seg[0].K;
+  const bool seg_ok =
+      j.nseg == 1 ? j.col_img != nullptr && j.seg[0].a.parts == 1 && j.seg[0].b.bs == 0 && j.img_bs == 0
+                  : j.nseg == 2 && !ef && j.col_img != nullptr && j.col_img2 != nullptr && j.seg[0].a.parts == 1 &&
+                        j.seg[1].a.parts == 1 && j.seg[1].K == K0 && j.img_bs >= 0 && j.img_bs2 >= 0;
+  const bool sweep = full && seg_ok && !j.mx_codes && !(quant && j.hits) && (K0 == 64 || K0 == 96 || K0 == 128) &&
+                     j.N % 128 == 0 && !j.shared && sw_units > 0 && sw_units < (1LL << 30) &&
+                     (int64_t)j.batch * j.geom.nbr * j.geom.nbc * kAmaxSlots < (1LL << 31);
   if (sweep) {
     // runs of four units (eight 64-column tiles) once the launch fills four
     // rounds of resident workgroups (two per CU), shorter runs below.
@@ -1293,22 +1383,32 @@ gift_status launch_lr_update(gift_ctx *ctx, const TileJob &j) {
     const int64_t upw = sw_units >= 4 * 512 ? 4 : std::max<int64_t>(1, sw_units / 512);
     a.upw = (int)upw;
     a.col_img = j.col_img;
+    a.img_bs = j.img_bs;
+    a.col_img2 = j.nseg == 2 ? j.col_img2 : nullptr;
+    a.img_bs2 = j.nseg == 2 ? j.img_bs2 : 0;
     const dim3 sgrid((unsigned)((sw_units + upw - 1) / upw));
-    auto sgo = [&](auto epi_c, auto ef_c) {
+    auto sgo = [&](auto epi_c, auto ef_c, auto nseg_c) {
       constexpr int E = decltype(epi_c)::value;
       constexpr bool R = decltype(ef_c)::value;
-      switch (j.seg[0].K) {
-        case 64: hipLaunchKernelGGL((lr_sweep_kernel<E, 2, R>), sgrid, dim3(kUpdThreads), 0, ctx->stream, a); break;
-        case 96: hipLaunchKernelGGL((lr_sweep_kernel<E, 3, R>), sgrid, dim3(kUpdThreads), 0, ctx->stream, a); break;
-        default: hipLaunchKernelGGL((lr_sweep_kernel<E, 4, R>), sgrid, dim3(kUpdThreads), 0, ctx->stream, a); break;
+      constexpr int S = decltype(nseg_c)::value;
+      if constexpr (S == 1 || !R) {
+        switch (K0) {
+          case 64: hipLaunchKernelGGL((lr_sweep_kernel<E, 2, R, S>), sgrid, dim3(kUpdThreads), 0, ctx->stream, a); break;
+          case 96: hipLaunchKernelGGL((lr_sweep_kernel<E, 3, R, S>), sgrid, dim3(kUpdThreads), 0, ctx->stream, a); break;
+          default: hipLaunchKernelGGL((lr_sweep_kernel<E, 4, R, S>), sgrid, dim3(kUpdThreads), 0, ctx->stream, a); break;
+        }
       }
     };
+    using One = std::integral_constant<int, 1>;
+    using Two = std::integral_constant<int, 2>;
     if (quant) {
-      if (ef) sgo(std::integral_constant<int, EPI_QUANT>{}, std::true_type{});
-      else sgo(std::integral_constant<int, EPI_QUANT>{}, std::false_type{});
+      if (ef) sgo(std::integral_constant<int, EPI_QUANT>{}, std::true_type{}, One{});
+      else if (j.nseg == 2) sgo(std::integral_constant<int, EPI_QUANT>{}, std::false_type{}, Two{});
+      else sgo(std::integral_constant<int, EPI_QUANT>{}, std::false_type{}, One{});
     } else {
-      if (ef) sgo(std::integral_constant<int, EPI_AMAX>{}, std::true_type{});
-      else sgo(std::integral_constant<int, EPI_AMAX>{}, std::false_type{});
+      if (ef) sgo(std::integral_constant<int, EPI_AMAX>{}, std::true_type{}, One{});
+      else if (j.nseg == 2) sgo(std::integral_constant<int, EPI_AMAX>{}, std::false_type{}, Two{});
+      else sgo(std::integral_constant<int, EPI_AMAX>{}, std::false_type{}, One{});
     }
     return check_launch("lr_sweep_kernel");
   }

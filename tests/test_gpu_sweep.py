@@ -11,6 +11,10 @@ takes the per-unit kernel.  Both form the same products in the same order
 bit; W~ is held to 1e-5 of the float64 transform and its codes to the
 oracle's quantization (Algorithm 1, Scale / Q; Sec. I, amax rule).
 
+The two-sided encode at equal ranks takes the two-segment sweep (the rank-2r
+update (U_G C_G) Q + L_2 U_A^T of eq. design_full_transform, segment 0's
+column operand Q per rank, segment 1's U_A^T shared); the same checks hold.
+
 The cases choose the run length (units of the launch: 1 below 1024, then
 units / 512, 4 from 2048 on) and make runs cross row blocks (an odd number
 of 128-column units per row), ranks (units per rank not a multiple of the
@@ -151,4 +155,55 @@ def test_sweep_error_feedback_matches_unit_kernel(ctx, N, m, n, r, br, bc):
         assert torch.equal(codes_s, codes_u), f"step {step}: codes differ"
         assert torch.equal(ef_s, ef_u), f"step {step}: residuals differ"
         assert float(ef_s.abs().max()) > 0.0
+    f.close()
+
+
+BOTH_CASES = [
+    # (N, m, n, r, block_rows, block_cols)
+    (3, 200, 384, 128, 0, 128),     # run 1, ragged last row block
+    (4, 1000, 2048, 96, 0, 128),    # run 1, rank 96
+    (6, 1100, 1664, 64, 64, 64),    # run 1, rank 64, a block per tile
+    (10, 1000, 1664, 128, 0, 256),  # run 2 across row blocks
+    (20, 640, 2048, 128, 0, 0),     # run 3 across ranks, per-tensor scale
+    (23, 800, 1664, 128, 0, 128),   # run 4 across row blocks and ranks, partial last run
+]
+
+
+@pytest.mark.parametrize("N,m,n,r,br,bc", BOTH_CASES)
+def test_two_sided_sweep_matches_unit_kernel_and_oracle(ctx, N, m, n, r, br, bc):
+    say(f"two-sided sweep encode N={N} m={m} n={n} r={r} block=({br},{bc}) run={run_length(N, m, n)}")
+    fA = codec.lowrank_factor(codec.factor_statistics(factor_inputs(27 + r, 4 * n, n)[0]), r).to_f32()
+    fG = codec.lowrank_factor(codec.factor_statistics(factor_inputs(37 + r, 4 * m, m)[0]), r).to_f32()
+    f = gift.Factor(ctx, m, n, r, gift.SIDE_BOTH)
+    for side, fx in ((gift.SIDE_INPUT, fA), (gift.SIDE_OUTPUT, fG)):
+        f.import_(side, t(fx.U.astype(np.float32)), t(fx.c_fwd.astype(np.float32)),
+                  t(fx.c_inv.astype(np.float32)), t(np.array([fx.sigma2], np.float32)))
+    grads = gradient_set(700 + m, 800 + n, N, m, n)
+    g = t(grads)
+    nbr, nbc = gift.scale_grid(m, n, br, bc)
+    codes_s = torch.empty((N, m, n), dtype=torch.uint8, device=DEV)
+    scales_s = torch.full((N, nbr, nbc), float("nan"), dtype=torch.float32, device=DEV)
+    gift.encode(ctx, f, g, codes_s, scales_s, br, bc, gift.SCALE_LOCAL)        # sweep
+    codes_u = torch.empty_like(codes_s)
+    scales_u = torch.full_like(scales_s, float("nan"))
+    tr = torch.empty((N, m, n), dtype=torch.float32, device=DEV)
+    gift.encode(ctx, f, g, codes_u, scales_u, br, bc, gift.SCALE_LOCAL, transformed=tr)   # per unit
+    torch.cuda.synchronize()
+    assert torch.equal(scales_s, scales_u)
+    assert torch.equal(codes_s, codes_u)
+    # first, middle and last rank against the float64 transform and the
+    # oracle's quantization of the stored W~
+    idx = sorted({0, N // 2, N - 1})
+    trh = tr.cpu().numpy()[idx]
+    e = rel(trh, codec.forward(grads[idx], fA, fG))
+    say(f"  W~ rel. error {e:.2e}")
+    assert e <= 1e-5
+    ref_codes, ref_scales = codec.quantize_transformed(trh, br, bc, False)
+    np.testing.assert_array_equal(scales_s.cpu().numpy()[idx], ref_scales)
+    np.testing.assert_array_equal(codes_s.cpu().numpy()[idx], ref_codes)
+    codes_2 = torch.empty_like(codes_s)
+    scales_2 = torch.empty_like(scales_s)
+    gift.encode(ctx, f, g, codes_2, scales_2, br, bc, gift.SCALE_LOCAL)
+    torch.cuda.synchronize()
+    assert torch.equal(codes_2, codes_s) and torch.equal(scales_2, scales_s)
     f.close()
