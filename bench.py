@@ -893,12 +893,21 @@ def main():
     iso_launches, iso_ms = fam_raw[dom]
     avg_ms = iso_ms / iso_launches
     fl_l, by_l = fl / per_step_launches, by / per_step_launches
-    peak_f = BF16_MFMA_TFLOPS if dom == "syrk" and wl.act_dtype == "bf16" else FP32_MFMA_TFLOPS
-    frac_f = fl_l / (avg_ms * 1e-3) / 1e12 / peak_f if fl else 0.0
+    # matrix-core basis: the statistics from bf16 tokens on BF16 MFMA; the
+    # encode's projections and rank-r update as three bf16 products of the
+    # split float32 operands (hi hi + hi lo + lo hi) on BF16 MFMA, so 3x the
+    # float32 flops against the bf16 peak; the rest on FP32 MFMA
+    if dom == "syrk" and wl.act_dtype == "bf16":
+        peak_f, mult, basis = BF16_MFMA_TFLOPS, 1, "bf16 MFMA"
+    elif dom in ("project", "update_amax", "update_quant"):
+        peak_f, mult, basis = BF16_MFMA_TFLOPS, 3, "3 bf16 MFMA products per float32 product (split operands)"
+    else:
+        peak_f, mult, basis = FP32_MFMA_TFLOPS, 1, "FP32 MFMA"
+    frac_f = mult * fl_l / (avg_ms * 1e-3) / 1e12 / peak_f if fl else 0.0
     frac_b = by_l / (avg_ms * 1e-3) / 1e9 / HBM_PEAK_GBS if by else 0.0
     if frac_f >= frac_b:
-        roof = {"bound": "mfma", "achieved": round(fl_l / (avg_ms * 1e-3) / 1e12, 3),
-                "peak": peak_f, "unit": "TFLOP/s", "frac": round(frac_f, 4)}
+        roof = {"bound": "mfma", "achieved": round(mult * fl_l / (avg_ms * 1e-3) / 1e12, 3),
+                "peak": peak_f, "unit": "TFLOP/s", "frac": round(frac_f, 4), "mfma_basis": basis}
     else:
         roof = {"bound": "hbm", "achieved": round(by_l / (avg_ms * 1e-3) / 1e9, 2),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(frac_b, 4)}

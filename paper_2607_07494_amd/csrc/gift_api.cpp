@@ -290,7 +290,9 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
   // that the update kernel sums (same conditions as that kernel's)
   // (the encode's split-bf16 projection has its own partial count)
   const bool aligned = (reinterpret_cast<uintptr_t>(W) & 15) == 0;
-  const bool pp_ok = useA && !useG && aligned && n % 4 == 0 && (A.r == 16 || A.r == 32 || A.r == 64 || A.r == 128);
+  // (both sides: the decode's projection alone, summed before its two uses)
+  const bool pp_ok = useA && (!useG || inverse) && aligned && n % 4 == 0 &&
+                     (A.r == 16 || A.r == 32 || A.r == 64 || A.r == 128);
   const int pparts = !pp_ok ? 1 : (inverse ? proj_parts(m, n, A.r, N) : lr_proj_parts(m, n, N));
   // the two-sided form's products with small grids (K = U_G^T P always, and
   // W^T U_G over few ranks: 4 to 64 tiles of 64 x 64) split their
@@ -303,7 +305,10 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
     return ks;
   };
   // (the in-order sum reads 16-byte groups: a partial's size a multiple of 4)
-  const int qsplit = useG && (n * G.r) % 4 == 0 ? small_split(n, G.r, N, m) : 1;
+  // The encode's U_G^T W at rank 64 or 128 takes the split-bf16 transposed
+  // projection with its own partial count.
+  const int pt_parts = useG && !inverse && aligned && al16p(G.Ut) ? lr_projT_parts(n, m, G.r, N) : 0;
+  const int qsplit = pt_parts > 0 ? pt_parts : useG && (n * G.r) % 4 == 0 ? small_split(n, G.r, N, m) : 1;
   const int ksplit_k = useA && useG && ((int64_t)G.r * A.r) % 4 == 0 ? small_split(G.r, A.r, N, m) : 1;
   size_t off = 0;
   float *P = nullptr, *Qm = nullptr, *Km = nullptr, *L2 = nullptr, *Psum = nullptr;
@@ -313,8 +318,9 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
     off += a256(sizeof(float) * N * pparts * m * A.r);
   }
   // the encode sums the projection's partials once (the update then reads
-  // one P per column range instead of all partials)
-  const bool presum = !inverse && pparts > 1;
+  // one P per column range instead of all partials), and so does the
+  // two-sided decode (K and L2 read P)
+  const bool presum = (!inverse || useG) && pparts > 1;
   if (presum) {
     Psum = reinterpret_cast<float *>(ws + off);
     off += a256(sizeof(float) * N * m * A.r);
@@ -391,7 +397,8 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
     j.cbs = n * G.r;
     j.ksplit = qsplit;
     j.kernel_family = inverse ? GIFT_KERNEL_DECODE_PROJECT : GIFT_KERNEL_PROJECT;
-    if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
+    j.split3 = pt_parts > 0;
+    if ((st = j.split3 ? launch_lr_projT(ctx, j) : launch_tile(ctx, j)) != GIFT_OK) return st;
     if (qsplit > 1 && (st = launch_lr_psum(ctx, Qpart, Qm, qsplit, n * G.r, N, j.kernel_family)) != GIFT_OK)
       return st;
   }
@@ -400,7 +407,7 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
       TileJob j;
       j.nseg = 1;
       j.seg[0].a = Operand{G.Ut, m, 0, true};
-      j.seg[0].b = Operand{P, A.r, m * A.r, false};
+      j.seg[0].b = Operand{presum ? Psum : P, A.r, m * A.r, false};
       j.seg[0].K = m;
       j.M = G.r;
       j.N = A.r;
@@ -427,7 +434,7 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
       j.C = L2;
       j.ldc = A.r;
       j.cbs = m * A.r;
-      j.D = P;
+      j.D = presum ? Psum : P;
       j.ldd = A.r;
       j.dbs = m * A.r;
       j.beta = 1.f;

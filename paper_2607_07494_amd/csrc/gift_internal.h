@@ -261,6 +261,13 @@ gift_status launch_lr_update(gift_ctx *ctx, const TileJob &job);
 bool lr_proj_eligible(const TileJob &job);
 gift_status launch_lr_proj(gift_ctx *ctx, const TileJob &job);
 int lr_proj_parts(int64_t M, int64_t K, int32_t batch);
+// the encode's output-side projection Q^T = W^T U_G with split bf16
+// operands (job: A = W read transposed, B = U^T k-major and shared, r = 64
+// or 128, M a multiple of 64): lr_projT_parts = its split-K partial count
+// for the shape (0: not this kernel), which the job's ksplit must equal
+int lr_projT_parts(int64_t M, int64_t K, int64_t r, int32_t batch);
+bool lr_projT_eligible(const TileJob &job);
+gift_status launch_lr_projT(gift_ctx *ctx, const TileJob &job);
 // the column-operand image of the encode's sweep update: col [N][K] (row
 // stride ld) -> bf16 hi / lo fragments of each 64-column tile, K = 64, 96 or
 // 128 and N a multiple of 128; lr_col_image_bytes = its size (0: no image

@@ -798,6 +798,21 @@ __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+// A workgroup barrier for LDS written by copies that other copies still in
+// flight do not touch: this wave's vector-memory operations down to N
+// outstanding (its copies that must have landed) and all its LDS accesses
+// done, then the barrier.  No memory fence: a workgroup-scope release would
+// also wait for the copies meant to stay in flight across the barrier.  The
+// empty asm statements keep the compiler from moving memory accesses across.
+template <int N>
+__device__ __forceinline__ void copies_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt is six bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (0 << 8));
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // The column-operand image: entry (tile T, chunk ch, column c, fg g) holds
 // the hi and lo fragments of col[64 T + c][32 ch + 4 g .. + 3] and
 // [32 ch + 16 + 4 g .. + 3] (split8), hi at T 2 TS + ch 256 + lds_slot(c, g)
@@ -1196,6 +1211,164 @@ __global__ __launch_bounds__(kUpdThreads) __attribute__((amdgpu_waves_per_eu(2, 
   lr_sweep_body<EPI, KC, EF, NSEG>(p);
 }
 
+// ---------------------------------------------------------------------------
+// Transposed projection Q^T = W^T U (the output side's U_G^T W of eq.
+// design_full_transform, stored n x r) with split-bf16 products: out[j][k] =
+// sum_i W[i][j] U[i][k] for k < r = 64 KGW, U given as U^T ([r][K] rows).
+// The contraction runs over W's rows, which no register layout reads
+// contiguously, so W goes through LDS: each 32-row stage of a 64-column
+// tile is copied HBM -> LDS with no registers (four-stage ring, three
+// stages in flight), the 16-column chunks of row i at chunk position
+// g ^ ((i >> 2) & 3), and each lane reads its eight rows of one column with
+// 32-bit LDS reads (conflict-free under that swizzle) and splits them into
+// the matrix-core operand.  A workgroup's four waves split r (16 KGW
+// columns each) and share the 64 columns of W; U^T comes straight from L2
+// (every workgroup reads all of it).  The products are those of the bf16
+// hi / lo split of both operands (hi hi + hi lo + lo hi), accumulated in
+// float32 over the stages in order: deterministic.  Split-K: workgroup z of
+// a column tile takes rows [z rps, (z + 1) rps) and writes partial z.
+// ---------------------------------------------------------------------------
+
+constexpr int kPtStage = 32;   // rows of W per stage (four-slot LDS ring)
+
+struct PTArgs {
+  const float *W = nullptr;    // [batch][K][M] (M contiguous)
+  int64_t wbs = 0;             // floats between ranks' W
+  int K = 0, M = 0;            // rows of W (contraction), columns of W (output rows)
+  const float *Ut = nullptr;   // [r][K], shared by the batch
+  float *C = nullptr;          // [batch][ks][M][r]
+  int64_t cbs = 0;             // floats between partials (M r)
+  int ks = 1, rps = 0;         // partials, rows per partial (a multiple of 32)
+};
+
+template <int KGW>
+__global__ __launch_bounds__(256) void lr_projT_kernel(const PTArgs p) {
+  constexpr int R = 64 * KGW;
+  // the four ring slots as separate arrays, so that the compiler's wait
+  // analysis tells the copies into one slot from reads of another
+  __shared__ __attribute__((aligned(1024))) float ring0[kPtStage * 64], ring1[kPtStage * 64],
+      ring2[kPtStage * 64], ring3[kPtStage * 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int fr = lane & 15, fg = lane >> 4;
+  const int tiles_j = p.M / 64;
+  const int lin = (int)blockIdx.x;
+  const int tj = lin % tiles_j;
+  const int bz = lin / tiles_j;
+  const int z = bz % p.ks, b = bz / p.ks;
+  const int j0 = 64 * tj;
+  const int ibeg = z * p.rps;
+  const int iend = ibeg + p.rps < p.K ? ibeg + p.rps : p.K;
+  // stages of the part, padded to whole rounds of the four-slot ring (rows
+  // at or past iend read zeros and add nothing)
+  const int nst = (iend - ibeg + 4 * kPtStage - 1) / (4 * kPtStage) * 4;   // >= 4 (launcher: part non-empty)
+  const int kb = wave * 16 * KGW;
+
+  // W stage s -> ring slot s % 4: piece 2 wave + h is LDS rows 4 (2 wave + h)
+  // .. + 3; lane l lands at row + (l >> 4), chunk position (l & 15) >> 2,
+  // float4 l & 3, so it fetches W[row][16 (pos ^ ((row >> 2) & 3)) + 4 (l & 3)]
+  const __amdgpu_buffer_rsrc_t rsW = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)(p.W + (int64_t)b * p.wbs), (short)0, (int)((int64_t)p.K * p.M * 4), 0x00020000);
+  int wrow[2], wcol[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    wrow[h] = 4 * (2 * wave + h) + (lane >> 4);
+    wcol[h] = j0 + 16 * (((lane & 15) >> 2) ^ ((wrow[h] >> 2) & 3)) + 4 * (lane & 3);
+  }
+  auto dma = [&](int s, float *dst) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int i = ibeg + kPtStage * s + wrow[h];
+      const uint32_t off = i < iend ? ((uint32_t)i * (uint32_t)p.M + (uint32_t)wcol[h]) * 4u : 0x80000000u;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsW, (GIFT_LDS void *)(dst + (2 * wave + h) * 256), 16, (int)off, 0,
+                                               0, 0);
+    }
+  };
+  // U^T rows kb + 16 g + fr, columns i0 + 4 fg and i0 + 16 + 4 fg of stage s
+  // (the k order of the matrix-core operand used throughout this file)
+  const __amdgpu_buffer_rsrc_t rsU =
+      __builtin_amdgcn_make_buffer_rsrc((void *)p.Ut, (short)0, (int)((int64_t)R * p.K * 4), 0x00020000);
+  typedef float4 BSet[KGW][2];
+  auto load_b = [&](int s, BSet &bs) {
+    const int i = ibeg + kPtStage * s + 4 * fg;
+#pragma unroll
+    for (int g = 0; g < KGW; ++g)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int ii = i + 16 * h;
+        const uint32_t off =
+            ii < iend ? ((uint32_t)(kb + 16 * g + fr) * (uint32_t)p.K + (uint32_t)ii) * 4u : 0x80000000u;
+        bs[g][h] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rsU, (int)off, 0, 0));
+      }
+  };
+
+  floatx4 acc[4][KGW];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int g = 0; g < KGW; ++g) acc[a][g] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  BSet bA, bB;
+  // prologue: U^T of stage 0, then W of stages 0 .. 2; the wait for stage
+  // 0's U^T covers nothing after it
+  load_b(0, bA);
+  dma(0, ring0);
+  dma(1, ring1);
+  dma(2, ring2);
+  copies_barrier<4>();   // stage 0 landed everywhere (stages 1, 2 may be in flight)
+
+  // stage s: U^T of stage s + 1 (into the other set), then W of stage s + 3
+  // into the slot read at stage s - 1 (all waves left it: barrier), then
+  // the products of stage s.  Completing U^T(s + 1) (waited for at stage
+  // s + 1) implies W(s + 2) landed (issued before it), so the W copies run
+  // two to three stages ahead of their use.
+  auto stage = [&](int s, const float *src, float *next3, BSet &cur, BSet &nxt) {
+    load_b(s + 1, nxt);
+    dma(s + 3, next3);
+    __builtin_amdgcn_sched_barrier(0);   // both issued ahead of this stage's products
+    uint4 bh[KGW], bl[KGW];
+#pragma unroll
+    for (int g = 0; g < KGW; ++g) split8(cur[g][0], cur[g][1], bh[g], bl[g]);
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      // column 16 a + fr, rows 4 fg .. + 3 and 16 + 4 fg .. + 3 (both with
+      // (row >> 2) & 3 = fg: chunk position a ^ fg)
+      const float *c = src + 16 * (a ^ fg) + fr;
+      float4 lo, hi;
+      lo.x = c[(4 * fg + 0) * 64];
+      lo.y = c[(4 * fg + 1) * 64];
+      lo.z = c[(4 * fg + 2) * 64];
+      lo.w = c[(4 * fg + 3) * 64];
+      hi.x = c[(16 + 4 * fg + 0) * 64];
+      hi.y = c[(16 + 4 * fg + 1) * 64];
+      hi.z = c[(16 + 4 * fg + 2) * 64];
+      hi.w = c[(16 + 4 * fg + 3) * 64];
+      uint4 ah, al;
+      split8(lo, hi, ah, al);
+#pragma unroll
+      for (int g = 0; g < KGW; ++g) acc[a][g] = mfma3(ah, al, bh[g], bl[g], acc[a][g]);
+    }
+    // this wave's W of stage s + 1 landed (only W(s + 2), U^T(s + 1) and
+    // W(s + 3) may be in flight: 2 + 2 KGW + 2), then everyone's; everyone
+    // is done with slot s % 4
+    copies_barrier<4 + 2 * KGW>();
+  };
+  for (int s = 0; s < nst; s += 4) {
+    stage(s, ring0, ring3, bA, bB);
+    stage(s + 1, ring1, ring0, bB, bA);
+    stage(s + 2, ring2, ring1, bA, bB);
+    stage(s + 3, ring3, ring2, bB, bA);
+  }
+
+  // lane holds out[j0 + 16 a + 4 fg + e][kb + 16 g + fr]
+  float *out = p.C + ((int64_t)b * p.ks + z) * p.cbs;
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int g = 0; g < KGW; ++g)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) out[(int64_t)(j0 + 16 * a + 4 * fg + e) * R + kb + 16 * g + fr] = acc[a][g][e];
+}
+
 bool al16(const void *q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; }
 
 }  // namespace
@@ -1259,6 +1432,60 @@ gift_status launch_lr_proj(gift_ctx *ctx, const TileJob &j) {
     default: hipLaunchKernelGGL(lr_proj_kernel<8>, grid, dim3(kProjThreads), 0, ctx->stream, a); break;
   }
   return check_launch("lr_proj_kernel");
+}
+
+// rows per part of a K-row contraction split ks ways (whole 128-row rounds)
+int64_t lr_projT_rows(int64_t K, int ks) {
+  return ((K + ks - 1) / ks + 4 * kPtStage - 1) / (4 * kPtStage) * (4 * kPtStage);
+}
+
+int lr_projT_parts(int64_t M, int64_t K, int64_t r, int32_t batch) {
+  if (!(r == 64 || r == 128) || M <= 0 || M % 64 != 0 || K <= 0 || K % 4 != 0 || K * M >= (1LL << 29) ||
+      batch < 1 || (M / 64) * (int64_t)batch >= (1LL << 30))
+    return 0;
+  // split the rows while the launch holds under 512 workgroups and each
+  // part keeps at least 128 rows; parts of whole rounds of the four-stage
+  // ring (128 rows)
+  const int64_t tiles = M / 64 * batch;
+  int ks = 1;
+  while (ks < 16 && tiles * ks < 512 && K / (2 * ks) >= 128) ks *= 2;
+  const int64_t rps = lr_projT_rows(K, ks);
+  return (int)((K + rps - 1) / rps);
+}
+
+bool lr_projT_eligible(const TileJob &j) {
+  if (j.nseg != 1 || j.split3 == false || j.D != nullptr || j.colscale != nullptr || j.alpha != 1.f ||
+      j.beta != 0.f || j.amax || j.codes || j.mx_codes || j.decode_tab)
+    return false;
+  const Segment &g = j.seg[0];
+  const int parts = lr_projT_parts(j.M, g.K, j.N, j.batch);
+  return parts > 0 && parts == j.ksplit && !g.a.kmajor && g.a.ld == j.M && g.a.bs == g.K * j.M && g.b.kmajor &&
+         g.b.ld == g.K && g.b.bs == 0 && g.b.parts <= 1 && g.a.parts <= 1 && j.ldc == j.N && j.cbs == j.M * j.N &&
+         al16(g.a.ptr) && al16(g.b.ptr) && al16(j.C);
+}
+
+gift_status launch_lr_projT(gift_ctx *ctx, const TileJob &j) {
+  if (!lr_projT_eligible(j)) return GIFT_EUNSUPPORTED;
+  const Segment &g = j.seg[0];
+  PTArgs a{};
+  a.W = g.a.ptr;
+  a.wbs = g.a.bs;
+  a.K = (int)g.K;
+  a.M = (int)j.M;
+  a.Ut = g.b.ptr;
+  a.C = j.C;
+  a.cbs = j.cbs;
+  a.ks = j.ksplit;
+  a.rps = (int)lr_projT_rows(g.K, j.ksplit);
+  // every part non-empty (lr_projT_parts)
+  if ((int64_t)(a.ks - 1) * a.rps >= g.K) return GIFT_EUNSUPPORTED;
+  const int64_t wgs = j.M / 64 * (int64_t)j.batch * j.ksplit;
+  ProfileScope prof(ctx, j.kernel_family);
+  if (j.N == 64)
+    hipLaunchKernelGGL(lr_projT_kernel<1>, dim3((unsigned)wgs), dim3(256), 0, ctx->stream, a);
+  else
+    hipLaunchKernelGGL(lr_projT_kernel<2>, dim3((unsigned)wgs), dim3(256), 0, ctx->stream, a);
+  return check_launch("lr_projT_kernel");
 }
 
 size_t lr_col_image_bytes(int64_t N, int K) {
