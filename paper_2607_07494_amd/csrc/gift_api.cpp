@@ -264,6 +264,10 @@ bool encode_recomputes(const gift_factor *f, int64_t n, const float *grads, cons
   if (f->m * n >= (1LL << 29)) return false;
   const int K = useA ? f->A.r : f->G.r;
   if (K > 128 || K % 4 != 0 || n % 4 != 0) return false;
+  // both sides at rank 96 or 128 without a residual: the rank-2r update is
+  // bound by the matrix cores, so the AMAX pass (sweep variant) stores W~
+  // and the quantize pass streams it rather than forming it again
+  if (useA && useG && K >= 96 && n % 128 == 0 && !ef) return false;
   return al16p(grads) && (!ef || al16p(ef)) && (!transformed || al16p(transformed)) &&
          (reinterpret_cast<uintptr_t>(codes) & 3) == 0;
 }
@@ -1028,6 +1032,7 @@ static gift_status encode_impl(gift_ctx *ctx, const gift_factor *f, const float 
   job.ef = ef;
   job.scales = scales;
   job.transformed = gemm ? wt : transformed;
+  job.sweep_store = gemm && !recompute;
   job.kernel_family = gemm ? GIFT_KERNEL_UPDATE_AMAX : GIFT_KERNEL_AMAX;
   // both passes must take the same kernel, or their W~ would differ
   if (recompute && !lr_update_eligible(job))

@@ -249,6 +249,9 @@ struct TileJob {
   const void *col_img = nullptr;
   const void *col_img2 = nullptr;
   int64_t img_bs = 0, img_bs2 = 0;
+  // the two-sided AMAX pass at rank 96 or 128 stores W~ to `transformed` in
+  // the sweep variant (the encode then quantizes the stored W~)
+  bool sweep_store = false;
 };
 
 gift_status launch_tile(gift_ctx *ctx, const TileJob &job);

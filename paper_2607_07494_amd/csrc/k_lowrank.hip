@@ -839,24 +839,28 @@ __global__ __launch_bounds__(256) void lr_col_image_kernel(const float *col, int
 }
 
 // ---------------------------------------------------------------------------
-// Sweep variant of the encode's two passes, for the input-side transform
-// alone at rank 32 NCH (N a multiple of 128, every 32 x 64 wave tile inside
-// one scale block, per-rank scales, no boundary-hit counts; with or without
-// the error-feedback residual): a workgroup walks a run of
-// `upw` consecutive 128 x 128 units of the batch, ordered (rank, row block,
-// column pair), 64 columns at a time.  Per tile it multiplies from one half
-// of a double-buffered LDS ring while the next tile's column operand is
-// copied into the other half straight from its pre-split image (no registers,
-// no conversions) and W of the tile after next is loading into the register
-// set just consumed; the row operand (the rows of P) is loaded and split once
-// per row block.  The products are those of lr_update_body in the same order
-// and the image holds the same splits, so W~, the block maxima and the codes
-// are bit-identical to it.
+// Sweep variant of the encode's two passes at rank 32 KC (64, 96, 128; N a
+// multiple of 128, every 32 x 64 wave tile inside one scale block, per-rank
+// scales, no boundary-hit counts): the input-side transform alone (one
+// segment, with or without the error-feedback residual) or both sides at
+// equal ranks (two segments, the rank-2r update, no residual).  A workgroup
+// walks a run of `upw` consecutive 128 x 128 units of the batch, ordered
+// (rank, row block, column pair), 64 columns at a time.  Per tile it
+// multiplies from one half of a double-buffered LDS ring while the next
+// tile's column operand is copied into the other half straight from its
+// pre-split image (no registers, no conversions) and W of the tile after
+// next is loading into the register set just consumed; the row operand (the
+// rows of P) is loaded and split once per row block.  The products are those
+// of lr_update_body in the same order and the image holds the same splits,
+// so W~, the block maxima and the codes are bit-identical to it.  WT: the
+// AMAX pass also stores W~ (both sides at rank 96 or 128, whose update is
+// bound by the matrix cores: the quantize pass then streams the stored W~).
 // ---------------------------------------------------------------------------
 
-template <int EPI, int KC, bool EF, int NSEG>
+template <int EPI, int KC, bool EF, int NSEG, bool WT>
 __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
   static_assert(EPI == EPI_AMAX || EPI == EPI_QUANT, "sweep: AMAX or QUANT");
+  static_assert(!WT || EPI == EPI_AMAX, "sweep: W~ stored by the AMAX pass");
   static_assert(NSEG == 1 || (NSEG == 2 && !EF), "sweep: two segments without a residual");
   constexpr int NCH = NSEG * KC;    // 32-step chunks over both segments
   // W (and the residual) of the tile after next in a second register set,
@@ -1119,6 +1123,17 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
         }
       const int bi = i0 / br, bj = j0 / bc;
       const int gb = b * nblk + bi * (int)p.nbc + bj;
+      if (WT) {   // W~ of the tile for the streaming quantize pass
+#pragma unroll
+        for (int g = 0; g < 2; ++g)
+          if (rv[g]) {
+            float *dst = p.transformed + (int64_t)b * MN + (int64_t)(i0 + 16 * g + fr) * N32 + j0 + 4 * fg;
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+              st_u128_untracked(dst + 16 * t, make_uint4(__float_as_uint(w[g][t][0]), __float_as_uint(w[g][t][1]),
+                                                         __float_as_uint(w[g][t][2]), __float_as_uint(w[g][t][3])));
+          }
+      }
       if (EPI == EPI_AMAX) {
         uint32_t m = 0u;
 #pragma unroll
@@ -1205,10 +1220,10 @@ __device__ __forceinline__ void lr_sweep_body(const LUArgs &p) {
     atomicMax(&p.amax[run_blk * kAmaxSlots + slot], run_max);
 }
 
-template <int EPI, int KC, bool EF = false, int NSEG = 1>
+template <int EPI, int KC, bool EF = false, int NSEG = 1, bool WT = false>
 __global__ __launch_bounds__(kUpdThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void lr_sweep_kernel(
     const LUArgs p) {
-  lr_sweep_body<EPI, KC, EF, NSEG>(p);
+  lr_sweep_body<EPI, KC, EF, NSEG, WT>(p);
 }
 
 // ---------------------------------------------------------------------------
@@ -1597,7 +1612,12 @@ gift_status launch_lr_update(gift_ctx *ctx, const TileJob &j) {
       j.nseg == 1 ? j.col_img != nullptr && j.seg[0].a.parts == 1 && j.seg[0].b.bs == 0 && j.img_bs == 0
                   : j.nseg == 2 && !ef && j.col_img != nullptr && j.col_img2 != nullptr && j.seg[0].a.parts == 1 &&
                         j.seg[1].a.parts == 1 && j.seg[1].K == K0 && j.img_bs >= 0 && j.img_bs2 >= 0;
-  const bool sweep = full && seg_ok && !j.mx_codes && !(quant && j.hits) && (K0 == 64 || K0 == 96 || K0 == 128) &&
+  // (the two-segment AMAX pass at rank 96 or 128 may also store W~ for a
+  // streaming quantize pass: sweep_store)
+  const bool wt_store = j.transformed != nullptr && j.sweep_store && !quant && j.nseg == 2 && (K0 == 96 || K0 == 128) &&
+                        al16(j.transformed);
+  const bool full_sw = full || (wt_store && lr_quant_reads_raw(j));
+  const bool sweep = full_sw && seg_ok && !j.mx_codes && !(quant && j.hits) && (K0 == 64 || K0 == 96 || K0 == 128) &&
                      j.N % 128 == 0 && !j.shared && sw_units > 0 && sw_units < (1LL << 30) &&
                      (int64_t)j.batch * j.geom.nbr * j.geom.nbc * kAmaxSlots < (1LL << 31);
   if (sweep) {
@@ -1618,6 +1638,15 @@ gift_status launch_lr_update(gift_ctx *ctx, const TileJob &j) {
       constexpr int E = decltype(epi_c)::value;
       constexpr bool R = decltype(ef_c)::value;
       constexpr int S = decltype(nseg_c)::value;
+      if constexpr (S == 2 && !R && E == EPI_AMAX) {
+        if (wt_store) {
+          if (K0 == 96)
+            hipLaunchKernelGGL((lr_sweep_kernel<E, 3, false, 2, true>), sgrid, dim3(kUpdThreads), 0, ctx->stream, a);
+          else
+            hipLaunchKernelGGL((lr_sweep_kernel<E, 4, false, 2, true>), sgrid, dim3(kUpdThreads), 0, ctx->stream, a);
+          return;
+        }
+      }
       if constexpr (S == 1 || !R) {
         switch (K0) {
           case 64: hipLaunchKernelGGL((lr_sweep_kernel<E, 2, R, S>), sgrid, dim3(kUpdThreads), 0, ctx->stream, a); break;

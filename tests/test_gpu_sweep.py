@@ -13,7 +13,12 @@ oracle's quantization (Algorithm 1, Scale / Q; Sec. I, amax rule).
 
 The two-sided encode at equal ranks takes the two-segment sweep (the rank-2r
 update (U_G C_G) Q + L_2 U_A^T of eq. design_full_transform, segment 0's
-column operand Q per rank, segment 1's U_A^T shared); the same checks hold.
+column operand Q per rank, segment 1's U_A^T shared).  At rank 64 it forms
+W~ in both passes (the same checks as above); at rank 96 and 128 its AMAX
+pass stores W~ and the quantize pass streams it, whatever the caller asks,
+so there the reference kernels are those of the error-feedback encode with a
+zero residual (per-unit, W~ + R formed in both passes): codes and scales
+bit-identical.
 
 The cases choose the run length (units of the launch: 1 below 1024, then
 units / 512, 4 from 2048 on) and make runs cross row blocks (an odd number
@@ -187,10 +192,22 @@ def test_two_sided_sweep_matches_unit_kernel_and_oracle(ctx, N, m, n, r, br, bc)
     codes_u = torch.empty_like(codes_s)
     scales_u = torch.full_like(scales_s, float("nan"))
     tr = torch.empty((N, m, n), dtype=torch.float32, device=DEV)
-    gift.encode(ctx, f, g, codes_u, scales_u, br, bc, gift.SCALE_LOCAL, transformed=tr)   # per unit
+    gift.encode(ctx, f, g, codes_u, scales_u, br, bc, gift.SCALE_LOCAL, transformed=tr)
     torch.cuda.synchronize()
     assert torch.equal(scales_s, scales_u)
     assert torch.equal(codes_s, codes_u)
+    if r >= 96:
+        # at rank 96 or 128 both calls above store W~ in the AMAX pass and
+        # quantize the stored values; with a (zero) residual the encode
+        # forms W~ + R in both passes with the per-unit kernels instead:
+        # the same codes and scales
+        codes_e = torch.empty_like(codes_s)
+        scales_e = torch.full_like(scales_s, float("nan"))
+        ef = torch.zeros((N, m, n), dtype=torch.float32, device=DEV)
+        gift.encode(ctx, f, g, codes_e, scales_e, br, bc, gift.SCALE_LOCAL, ef=ef)
+        torch.cuda.synchronize()
+        assert torch.equal(scales_e, scales_s)
+        assert torch.equal(codes_e, codes_s)
     # first, middle and last rank against the float64 transform and the
     # oracle's quantization of the stored W~
     idx = sorted({0, N // 2, N - 1})
