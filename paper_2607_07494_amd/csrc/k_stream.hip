@@ -295,7 +295,11 @@ __global__ __launch_bounds__(kThreads) void stream_reduce_kernel(const SArgs p) 
       for (int j = 0; j < NR; ++j) {
         if constexpr (W == 4) {
           uint4 v = make_uint4(0u, 0u, 0u, 0u);
-          if (ok) v = *reinterpret_cast<const uint4 *>(p.codes + j * mn + off);
+          if (ok) {
+            typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+            const u32x4 t = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p.codes + j * mn + off));
+            v = make_uint4(t.x, t.y, t.z, t.w);
+          }
           st.c[u][j][0] = v.x;
           st.c[u][j][1] = v.y;
           st.c[u][j][2] = v.z;
