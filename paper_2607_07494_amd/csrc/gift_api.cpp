@@ -280,6 +280,17 @@ struct LowRankPlan {
   bool active = false;
 };
 
+// The two-sided form's products with small grids (K = U_G^T P always, and
+// W^T U_G over few ranks: 4 to 64 tiles of 64 x 64) split their contraction
+// over the rows into partials, summed in order: enough workgroups to fill
+// the GPU.
+int small_split(int64_t M, int64_t Nc, int64_t batch, int64_t K) {
+  const int64_t tiles = (M + 63) / 64 * ((Nc + 63) / 64) * batch;
+  int ks = 1;
+  while (ks < 16 && tiles * ks < 512 && K / (2 * ks) >= 64) ks *= 2;
+  return ks;
+}
+
 gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, int32_t N,
                           int64_t m, int64_t n, bool inverse, char *ws, size_t *used,
                           LowRankPlan *plan) {
@@ -298,16 +309,6 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
   const bool pp_ok = useA && (!useG || inverse) && aligned && n % 4 == 0 &&
                      (A.r == 16 || A.r == 32 || A.r == 64 || A.r == 128);
   const int pparts = !pp_ok ? 1 : (inverse ? proj_parts(m, n, A.r, N) : lr_proj_parts(m, n, N));
-  // the two-sided form's products with small grids (K = U_G^T P always, and
-  // W^T U_G over few ranks: 4 to 64 tiles of 64 x 64) split their
-  // contraction over the rows into partials, summed in order: enough
-  // workgroups to fill the GPU
-  auto small_split = [](int64_t M, int64_t Nc, int64_t batch, int64_t K) -> int {
-    const int64_t tiles = (M + 63) / 64 * ((Nc + 63) / 64) * batch;
-    int ks = 1;
-    while (ks < 16 && tiles * ks < 512 && K / (2 * ks) >= 64) ks *= 2;
-    return ks;
-  };
   // (the in-order sum reads 16-byte groups: a partial's size a multiple of 4)
   // The encode's U_G^T W at rank 64 or 128 takes the split-bf16 transposed
   // projection with its own partial count.
@@ -1297,6 +1298,195 @@ gift_status gift_decode(gift_ctx *ctx, const gift_factor *f, const float *mean, 
   return launch_tile(ctx, job);
 }
 
+// gift_decode_batch for two-sided low-rank factors of one rank r (both
+// sides, 16 to 128): one launch per product over all matrices, each
+// matrix's mean, output and factor operands reached through device pointer
+// tables; every product takes the kernel, split-K partials and summation
+// order that gift_decode takes for one matrix (eq. design_full_inverse_transform:
+// P = M U_A, Q = U_G^T M, K = U_G^T P, L2 = (P + U_G C'_G K) C'_A, then
+// out = M + (U_G C'_G) Q + L2 U_A^T), so the outputs equal its bit for bit.
+// Returns GIFT_EUNSUPPORTED (nothing enqueued) when the shapes do not allow it.
+static gift_status decode_batch_both(gift_ctx *ctx, int32_t count, const gift_factor *const *factors,
+                                     const float *const *means, float *const *outs, int64_t m, int64_t n) {
+  const gift_factor *f0 = factors[0];
+  const int32_t r = f0->A.r;
+  if (count < 2 || !(r == 16 || r == 32 || r == 64 || r == 128) || f0->G.r != r || n % 4 != 0 ||
+      m * n >= (1LL << 29))
+    return GIFT_EUNSUPPORTED;
+  for (int32_t i = 0; i < count; ++i) {
+    const gift_factor *f = factors[i];
+    if (!f || f->chol || !side_in(f->sides, GIFT_SIDE_INPUT) || !side_in(f->sides, GIFT_SIDE_OUTPUT) ||
+        f->A.r != r || f->G.r != r || !al16p(means[i]) || !al16p(outs[i]) || !al16p(f->A.Ut) ||
+        !al16p(f->A.U) || !al16p(f->A.c_inv) || !al16p(f->G.Ut) || !al16p(f->G.Uci))
+      return GIFT_EUNSUPPORTED;
+  }
+  // gift_decode's partial counts for one matrix
+  const int pparts = proj_parts(m, n, r, 1);
+  const bool presum = pparts > 1;
+  const int qsplit = (n * r) % 4 == 0 ? small_split(n, r, 1, m) : 1;
+  const int ksplit = ((int64_t)r * r) % 4 == 0 ? small_split(r, r, 1, m) : 1;
+  TileJob pj;
+  pj.nseg = 1;
+  pj.seg[0].a = Operand{means[0], n, 0, true};
+  pj.seg[0].b = Operand{f0->A.Ut, n, 0, true};
+  pj.seg[0].K = n;
+  pj.M = m;
+  pj.N = r;
+  pj.batch = count;
+  pj.ldc = r;
+  pj.cbs = m * r;
+  pj.ksplit = pparts;
+  pj.kernel_family = GIFT_KERNEL_DECODE_PROJECT;
+  // workspace: P (partials), its sum, Q (partials), K (partials), L2
+  const int64_t C = count;
+  size_t off = 0;
+  auto carve = [&](size_t floats) {
+    const size_t at = off;
+    off += a256(sizeof(float) * floats);
+    return at;
+  };
+  const size_t oP = carve((size_t)C * pparts * m * r), oPs = presum ? carve((size_t)C * m * r) : 0;
+  const size_t oQ = carve((size_t)C * n * r), oQp = qsplit > 1 ? carve((size_t)C * qsplit * n * r) : 0;
+  const size_t oK = carve((size_t)C * r * r), oKp = ksplit > 1 ? carve((size_t)C * ksplit * r * r) : 0;
+  const size_t oL = carve((size_t)C * m * r);
+  void *ws = nullptr;
+  pj.C = reinterpret_cast<float *>(off);   // placeholder for the eligibility check (aligned)
+  if (!proj_staged_eligible(pj)) return GIFT_EUNSUPPORTED;
+  // the final update on the register-direct kernel, as gift_decode's
+  TileJob uj;
+  uj.nseg = 2;
+  uj.seg[0].a = Operand{nullptr, r, 0, true};
+  uj.seg[0].b = Operand{nullptr, r, n * r, true};
+  uj.seg[0].K = r;
+  uj.seg[1].a = Operand{nullptr, r, m * r, true};
+  uj.seg[1].b = Operand{nullptr, r, 0, true};
+  uj.seg[1].K = r;
+  uj.M = m;
+  uj.N = n;
+  uj.batch = count;
+  uj.ldc = n;
+  uj.cbs = m * n;
+  uj.ldd = n;
+  uj.dbs = m * n;
+  uj.beta = 1.f;
+  uj.kernel_family = GIFT_KERNEL_UPDATE_STORE;
+  // device tables: means, outputs, U_G^T, U_G diag(c'_G), U_A, c'_A per matrix
+  std::vector<const void *> host((size_t)6 * count);
+  for (int32_t i = 0; i < count; ++i) {
+    host[0 * (size_t)count + i] = means[i];
+    host[1 * (size_t)count + i] = outs[i];
+    host[2 * (size_t)count + i] = factors[i]->G.Ut;
+    host[3 * (size_t)count + i] = factors[i]->G.Uci;
+    host[4 * (size_t)count + i] = factors[i]->A.U;
+    host[5 * (size_t)count + i] = factors[i]->A.c_inv;
+  }
+  // (the eligibility of the update with its tables set: placeholders, not dereferenced)
+  {
+    const float *const *dummy = reinterpret_cast<const float *const *>(host.data());
+    TileJob chk = uj;
+    chk.seg[0].a.tab = dummy;
+    chk.seg[1].b.tab = dummy;
+    chk.seg[0].b.ptr = reinterpret_cast<const float *>(off);
+    chk.seg[1].a.ptr = reinterpret_cast<const float *>(off);
+    chk.d_tab = dummy;
+    chk.c_tab = const_cast<float *const *>(reinterpret_cast<const float *const *>(dummy));
+    if (!update_kernel_eligible(chk)) return GIFT_EUNSUPPORTED;
+  }
+  gift_status st;
+  if ((st = workspace(ctx, off, &ws)) != GIFT_OK) return st;
+  char *w = static_cast<char *>(ws);
+  float *P = reinterpret_cast<float *>(w + oP), *Ps = presum ? reinterpret_cast<float *>(w + oPs) : P;
+  float *Qm = reinterpret_cast<float *>(w + oQ), *Qp = reinterpret_cast<float *>(w + oQp);
+  float *Km = reinterpret_cast<float *>(w + oK), *Kp = reinterpret_cast<float *>(w + oKp);
+  float *L2 = reinterpret_cast<float *>(w + oL);
+  void *tb = nullptr;
+  if ((st = upload_table(ctx, TAB_DECODE_BOTH, f0, host.data(), sizeof(void *) * host.size(), &tb)) != GIFT_OK)
+    return st;
+  const float *const *t_mean = static_cast<const float *const *>(tb);
+  float *const *t_out = const_cast<float *const *>(t_mean + count);
+  const float *const *t_gut = t_mean + 2 * count, *const *t_guci = t_mean + 3 * count;
+  const float *const *t_au = t_mean + 4 * count, *const *t_acinv = t_mean + 5 * count;
+  std::vector<DecodePtrs> dp(count);
+  for (int32_t i = 0; i < count; ++i) dp[i] = DecodePtrs{means[i], factors[i]->A.Ut, factors[i]->A.Uci, outs[i]};
+  void *dt = nullptr;
+  if ((st = upload_table(ctx, TAB_DECODE, f0, dp.data(), sizeof(DecodePtrs) * (size_t)count, &dt)) != GIFT_OK)
+    return st;
+  // P = M U_A (partials, summed in order)
+  pj.C = P;
+  pj.decode_tab = static_cast<const DecodePtrs *>(dt);
+  if ((st = launch_proj(ctx, pj)) != GIFT_OK) return st;
+  if (presum && (st = launch_lr_psum(ctx, P, Ps, pparts, m * r, count, GIFT_KERNEL_DECODE_PROJECT)) != GIFT_OK)
+    return st;
+  {  // Q^T = M^T U_G
+    TileJob j;
+    j.nseg = 1;
+    j.seg[0].a = Operand{nullptr, n, m * n, false};
+    j.seg[0].a.tab = t_mean;
+    j.seg[0].b = Operand{nullptr, m, 0, true};
+    j.seg[0].b.tab = t_gut;
+    j.seg[0].K = m;
+    j.M = n;
+    j.N = r;
+    j.batch = count;
+    j.C = qsplit > 1 ? Qp : Qm;
+    j.ldc = r;
+    j.cbs = n * r;
+    j.ksplit = qsplit;
+    j.kernel_family = GIFT_KERNEL_DECODE_PROJECT;
+    if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
+    if (qsplit > 1 && (st = launch_lr_psum(ctx, Qp, Qm, qsplit, n * r, count, j.kernel_family)) != GIFT_OK)
+      return st;
+  }
+  {  // K = U_G^T P
+    TileJob j;
+    j.nseg = 1;
+    j.seg[0].a = Operand{nullptr, m, 0, true};
+    j.seg[0].a.tab = t_gut;
+    j.seg[0].b = Operand{Ps, r, m * r, false};
+    j.seg[0].K = m;
+    j.M = r;
+    j.N = r;
+    j.batch = count;
+    j.C = ksplit > 1 ? Kp : Km;
+    j.ldc = r;
+    j.cbs = (int64_t)r * r;
+    j.ksplit = ksplit;
+    j.kernel_family = GIFT_KERNEL_DECODE_PROJECT;
+    if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
+    if (ksplit > 1 && (st = launch_lr_psum(ctx, Kp, Km, ksplit, (int64_t)r * r, count, j.kernel_family)) != GIFT_OK)
+      return st;
+  }
+  {  // L2 = (P + U_G C'_G K) C'_A
+    TileJob j;
+    j.nseg = 1;
+    j.seg[0].a = Operand{nullptr, r, 0, true};
+    j.seg[0].a.tab = t_guci;
+    j.seg[0].b = Operand{Km, r, (int64_t)r * r, false};
+    j.seg[0].K = r;
+    j.M = m;
+    j.N = r;
+    j.batch = count;
+    j.C = L2;
+    j.ldc = r;
+    j.cbs = m * r;
+    j.D = Ps;
+    j.ldd = r;
+    j.dbs = m * r;
+    j.beta = 1.f;
+    j.colscale_tab = t_acinv;
+    j.kernel_family = GIFT_KERNEL_DECODE_PROJECT;
+    if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
+  }
+  // out = M + (U_G C'_G) Q + L2 U_A^T
+  uj.seg[0].a.tab = t_guci;
+  uj.seg[0].b.ptr = Qm;
+  uj.seg[1].a.ptr = L2;
+  uj.seg[1].b.tab = t_au;
+  uj.d_tab = t_mean;
+  uj.c_tab = t_out;
+  return launch_tile(ctx, uj);
+}
+
 gift_status gift_decode_batch(gift_ctx *ctx, int32_t count, const gift_factor *const *factors,
                               const float *const *means, float *const *outs, int64_t m, int64_t n) {
   if (!ctx) return set_error(GIFT_EINVAL, "gift_decode_batch: ctx is NULL");
@@ -1315,10 +1505,14 @@ gift_status gift_decode_batch(gift_ctx *ctx, int32_t count, const gift_factor *c
       if (outs[j] == outs[i]) return set_error(GIFT_EINVAL, "gift_decode_batch: an output appears twice");
   }
   if ((st = bind_device(ctx)) != GIFT_OK) return st;
+  const gift_factor *f0 = factors[0];
+  if (count > 1 && f0 && !f0->chol && f0->A.r > 0 && f0->G.r > 0) {
+    st = decode_batch_both(ctx, count, factors, means, outs, m, n);
+    if (st != GIFT_EUNSUPPORTED) return st;
+  }
   // one launch per pass for input-side low-rank factors of one rank: the
   // kernels, split-K partials and summation order of gift_decode, with the
   // batch index running over the matrices
-  const gift_factor *f0 = factors[0];
   bool grouped = count > 1 && f0 && !f0->chol && f0->A.r > 0 && f0->G.r == 0 && n % 4 == 0 &&
                  m * n < (1LL << 29);
   const int32_t r = grouped ? f0->A.r : 0;

@@ -50,7 +50,8 @@ struct TableSlot {
   hipEvent_t copied = nullptr;   // the last copy out of `pinned`
   bool valid = false;
 };
-enum TableKind { TAB_REFRESH = 0, TAB_STATS = 1, TAB_CHOL_STATS = 2, TAB_CHOL_BLOCKS = 3, TAB_DECODE = 4 };
+enum TableKind { TAB_REFRESH = 0, TAB_STATS = 1, TAB_CHOL_STATS = 2, TAB_CHOL_BLOCKS = 3, TAB_DECODE = 4,
+                 TAB_DECODE_BOTH = 5 };
 
 // Per-matrix operands of a grouped decode (one batch entry per matrix): the
 // rank mean, the factor's U^T and U diag(c'), and the output.
@@ -183,6 +184,10 @@ struct Operand {
   // the operand is the sum of `parts` split-K partials, partial z of batch b
   // at ptr + (b * parts + z) * bs (register-direct update kernel only)
   int parts = 1;
+  // grouped decode of many matrices: batch entry b's operand starts at
+  // tab[b] (device array; ptr and bs unused).  Taken by the tile kernel and
+  // the register-direct update kernel only (job_has_tabs).
+  const float *const *tab = nullptr;
 };
 
 struct Segment {
@@ -249,12 +254,24 @@ struct TileJob {
   const void *col_img = nullptr;
   const void *col_img2 = nullptr;
   int64_t img_bs = 0, img_bs2 = 0;
+  // grouped decode: per-entry column scales (tile kernel), addend and output
+  // (update kernel), device arrays indexed by the batch entry
+  const float *const *colscale_tab = nullptr;
+  const float *const *d_tab = nullptr;
+  float *const *c_tab = nullptr;
   // the two-sided AMAX pass at rank 96 or 128 stores W~ to `transformed` in
   // the sweep variant (the encode then quantizes the stored W~)
   bool sweep_store = false;
 };
 
 gift_status launch_tile(gift_ctx *ctx, const TileJob &job);
+// the job reaches some operand, addend, output or column scale through a
+// per-entry pointer table
+inline bool job_has_tabs(const TileJob &j) {
+  for (int s = 0; s < j.nseg && s < 2; ++s)
+    if (j.seg[s].a.tab || j.seg[s].b.tab) return true;
+  return j.colscale_tab || j.d_tab || j.c_tab;
+}
 // k_lowrank.hip: the encode's projection and rank-r update with split bf16
 // operands; lr_proj_parts = split-K partials of the projection
 bool lr_update_eligible(const TileJob &job);

@@ -36,6 +36,7 @@ struct OperandP {
   const float *ptr;
   int64_t ld, bs;
   int vec;  // 16-byte loads allowed
+  const float *const *tab;   // batch entry b at tab[b] (grouped decode), else ptr + b bs
 };
 struct SegmentP {
   OperandP a, b;
@@ -54,6 +55,7 @@ struct KArgs {
   int64_t ldd, dbs;
   float alpha, beta;
   const float *colscale;
+  const float *const *colscale_tab;   // per batch entry (grouped decode), else colscale
   uint32_t *amax;
   uint8_t *codes;
   uint32_t *hits;        // QUANT: boundary-hit counters [batch][2] or null
@@ -75,7 +77,7 @@ struct TileLoader {
 
   __device__ __forceinline__ void load(const OperandP &op, int b, int64_t row0, int64_t rows,
                                        int64_t k0, int64_t K, int tid) {
-    const float *base = op.ptr + (int64_t)b * op.bs;
+    const float *base = op.tab ? op.tab[b] : op.ptr + (int64_t)b * op.bs;
 #pragma unroll
     for (int s = 0; s < kPerThread; ++s) {
       const int q = tid + s * kThreads;
@@ -355,13 +357,14 @@ __global__ __launch_bounds__(kThreads) void tile_kernel(const KArgs p) {
       if (EPI == EPI_STORE) {
         float *cp = p.C + (int64_t)zb * p.cbs + gi * p.ldc + gj;
         const float *dp = p.D ? p.D + (int64_t)b * p.dbs + gi * p.ldd + gj : nullptr;
+        const float *cs = p.colscale_tab ? p.colscale_tab[b] : p.colscale;
         float o[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           if (gj + e < p.N) {
             float val = p.alpha * acc4[e];
             if (dp) val += p.beta * dp[e];
-            if (p.colscale) val *= p.colscale[gj + e];
+            if (cs) val *= cs[gj + e];
             o[e] = val;
           }
         }
@@ -527,12 +530,14 @@ __global__ void copy_f32_kernel(float *dst, const float *src, int64_t n) {
 
 KArgs make_args(const TileJob &j) {
   KArgs a{};
+  // (a table's pointers are 16-byte aligned: the grouped decode checks them)
   auto op = [](const Operand &o) {
-    OperandP r;
+    OperandP r{};
     r.ptr = o.ptr;
     r.ld = o.ld;
     r.bs = o.bs;
     r.vec = (o.ld % 4 == 0) && (o.bs % 4 == 0) && ((reinterpret_cast<uintptr_t>(o.ptr) & 15) == 0);
+    r.tab = o.tab;
     return r;
   };
   for (int s = 0; s < 2; ++s) {
@@ -554,6 +559,7 @@ KArgs make_args(const TileJob &j) {
   a.alpha = j.alpha;
   a.beta = j.beta;
   a.colscale = j.colscale;
+  a.colscale_tab = j.colscale_tab;
   a.amax = j.amax;
   a.codes = j.codes;
   a.hits = j.codes ? j.hits : nullptr;
@@ -595,18 +601,25 @@ void launch_layouts(const KArgs &a, bool ak, bool bk, int zdim, hipStream_t st) 
 
 gift_status launch_tile(gift_ctx *ctx, const TileJob &job) {
   if (job.M <= 0 || job.N <= 0 || job.batch <= 0) return GIFT_OK;
+  // per-entry pointer tables (grouped decode): the register-direct update
+  // kernel (operands, addend, output) or this file's store tile (operands,
+  // column scales), nothing else
+  const bool tabs = job_has_tabs(job);
   // the encode's products on the bf16 matrix cores (split operands)
-  if (job.split3 && job.nseg > 0 && job.amax != nullptr && lr_update_eligible(job))
+  if (!tabs && job.split3 && job.nseg > 0 && job.amax != nullptr && lr_update_eligible(job))
     return launch_lr_update(ctx, job);
-  if (job.split3 && job.nseg > 0 && job.amax == nullptr && lr_proj_eligible(job))
+  if (!tabs && job.split3 && job.nseg > 0 && job.amax == nullptr && lr_proj_eligible(job))
     return launch_lr_proj(ctx, job);
   // register-direct kernels for the rank-r update and the projections
-  if (job.nseg > 0 && (job.amax != nullptr || job.D != nullptr) && update_kernel_eligible(job))
+  if (job.nseg > 0 && (job.amax != nullptr || job.D != nullptr || job.d_tab != nullptr) &&
+      update_kernel_eligible(job))
     return launch_update(ctx, job);
   for (int s = 0; s < job.nseg; ++s)
     if (job.seg[s].a.parts != 1 || job.seg[s].b.parts != 1)
       return set_error(GIFT_EUNSUPPORTED, "split-K partial operand outside the update kernel");
-  if (job.amax == nullptr && job.nseg > 0 && proj_kernel_eligible(job)) return launch_proj(ctx, job);
+  if (!tabs && job.amax == nullptr && job.nseg > 0 && proj_kernel_eligible(job)) return launch_proj(ctx, job);
+  if (tabs && (job.amax != nullptr || job.d_tab != nullptr || job.c_tab != nullptr || job.nseg == 0))
+    return set_error(GIFT_EUNSUPPORTED, "internal: pointer tables outside the update and store tile kernels");
   const bool gemm = job.nseg > 0;
   if (job.amax != nullptr && !gemm &&
       stream_eligible(job.M, job.N, job.geom, job.D, job.codes, job.ef, job.transformed))

@@ -49,6 +49,10 @@ struct USeg {
   const float *col;   // [batch][N][K]
   int64_t col_ld, col_bs;
   int K;
+  // grouped decode: batch entry b's row / column operand at row_tab[b] /
+  // col_tab[b] (one partial), else as above
+  const float *const *row_tab;
+  const float *const *col_tab;
 };
 
 struct UArgs {
@@ -68,6 +72,10 @@ struct UArgs {
   int nbr, nbc;
   int shared;
   const DecodePtrs *tab;  // grouped decode: per-entry column operand, D and C
+  // grouped decode with both factors: per-entry D and C (the operands through
+  // the segments' tables)
+  const float *const *d_tab;
+  float *const *c_tab;
 };
 
 __device__ __forceinline__ float4 ld4(const float *p) { return *reinterpret_cast<const float4 *>(p); }
@@ -138,7 +146,8 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const UArgs p) {
 #pragma unroll
   for (int s = 0; s < NSEG; ++s) {
     const int np = p.seg[s].row_parts;
-    const float *base = p.seg[s].row + (int64_t)b * np * p.seg[s].row_bs + rc * p.seg[s].row_ld + 4 * fg;
+    const float *base = (p.seg[s].row_tab ? p.seg[s].row_tab[b] : p.seg[s].row + (int64_t)b * np * p.seg[s].row_bs) +
+                        rc * p.seg[s].row_ld + 4 * fg;
 #pragma unroll
     for (int q = 0; q < K16; ++q) bfr[s][q] = ld4(base + 16 * q);
     for (int z = 1; z < np; ++z) {
@@ -169,7 +178,9 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const UArgs p) {
       const int64_t cj = j0 + col;
       // clamped address, unconditional load; columns past N are zeroed when
       // the tile goes to LDS
-      const float *colb = p.tab ? p.tab[b].uci : p.seg[s].col + (int64_t)b * p.seg[s].col_bs;
+      const float *colb = p.seg[s].col_tab ? p.seg[s].col_tab[b]
+                          : p.tab        ? p.tab[b].uci
+                                         : p.seg[s].col + (int64_t)b * p.seg[s].col_bs;
       creg[u] = ld4(colb + (cj < p.N ? cj : 0) * p.seg[s].col_ld + kk);
     }
   };
@@ -184,8 +195,8 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const UArgs p) {
   };
   // W (and residual) by unconditional buffer loads over this rank's slice:
   // rows past M read zeros, columns past N are left out by the epilogue
-  const float *Db = p.tab ? p.tab[b].mean : p.D + (int64_t)b * MN;
-  float *Cb = p.tab ? p.tab[b].out : (p.C ? p.C + (int64_t)b * MN : nullptr);
+  const float *Db = p.d_tab ? p.d_tab[b] : p.tab ? p.tab[b].mean : p.D + (int64_t)b * MN;
+  float *Cb = p.c_tab ? p.c_tab[b] : p.tab ? p.tab[b].out : (p.C ? p.C + (int64_t)b * MN : nullptr);
   const __amdgpu_buffer_rsrc_t rsD =
       __builtin_amdgcn_make_buffer_rsrc((void *)Db, (short)0, (int)(MN * 4), 0x00020000);
   const __amdgpu_buffer_rsrc_t rsE = __builtin_amdgcn_make_buffer_rsrc(
@@ -592,6 +603,14 @@ bool proj_staged_eligible(const TileJob &j) { return proj_kernel_eligible(j) && 
 
 bool update_kernel_eligible(const TileJob &j) {
   if (j.N % 4 != 0 || j.nseg < 1 || j.nseg > 2) return false;
+  // per-entry tables: a store with the decode's table for neither, a
+  // partial-free operand behind each table, no column scales
+  if (job_has_tabs(j)) {
+    if (j.amax != nullptr || j.decode_tab != nullptr || j.colscale_tab != nullptr || !j.d_tab || !j.c_tab)
+      return false;
+    for (int s = 0; s < j.nseg; ++s)
+      if ((j.seg[s].a.tab && j.seg[s].a.parts != 1) || (j.seg[s].b.tab && j.seg[s].b.parts != 1)) return false;
+  }
   if (j.M * j.N >= (1LL << 29)) return false;   // one rank's slice within a 32-bit buffer range
   const int64_t K = j.seg[0].K;
   if (K != 16 && K != 32 && K != 64 && K != 128) return false;
@@ -601,7 +620,7 @@ bool update_kernel_eligible(const TileJob &j) {
     if (g.a.ld % 4 || g.b.ld % 4 || g.a.bs % 4 || g.b.bs % 4) return false;
     if (!al16(g.a.ptr) || !al16(g.b.ptr)) return false;
   }
-  if (!al16(j.D) || (j.C && !al16(j.C)) || (j.transformed && !al16(j.transformed)) ||
+  if (!al16(j.D) || (j.C && !al16(j.C)) || (!j.D && !j.d_tab) || (j.transformed && !al16(j.transformed)) ||
       (j.ef && !al16(j.ef)) || (j.codes && (reinterpret_cast<uintptr_t>(j.codes) & 3)))
     return false;
   if (j.amax == nullptr) {  // decode store: dense output, D dense
@@ -623,6 +642,8 @@ gift_status launch_update(gift_ctx *ctx, const TileJob &j) {
     a.seg[s].col_ld = j.seg[s].b.ld;
     a.seg[s].col_bs = j.seg[s].b.bs;
     a.seg[s].K = (int)j.seg[s].K;
+    a.seg[s].row_tab = j.seg[s].a.tab;
+    a.seg[s].col_tab = j.seg[s].b.tab;
   }
   a.nseg = j.nseg;
   a.M = j.M;
@@ -642,6 +663,8 @@ gift_status launch_update(gift_ctx *ctx, const TileJob &j) {
   a.nbc = j.geom.nbc;
   a.shared = j.shared ? 1 : 0;
   a.tab = j.decode_tab;
+  a.d_tab = j.d_tab;
+  a.c_tab = j.c_tab;
   ProfileScope prof(ctx, j.kernel_family);
   dim3 grid((unsigned)((j.N + kColsPerUnit - 1) / kColsPerUnit), (unsigned)((j.M + 63) / 64),
             (unsigned)j.batch);

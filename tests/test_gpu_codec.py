@@ -420,13 +420,20 @@ def test_error_feedback_two_steps(ctx, N, m, n, r, sides, br, bc):
     ("grouped r=64, ragged rows", 333, 256, [64] * 5, gift.SIDE_INPUT, []),
     ("grouped r=16", 520, 384, [16, 16], gift.SIDE_INPUT, []),
     ("mixed ranks: per-matrix calls", 300, 256, [32, 64], gift.SIDE_INPUT, []),
-    ("two-sided: per-matrix calls", 200, 256, [32, 32], gift.SIDE_BOTH, []),
+    ("two-sided grouped r=32", 200, 256, [32, 32], gift.SIDE_BOTH, []),
+    ("two-sided grouped r=128", 300, 512, [128, 128, 128], gift.SIDE_BOTH, []),
+    ("two-sided grouped r=64, ragged rows", 333, 256, [64] * 5, gift.SIDE_BOTH, []),
+    ("two-sided grouped r=16", 520, 384, [16, 16], gift.SIDE_BOTH, []),
+    ("two-sided grouped r=128, long rows", 1536, 1536, [128] * 3, gift.SIDE_BOTH, []),
+    ("two-sided mixed ranks: per-matrix calls", 200, 256, [32, 64], gift.SIDE_BOTH, []),
     ("identity entry: per-matrix calls", 300, 256, [64, 64, 64], gift.SIDE_INPUT, [1]),
 ])
 def test_decode_batch_equals_separate_decodes(ctx, label, m, n, ranks, sides, nulls):
     """gift_decode_batch over matrices of one shape gives exactly what one
     gift_decode per matrix gives (the grouped launch runs the same kernels,
-    split-K partials and summation order), also after the factors change."""
+    split-K partials and summation order: input-side factors of one rank, and
+    two-sided factors of one rank with every matrix's operands through device
+    tables), also after the factors change."""
     say(f"decode batch: {label} m={m} n={n} ranks={ranks}")
     fs = [None if i in nulls else make_factor(ctx, m, n, r, sides, seed=17 * i + m)[0]
           for i, r in enumerate(ranks)]
@@ -442,10 +449,14 @@ def test_decode_batch_equals_separate_decodes(ctx, label, m, n, ranks, sides, nu
             assert torch.equal(o, ref)
         # a refreshed factor set (new pointers' contents, same table)
         for f, r in zip(fs, ranks):
-            if f is not None and sides == gift.SIDE_INPUT:
-                fA = codec.lowrank_factor(codec.factor_statistics(factor_inputs(900 + rep, 4 * n, n)[0]), r).to_f32()
-                f.import_(gift.SIDE_INPUT, t(fA.U.astype(np.float32)), t(fA.c_fwd.astype(np.float32)),
-                          t(fA.c_inv.astype(np.float32)), t(np.array([fA.sigma2], np.float32)))
+            if f is None:
+                continue
+            for side, dim in ((gift.SIDE_INPUT, n), (gift.SIDE_OUTPUT, m)):
+                if sides & side:
+                    fx = codec.lowrank_factor(codec.factor_statistics(factor_inputs(900 + rep + dim, 4 * dim, dim)[0]),
+                                              r).to_f32()
+                    f.import_(side, t(fx.U.astype(np.float32)), t(fx.c_fwd.astype(np.float32)),
+                              t(fx.c_inv.astype(np.float32)), t(np.array([fx.sigma2], np.float32)))
     for f in fs:
         if f is not None:
             f.close()
