@@ -364,15 +364,19 @@ gift_status gift_decode(gift_ctx *ctx, const gift_factor *f, const float *mean,
  * factors, means and outs are HOST arrays of count device handles /
  * pointers; every mean and out is [m, n] float32, outs distinct and not
  * aliasing their means.  When every factor is a low-rank input-side factor
- * of one rank r in {16, 32, 64, 128} (and the buffers are 16-byte aligned),
- * each pass runs as one launch over all matrices with the kernels,
- * split-K partials and summation order of gift_decode, so the results equal
- * count separate gift_decode calls bit for bit; the per-matrix operand
- * pointers come from a device table the context uploads (through its pinned
- * buffer) only when they change.  Otherwise the call runs count gift_decode
- * calls.  Uses the context workspace (count * parts * m * r floats of
- * projections).  Errors: as gift_decode; GIFT_EINVAL for NULL arrays, a
- * count outside [0, 65535] or an output listed twice. */
+ * of one rank r in {16, 32, 64, 128}, or every factor is a two-sided
+ * low-rank factor with rank r in that set on both sides (eq.
+ * design_full_inverse_transform), and the buffers are 16-byte aligned, each
+ * pass (each product of the inverse) runs as one launch over all matrices
+ * with the kernels, split-K partials and summation order of gift_decode, so
+ * the results equal count separate gift_decode calls bit for bit; the
+ * per-matrix operand pointers come from device tables the context uploads
+ * (through its pinned buffer) only when they change.  Otherwise the call
+ * runs count gift_decode calls.  Uses the context workspace (the
+ * projections of all count matrices: count * parts * m * r floats, and for
+ * two-sided factors also their Q, K and L2 terms).  Errors: as gift_decode;
+ * GIFT_EINVAL for NULL arrays, a count outside [0, 65535] or an output
+ * listed twice. */
 gift_status gift_decode_batch(gift_ctx *ctx, int32_t count, const gift_factor *const *factors,
                               const float *const *means, float *const *outs, int64_t m, int64_t n);
 
