@@ -314,7 +314,12 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
   // projection with its own partial count.
   const int pt_parts = useG && !inverse && aligned && al16p(G.Ut) ? lr_projT_parts(n, m, G.r, N) : 0;
   const int qsplit = pt_parts > 0 ? pt_parts : useG && (n * G.r) % 4 == 0 ? small_split(n, G.r, N, m) : 1;
-  const int ksplit_k = useA && useG && ((int64_t)G.r * A.r) % 4 == 0 ? small_split(G.r, A.r, N, m) : 1;
+  // the encode's K at ranks 64 / 128 as Kᵀ = Pᵀ U_G on the same transposed
+  // split-bf16 projection (Kᵀ [r_A][r_G] then feeds L2 K-major)
+  const int kt_parts = useA && useG && !inverse && al16p(G.Ut) ? lr_projT_parts(A.r, m, G.r, N) : 0;
+  const int ksplit_k = kt_parts > 0                                  ? kt_parts
+                       : useA && useG && ((int64_t)G.r * A.r) % 4 == 0 ? small_split(G.r, A.r, N, m)
+                                                                       : 1;
   size_t off = 0;
   float *P = nullptr, *Qm = nullptr, *Km = nullptr, *L2 = nullptr, *Psum = nullptr;
   float *Qpart = nullptr, *Kpart = nullptr;
@@ -408,21 +413,30 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
       return st;
   }
   if (useA && useG) {
-    {  // K = U_G^T P  (r_G x r_A)
+    {  // K = U_G^T P  (r_G x r_A), or Kᵀ = Pᵀ U_G  (r_A x r_G)
       TileJob j;
       j.nseg = 1;
-      j.seg[0].a = Operand{G.Ut, m, 0, true};
-      j.seg[0].b = Operand{presum ? Psum : P, A.r, m * A.r, false};
+      if (kt_parts > 0) {
+        j.seg[0].a = Operand{presum ? Psum : P, A.r, m * A.r, false};
+        j.seg[0].b = Operand{G.Ut, m, 0, true};
+        j.M = A.r;
+        j.N = G.r;
+        j.ldc = G.r;
+        j.split3 = true;
+      } else {
+        j.seg[0].a = Operand{G.Ut, m, 0, true};
+        j.seg[0].b = Operand{presum ? Psum : P, A.r, m * A.r, false};
+        j.M = G.r;
+        j.N = A.r;
+        j.ldc = A.r;
+      }
       j.seg[0].K = m;
-      j.M = G.r;
-      j.N = A.r;
       j.batch = N;
       j.C = ksplit_k > 1 ? Kpart : Km;
-      j.ldc = A.r;
       j.cbs = (int64_t)G.r * A.r;
       j.ksplit = ksplit_k;
       j.kernel_family = inverse ? GIFT_KERNEL_DECODE_PROJECT : GIFT_KERNEL_PROJECT;
-      if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
+      if ((st = kt_parts > 0 ? launch_lr_projT(ctx, j) : launch_tile(ctx, j)) != GIFT_OK) return st;
       if (ksplit_k > 1 &&
           (st = launch_lr_psum(ctx, Kpart, Km, ksplit_k, (int64_t)G.r * A.r, N, j.kernel_family)) != GIFT_OK)
         return st;
@@ -431,7 +445,8 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
       TileJob j;
       j.nseg = 1;
       j.seg[0].a = Operand{UcG, G.r, 0, true};
-      j.seg[0].b = Operand{Km, A.r, (int64_t)G.r * A.r, false};
+      j.seg[0].b = kt_parts > 0 ? Operand{Km, G.r, (int64_t)G.r * A.r, true}
+                                : Operand{Km, A.r, (int64_t)G.r * A.r, false};
       j.seg[0].K = G.r;
       j.M = m;
       j.N = A.r;

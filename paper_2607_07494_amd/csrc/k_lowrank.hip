@@ -1470,7 +1470,7 @@ int lr_projT_parts(int64_t M, int64_t K, int64_t r, int32_t batch) {
 
 bool lr_projT_eligible(const TileJob &j) {
   if (j.nseg != 1 || j.split3 == false || j.D != nullptr || j.colscale != nullptr || j.alpha != 1.f ||
-      j.beta != 0.f || j.amax || j.codes || j.mx_codes || j.decode_tab)
+      j.beta != 0.f || j.amax || j.codes || j.mx_codes || j.decode_tab || job_has_tabs(j))
     return false;
   const Segment &g = j.seg[0];
   const int parts = lr_projT_parts(j.M, g.K, j.N, j.batch);
