@@ -459,6 +459,7 @@ gift_status plan_low_rank(gift_ctx *ctx, const gift_factor *f, const float *W, i
       j.dbs = m * A.r;
       j.beta = 1.f;
       j.colscale = inverse ? A.c_inv : A.c_fwd;
+      j.split3 = kt_parts > 0;   // the split-bf16 projection kernel with its addend and scales
       j.kernel_family = inverse ? GIFT_KERNEL_DECODE_PROJECT : GIFT_KERNEL_PROJECT;
       if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
     }

@@ -130,6 +130,11 @@ struct LPArgs {
   int64_t kper;      // contraction steps per part (multiple of kProjStage)
   int out_t;         // store transposed (parts = 1)
   int64_t out_ld, out_bs;
+  // parts = 1, not transposed: out = (acc + D) * colscale, D [batch][M][C]
+  // (d_bs floats apart) and colscale [C] each optional
+  const float *D;
+  int64_t d_bs;
+  const float *colscale;
 };
 
 template <int NT>
@@ -225,9 +230,20 @@ __global__ __launch_bounds__(kProjThreads) void lr_proj_kernel(const LPArgs p) {
     return;
   }
   float *ob = p.out + (((int64_t)b * p.parts + z) * p.M + ri) * C;
+  const float *db = p.D ? p.D + (int64_t)b * p.d_bs + ri * C : nullptr;
 #pragma unroll
-  for (int t = 0; t < NT; ++t)
-    *reinterpret_cast<float4 *>(ob + 16 * t + 4 * fg) = make_float4(acc[t][0], acc[t][1], acc[t][2], acc[t][3]);
+  for (int t = 0; t < NT; ++t) {
+    float4 v = make_float4(acc[t][0], acc[t][1], acc[t][2], acc[t][3]);
+    if (db) {
+      const float4 d = ld4(db + 16 * t + 4 * fg);
+      v.x += d.x; v.y += d.y; v.z += d.z; v.w += d.w;
+    }
+    if (p.colscale) {
+      const float4 c = ld4(p.colscale + 16 * t + 4 * fg);
+      v.x *= c.x; v.y *= c.y; v.z *= c.z; v.w *= c.w;
+    }
+    *reinterpret_cast<float4 *>(ob + 16 * t + 4 * fg) = v;
+  }
 }
 
 // P[b][i][c] = sum_z partial[b][z][i][c], z in order (float32), so that the
@@ -1412,10 +1428,15 @@ bool lr_proj_eligible(const TileJob &j) {
   const bool tr = lr_strip_is_b(j);
   const int64_t C = tr ? j.M : j.N;
   const Operand &xs = tr ? g.b : g.a, &ys = tr ? g.a : g.b;
-  if (!(j.split3 && j.nseg == 1 && j.amax == nullptr && j.D == nullptr && j.colscale == nullptr &&
-        j.alpha == 1.f && (C == 16 || C == 32 || C == 64 || C == 128) && g.a.kmajor && g.b.kmajor &&
-        g.K % 4 == 0 && xs.ld == g.K && ys.ld == g.K && xs.bs % 4 == 0 && ys.bs % 4 == 0 && al16(xs.ptr) &&
-        al16(ys.ptr)))
+  if (!(j.split3 && j.nseg == 1 && j.amax == nullptr && j.alpha == 1.f &&
+        (C == 16 || C == 32 || C == 64 || C == 128) && g.a.kmajor && g.b.kmajor && g.K % 4 == 0 &&
+        xs.ld == g.K && ys.ld == g.K && xs.bs % 4 == 0 && ys.bs % 4 == 0 && al16(xs.ptr) && al16(ys.ptr) &&
+        !job_has_tabs(j)))
+    return false;
+  // an addend and column scales: whole, untransposed, one partial
+  if ((j.D || j.colscale) &&
+      (tr || j.ksplit > 1 || j.beta != 1.f || (j.D && (!al16(j.D) || j.ldd != C || j.dbs != j.M * C)) ||
+       (j.colscale && !al16(j.colscale))))
     return false;
   if (tr) return j.ksplit <= 1;
   return al16(j.C) && j.ldc == C && j.cbs == j.M * C && (j.ksplit <= 1 || ys.bs == 0);
@@ -1438,6 +1459,9 @@ gift_status launch_lr_proj(gift_ctx *ctx, const TileJob &j) {
   a.out_t = tr ? 1 : 0;
   a.out_ld = j.ldc;
   a.out_bs = j.cbs;
+  a.D = j.D;
+  a.d_bs = j.dbs;
+  a.colscale = j.colscale;
   ProfileScope prof(ctx, j.kernel_family);
   const dim3 grid((unsigned)((a.M + kProjRows - 1) / kProjRows), (unsigned)a.parts, (unsigned)j.batch);
   switch (C) {
