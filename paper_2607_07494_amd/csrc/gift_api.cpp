@@ -1366,26 +1366,13 @@ static gift_status decode_batch_both(gift_ctx *ctx, int32_t count, const gift_fa
   const size_t oK = carve((size_t)C * r * r), oKp = ksplit > 1 ? carve((size_t)C * ksplit * r * r) : 0;
   const size_t oL = carve((size_t)C * m * r);
   void *ws = nullptr;
-  pj.C = reinterpret_cast<float *>(off);   // placeholder for the eligibility check (aligned)
-  if (!proj_staged_eligible(pj)) return GIFT_EUNSUPPORTED;
-  // the final update on the register-direct kernel, as gift_decode's
-  TileJob uj;
-  uj.nseg = 2;
-  uj.seg[0].a = Operand{nullptr, r, 0, true};
-  uj.seg[0].b = Operand{nullptr, r, n * r, true};
-  uj.seg[0].K = r;
-  uj.seg[1].a = Operand{nullptr, r, m * r, true};
-  uj.seg[1].b = Operand{nullptr, r, 0, true};
-  uj.seg[1].K = r;
-  uj.M = m;
-  uj.N = n;
-  uj.batch = count;
-  uj.ldc = n;
-  uj.cbs = m * n;
-  uj.ldd = n;
-  uj.dbs = m * n;
-  uj.beta = 1.f;
-  uj.kernel_family = GIFT_KERNEL_UPDATE_STORE;
+  gift_status st;
+  if ((st = workspace(ctx, off, &ws)) != GIFT_OK) return st;
+  char *w = static_cast<char *>(ws);
+  float *P = reinterpret_cast<float *>(w + oP), *Ps = presum ? reinterpret_cast<float *>(w + oPs) : P;
+  float *Qm = reinterpret_cast<float *>(w + oQ), *Qp = reinterpret_cast<float *>(w + oQp);
+  float *Km = reinterpret_cast<float *>(w + oK), *Kp = reinterpret_cast<float *>(w + oKp);
+  float *L2 = reinterpret_cast<float *>(w + oL);
   // device tables: means, outputs, U_G^T, U_G diag(c'_G), U_A, c'_A per matrix
   std::vector<const void *> host((size_t)6 * count);
   for (int32_t i = 0; i < count; ++i) {
@@ -1396,25 +1383,6 @@ static gift_status decode_batch_both(gift_ctx *ctx, int32_t count, const gift_fa
     host[4 * (size_t)count + i] = factors[i]->A.U;
     host[5 * (size_t)count + i] = factors[i]->A.c_inv;
   }
-  // (the eligibility of the update with its tables set: placeholders, not dereferenced)
-  {
-    const float *const *dummy = reinterpret_cast<const float *const *>(host.data());
-    TileJob chk = uj;
-    chk.seg[0].a.tab = dummy;
-    chk.seg[1].b.tab = dummy;
-    chk.seg[0].b.ptr = reinterpret_cast<const float *>(off);
-    chk.seg[1].a.ptr = reinterpret_cast<const float *>(off);
-    chk.d_tab = dummy;
-    chk.c_tab = const_cast<float *const *>(reinterpret_cast<const float *const *>(dummy));
-    if (!update_kernel_eligible(chk)) return GIFT_EUNSUPPORTED;
-  }
-  gift_status st;
-  if ((st = workspace(ctx, off, &ws)) != GIFT_OK) return st;
-  char *w = static_cast<char *>(ws);
-  float *P = reinterpret_cast<float *>(w + oP), *Ps = presum ? reinterpret_cast<float *>(w + oPs) : P;
-  float *Qm = reinterpret_cast<float *>(w + oQ), *Qp = reinterpret_cast<float *>(w + oQp);
-  float *Km = reinterpret_cast<float *>(w + oK), *Kp = reinterpret_cast<float *>(w + oKp);
-  float *L2 = reinterpret_cast<float *>(w + oL);
   void *tb = nullptr;
   if ((st = upload_table(ctx, TAB_DECODE_BOTH, f0, host.data(), sizeof(void *) * host.size(), &tb)) != GIFT_OK)
     return st;
@@ -1427,9 +1395,35 @@ static gift_status decode_batch_both(gift_ctx *ctx, int32_t count, const gift_fa
   void *dt = nullptr;
   if ((st = upload_table(ctx, TAB_DECODE, f0, dp.data(), sizeof(DecodePtrs) * (size_t)count, &dt)) != GIFT_OK)
     return st;
-  // P = M U_A (partials, summed in order)
   pj.C = P;
   pj.decode_tab = static_cast<const DecodePtrs *>(dt);
+  // the final update on the register-direct kernel, as gift_decode's:
+  // out = M + (U_G C'_G) Q + L2 U_A^T
+  TileJob uj;
+  uj.nseg = 2;
+  uj.seg[0].a = Operand{nullptr, r, 0, true};
+  uj.seg[0].a.tab = t_guci;
+  uj.seg[0].b = Operand{Qm, r, n * r, true};
+  uj.seg[0].K = r;
+  uj.seg[1].a = Operand{L2, r, m * r, true};
+  uj.seg[1].b = Operand{nullptr, r, 0, true};
+  uj.seg[1].b.tab = t_au;
+  uj.seg[1].K = r;
+  uj.M = m;
+  uj.N = n;
+  uj.batch = count;
+  uj.d_tab = t_mean;
+  uj.c_tab = t_out;
+  uj.ldc = n;
+  uj.cbs = m * n;
+  uj.ldd = n;
+  uj.dbs = m * n;
+  uj.beta = 1.f;
+  uj.kernel_family = GIFT_KERNEL_UPDATE_STORE;
+  // both ends on the kernels gift_decode takes, or nothing is enqueued (the
+  // tables and workspace stay for later calls)
+  if (!proj_staged_eligible(pj) || !update_kernel_eligible(uj)) return GIFT_EUNSUPPORTED;
+  // P = M U_A (partials, summed in order)
   if ((st = launch_proj(ctx, pj)) != GIFT_OK) return st;
   if (presum && (st = launch_lr_psum(ctx, P, Ps, pparts, m * r, count, GIFT_KERNEL_DECODE_PROJECT)) != GIFT_OK)
     return st;
@@ -1493,13 +1487,6 @@ static gift_status decode_batch_both(gift_ctx *ctx, int32_t count, const gift_fa
     j.kernel_family = GIFT_KERNEL_DECODE_PROJECT;
     if ((st = launch_tile(ctx, j)) != GIFT_OK) return st;
   }
-  // out = M + (U_G C'_G) Q + L2 U_A^T
-  uj.seg[0].a.tab = t_guci;
-  uj.seg[0].b.ptr = Qm;
-  uj.seg[1].a.ptr = L2;
-  uj.seg[1].b.tab = t_au;
-  uj.d_tab = t_mean;
-  uj.c_tab = t_out;
   return launch_tile(ctx, uj);
 }
 
