@@ -62,6 +62,7 @@ constexpr int kLdsK = 128;   // k handled in LDS by the small kernels
 // float32 products (relative noise ~1e-7), so rotating further changes nothing
 // the codec can see.
 constexpr double kJacobiTol = 1e-10;
+constexpr int kEigRegs = 16;   // global eigensolver: a column pair in registers up to k = 256
 
 // One factor side of the refresh.  The side's persistent state, then its
 // slices of the group buffers.
@@ -604,11 +605,13 @@ __global__ __launch_bounds__(kEigThreads) void rr_eig_lds_kernel(const SmallJob 
   rr_emit(W, norms, perm, k, J.out, J.theta);
 }
 
-// Global-memory eigensolver for k > 128 (same ordering and rotations; lanes
-// re-read the columns).
+// Global-memory eigensolver for k > 128 (same ordering, rotations and stop
+// rule as the LDS one): up to k = 256 each lane loads its elements of a
+// column pair into registers together, then rotates them from there; past
+// that it re-reads the columns.
 __global__ __launch_bounds__(kSmallThreads) void rr_eig_global_kernel(const SmallJob *jobs,
                                                                       int max_sweeps) {
-  __shared__ int any_rot;
+  __shared__ int any_rot, any_big;
   __shared__ int perm_dummy[1];
   (void)perm_dummy;
   const SmallJob J = jobs[blockIdx.x];
@@ -620,8 +623,12 @@ __global__ __launch_bounds__(kSmallThreads) void rr_eig_global_kernel(const Smal
   __syncthreads();
   const int kp = (k + 1) & ~1, npairs = kp / 2;
   const int l16 = tid & 15, groups = nt / 16;
+  const double last2 = kJacobiLast * kJacobiLast;
   for (int sweep = 0; sweep < max_sweeps; ++sweep) {
-    if (tid == 0) any_rot = 0;
+    if (tid == 0) {
+      any_rot = 0;
+      any_big = 0;
+    }
     __syncthreads();
     for (int round = 0; round < kp - 1; ++round) {
       for (int pb = 0; pb < npairs; pb += groups) {
@@ -634,33 +641,75 @@ __global__ __launch_bounds__(kSmallThreads) void rr_eig_global_kernel(const Smal
         }
         double alpha = 0.0, beta = 0.0, gamma = 0.0;
         double *cp = W + (int64_t)p * k, *cq = W + (int64_t)q * k;
-        if (valid) {
-          for (int i = l16; i < k; i += 16) {
-            const double a = cp[i], b = cq[i];
-            alpha += a * a;
-            beta += b * b;
-            gamma += a * b;
+        if (k <= 16 * kEigRegs) {
+          // the lane's elements of both columns loaded together into registers
+          // (one round trip, not one per element), the same sums in the same
+          // order, and the rotation from the registers
+          double va[kEigRegs], vb[kEigRegs];
+#pragma unroll
+          for (int u = 0; u < kEigRegs; ++u) {
+            const int i = l16 + 16 * u;
+            va[u] = valid && i < k ? cp[i] : 0.0;
+            vb[u] = valid && i < k ? cq[i] : 0.0;
           }
-        }
-        alpha = row16_sum(alpha);
-        beta = row16_sum(beta);
-        gamma = row16_sum(gamma);
-        if (valid && gamma != 0.0 && fabs(gamma) > kJacobiTol * sqrt(alpha * beta)) {
-          double c, s;
-          jacobi_cs(alpha, beta, gamma, c, s);
-          for (int i = l16; i < k; i += 16) {
-            const double a = cp[i], b = cq[i];
-            cp[i] = c * a - s * b;
-            cq[i] = s * a + c * b;
+#pragma unroll
+          for (int u = 0; u < kEigRegs; ++u)
+            if (l16 + 16 * u < k) {
+              alpha += va[u] * va[u];
+              beta += vb[u] * vb[u];
+              gamma += va[u] * vb[u];
+            }
+          alpha = row16_sum(alpha);
+          beta = row16_sum(beta);
+          gamma = row16_sum(gamma);
+          if (valid && gamma != 0.0 && fabs(gamma) > kJacobiTol * sqrt(alpha * beta)) {
+            double c, s;
+            jacobi_cs(alpha, beta, gamma, c, s);
+#pragma unroll
+            for (int u = 0; u < kEigRegs; ++u) {
+              const int i = l16 + 16 * u;
+              if (i < k) {
+                cp[i] = c * va[u] - s * vb[u];
+                cq[i] = s * va[u] + c * vb[u];
+              }
+            }
+            if (l16 == 0) {
+              any_rot = 1;
+              if (gamma * gamma > last2 * (alpha * beta)) any_big = 1;
+            }
           }
-          if (l16 == 0) any_rot = 1;
+        } else {
+          if (valid) {
+            for (int i = l16; i < k; i += 16) {
+              const double a = cp[i], b = cq[i];
+              alpha += a * a;
+              beta += b * b;
+              gamma += a * b;
+            }
+          }
+          alpha = row16_sum(alpha);
+          beta = row16_sum(beta);
+          gamma = row16_sum(gamma);
+          if (valid && gamma != 0.0 && fabs(gamma) > kJacobiTol * sqrt(alpha * beta)) {
+            double c, s;
+            jacobi_cs(alpha, beta, gamma, c, s);
+            for (int i = l16; i < k; i += 16) {
+              const double a = cp[i], b = cq[i];
+              cp[i] = c * a - s * b;
+              cq[i] = s * a + c * b;
+            }
+            if (l16 == 0) {
+              any_rot = 1;
+              if (gamma * gamma > last2 * (alpha * beta)) any_big = 1;
+            }
+          }
         }
         __syncthreads();
       }
     }
-    const int rotated = any_rot;
+    const int rotated = any_rot, big = any_big;
     __syncthreads();
-    if (!rotated) break;
+    if (!rotated || !big) break;
   }
   for (int c = tid / 16; c < k; c += groups) {
     double s = 0.0;
