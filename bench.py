@@ -212,7 +212,9 @@ def calibrate():
     blocks = 256 * 8                       # 8 waves per SIMD
     buf = torch.empty(blocks * 256, dtype=torch.float32, device=dev)
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
-    for kind, name, flops_per, iters in ((0, "mfma_bf16_tflops", 16384, 2000), (1, "mfma_f32_tflops", 2048, 1000)):
+    for kind, name, flops_per, iters in ((0, "mfma_bf16_tflops", 16384, 2000), (1, "mfma_f32_tflops", 2048, 1000),
+                                         (2, "mfma_bf16_32x32x16_tflops", 32768, 1000),
+                                         (3, "mfma_f32_32x32x2_tflops", 4096, 500)):
         for _ in range(2):
             assert lib.gift_calib_mfma(stream, kind, ctypes.c_void_p(buf.data_ptr()), blocks, 50) == 0
         e0, e1 = ev(), ev()

@@ -2,7 +2,8 @@
 // codec): matrix-core loops with no memory traffic, whose rate is the
 // achievable dense MFMA throughput of this GPU for the two instruction kinds
 // the codec uses (bf16 16x16x32 for the statistics and the split-bf16
-// transforms, float32 16x16x4 for the inverse transform), and a streaming
+// transforms, float32 16x16x4 for the inverse transform) and for their
+// 32 x 32 output forms (bf16 32x32x16, float32 32x32x2), and a streaming
 // read, the achievable HBM read rate (the encode is almost all reads).
 // Built into libgift_calib.so, called by bench.py --calibrate.
 
@@ -12,6 +13,7 @@
 namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kChains = 8;   // independent accumulators per wave (hides the MFMA latency)
@@ -45,6 +47,42 @@ __global__ __launch_bounds__(256) void mfma_loop_f32(float *out, int iters) {
   }
   float s = 0.f;
   for (int c = 0; c < kChains; ++c) s += acc[c][0] + acc[c][1] + acc[c][2] + acc[c][3];
+  out[(int64_t)blockIdx.x * blockDim.x + threadIdx.x] = s;
+}
+
+__global__ __launch_bounds__(256) void mfma_loop_bf16_32(float *out, int iters) {
+  const int lane = threadIdx.x & 63;
+  bf16x8 a, b;
+  for (int i = 0; i < 8; ++i) {
+    a[i] = (__bf16)(0.001f * (lane + i));
+    b[i] = (__bf16)(0.002f * (lane - i));
+  }
+  floatx16 acc[kChains];
+  for (int c = 0; c < kChains; ++c)
+    for (int e = 0; e < 16; ++e) acc[c][e] = 0.f;
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int c = 0; c < kChains; ++c) acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[c], 0, 0, 0);
+  }
+  float s = 0.f;
+  for (int c = 0; c < kChains; ++c)
+    for (int e = 0; e < 16; ++e) s += acc[c][e];
+  out[(int64_t)blockIdx.x * blockDim.x + threadIdx.x] = s;
+}
+
+__global__ __launch_bounds__(256) void mfma_loop_f32_32(float *out, int iters) {
+  const int lane = threadIdx.x & 63;
+  const float a = 0.001f * lane, b = 0.002f * (64 - lane);
+  floatx16 acc[kChains];
+  for (int c = 0; c < kChains; ++c)
+    for (int e = 0; e < 16; ++e) acc[c][e] = 0.f;
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int c = 0; c < kChains; ++c) acc[c] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc[c], 0, 0, 0);
+  }
+  float s = 0.f;
+  for (int c = 0; c < kChains; ++c)
+    for (int e = 0; e < 16; ++e) s += acc[c][e];
   out[(int64_t)blockIdx.x * blockDim.x + threadIdx.x] = s;
 }
 
@@ -86,14 +124,20 @@ int gift_calib_read(void *stream, int kind, const void *src, int64_t bytes, floa
 
 // Launches `blocks` workgroups of 256 threads, each wave running `iters`
 // rounds of kChains matrix-core instructions (kind 0: bf16 16x16x32, 16384
-// flops each; kind 1: float32 16x16x4, 2048 flops each).  out: device
-// float32 [blocks * 256], written once per lane.  Returns the HIP status of
-// the launch; flops = blocks * 4 * iters * kChains * flops per instruction.
+// flops each; 1: float32 16x16x4, 2048 flops; 2: bf16 32x32x16, 32768
+// flops; 3: float32 32x32x2, 4096 flops).  out: device float32
+// [blocks * 256], written once per lane.  Returns the HIP status of the
+// launch (invalid kind: hipErrorInvalidValue, nothing launched); flops =
+// blocks * 4 * iters * kChains * flops per instruction.
 int gift_calib_mfma(void *stream, int kind, float *out, int blocks, int iters) {
-  if (kind == 0)
-    hipLaunchKernelGGL(mfma_loop_bf16, dim3(blocks), dim3(256), 0, static_cast<hipStream_t>(stream), out, iters);
-  else
-    hipLaunchKernelGGL(mfma_loop_f32, dim3(blocks), dim3(256), 0, static_cast<hipStream_t>(stream), out, iters);
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  switch (kind) {
+    case 0: hipLaunchKernelGGL(mfma_loop_bf16, dim3(blocks), dim3(256), 0, s, out, iters); break;
+    case 1: hipLaunchKernelGGL(mfma_loop_f32, dim3(blocks), dim3(256), 0, s, out, iters); break;
+    case 2: hipLaunchKernelGGL(mfma_loop_bf16_32, dim3(blocks), dim3(256), 0, s, out, iters); break;
+    case 3: hipLaunchKernelGGL(mfma_loop_f32_32, dim3(blocks), dim3(256), 0, s, out, iters); break;
+    default: return (int)hipErrorInvalidValue;
+  }
   return (int)hipGetLastError();
 }
 
