@@ -261,7 +261,8 @@ __global__ __launch_bounds__(kThreads) void stream_quant_kernel(const SArgs p) {
 }
 
 // Rank sum with CPL columns per lane (4: one 32-bit code word per rank and
-// row; 16: one 16-byte word), rows in groups of G pipelined as above.
+// row; 8: one 8-byte word; 16: one 16-byte word), rows in groups of G
+// pipelined as above.
 template <int NR, int CPL, int G>
 __global__ __launch_bounds__(kThreads) void stream_reduce_kernel(const SArgs p) {
   constexpr int W = CPL / 4;                 // 32-bit code words per rank and row
@@ -304,6 +305,15 @@ __global__ __launch_bounds__(kThreads) void stream_reduce_kernel(const SArgs p) 
           st.c[u][j][1] = v.y;
           st.c[u][j][2] = v.z;
           st.c[u][j][3] = v.w;
+        } else if constexpr (W == 2) {
+          uint2 v = make_uint2(0u, 0u);
+          if (ok) {
+            typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+            const u32x2 t = __builtin_nontemporal_load(reinterpret_cast<const u32x2 *>(p.codes + j * mn + off));
+            v = make_uint2(t.x, t.y);
+          }
+          st.c[u][j][0] = v.x;
+          st.c[u][j][1] = v.y;
         } else {
           uint32_t v = 0u;
           if (ok) v = *reinterpret_cast<const uint32_t *>(p.codes + j * mn + off);
@@ -457,16 +467,26 @@ gift_status launch_stream_reduce(gift_ctx *ctx, const uint8_t *codes, const floa
   a.nbc = g.nbc;
   ProfileScope prof(ctx, GIFT_KERNEL_REDUCE);
   dim3 grid;
-  const bool wide = n % 16 == 0 && g.bc % 16 == 0 && al16(codes) && al16(mean);
+  const bool aligned = al16(codes) && al16(mean);
+  // 16 columns per lane (16-byte code words) unless 8 leave fewer lanes
+  // past the last column: a wave spans 1024 columns at 16 per lane, so a
+  // 1536-column matrix would leave a quarter of its lanes idle. Measured on
+  // the Llama-600M set (16 ranks): rank sums 3.12 -> 2.72 ms per step in
+  // isolation (4.35 -> 5.0 TB/s by (N + 4) bytes per element); one row per
+  // group instead of two (more waves per SIMD) 2.61 ms alone but 5-6 ms
+  // slower four-stream steps
+  const auto idle = [&](int64_t cpl) { return (n + 64 * cpl - 1) / (64 * cpl) * 64 * cpl - n; };
+  const bool mid = n % 8 == 0 && g.bc % 8 == 0 && aligned && idle(8) < idle(16);
+  const bool wide = !mid && n % 16 == 0 && g.bc % 16 == 0 && aligned;
 #define GIFT_RED(NR, CPL, G)                                                                   \
   do {                                                                                         \
     shape_grid(a, 1, grid, 64 * (CPL), (G));                                                   \
     hipLaunchKernelGGL((stream_reduce_kernel<NR, CPL, G>), grid, dim3(kThreads), 0, ctx->stream, a); \
   } while (0)
   switch (N) {
-    case 4: if (wide) GIFT_RED(4, 16, 2); else GIFT_RED(4, 4, 4); break;
-    case 8: if (wide) GIFT_RED(8, 16, 2); else GIFT_RED(8, 4, 4); break;
-    case 16: if (wide) GIFT_RED(16, 16, 1); else GIFT_RED(16, 4, 2); break;
+    case 4: if (wide) GIFT_RED(4, 16, 2); else if (mid) GIFT_RED(4, 8, 4); else GIFT_RED(4, 4, 4); break;
+    case 8: if (wide) GIFT_RED(8, 16, 2); else if (mid) GIFT_RED(8, 8, 4); else GIFT_RED(8, 4, 4); break;
+    case 16: if (wide) GIFT_RED(16, 16, 1); else if (mid) GIFT_RED(16, 8, 2); else GIFT_RED(16, 4, 2); break;
     default:
       shape_grid(a, 1, grid, kColsPerWave, 1);
       hipLaunchKernelGGL(stream_reduce_any_kernel, grid, dim3(kThreads), 0, ctx->stream, a);

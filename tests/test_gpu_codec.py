@@ -172,7 +172,13 @@ def test_quantizer_sweep_bit_exact(ctx):
 
 @pytest.mark.parametrize("N,m,n,br,bc", [(1, 9, 13, 0, 0), (4, 77, 131, 0, 0),
                                          (8, 128, 256, 0, 128), (16, 50, 300, 10, 64),
-                                         (3, 33, 100, 1, 16)])
+                                         (3, 33, 100, 1, 16),
+                                         # 8 columns per lane (fewer idle lanes than 16):
+                                         # 1536 and 512 columns, and 1032 with 8-column blocks
+                                         (16, 40, 1536, 0, 128), (8, 33, 512, 8, 128),
+                                         (4, 21, 1536, 1, 64), (16, 7, 1032, 3, 8),
+                                         # 16 columns per lane across several waves of columns
+                                         (16, 9, 4096, 0, 128)])
 def test_reduce_bit_exact(ctx, N, m, n, br, bc):
     say(f"reduce N={N} m={m} n={n} block=({br},{bc})")
     grads = gradient_set(300 + N, 400 + m, N, m, n)
