@@ -1410,10 +1410,16 @@ int lr_proj_parts(int64_t M, int64_t K, int32_t batch) {
   // so more of them than that costs more HBM traffic than the extra
   // parallelism saves (measured on the MLP shapes: 2 instead of 4 partials
   // for the 5632 x 1024 gate + up bucket, 1408 -> 704 workgroups, makes the
-  // projection 7 % faster and the concurrent step 1.5 %)
+  // projection 7 % faster and the concurrent step 1.5 %). Launches of 128
+  // row tiles or more stop at two partials (one workgroup per CU already):
+  // on the Llama-600M o and down buckets (192 tiles of 16 ranks) 2 instead
+  // of 4 made the projection about 2 % slower alone and the four-stream
+  // codec step 37.38-37.50 -> 37.29-37.33 ms over three alternating runs
+  // (half the partials' traffic; the step is bound by its HBM bytes)
   const int64_t tiles = (M + kProjRows - 1) / kProjRows * batch;
+  const int max_parts = tiles >= 128 ? 2 : 4;
   int parts = 1;
-  while (parts < 4 && tiles * parts < 512 && K / (2 * parts) >= 2 * kProjStage) parts *= 2;
+  while (parts < max_parts && tiles * parts < 512 && K / (2 * parts) >= 2 * kProjStage) parts *= 2;
   return parts;
 }
 
