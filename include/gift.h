@@ -65,7 +65,7 @@ typedef enum {
   GIFT_ESHAPE = -2,        /* sizes inconsistent or out of the supported range */
   GIFT_ENOMEM = -3,        /* device or host allocation failed                */
   GIFT_EHIP = -4,          /* HIP runtime error while enqueueing              */
-  GIFT_EUNSUPPORTED = -5   /* valid request this build does not implement     */
+  GIFT_EUNSUPPORTED = -5   /* valid request the library does not implement   */
 } gift_status;
 
 typedef enum { GIFT_F32 = 0, GIFT_BF16 = 1 } gift_dtype;
