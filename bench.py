@@ -21,9 +21,11 @@ around each step), and ``ms_per_step`` / ``value`` are the cadence's average
 ``ms_per_step_raw`` is the plain mean over the timed steps.
 
 Independent matrices are spread over several HIP streams (one library
-context each): a matrix's encode, rank sum and decode stay in order on its
-stream, and each stream decodes its same-shape matrices in one grouped call
-after their rank sums.  The factor refresh runs once per factor shape (the smallest group on
+context each; for the Llama-600M set 6 streams over 8 hardware queues, each
+bucket to the stream with the fewest gradient bytes so far; otherwise 4
+streams dealt in turn): a matrix's encode, rank sum and decode stay in
+order on its stream, and each stream decodes its same-shape matrices in one
+grouped call after their rank sums.  The factor refresh runs once per factor shape (the smallest group on
 the main stream, the others on further streams), and a GIFT matrix's encode
 waits only for its own group's refresh; the Euclidean matrices run beside the
 refresh.
@@ -88,14 +90,27 @@ def parse():
                          "also holds the Euclidean matrices until the largest factor group's "
                          "refresh is done, euclid-after-statistics only until its statistics "
                          "kernel is done (the compute-bound part that cannot share CUs)")
-    ap.add_argument("--streams", type=int, default=4,
+    ap.add_argument("--streams", type=int, default=None,
                     help="HIP streams (one library context each); each matrix's encode -> rank sum "
-                         "-> decode stays on its stream")
-    ap.add_argument("--assign", choices=["round-robin", "balance"], default="round-robin",
+                         "-> decode stays on its stream (default 6 for the Llama-600M set, 4 "
+                         "otherwise)")
+    ap.add_argument("--assign", choices=["round-robin", "balance"], default=None,
                     help="GIFT buckets to streams: dealt in turn (in layer order, each layer's "
                          "buckets land on the same streams), or each to the stream with the fewest "
-                         "gradient bytes so far (measured slower on the Llama-600M set: 47.6 against "
-                         "38.0 ms per codec step, more kernels running at once)")
+                         "gradient bytes so far (default balance for the Llama-600M set, "
+                         "round-robin otherwise)")
+    ap.add_argument("--hw-queues", type=int, default=None,
+                    help="hardware queues of this process (GPU_MAX_HW_QUEUES, set before the HIP "
+                         "runtime starts; 0 keeps the environment's value; default 8 for the "
+                         "Llama-600M set, 4 (HIP's own) otherwise). Measured on the Llama-600M "
+                         "set (codec-only step): 4 queues, 4 streams dealt in turn 37.1-38.1 ms "
+                         "(the best with 4 queues; 2, 3, 6 streams and the balanced assignment "
+                         "slower); 8 queues, 6 streams balanced 33.1-34.2 ms over seven runs on "
+                         "three boxes (against 37.9-38.1 for the former on the same box), 5 / 7 / 8 "
+                         "streams 51.1 / 42.5 / 35.3-36.6 ms, 6 streams in turn 48.2 ms; 16 queues, "
+                         "6 / 8 / 12 streams balanced 33.2 / 33.8-34.9 / 50.8 ms. The Llama-300M "
+                         "set keeps 4 streams in turn: 13.0 ms per step, 16.9 with 6 balanced on "
+                         "8 queues")
     ap.add_argument("--breakdown-steps", type=int, default=2,
                     help="untimed steps with every kernel family bracketed by events")
     ap.add_argument("--format", choices=["fp8", "mxfp4"], default="fp8",
@@ -129,7 +144,16 @@ def parse():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run the library's plain copy kernel on 256 MiB (5 launches), "
                          "the known-size reference for the HBM byte counters")
-    return ap.parse_args()
+    args = ap.parse_args()
+    # the schedule measured best for each workload (see --hw-queues)
+    big = args.config == 5
+    if args.streams is None:
+        args.streams = 6 if big else 4
+    if args.assign is None:
+        args.assign = "balance" if big else "round-robin"
+    if args.hw_queues is None:
+        args.hw_queues = 8 if big else 4
+    return args
 
 
 def source_sha256(rel):
@@ -641,6 +665,9 @@ def fidelity_study(args):
 
 def main():
     args = parse()
+    if args.hw_queues > 0:
+        # read by the HIP runtime when it starts (nothing above has touched it)
+        os.environ["GPU_MAX_HW_QUEUES"] = str(args.hw_queues)
     if args.gpus != 1:
         print(f"bench.py runs on one GPU: the codec simulates its N data-parallel ranks locally "
               f"and has no multi-GPU path (asked for --gpus {args.gpus}).", file=sys.stderr)
@@ -956,7 +983,8 @@ def main():
                    "grad_gb": round(grad_bytes / 1e9, 3), "factor_refresh_every": wl.refresh,
                    "refreshes_timed": len(ref_ms), "subspace_iters": args.iters,
                    "mall_flushed": bool(args.flush_mall), "decode": args.decode,
-                   "assign": args.assign, "stream_gb": [round(x * 4 / 1e9, 2) for x in stream_load]},
+                   "assign": args.assign, "hw_queues": int(os.environ.get("GPU_MAX_HW_QUEUES", "0") or 0),
+                   "stream_gb": [round(x * 4 / 1e9, 2) for x in stream_load]},
         "transform_tflops": round(tf_flops / (tf_ms * 1e-3) / 1e12, 3) if tf_ms else None,
         "roofline": roof,
         "kernels": kernels,
