@@ -92,8 +92,8 @@ def parse():
                          "kernel is done (the compute-bound part that cannot share CUs)")
     ap.add_argument("--streams", type=int, default=None,
                     help="HIP streams (one library context each); each matrix's encode -> rank sum "
-                         "-> decode stays on its stream (default 6 for the Llama-600M set, 4 "
-                         "otherwise)")
+                         "-> decode stays on its stream (default 6 for the Llama-600M set, 8 "
+                         "with error feedback there, 4 otherwise)")
     ap.add_argument("--assign", choices=["round-robin", "balance"], default=None,
                     help="GIFT buckets to streams: dealt in turn (in layer order, each layer's "
                          "buckets land on the same streams), or each to the stream with the fewest "
@@ -110,7 +110,9 @@ def parse():
                          "streams 51.1 / 42.5 / 35.3-36.6 ms, 6 streams in turn 48.2 ms; 16 queues, "
                          "6 / 8 / 12 streams balanced 33.2 / 33.8-34.9 / 50.8 ms. The Llama-300M "
                          "set keeps 4 streams in turn: 13.0 ms per step, 16.9 with 6 balanced on "
-                         "8 queues")
+                         "8 queues. With error feedback (Llama-600M) 8 balanced streams on 8 "
+                         "queues: 44.2-46.7 ms per codec step, 6: 55.0-55.3, 4 in turn on 4 "
+                         "queues: 52.5")
     ap.add_argument("--breakdown-steps", type=int, default=2,
                     help="untimed steps with every kernel family bracketed by events")
     ap.add_argument("--format", choices=["fp8", "mxfp4"], default="fp8",
@@ -148,7 +150,7 @@ def parse():
     # the schedule measured best for each workload (see --hw-queues)
     big = args.config == 5
     if args.streams is None:
-        args.streams = 6 if big else 4
+        args.streams = (8 if args.ef else 6) if big else 4
     if args.assign is None:
         args.assign = "balance" if big else "round-robin"
     if args.hw_queues is None:
