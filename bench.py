@@ -667,13 +667,13 @@ def fidelity_study(args):
 
 def main():
     args = parse()
-    if args.hw_queues > 0:
-        # read by the HIP runtime when it starts (nothing above has touched it)
-        os.environ["GPU_MAX_HW_QUEUES"] = str(args.hw_queues)
     if args.gpus != 1:
         print(f"bench.py runs on one GPU: the codec simulates its N data-parallel ranks locally "
               f"and has no multi-GPU path (asked for --gpus {args.gpus}).", file=sys.stderr)
         sys.exit(2)
+    if args.hw_queues > 0:
+        # read by the HIP runtime when it starts (nothing above has touched it)
+        os.environ["GPU_MAX_HW_QUEUES"] = str(args.hw_queues)
     if args.copy_calibration:
         copy_calibration()
         return
